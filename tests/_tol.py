@@ -1,0 +1,41 @@
+"""Parity bars shared by the tests.
+
+Attention output O (bf16 inputs, fp32 accumulation) against the fp64 oracle:
+max|err| <= 1e-2 * max|ref| and mean|err| <= 1e-3, over all elements of one
+(configuration, layer).
+
+bf16-stored intermediates of unit scale (q, q_hat, k_hat): their storage alone
+gives a mean error of about 2^-9 * mean|ref|, so they are held to
+max|err| <= 1e-2 * max|ref| and mean|err| <= 2^-8 * mean|ref|.
+"""
+
+import numpy as np
+
+
+def o_errors(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    err = np.abs(got - ref)
+    return float(err.max()), float(err.mean()), float(np.abs(ref).max())
+
+
+def assert_o_close(got, ref, what="O"):
+    mx, mean, ref_max = o_errors(got, ref)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    assert mx <= 1e-2 * ref_max, f"{what}: max|err| {mx:.3e} > 1e-2 * max|ref| ({ref_max:.3e})"
+    assert mean <= 1e-3, f"{what}: mean|err| {mean:.3e} > 1e-3"
+    return mx, mean
+
+
+def o_within(got, ref) -> bool:
+    mx, mean, ref_max = o_errors(got, ref)
+    return mx <= 1e-2 * ref_max and mean <= 1e-3
+
+
+def assert_intermediate_close(got, ref, what="intermediate"):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    err = np.abs(got - ref)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    assert err.max() <= 1e-2 * np.abs(ref).max(), f"{what}: max|err| {err.max():.3e} vs max|ref| {np.abs(ref).max():.3e}"
+    assert err.mean() <= 2.0 ** -8 * np.abs(ref).mean(), f"{what}: mean|err| {err.mean():.3e} vs mean|ref| {np.abs(ref).mean():.3e}"
