@@ -1,0 +1,248 @@
+/*
+ * attuner.h -- C ABI of the Attuner suffix-prefill library (libattuner.so).
+ *
+ * What it computes (Attuner, "Recomputation-Free KV Cache Reuse via
+ * Query-Side Adaptation"): prefill of a request's online suffix over a frozen,
+ * position-independent artifact cache.
+ *   - Artifacts are encoded once, alone, with keys rotated at their own local
+ *     positions 0..L-1 (section 2, eq. 2, PIC; appendix C.1, PIC).  The library
+ *     keeps their per-layer K/V in a paged pool in device memory.
+ *   - A request's cached blocks are put together in prompt order without
+ *     re-encoding or re-rotation (section 2, the PIC box; appendix A.3,
+ *     "Cache construction and reuse").
+ *   - Suffix tokens get the query-side LoRA projection q = W_q h + s B (A h),
+ *     s = alpha / r (section 4, eq. 4); keys and values use the plain
+ *     projections, and stored artifact K/V is never modified.
+ *   - q and k pass through the per-head RMSNorm and RoPE (section 4), then
+ *     scaled dot-product GQA attention runs over [artifact keys ; suffix keys]
+ *     with every artifact key visible and a causal mask inside the suffix
+ *     (eq. 3 gives the form; appendix A.5, Deployment).
+ *   - attuner_full_prefill runs the same kernels on a whole request with no
+ *     cache (section 2, Full; appendix C.1, Full): the speed baseline, and,
+ *     on an artifact alone at position 0, the artifact encoder.
+ *
+ * Conventions shared by every call:
+ *   - All tensors are bfloat16 (raw 16-bit patterns) unless stated, row-major,
+ *     densely packed unless a leading dimension ("ld", in elements) is given.
+ *   - "device" pointers are device memory owned by the caller; the library
+ *     never frees them.  "host" pointers are read before the call returns.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Every call only
+ *     enqueues work on `stream` and returns without waiting for it, except
+ *     where noted; results are valid once the stream has reached that point.
+ *   - Every call returns a status; on failure nothing is enqueued, and
+ *     attuner_last_error() describes the cause.  Arguments are validated on
+ *     the host before any launch.
+ *   - One context may be used from one host thread and one stream at a time:
+ *     its internal workspaces are shared by all of its calls.
+ *   - Model geometry is fixed at create time; the kernels require
+ *     head_dim == 128, page_tokens == 16, n_q_heads == 4 * n_kv_heads and
+ *     hidden % 64 == 0.
+ */
+#ifndef ATTUNER_H
+#define ATTUNER_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ATTUNER_OK = 0,
+  ATTUNER_EINVAL = -1,  /* bad argument: null pointer, shape, rank, geometry  */
+  ATTUNER_ENOMEM = -2,  /* page pool full, or a device allocation failed       */
+  ATTUNER_ENOENT = -3,  /* unknown artifact id                                */
+  ATTUNER_EDEVICE = -4, /* a HIP runtime call failed                          */
+  ATTUNER_ERANGE = -5   /* a size beyond a documented limit                   */
+} attuner_status;
+
+typedef struct {
+  int32_t n_layers;    /* transformer layers whose K/V the pool holds          */
+  int32_t hidden;      /* model width H (projection input size)                */
+  int32_t n_q_heads;   /* Hq                                                   */
+  int32_t n_kv_heads;  /* Hkv; Hq / Hkv query heads share one K/V head         */
+  int32_t head_dim;    /* d (must be 128)                                      */
+  int32_t page_tokens; /* tokens per pool page (must be 16)                    */
+  float rope_theta;    /* rotary base (Qwen3: 1e6)                             */
+  float rms_eps;       /* RMSNorm epsilon (Qwen3: 1e-6)                        */
+} attuner_model_cfg;
+
+typedef struct attuner_ctx attuner_ctx;
+
+/* Largest number of requests in one assemble / attention call. */
+#define ATTUNER_MAX_REQUESTS 64
+/* Largest LoRA rank. */
+#define ATTUNER_MAX_RANK 64
+
+/* Thread-local description of the last failed call on this thread ("" if none). */
+const char* attuner_last_error(void);
+
+/* Create a context on HIP device `device` with a pool of `pool_pages` pages.
+ * A page holds page_tokens tokens of K and V for every layer and KV head:
+ * n_layers * 2 * n_kv_heads * page_tokens * head_dim * 2 bytes (see
+ * attuner_pool_info).  The pool is the only memory allocated here; it is
+ * released by attuner_destroy.  Synchronous.
+ * Errors: EINVAL (geometry), ENOMEM (allocation), EDEVICE. */
+attuner_status attuner_create(const attuner_model_cfg* cfg, int64_t pool_pages, int32_t device,
+                              attuner_ctx** out);
+
+/* Release the context, its pool and workspaces.  Waits for the device. */
+void attuner_destroy(attuner_ctx* ctx);
+
+/* Pool geometry and occupancy (host outputs; any may be NULL). */
+attuner_status attuner_pool_info(const attuner_ctx* ctx, int64_t* pool_pages, int64_t* free_pages,
+                                 int64_t* page_bytes);
+
+/* --------------------------------------------------------------------------
+ * a0: store a frozen artifact (cache construction, section 2 eq. 2, PIC).
+ *
+ * k, v: device [n_layers][n_kv_heads][n_tokens][head_dim], k already
+ * normalised and rotated at local positions 0..n_tokens-1.  The values are
+ * copied bit for bit into ceil(n_tokens / page_tokens) pool pages (unused
+ * rows of the last page are zero).  The caller keeps ownership of k and v and
+ * may reuse them once the stream has passed this call.  *artifact_id receives
+ * a new id (>= 0).
+ * Errors: EINVAL (n_tokens <= 0, null pointer), ENOMEM (pool full).
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_store_artifact(attuner_ctx* ctx, int32_t n_tokens, const void* k, const void* v,
+                                      void* stream, int32_t* artifact_id);
+
+/* Return an artifact's pages to the pool.  Work already enqueued that reads
+ * them must have completed before the pages are reused by a later store.
+ * Errors: ENOENT. */
+attuner_status attuner_release_artifact(attuner_ctx* ctx, int32_t artifact_id);
+
+/* Physical page ids of an artifact, in token order (host output of up to
+ * max_pages entries), its page count and its token count.  Errors: ENOENT,
+ * ERANGE (max_pages too small; *n_pages still set). */
+attuner_status attuner_artifact_pages(const attuner_ctx* ctx, int32_t artifact_id, int32_t* pages_out,
+                                      int32_t max_pages, int32_t* n_pages, int32_t* n_tokens);
+
+/* --------------------------------------------------------------------------
+ * a1 + a2: assemble request caches (section 2, the PIC box; appendix A.3).
+ *
+ * A batch of n_req requests, CSR over host arrays: request r uses artifacts
+ * artifact_ids[req_ptr[r] .. req_ptr[r+1]) in that (prompt) order; ids may
+ * repeat; a request may have none.  suffix_cap[r] rows are reserved after
+ * its artifacts for the suffix tokens.
+ *
+ * Request r owns rows [cu_ctx[r], cu_ctx[r+1]) of the assembled cache, with
+ * cu_ctx[0] = 0 and cu_ctx[r+1] = cu_ctx[r] + art_len[r] + suffix_cap[r];
+ * its artifacts fill rows cu_ctx[r] .. cu_ctx[r] + art_len[r] - 1 back to
+ * back.  The cache (req_kv, device) is laid out
+ *     [n_layers][2 (K, V)][n_kv_heads][cache_rows][head_dim]
+ * with cache_rows = cu_ctx[n_req].  attuner_assemble_plan returns n_entries
+ * and cache_rows so the caller can size its buffers.
+ *
+ * The block table (device, n_entries x 4 int32) gets one entry per logical
+ * page, in request, artifact, page order:
+ *     { physical page, valid tokens, first destination row, request }.
+ * It is built on the host and copied to block_table asynchronously; the
+ * gather kernel then copies every page of every layer into req_kv (one
+ * launch).  Rows outside the artifacts (the suffix rows) are not written.
+ * cu_ctx (host, n_req + 1) and art_len (host, n_req) receive the layout.
+ * Errors: EINVAL, ENOENT (unknown id), ERANGE (n_req > ATTUNER_MAX_REQUESTS,
+ * or cache_rows does not match the plan).
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_assemble_plan(const attuner_ctx* ctx, int32_t n_req, const int32_t* req_ptr,
+                                     const int32_t* artifact_ids, const int32_t* suffix_cap,
+                                     int64_t* n_entries, int64_t* cache_rows);
+
+attuner_status attuner_assemble_kv(attuner_ctx* ctx, int32_t n_req, const int32_t* req_ptr,
+                                   const int32_t* artifact_ids, const int32_t* suffix_cap,
+                                   int32_t* block_table, int32_t* cu_ctx, int32_t* art_len,
+                                   void* req_kv, int64_t cache_rows, void* stream);
+
+/* --------------------------------------------------------------------------
+ * a3: LoRA-adapted projection (section 4, eq. 4; fused q/k/v weights).
+ *
+ *   out[i][n] = sum_k x[i][k] w[n][k]
+ *             + (n < lora_cols ? scale * sum_j (sum_k x[i][k] a[j][k]) b[n][j] : 0)
+ *
+ * x: device [n_tok][hidden]; w: device [n_out][hidden]; a: device
+ * [rank][hidden]; b: device [lora_cols][rank]; out: device [n_tok][n_out].
+ * Accumulation is fp32; out is rounded to bf16 once.  rank == 0 (a, b may be
+ * NULL) is the plain projection, i.e. the merged-weight deployment form.
+ * With w = [W_q; W_k; W_v] and lora_cols = n_q_heads * head_dim the keys and
+ * values stay unadapted, as the method requires.
+ * Requires n_out % 128 == 0, lora_cols % 32 == 0, lora_cols <= n_out,
+ * 0 <= rank <= ATTUNER_MAX_RANK, n_tok >= 0.  Uses a context workspace
+ * (grown with hipMalloc on first use at a larger n_tok or rank).
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_qproj_lora(attuner_ctx* ctx, int32_t n_tok, const void* x, const void* w,
+                                  int32_t n_out, const void* a, const void* b, int32_t rank, float scale,
+                                  int32_t lora_cols, void* out, void* stream);
+
+/* --------------------------------------------------------------------------
+ * a4: per-head QK-RMSNorm + RoPE of the suffix (section 4: the adapted query
+ * passes through the model's own query normalisation and RoPE).
+ *
+ * Per request r (host arrays of n_req entries, cu_q of n_req + 1): suffix
+ * tokens are rows cu_q[r] .. cu_q[r+1]-1 of q_raw/k_raw/v_raw; token i of the
+ * request sits at position pos0[r] + i.
+ *   q_hat = rope(gamma_q * q / sqrt(mean(q^2) + eps))   per query head
+ *   k_hat = rope(gamma_k * k / sqrt(mean(k^2) + eps))   per KV head
+ * rope pairs dimension j with j + 64 and turns it by (pos) * theta^(-2j/128)
+ * (angles from an fp64 host table, stored fp32).
+ * q_raw: device, row stride ld_q, Hq*d columns; k_raw, v_raw: device, row
+ * stride ld_kv, Hkv*d columns; gamma_q, gamma_k: device [head_dim].
+ * q_hat: device [T_q][Hq][d].  k_hat and v of request r's token i are written
+ * to cache row cu_ctx[r] + art_len[r] + i of layer `layer` of req_kv
+ * (layout of attuner_assemble_kv).  Requires art_len[r] + (cu_q[r+1] -
+ * cu_q[r]) <= cu_ctx[r+1] - cu_ctx[r].
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_qk_norm_rope(attuner_ctx* ctx, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                    const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                    const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                    int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* q_hat,
+                                    void* req_kv, int64_t cache_rows, void* stream);
+
+/* --------------------------------------------------------------------------
+ * a5: multi-segment GQA attention over an assembled cache (eq. 3 form with
+ * the causal mask; appendix A.5).
+ *
+ * Suffix token i of request r, query head h, reads KV head h / (Hq / Hkv) at
+ * cache rows cu_ctx[r] + j for j = 0 .. art_len[r] + i: all artifact keys and
+ * the suffix causally.  o[t][h][:] = sum_j softmax_j(q_hat . k_j / sqrt(d)) v_j.
+ * q_hat: device [T_q][Hq][d]; o: device [T_q][Hq][d] (bf16);
+ * lse: device [T_q][Hq] fp32 natural-log sum of exp of the scaled scores, or
+ * NULL.  o may alias q_hat exactly (same pointer).  The cached rows
+ * art_len[r] .. art_len[r] + q_len - 1 must already hold the suffix keys and
+ * values (attuner_qk_norm_rope writes them).
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_attention(attuner_ctx* ctx, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                 const int32_t* cu_ctx, const int32_t* art_len, const void* q_hat,
+                                 const void* req_kv, int64_t cache_rows, void* o, float* lse, void* stream);
+
+/* a4 + a5 in one call: q_raw/k_raw/v_raw as in attuner_qk_norm_rope; the
+ * normalised queries are staged in `o`, which then receives the attention
+ * output [T_q][Hq][d]. */
+attuner_status attuner_suffix_attn(attuner_ctx* ctx, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                   const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                   const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                   int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                   int64_t cache_rows, void* o, float* lse, void* stream);
+
+/* --------------------------------------------------------------------------
+ * a6: full-context prefill of one layer with the same kernels (section 2,
+ * Full; appendix C.1, Full).
+ *
+ * x: device [n_tok][hidden] at positions pos0 .. pos0 + n_tok - 1; wqkv: device
+ * [(Hq + 2 Hkv) d][hidden] (rows W_q, then W_k, then W_v); a, b, rank, scale
+ * as in attuner_qproj_lora on the query rows (rank 0 = no adapter, the
+ * paper's Full).  Plain causal attention over the n_tok tokens.
+ * o: device [n_tok][Hq][d]; k_out, v_out: device [n_kv_heads][n_tok][d]
+ * (normalised/rotated keys and raw values: with pos0 = 0 on an artifact
+ * alone, the K/V attuner_store_artifact expects for one layer);
+ * lse: device [n_tok][Hq] fp32 or NULL.  Uses context workspaces.
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_full_prefill(attuner_ctx* ctx, int32_t n_tok, int32_t pos0, const void* x,
+                                    const void* wqkv, const void* a, const void* b, int32_t rank,
+                                    float scale, const void* gamma_q, const void* gamma_k, void* o,
+                                    void* k_out, void* v_out, float* lse, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTUNER_H */

@@ -1,0 +1,69 @@
+"""ctypes loader of libattuner.so (built in-tree by ``paper_2609_36722_amd.build``).
+
+Loading fails loudly when the library is missing: there is no fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libattuner.so")
+
+STATUS = {0: "ATTUNER_OK", -1: "ATTUNER_EINVAL", -2: "ATTUNER_ENOMEM", -3: "ATTUNER_ENOENT",
+          -4: "ATTUNER_EDEVICE", -5: "ATTUNER_ERANGE"}
+
+MAX_REQUESTS = 64
+MAX_RANK = 64
+
+
+class ModelCfgC(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("hidden", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("page_tokens", C.c_int32),
+                ("rope_theta", C.c_float), ("rms_eps", C.c_float)]
+
+
+_i32p = C.POINTER(C.c_int32)
+_i64p = C.POINTER(C.c_int64)
+_vp = C.c_void_p
+_i32 = C.c_int32
+_i64 = C.c_int64
+
+# name -> (restype, argtypes); the exported C ABI of include/attuner.h
+SIGNATURES = {
+    "attuner_last_error": (C.c_char_p, []),
+    "attuner_create": (C.c_int, [C.POINTER(ModelCfgC), _i64, _i32, C.POINTER(_vp)]),
+    "attuner_destroy": (None, [_vp]),
+    "attuner_pool_info": (C.c_int, [_vp, _i64p, _i64p, _i64p]),
+    "attuner_store_artifact": (C.c_int, [_vp, _i32, _vp, _vp, _vp, _i32p]),
+    "attuner_release_artifact": (C.c_int, [_vp, _i32]),
+    "attuner_artifact_pages": (C.c_int, [_vp, _i32, _i32p, _i32, _i32p, _i32p]),
+    "attuner_assemble_plan": (C.c_int, [_vp, _i32, _i32p, _i32p, _i32p, _i64p, _i64p]),
+    "attuner_assemble_kv": (C.c_int, [_vp, _i32, _i32p, _i32p, _i32p, _vp, _i32p, _i32p, _vp, _i64, _vp]),
+    "attuner_qproj_lora": (C.c_int, [_vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, C.c_float, _i32, _vp, _vp]),
+    "attuner_qk_norm_rope": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64,
+                                       _vp, _vp, _vp, _vp, _i64, _vp]),
+    "attuner_attention": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "attuner_suffix_attn": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64,
+                                      _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "attuner_full_prefill": (C.c_int, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, C.c_float, _vp, _vp, _vp, _vp,
+                                       _vp, _vp, _vp]),
+}
+
+_LIB = None
+
+
+def lib() -> C.CDLL:
+    """Load libattuner.so once and declare its exports."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2609_36722_amd.build` "
+                               "(or __graft_entry__.build()) first")
+        handle = C.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = handle
+    return _LIB

@@ -1,0 +1,692 @@
+// Host runtime of libattuner: context, paged artifact pool, block-table
+// builder, workspaces, launch planning and the C ABI declared in attuner.h.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <new>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "attuner.h"
+#include "kernels.h"
+
+using namespace attuner;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+attuner_status fail(attuner_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+#define HIP_TRY(expr)                                                                        \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(ATTUNER_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Growable device buffer.  Growth waits for the device, so buffers are never
+// freed under queued work.
+struct DeviceBuf {
+  void* ptr = nullptr;
+  size_t cap = 0;
+  hipError_t ensure(size_t bytes) {
+    if (bytes <= cap) return hipSuccess;
+    if (ptr) {
+      hipError_t e = hipDeviceSynchronize();
+      if (e != hipSuccess) return e;
+      e = hipFree(ptr);
+      ptr = nullptr;
+      cap = 0;
+      if (e != hipSuccess) return e;
+    }
+    size_t want = std::max(bytes, cap * 2);
+    hipError_t e = hipMalloc(&ptr, want);
+    if (e != hipSuccess) {
+      ptr = nullptr;
+      return e;
+    }
+    cap = want;
+    return hipSuccess;
+  }
+  void release() {
+    if (ptr) (void)hipFree(ptr);
+    ptr = nullptr;
+    cap = 0;
+  }
+};
+
+// Pinned host staging for small host->device uploads (block tables, page
+// lists).  Two slots used in turn; a slot is refilled only after the copy
+// that last read it has completed.
+struct Staging {
+  void* host[2] = {nullptr, nullptr};
+  size_t cap[2] = {0, 0};
+  hipEvent_t done[2] = {nullptr, nullptr};
+  bool pending[2] = {false, false};
+  int next = 0;
+
+  hipError_t upload(const void* src, size_t bytes, void* dst_dev, hipStream_t stream) {
+    if (bytes == 0) return hipSuccess;
+    const int s = next;
+    next ^= 1;
+    hipError_t e;
+    if (pending[s]) {
+      e = hipEventSynchronize(done[s]);
+      if (e != hipSuccess) return e;
+      pending[s] = false;
+    }
+    if (done[s] == nullptr) {
+      e = hipEventCreateWithFlags(&done[s], hipEventDisableTiming);
+      if (e != hipSuccess) return e;
+    }
+    if (cap[s] < bytes) {
+      if (host[s]) (void)hipHostFree(host[s]);
+      host[s] = nullptr;
+      cap[s] = 0;
+      const size_t want = std::max(bytes, (size_t)1 << 16);
+      e = hipHostMalloc(&host[s], want, hipHostMallocDefault);
+      if (e != hipSuccess) {
+        host[s] = nullptr;
+        return e;
+      }
+      cap[s] = want;
+    }
+    memcpy(host[s], src, bytes);
+    e = hipMemcpyAsync(dst_dev, host[s], bytes, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(done[s], stream);
+    if (e != hipSuccess) return e;
+    pending[s] = true;
+    return hipSuccess;
+  }
+  void release() {
+    for (int s = 0; s < 2; ++s) {
+      if (pending[s]) (void)hipEventSynchronize(done[s]);
+      if (done[s]) (void)hipEventDestroy(done[s]);
+      if (host[s]) (void)hipHostFree(host[s]);
+      host[s] = nullptr;
+      done[s] = nullptr;
+    }
+  }
+};
+
+struct Artifact {
+  std::vector<int32_t> pages;
+  int32_t n_tokens;
+};
+
+}  // namespace
+
+struct attuner_ctx {
+  attuner_model_cfg cfg;
+  int device = 0;
+  int64_t pool_pages = 0;
+  int64_t page_bytes = 0;  // one page, all layers
+  uint16_t* pool = nullptr;
+  std::set<int32_t> free_pages;
+  std::map<int32_t, Artifact> artifacts;
+  int32_t next_id = 0;
+
+  DeviceBuf ws_pages;   // page list of the artifact being stored
+  DeviceBuf ws_lora;    // t_hi, t_lo of the LoRA-down pass
+  DeviceBuf ws_part;    // split-KV partials
+  DeviceBuf ws_qkv;     // full prefill: fused projection output
+  DeviceBuf rope;       // (cos, sin) table [rope_pos][64]
+  int64_t rope_pos = 0;
+  Staging staging;
+};
+
+namespace {
+
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) (void)hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+int q_dim(const attuner_ctx* c) { return c->cfg.n_q_heads * c->cfg.head_dim; }
+int kv_dim(const attuner_ctx* c) { return c->cfg.n_kv_heads * c->cfg.head_dim; }
+
+// (cos, sin) of pos * theta^(-2j/128) for pos < n, evaluated in double.
+attuner_status ensure_rope(attuner_ctx* c, int64_t n) {
+  if (n <= c->rope_pos) return ATTUNER_OK;
+  int64_t want = 4096;
+  while (want < n) want *= 2;
+  std::vector<float> tab((size_t)want * 64 * 2);
+  const double theta = c->cfg.rope_theta;
+  for (int j = 0; j < 64; ++j) {
+    const double inv_freq = std::pow(theta, -2.0 * j / 128.0);
+    for (int64_t p = 0; p < want; ++p) {
+      const double ang = (double)p * inv_freq;
+      tab[((size_t)p * 64 + j) * 2] = (float)std::cos(ang);
+      tab[((size_t)p * 64 + j) * 2 + 1] = (float)std::sin(ang);
+    }
+  }
+  HIP_TRY(c->rope.ensure(tab.size() * sizeof(float)));
+  HIP_TRY(hipMemcpy(c->rope.ptr, tab.data(), tab.size() * sizeof(float), hipMemcpyHostToDevice));
+  c->rope_pos = want;
+  return ATTUNER_OK;
+}
+
+// One request of a norm+rope / attention batch, in host form.
+struct ReqDesc {
+  int32_t q_start, q_len, kv_start, art_len, pos0;
+};
+
+attuner_status run_norm_rope(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int32_t total_q, const void* q_raw,
+                             int64_t ld_q, const void* k_raw, const void* v_raw, int64_t ld_kv, const void* gamma_q,
+                             const void* gamma_k, void* q_hat, uint16_t* k_plane, uint16_t* v_plane,
+                             int64_t head_stride, hipStream_t stream) {
+  int64_t max_pos = 0;
+  for (const auto& r : reqs) max_pos = std::max<int64_t>(max_pos, (int64_t)r.pos0 + r.q_len);
+  attuner_status st = ensure_rope(c, max_pos);
+  if (st != ATTUNER_OK) return st;
+  NormRopeParams p;
+  memset(&p, 0, sizeof p);
+  p.q_raw = static_cast<const uint16_t*>(q_raw);
+  p.k_raw = static_cast<const uint16_t*>(k_raw);
+  p.v_raw = static_cast<const uint16_t*>(v_raw);
+  p.ld_q = ld_q;
+  p.ld_kv = ld_kv;
+  p.gamma_q = static_cast<const uint16_t*>(gamma_q);
+  p.gamma_k = static_cast<const uint16_t*>(gamma_k);
+  p.rope = static_cast<const float2*>(c->rope.ptr);
+  p.q_hat = static_cast<uint16_t*>(q_hat);
+  p.k_cache = k_plane;
+  p.v_cache = v_plane;
+  p.kv_head_stride = head_stride;
+  p.n_q_heads = c->cfg.n_q_heads;
+  p.n_kv_heads = c->cfg.n_kv_heads;
+  p.total_q = total_q;
+  p.eps = c->cfg.rms_eps;
+  p.n_req = (int32_t)reqs.size();
+  for (size_t r = 0; r < reqs.size(); ++r) {
+    p.req[r].q_start = reqs[r].q_start;
+    p.req[r].q_len = reqs[r].q_len;
+    p.req[r].kv_row0 = reqs[r].kv_start + reqs[r].art_len;
+    p.req[r].pos0 = reqs[r].pos0;
+  }
+  HIP_TRY(launch_qk_norm_rope(p, stream));
+  return ATTUNER_OK;
+}
+
+attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int32_t total_q, const void* q,
+                             const uint16_t* k_plane, const uint16_t* v_plane, int64_t head_stride, void* o,
+                             float* lse, hipStream_t stream) {
+  AttnParams p;
+  memset(&p, 0, sizeof p);
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = k_plane;
+  p.v = v_plane;
+  p.kv_head_stride = head_stride;
+  p.o = static_cast<uint16_t*>(o);
+  p.lse = lse;
+  p.n_q_heads = c->cfg.n_q_heads;
+  p.n_kv_heads = c->cfg.n_kv_heads;
+  p.total_q = total_q;
+  p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c->cfg.head_dim));
+  p.n_req = (int32_t)reqs.size();
+
+  // Split the keys of each query block when the blocks alone would not give
+  // every CU two workgroups; keep at least four 64-key tiles per split.
+  int64_t blocks = 0;
+  int64_t min_tiles = INT64_MAX;
+  for (const auto& r : reqs) {
+    if (r.q_len <= 0) continue;
+    blocks += (r.q_len + 31) / 32;
+    min_tiles = std::min<int64_t>(min_tiles, (r.art_len + r.q_len + 63) / 64);
+  }
+  const int64_t base = blocks * c->cfg.n_kv_heads;
+  int n_split = 1;
+  if (base > 0 && base < 512) {
+    n_split = (int)std::min<int64_t>(16, (512 + base - 1) / base);
+    n_split = (int)std::max<int64_t>(1, std::min<int64_t>(n_split, min_tiles / 4));
+  }
+  p.n_split = n_split;
+  int32_t units = 0;
+  for (size_t r = 0; r < reqs.size(); ++r) {
+    const int nq = (reqs[r].q_len + 31) / 32;
+    p.req[r].q_start = reqs[r].q_start;
+    p.req[r].q_len = reqs[r].q_len;
+    p.req[r].kv_start = reqs[r].kv_start;
+    p.req[r].art_len = reqs[r].art_len;
+    p.req[r].n_qblk = nq;
+    p.req[r].wg_start = units;
+    units += nq * n_split;
+  }
+  p.n_units = units;
+  if (n_split > 1) {
+    const size_t rows = (size_t)n_split * total_q * c->cfg.n_q_heads;
+    const size_t po = rows * c->cfg.head_dim * sizeof(float);
+    HIP_TRY(c->ws_part.ensure(po + rows * 2 * sizeof(float)));
+    p.part_o = static_cast<float*>(c->ws_part.ptr);
+    p.part_ml = reinterpret_cast<float*>(static_cast<char*>(c->ws_part.ptr) + po);
+  }
+  HIP_TRY(launch_attention(p, stream));
+  if (n_split > 1) HIP_TRY(launch_attn_combine(p, stream));
+  return ATTUNER_OK;
+}
+
+// Validate the per-request host arrays of a norm/attention call against a cache.
+attuner_status build_reqs(const attuner_ctx* c, int32_t n_req, const int32_t* cu_q, const int32_t* cu_ctx,
+                          const int32_t* art_len, const int32_t* pos0, int64_t cache_rows,
+                          std::vector<ReqDesc>* out, int32_t* total_q) {
+  if (n_req < 0 || n_req > ATTUNER_MAX_REQUESTS)
+    return fail(ATTUNER_ERANGE, "n_req %d outside [0, %d]", n_req, ATTUNER_MAX_REQUESTS);
+  if (n_req > 0 && (!cu_q || !cu_ctx || !art_len)) return fail(ATTUNER_EINVAL, "null request array");
+  (void)c;
+  out->clear();
+  if (n_req == 0) {
+    *total_q = 0;
+    return ATTUNER_OK;
+  }
+  if (cu_q[0] != 0 || cu_ctx[0] != 0) return fail(ATTUNER_EINVAL, "cu_q[0] and cu_ctx[0] must be 0");
+  for (int r = 0; r < n_req; ++r) {
+    ReqDesc d;
+    d.q_start = cu_q[r];
+    d.q_len = cu_q[r + 1] - cu_q[r];
+    d.kv_start = cu_ctx[r];
+    d.art_len = art_len[r];
+    d.pos0 = pos0 ? pos0[r] : art_len[r];
+    const int64_t rows = (int64_t)cu_ctx[r + 1] - cu_ctx[r];
+    if (d.q_len < 0 || rows < 0 || d.art_len < 0 || d.pos0 < 0)
+      return fail(ATTUNER_EINVAL, "request %d: negative length or position", r);
+    if ((int64_t)d.art_len + d.q_len > rows)
+      return fail(ATTUNER_EINVAL, "request %d: art_len %d + suffix %d exceeds its %lld cache rows", r, d.art_len,
+                  d.q_len, (long long)rows);
+    out->push_back(d);
+  }
+  if ((int64_t)cu_ctx[n_req] > cache_rows)
+    return fail(ATTUNER_EINVAL, "cu_ctx[n_req] = %d exceeds cache_rows %lld", cu_ctx[n_req], (long long)cache_rows);
+  *total_q = cu_q[n_req];
+  return ATTUNER_OK;
+}
+
+attuner_status check_layer(const attuner_ctx* c, int32_t layer) {
+  if (layer < 0 || layer >= c->cfg.n_layers)
+    return fail(ATTUNER_EINVAL, "layer %d outside [0, %d)", layer, c->cfg.n_layers);
+  return ATTUNER_OK;
+}
+
+uint16_t* cache_plane(void* req_kv, const attuner_ctx* c, int layer, int kv, int64_t cache_rows) {
+  return static_cast<uint16_t*>(req_kv) +
+         ((int64_t)layer * 2 + kv) * c->cfg.n_kv_heads * cache_rows * c->cfg.head_dim;
+}
+
+attuner_status qproj_impl(attuner_ctx* c, int32_t n_tok, const void* x, const void* w, int32_t n_out,
+                          const void* a, const void* b, int32_t rank, float scale, int32_t lora_cols, void* out,
+                          hipStream_t stream) {
+  if (n_tok < 0) return fail(ATTUNER_EINVAL, "n_tok < 0");
+  if (rank < 0 || rank > ATTUNER_MAX_RANK) return fail(ATTUNER_ERANGE, "rank %d outside [0, %d]", rank, ATTUNER_MAX_RANK);
+  if (n_out <= 0 || n_out % 128 != 0) return fail(ATTUNER_EINVAL, "n_out %d must be a positive multiple of 128", n_out);
+  if (rank > 0 && (lora_cols < 0 || lora_cols % 32 != 0 || lora_cols > n_out))
+    return fail(ATTUNER_EINVAL, "lora_cols %d must be a multiple of 32 in [0, n_out]", lora_cols);
+  if (n_tok == 0) return ATTUNER_OK;
+  if (!x || !w || !out) return fail(ATTUNER_EINVAL, "null x, w or out");
+  if (rank > 0 && (!a || !b)) return fail(ATTUNER_EINVAL, "rank %d needs a and b", rank);
+  if (!aligned16(x) || !aligned16(w) || !aligned16(out) || (rank > 0 && !aligned16(a)))
+    return fail(ATTUNER_EINVAL, "x, w, a and out must be 16-byte aligned");
+  const int hidden = c->cfg.hidden;
+  const int r_pad = rank > 0 && lora_cols > 0 ? (rank + 15) / 16 * 16 : 0;
+  uint16_t* t_hi = nullptr;
+  uint16_t* t_lo = nullptr;
+  if (r_pad > 0) {
+    const size_t bytes = (size_t)n_tok * r_pad * sizeof(uint16_t);
+    HIP_TRY(c->ws_lora.ensure(2 * bytes));
+    t_hi = static_cast<uint16_t*>(c->ws_lora.ptr);
+    t_lo = t_hi + (size_t)n_tok * r_pad;
+    HIP_TRY(launch_lora_down(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(a), n_tok, hidden, rank,
+                             r_pad, scale, t_hi, t_lo, stream));
+  }
+  HIP_TRY(launch_gemm_lora(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), n_tok, n_out, hidden,
+                           static_cast<const uint16_t*>(b), rank, r_pad, lora_cols, t_hi, t_lo,
+                           static_cast<uint16_t*>(out), stream));
+  return ATTUNER_OK;
+}
+
+}  // namespace
+
+// ============================================================================
+// C ABI
+// ============================================================================
+
+extern "C" {
+
+const char* attuner_last_error(void) { return g_last_error.c_str(); }
+
+attuner_status attuner_create(const attuner_model_cfg* cfg, int64_t pool_pages, int32_t device, attuner_ctx** out) {
+  g_last_error.clear();
+  if (!cfg || !out) return fail(ATTUNER_EINVAL, "null cfg or out");
+  *out = nullptr;
+  if (cfg->head_dim != kHeadDim) return fail(ATTUNER_EINVAL, "head_dim %d: kernels are built for 128", cfg->head_dim);
+  if (cfg->page_tokens != kPageTokens)
+    return fail(ATTUNER_EINVAL, "page_tokens %d: kernels are built for 16", cfg->page_tokens);
+  if (cfg->n_kv_heads <= 0 || cfg->n_q_heads != 4 * cfg->n_kv_heads)
+    return fail(ATTUNER_EINVAL, "n_q_heads %d must be 4 * n_kv_heads (%d)", cfg->n_q_heads, cfg->n_kv_heads);
+  if (cfg->hidden <= 0 || cfg->hidden % 64 != 0) return fail(ATTUNER_EINVAL, "hidden %d must be a multiple of 64", cfg->hidden);
+  if (cfg->n_layers <= 0 || cfg->n_layers > 65535) return fail(ATTUNER_EINVAL, "n_layers %d outside [1, 65535]", cfg->n_layers);
+  if (!(cfg->rope_theta > 1.0f) || !(cfg->rms_eps >= 0.0f)) return fail(ATTUNER_EINVAL, "bad rope_theta or rms_eps");
+  if (pool_pages < 0 || pool_pages > INT32_MAX) return fail(ATTUNER_ERANGE, "pool_pages %lld", (long long)pool_pages);
+  int n_dev = 0;
+  HIP_TRY(hipGetDeviceCount(&n_dev));
+  if (device < 0 || device >= n_dev) return fail(ATTUNER_EINVAL, "device %d of %d", device, n_dev);
+  attuner_ctx* c = new (std::nothrow) attuner_ctx;
+  if (!c) return fail(ATTUNER_ENOMEM, "host allocation");
+  c->cfg = *cfg;
+  c->device = device;
+  c->pool_pages = pool_pages;
+  c->page_bytes = (int64_t)cfg->n_layers * 2 * cfg->n_kv_heads * kPageTokens * kHeadDim * 2;
+  DeviceGuard dg(device);
+  if (pool_pages > 0) {
+    hipError_t e = hipMalloc(reinterpret_cast<void**>(&c->pool), (size_t)(pool_pages * c->page_bytes));
+    if (e != hipSuccess) {
+      const long long bytes = (long long)(pool_pages * c->page_bytes);
+      delete c;
+      return fail(ATTUNER_ENOMEM, "pool of %lld pages (%lld bytes): %s", (long long)pool_pages, bytes,
+                  hipGetErrorString(e));
+    }
+  }
+  for (int32_t p = 0; p < (int32_t)pool_pages; ++p) c->free_pages.insert(c->free_pages.end(), p);
+  *out = c;
+  return ATTUNER_OK;
+}
+
+void attuner_destroy(attuner_ctx* c) {
+  if (!c) return;
+  DeviceGuard dg(c->device);
+  (void)hipDeviceSynchronize();
+  c->staging.release();
+  c->ws_pages.release();
+  c->ws_lora.release();
+  c->ws_part.release();
+  c->ws_qkv.release();
+  c->rope.release();
+  if (c->pool) (void)hipFree(c->pool);
+  delete c;
+}
+
+attuner_status attuner_pool_info(const attuner_ctx* c, int64_t* pool_pages, int64_t* free_pages, int64_t* page_bytes) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (pool_pages) *pool_pages = c->pool_pages;
+  if (free_pages) *free_pages = (int64_t)c->free_pages.size();
+  if (page_bytes) *page_bytes = c->page_bytes;
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_store_artifact(attuner_ctx* c, int32_t n_tokens, const void* k, const void* v, void* stream,
+                                      int32_t* artifact_id) {
+  if (!c || !artifact_id) return fail(ATTUNER_EINVAL, "null ctx or artifact_id");
+  if (n_tokens <= 0) return fail(ATTUNER_EINVAL, "an artifact holds at least one token (got %d)", n_tokens);
+  if (!k || !v) return fail(ATTUNER_EINVAL, "null k or v");
+  if (!aligned16(k) || !aligned16(v)) return fail(ATTUNER_EINVAL, "k and v must be 16-byte aligned");
+  const int64_t need = (n_tokens + kPageTokens - 1) / kPageTokens;
+  if (need > (int64_t)c->free_pages.size())
+    return fail(ATTUNER_ENOMEM, "pool full: artifact needs %lld pages, %zu free", (long long)need, c->free_pages.size());
+  DeviceGuard dg(c->device);
+  try {
+    HIP_TRY(c->ws_pages.ensure((size_t)need * sizeof(int32_t)));
+    Artifact art;
+    art.n_tokens = n_tokens;
+    auto it = c->free_pages.begin();
+    for (int64_t i = 0; i < need; ++i) art.pages.push_back(*it++);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(c->staging.upload(art.pages.data(), art.pages.size() * sizeof(int32_t), c->ws_pages.ptr, s));
+    HIP_TRY(launch_store_pages(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), n_tokens,
+                               static_cast<const int32_t*>(c->ws_pages.ptr), (int)need, c->pool, c->pool_pages,
+                               c->cfg.n_layers, c->cfg.n_kv_heads, s));
+    for (int32_t pg : art.pages) c->free_pages.erase(pg);
+    const int32_t id = c->next_id++;
+    c->artifacts.emplace(id, std::move(art));
+    *artifact_id = id;
+  } catch (const std::bad_alloc&) {
+    return fail(ATTUNER_ENOMEM, "host allocation");
+  }
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_release_artifact(attuner_ctx* c, int32_t artifact_id) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  auto it = c->artifacts.find(artifact_id);
+  if (it == c->artifacts.end()) return fail(ATTUNER_ENOENT, "unknown artifact id %d", artifact_id);
+  for (int32_t pg : it->second.pages) c->free_pages.insert(pg);
+  c->artifacts.erase(it);
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_artifact_pages(const attuner_ctx* c, int32_t artifact_id, int32_t* pages_out, int32_t max_pages,
+                                      int32_t* n_pages, int32_t* n_tokens) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  auto it = c->artifacts.find(artifact_id);
+  if (it == c->artifacts.end()) return fail(ATTUNER_ENOENT, "unknown artifact id %d", artifact_id);
+  const int32_t np = (int32_t)it->second.pages.size();
+  if (n_pages) *n_pages = np;
+  if (n_tokens) *n_tokens = it->second.n_tokens;
+  if (pages_out) {
+    if (max_pages < np) return fail(ATTUNER_ERANGE, "max_pages %d < %d pages", max_pages, np);
+    memcpy(pages_out, it->second.pages.data(), (size_t)np * sizeof(int32_t));
+  }
+  return ATTUNER_OK;
+}
+
+static attuner_status plan_impl(const attuner_ctx* c, int32_t n_req, const int32_t* req_ptr,
+                                const int32_t* artifact_ids, const int32_t* suffix_cap, int64_t* n_entries,
+                                int64_t* cache_rows, std::vector<int32_t>* table, int32_t* cu_ctx,
+                                int32_t* art_len) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (n_req < 0 || n_req > ATTUNER_MAX_REQUESTS)
+    return fail(ATTUNER_ERANGE, "n_req %d outside [0, %d]", n_req, ATTUNER_MAX_REQUESTS);
+  if (n_req > 0 && (!req_ptr || !suffix_cap)) return fail(ATTUNER_EINVAL, "null req_ptr or suffix_cap");
+  if (n_req > 0 && req_ptr[0] != 0) return fail(ATTUNER_EINVAL, "req_ptr[0] must be 0");
+  int64_t entries = 0, row = 0;
+  if (cu_ctx) cu_ctx[0] = 0;
+  for (int r = 0; r < n_req; ++r) {
+    if (req_ptr[r + 1] < req_ptr[r]) return fail(ATTUNER_EINVAL, "req_ptr not monotone at %d", r);
+    if (suffix_cap[r] < 0) return fail(ATTUNER_EINVAL, "suffix_cap[%d] < 0", r);
+    if (req_ptr[r + 1] > req_ptr[r] && !artifact_ids) return fail(ATTUNER_EINVAL, "null artifact_ids");
+    int64_t alen = 0;
+    for (int32_t j = req_ptr[r]; j < req_ptr[r + 1]; ++j) {
+      auto it = c->artifacts.find(artifact_ids[j]);
+      if (it == c->artifacts.end()) return fail(ATTUNER_ENOENT, "request %d: unknown artifact id %d", r, artifact_ids[j]);
+      const Artifact& a = it->second;
+      if (table) {
+        int32_t left = a.n_tokens;
+        for (int32_t pg : a.pages) {
+          const int32_t nv = std::min(left, kPageTokens);
+          table->push_back(pg);
+          table->push_back(nv);
+          table->push_back((int32_t)(row + alen));
+          table->push_back(r);
+          alen += nv;
+          left -= nv;
+        }
+      } else {
+        alen += a.n_tokens;
+      }
+      entries += (int64_t)a.pages.size();
+    }
+    row += alen + suffix_cap[r];
+    if (row > INT32_MAX) return fail(ATTUNER_ERANGE, "cache rows exceed 2^31");
+    if (art_len) art_len[r] = (int32_t)alen;
+    if (cu_ctx) cu_ctx[r + 1] = (int32_t)row;
+  }
+  if (n_entries) *n_entries = entries;
+  if (cache_rows) *cache_rows = row;
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_assemble_plan(const attuner_ctx* c, int32_t n_req, const int32_t* req_ptr,
+                                     const int32_t* artifact_ids, const int32_t* suffix_cap, int64_t* n_entries,
+                                     int64_t* cache_rows) {
+  return plan_impl(c, n_req, req_ptr, artifact_ids, suffix_cap, n_entries, cache_rows, nullptr, nullptr, nullptr);
+}
+
+attuner_status attuner_assemble_kv(attuner_ctx* c, int32_t n_req, const int32_t* req_ptr, const int32_t* artifact_ids,
+                                   const int32_t* suffix_cap, int32_t* block_table, int32_t* cu_ctx,
+                                   int32_t* art_len, void* req_kv, int64_t cache_rows, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  std::vector<int32_t> table;
+  std::vector<int32_t> cu(n_req > 0 ? n_req + 1 : 1), al(n_req > 0 ? n_req : 1);
+  int64_t entries = 0, rows = 0;
+  try {
+    attuner_status st = plan_impl(c, n_req, req_ptr, artifact_ids, suffix_cap, &entries, &rows, &table, cu.data(),
+                                  al.data());
+    if (st != ATTUNER_OK) return st;
+  } catch (const std::bad_alloc&) {
+    return fail(ATTUNER_ENOMEM, "host allocation");
+  }
+  if (rows != cache_rows)
+    return fail(ATTUNER_ERANGE, "cache_rows %lld does not match the plan (%lld)", (long long)cache_rows, (long long)rows);
+  if (entries > 0 && (!block_table || !req_kv)) return fail(ATTUNER_EINVAL, "null block_table or req_kv");
+  if (req_kv && !aligned16(req_kv)) return fail(ATTUNER_EINVAL, "req_kv must be 16-byte aligned");
+  if (entries > INT32_MAX) return fail(ATTUNER_ERANGE, "block table of %lld entries", (long long)entries);
+  if (cu_ctx) memcpy(cu_ctx, cu.data(), (size_t)(n_req + 1) * sizeof(int32_t));
+  if (art_len && n_req > 0) memcpy(art_len, al.data(), (size_t)n_req * sizeof(int32_t));
+  if (entries == 0) return ATTUNER_OK;
+  DeviceGuard dg(c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(c->staging.upload(table.data(), table.size() * sizeof(int32_t), block_table, s));
+  HIP_TRY(launch_gather(block_table, entries, c->pool, c->pool_pages, c->cfg.n_layers, c->cfg.n_kv_heads,
+                        static_cast<uint16_t*>(req_kv), cache_rows, s));
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_qproj_lora(attuner_ctx* c, int32_t n_tok, const void* x, const void* w, int32_t n_out,
+                                  const void* a, const void* b, int32_t rank, float scale, int32_t lora_cols,
+                                  void* out, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  DeviceGuard dg(c->device);
+  return qproj_impl(c, n_tok, x, w, n_out, a, b, rank, scale, lora_cols, out, static_cast<hipStream_t>(stream));
+}
+
+static attuner_status check_norm_args(const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                      int64_t ld_kv, const void* gamma_q, const void* gamma_k, const attuner_ctx* c) {
+  if (!q_raw || !k_raw || !v_raw || !gamma_q || !gamma_k) return fail(ATTUNER_EINVAL, "null q/k/v or gamma");
+  if (ld_q < q_dim(c) || ld_kv < kv_dim(c)) return fail(ATTUNER_EINVAL, "ld_q %lld / ld_kv %lld too small", (long long)ld_q, (long long)ld_kv);
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_qk_norm_rope(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                    const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                    const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                    int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* q_hat,
+                                    void* req_kv, int64_t cache_rows, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  attuner_status st = check_layer(c, layer);
+  if (st != ATTUNER_OK) return st;
+  std::vector<ReqDesc> reqs;
+  int32_t total_q = 0;
+  st = build_reqs(c, n_req, cu_q, cu_ctx, art_len, pos0, cache_rows, &reqs, &total_q);
+  if (st != ATTUNER_OK) return st;
+  if (total_q == 0) return ATTUNER_OK;
+  st = check_norm_args(q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, c);
+  if (st != ATTUNER_OK) return st;
+  if (!q_hat || !req_kv || !aligned16(q_hat) || !aligned16(req_kv))
+    return fail(ATTUNER_EINVAL, "q_hat and req_kv must be non-null and 16-byte aligned");
+  DeviceGuard dg(c->device);
+  const int64_t hs = cache_rows * c->cfg.head_dim;
+  return run_norm_rope(c, reqs, total_q, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, q_hat,
+                       cache_plane(req_kv, c, layer, 0, cache_rows), cache_plane(req_kv, c, layer, 1, cache_rows), hs,
+                       static_cast<hipStream_t>(stream));
+}
+
+attuner_status attuner_attention(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                 const int32_t* cu_ctx, const int32_t* art_len, const void* q_hat,
+                                 const void* req_kv, int64_t cache_rows, void* o, float* lse, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  attuner_status st = check_layer(c, layer);
+  if (st != ATTUNER_OK) return st;
+  std::vector<ReqDesc> reqs;
+  int32_t total_q = 0;
+  st = build_reqs(c, n_req, cu_q, cu_ctx, art_len, nullptr, cache_rows, &reqs, &total_q);
+  if (st != ATTUNER_OK) return st;
+  if (total_q == 0) return ATTUNER_OK;
+  if (!q_hat || !req_kv || !o || !aligned16(q_hat) || !aligned16(req_kv) || !aligned16(o))
+    return fail(ATTUNER_EINVAL, "q_hat, req_kv and o must be non-null and 16-byte aligned");
+  DeviceGuard dg(c->device);
+  const int64_t hs = cache_rows * c->cfg.head_dim;
+  return run_attention(c, reqs, total_q, q_hat, cache_plane(const_cast<void*>(req_kv), c, layer, 0, cache_rows),
+                       cache_plane(const_cast<void*>(req_kv), c, layer, 1, cache_rows), hs, o, lse,
+                       static_cast<hipStream_t>(stream));
+}
+
+attuner_status attuner_suffix_attn(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                   const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                   const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                   int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                   int64_t cache_rows, void* o, float* lse, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  attuner_status st = check_layer(c, layer);
+  if (st != ATTUNER_OK) return st;
+  std::vector<ReqDesc> reqs;
+  int32_t total_q = 0;
+  st = build_reqs(c, n_req, cu_q, cu_ctx, art_len, pos0, cache_rows, &reqs, &total_q);
+  if (st != ATTUNER_OK) return st;
+  if (total_q == 0) return ATTUNER_OK;
+  st = check_norm_args(q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, c);
+  if (st != ATTUNER_OK) return st;
+  if (!req_kv || !o || !aligned16(req_kv) || !aligned16(o))
+    return fail(ATTUNER_EINVAL, "req_kv and o must be non-null and 16-byte aligned");
+  DeviceGuard dg(c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t hs = cache_rows * c->cfg.head_dim;
+  uint16_t* kp = cache_plane(req_kv, c, layer, 0, cache_rows);
+  uint16_t* vp = cache_plane(req_kv, c, layer, 1, cache_rows);
+  st = run_norm_rope(c, reqs, total_q, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, o, kp, vp, hs, s);
+  if (st != ATTUNER_OK) return st;
+  return run_attention(c, reqs, total_q, o, kp, vp, hs, o, lse, s);
+}
+
+attuner_status attuner_full_prefill(attuner_ctx* c, int32_t n_tok, int32_t pos0, const void* x, const void* wqkv,
+                                    const void* a, const void* b, int32_t rank, float scale, const void* gamma_q,
+                                    const void* gamma_k, void* o, void* k_out, void* v_out, float* lse,
+                                    void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (n_tok < 0 || pos0 < 0) return fail(ATTUNER_EINVAL, "negative n_tok or pos0");
+  if (n_tok == 0) return ATTUNER_OK;
+  if (!gamma_q || !gamma_k || !o || !k_out || !v_out) return fail(ATTUNER_EINVAL, "null gamma or output");
+  if (!aligned16(o) || !aligned16(k_out) || !aligned16(v_out)) return fail(ATTUNER_EINVAL, "outputs must be 16-byte aligned");
+  DeviceGuard dg(c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nq = q_dim(c), nkv = kv_dim(c), n_out = nq + 2 * nkv;
+  HIP_TRY(c->ws_qkv.ensure((size_t)n_tok * n_out * sizeof(uint16_t)));
+  uint16_t* qkv = static_cast<uint16_t*>(c->ws_qkv.ptr);
+  attuner_status st = qproj_impl(c, n_tok, x, wqkv, n_out, a, b, rank, scale, nq, qkv, s);
+  if (st != ATTUNER_OK) return st;
+  std::vector<ReqDesc> reqs(1);
+  reqs[0].q_start = 0;
+  reqs[0].q_len = n_tok;
+  reqs[0].kv_start = 0;
+  reqs[0].art_len = 0;
+  reqs[0].pos0 = pos0;
+  const int64_t hs = (int64_t)n_tok * c->cfg.head_dim;
+  st = run_norm_rope(c, reqs, n_tok, qkv, n_out, qkv + nq, qkv + nq + nkv, n_out, gamma_q, gamma_k, o,
+                     static_cast<uint16_t*>(k_out), static_cast<uint16_t*>(v_out), hs, s);
+  if (st != ATTUNER_OK) return st;
+  return run_attention(c, reqs, n_tok, o, static_cast<const uint16_t*>(k_out), static_cast<const uint16_t*>(v_out), hs,
+                       o, lse, s);
+}
+
+}  // extern "C"

@@ -1,0 +1,110 @@
+// K1: paged artifact pool -- store and block-table gather (bit-exact copies).
+//
+// Pool layout: [n_layers][pool_pages][2 (K, V)][n_kv][16 tokens][128] bf16, so
+// one page of one layer is a contiguous 2 * n_kv * 4 KiB block and each
+// (K|V, head) slab of it is 4 KiB.  Request cache layout:
+// [n_layers][2][n_kv][cache_rows][128].
+//
+// One workgroup of 256 threads moves one page of one layer: thread t owns row
+// t / 16 and 16-byte chunk t % 16 of every slab, so each slab is read as one
+// contiguous 4 KiB span and written as n_valid contiguous 256-byte rows.
+// Eight slabs are in flight per thread before any store is issued.
+
+#include "common.h"
+#include "kernels.h"
+
+namespace attuner {
+
+namespace {
+
+constexpr int kSlabBatch = 8;
+
+__global__ __launch_bounds__(256) void store_pages_kernel(const u32x4* __restrict__ k, const u32x4* __restrict__ v,
+                                                          int n_tokens, const int32_t* __restrict__ pages,
+                                                          u32x4* __restrict__ pool, int64_t pool_pages, int n_kv) {
+  const int pi = blockIdx.x;      // page index within the artifact
+  const int layer = blockIdx.y;
+  const int page = pages[pi];
+  const int rr = threadIdx.x >> 4;
+  const int chunk = threadIdx.x & 15;
+  const int tok = pi * kPageTokens + rr;
+  const bool valid = tok < n_tokens;
+  const int n_slab = 2 * n_kv;
+  for (int s0 = 0; s0 < n_slab; s0 += kSlabBatch) {
+    u32x4 buf[kSlabBatch];
+#pragma unroll
+    for (int i = 0; i < kSlabBatch; ++i) {
+      const int s = s0 + i;
+      buf[i] = u32x4{0u, 0u, 0u, 0u};
+      if (s < n_slab && valid) {
+        const int c = s / n_kv, g = s % n_kv;
+        const u32x4* src = c ? v : k;
+        buf[i] = src[(((int64_t)layer * n_kv + g) * n_tokens + tok) * 16 + chunk];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kSlabBatch; ++i) {
+      const int s = s0 + i;
+      if (s < n_slab) {
+        const int64_t slab = ((int64_t)layer * pool_pages + page) * n_slab + s;
+        pool[(slab * kPageTokens + rr) * 16 + chunk] = buf[i];
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ table, const u32x4* __restrict__ pool,
+                                                     int64_t pool_pages, int n_kv, u32x4* __restrict__ req_kv,
+                                                     int64_t cache_rows) {
+  const int64_t e = blockIdx.x;
+  const int layer = blockIdx.y;
+  const int4 ent = table[e];  // {page, n_valid, dst_row, request}
+  const int rr = threadIdx.x >> 4;
+  const int chunk = threadIdx.x & 15;
+  if (rr >= ent.y) return;
+  const int n_slab = 2 * n_kv;
+  const int64_t src_base = ((int64_t)layer * pool_pages + ent.x) * n_slab;
+  const int64_t dst_row = ent.z + rr;
+  for (int s0 = 0; s0 < n_slab; s0 += kSlabBatch) {
+    u32x4 buf[kSlabBatch];
+#pragma unroll
+    for (int i = 0; i < kSlabBatch; ++i) {
+      const int s = s0 + i;
+      if (s < n_slab) buf[i] = pool[((src_base + s) * kPageTokens + rr) * 16 + chunk];
+    }
+#pragma unroll
+    for (int i = 0; i < kSlabBatch; ++i) {
+      const int s = s0 + i;
+      if (s < n_slab) {
+        // slab s = c * n_kv + g maps to cache plane (layer * 2 + c) * n_kv + g
+        const int64_t plane = (int64_t)layer * n_slab + s;
+        req_kv[(plane * cache_rows + dst_row) * 16 + chunk] = buf[i];
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens, const int32_t* pages_dev,
+                              int n_pages, uint16_t* pool, int64_t pool_pages, int n_layers, int n_kv,
+                              hipStream_t stream) {
+  if (n_pages == 0) return hipSuccess;
+  dim3 grid(n_pages, n_layers);
+  hipLaunchKernelGGL(store_pages_kernel, grid, dim3(256), 0, stream, reinterpret_cast<const u32x4*>(k),
+                     reinterpret_cast<const u32x4*>(v), n_tokens, pages_dev, reinterpret_cast<u32x4*>(pool),
+                     pool_pages, n_kv);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint16_t* pool, int64_t pool_pages,
+                         int n_layers, int n_kv, uint16_t* req_kv, int64_t cache_rows, hipStream_t stream) {
+  if (n_entries == 0) return hipSuccess;
+  dim3 grid(static_cast<unsigned>(n_entries), n_layers);
+  hipLaunchKernelGGL(gather_kernel, grid, dim3(256), 0, stream, reinterpret_cast<const int4*>(table_dev),
+                     reinterpret_cast<const u32x4*>(pool), pool_pages, n_kv, reinterpret_cast<u32x4*>(req_kv),
+                     cache_rows);
+  return hipGetLastError();
+}
+
+}  // namespace attuner

@@ -1,0 +1,103 @@
+// Internal launch interface between the host runtime and the gfx950 kernels.
+// Every launcher validates nothing: the runtime has checked shapes and bounds
+// before calling it.  Each returns the hipError_t of its launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace attuner {
+
+constexpr int kMaxReq = 64;
+constexpr int kHeadDim = 128;    // the kernels are built for this head size
+constexpr int kPageTokens = 16;  // tokens per pool page
+
+// ---- a0 / a2: pool store and block-table gather ---------------------------
+
+// Copy one artifact (k, v: [n_layers][n_kv][n_tokens][128]) into its pages.
+// pool layout: [n_layers][pool_pages][2][n_kv][16][128].
+hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens, const int32_t* pages_dev,
+                              int n_pages, uint16_t* pool, int64_t pool_pages, int n_layers, int n_kv,
+                              hipStream_t stream);
+
+// Copy every entry {page, n_valid, dst_row, request} of the block table, for
+// every layer, into req_kv [n_layers][2][n_kv][cache_rows][128].
+hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint16_t* pool, int64_t pool_pages,
+                         int n_layers, int n_kv, uint16_t* req_kv, int64_t cache_rows, hipStream_t stream);
+
+// ---- a3: LoRA-down and the projection GEMM --------------------------------
+
+// t = scale * x a^T, stored as bf16 hi/lo pairs: t_hi[i][j] = bf16(t),
+// t_lo[i][j] = bf16(t - t_hi); columns rank .. r_pad-1 are zero.
+hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int hidden, int rank, int r_pad,
+                            float scale, uint16_t* t_hi, uint16_t* t_lo, hipStream_t stream);
+
+// out[i][n] = x[i] . w[n] + (n < lora_cols ? t[i] . b[n] : 0), with t given as
+// hi/lo bf16 pairs [n_tok][r_pad] (r_pad = 0: no adapter).
+hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
+                            const uint16_t* b, int rank, int r_pad, int lora_cols, const uint16_t* t_hi,
+                            const uint16_t* t_lo, uint16_t* out, hipStream_t stream);
+
+// ---- a4: QK-RMSNorm + RoPE ------------------------------------------------
+
+struct NormRopeReq {
+  int32_t q_start;   // first row of the request in q_raw / k_raw / v_raw / q_hat
+  int32_t q_len;     // suffix tokens
+  int32_t kv_row0;   // cache row of suffix token 0
+  int32_t pos0;      // rotary position of suffix token 0
+};
+
+struct NormRopeParams {
+  const uint16_t* q_raw;
+  const uint16_t* k_raw;
+  const uint16_t* v_raw;
+  int64_t ld_q, ld_kv;
+  const uint16_t* gamma_q;
+  const uint16_t* gamma_k;
+  const float2* rope;        // [max_pos][64] (cos, sin)
+  uint16_t* q_hat;           // [T_q][Hq][128]
+  uint16_t* k_cache;         // K head 0 of the layer; head stride kv_head_stride
+  uint16_t* v_cache;
+  int64_t kv_head_stride;    // elements between heads (= cache rows * 128)
+  int32_t n_q_heads, n_kv_heads;
+  int32_t total_q;
+  float eps;
+  int32_t n_req;
+  NormRopeReq req[kMaxReq];
+};
+
+hipError_t launch_qk_norm_rope(const NormRopeParams& p, hipStream_t stream);
+
+// ---- a5: attention ---------------------------------------------------------
+
+struct AttnReq {
+  int32_t q_start;   // first row in q_hat / o
+  int32_t q_len;
+  int32_t kv_start;  // cache row of key 0 of the request
+  int32_t art_len;   // cached artifact keys; row i sees keys 0 .. art_len + i
+  int32_t n_qblk;    // ceil(q_len / 32)
+  int32_t wg_start;  // first work unit of the request (units = qblocks * n_split)
+};
+
+struct AttnParams {
+  const uint16_t* q;       // [T_q][Hq][128]
+  const uint16_t* k;       // K head 0; head stride kv_head_stride
+  const uint16_t* v;
+  int64_t kv_head_stride;
+  uint16_t* o;             // [T_q][Hq][128]
+  float* lse;              // [T_q][Hq] or null
+  float* part_o;           // [n_split][T_q][Hq][128]   (n_split > 1)
+  float* part_ml;          // [n_split][T_q][Hq][2]      (n_split > 1)
+  int32_t n_q_heads, n_kv_heads;
+  int32_t total_q;
+  int32_t n_split;
+  int32_t n_units;         // work units per KV head
+  float score_scale;       // log2(e) / sqrt(d)
+  int32_t n_req;
+  AttnReq req[kMaxReq];
+};
+
+hipError_t launch_attention(const AttnParams& p, hipStream_t stream);
+hipError_t launch_attn_combine(const AttnParams& p, hipStream_t stream);
+
+}  // namespace attuner

@@ -39,3 +39,18 @@ def assert_intermediate_close(got, ref, what="intermediate"):
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
     assert err.max() <= 1e-2 * np.abs(ref).max(), f"{what}: max|err| {err.max():.3e} vs max|ref| {np.abs(ref).max():.3e}"
     assert err.mean() <= 2.0 ** -8 * np.abs(ref).mean(), f"{what}: mean|err| {err.mean():.3e} vs mean|ref| {np.abs(ref).mean():.3e}"
+
+
+def lse_bar(q_hat, keys, n_q_heads, n_kv_heads) -> float:
+    """Bar on the log-sum-exp output when q_hat and the keys went through bf16
+    storage: each rounding moves a score z = q.k/sqrt(d) by at most 2^-9 |z|
+    relative (two roundings: 2^-8), and d lse / d z_j = p_j sums to one, so
+    |d lse| <= 2^-8 max|z|; 1e-3 covers fp32 accumulation."""
+    q = np.asarray(q_hat, np.float64)
+    k = np.asarray(keys, np.float64)
+    G = n_q_heads // n_kv_heads
+    zmax = 0.0
+    for g in range(n_kv_heads):
+        z = np.einsum("shd,nd->shn", q[:, g * G:(g + 1) * G, :], k[:, g, :]) / np.sqrt(q.shape[-1])
+        zmax = max(zmax, float(np.abs(z).max()))
+    return 2.0 ** -8 * zmax + 1e-3

@@ -1,0 +1,49 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every entry point include/attuner.h declares, and rejects bad geometry before
+touching a device."""
+
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2609_36722_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "attuner.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(attuner_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_entry_point():
+    lib = _lib.lib()
+    names = _declared()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), f"{n} not exported"
+    assert set(names) == set(_lib.SIGNATURES), "binding and header disagree"
+
+
+def test_bad_geometry_rejected_without_a_device():
+    lib = _lib.lib()
+    h = C.c_void_p()
+    for field, val in [("head_dim", 64), ("page_tokens", 32), ("n_q_heads", 16), ("hidden", 100), ("n_layers", 0)]:
+        cfg = _lib.ModelCfgC(36, 2560, 32, 8, 128, 16, 1e6, 1e-6)
+        setattr(cfg, field, val)
+        assert lib.attuner_create(C.byref(cfg), 16, 0, C.byref(h)) == -1
+        assert field.split("_")[0] in lib.attuner_last_error().decode() or lib.attuner_last_error()
+    assert lib.attuner_create(None, 16, 0, C.byref(h)) == -1
+
+
+def test_null_context_is_an_error_not_a_crash():
+    lib = _lib.lib()
+    out = C.c_int32()
+    assert lib.attuner_store_artifact(None, 4, None, None, None, C.byref(out)) == -1
+    assert lib.attuner_release_artifact(None, 0) == -1
+    assert lib.attuner_pool_info(None, None, None, None) == -1
+    assert lib.attuner_qproj_lora(None, 1, None, None, 128, None, None, 0, 0.0, 0, None, None) == -1
+    lib.attuner_destroy(None)
