@@ -1,0 +1,380 @@
+#!/usr/bin/env python3
+"""Benchmark of Attuner suffix prefill on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2]
+
+A step is one pass of the whole suffix path over one batch, every layer of the
+stack, with all inputs resident in HBM before timing starts:
+  a1+a2  attuner_assemble_kv   block table on the host -> H2D -> gather of every
+                               layer's artifact K/V into the request cache
+  per layer:
+  a3     attuner_qproj_lora    fused [W_q; W_k; W_v] projection + rank-r LoRA on q
+  a4     attuner_qk_norm_rope  q/k RMSNorm + RoPE, suffix k/v into the cache
+  a5     attuner_attention     multi-segment GQA attention -> O
+The same kernels then run the full-context prefill of the whole request
+(attuner_full_prefill, every layer, no adapter) for the speedup.
+
+Default workload: the Qwen3-4B-shaped 36-layer stack (8 artifacts x 1024
+tokens, 256-token suffix, LoRA rank 16).  One layer's seeded inputs are drawn
+and copied into a distinct device buffer per layer, so every layer reads its
+own memory.
+
+Prints one JSON line.  The CPU baseline times the fp64 oracle on a bounded
+sample of the same workload on the host.
+"""
+
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+PAPER_CONTEXT = ("paper: up to 3.73x TTFT vs full prefill (Qwen3-8B, out-of-domain geometric mean, "
+                 "end-to-end HF Transformers + SDPA, BF16, GPU not stated)")
+METRIC = "suffix-prefill tokens/s + attention TFLOP/s (% MFMA peak), speedup vs full prefill"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2", choices=["c2", "c3", "c5", "c1", "c4"])
+    ap.add_argument("--full-steps", type=int, default=3, help="timed full-prefill passes (0: skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline (0: skip)")
+    ap.add_argument("--quiet", action="store_true")
+    return ap.parse_args()
+
+
+def log(args, msg):
+    if not args.quiet:
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# ----------------------------------------------------------------------------
+# algorithmic work
+# ----------------------------------------------------------------------------
+
+def attention_flops(shape, reqs):
+    """4 d Hq (S L_art + S (S + 1) / 2) per layer: QK^T and PV over visible keys."""
+    tot = 0
+    for L, S in reqs:
+        tot += S * L + S * (S + 1) // 2
+    return 4 * shape.head_dim * shape.n_q_heads * tot
+
+
+def gemm_flops(shape, n_tok, rank):
+    n_out = shape.q_dim + 2 * shape.kv_dim
+    return 2 * n_tok * shape.hidden * n_out + (2 * n_tok * rank * (shape.hidden + shape.q_dim) if rank else 0)
+
+
+def gather_bytes(shape, art_tokens, n_layers):
+    """K and V of every cached token, read once from the pool and written once."""
+    return 2 * 2 * art_tokens * shape.n_kv_heads * shape.head_dim * 2 * n_layers
+
+
+# ----------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample
+# ----------------------------------------------------------------------------
+
+def cpu_baseline(wl, budget_s, args):
+    import numpy as np
+    import oracle
+    import synthdata as sd
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    s = wl.shape
+    layers_done, t_total = 0, 0.0
+    while layers_done < wl.n_layers and (layers_done == 0 or t_total < budget_s):
+        l = layers_done
+        w = {k: oracle.decode_bf16(v) for k, v in sd.layer_weights(wl, l).items()}
+        t0 = time.perf_counter()
+        for r, req in enumerate(wl.requests):
+            kv = [sd.artifact_kv(wl, a, l) for a in req.artifact_ids]
+            ka = np.concatenate([oracle.decode_bf16(k) for k, _ in kv])
+            va = np.concatenate([oracle.decode_bf16(v) for _, v in kv])
+            x = oracle.decode_bf16(sd.suffix_hidden(wl, r, l))
+            oracle.suffix_layer(x, w["wq"], w["wk"], w["wv"], w["a"], w["b"], wl.scale, w["gamma_q"], w["gamma_k"],
+                                ka, va, wl.pos0(req), s.n_q_heads, s.n_kv_heads, s.rope_theta, s.rms_eps)
+        t_total += time.perf_counter() - t0
+        layers_done += 1
+        log(args, f"cpu oracle: layer {l} done ({t_total:.1f} s so far)")
+    per_layer = t_total / layers_done
+    value = wl.total_suffix / (per_layer * wl.n_layers)
+    return {"value": value, "unit": "suffix tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{layers_done} of {wl.n_layers} layers of {wl.name} (all suffix rows), fp64 numpy; "
+                      f"{per_layer:.2f} s per layer, stack time extrapolated x{wl.n_layers}/{layers_done}"}
+
+
+# ----------------------------------------------------------------------------
+# roofline traffic from committed counter summaries
+# ----------------------------------------------------------------------------
+
+def kernel_traffic(kernel_file, workload):
+    """HBM bytes per launch from profiles/<kernel>_<workload>_traffic.json, only
+    if the kernel source is unchanged since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"attention_{workload}_traffic.json")
+    src = os.path.join(ROOT, "paper_2609_36722_amd", "csrc", kernel_file)
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        if rec.get("source_sha256") != sha:
+            return None
+        return float(rec["hbm_bytes_per_launch"])
+    except Exception:
+        return None
+
+
+# ----------------------------------------------------------------------------
+# main
+# ----------------------------------------------------------------------------
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synthdata as sd
+    from paper_2609_36722_amd import _lib
+    from paper_2609_36722_amd.api import Context, ModelCfg, bf16_to_device
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    lib = _lib.lib()
+    wl = sd.make_workload(args.workload)
+    s = wl.shape
+    NL = wl.n_layers
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    sp = C.c_void_p(stream.cuda_stream)
+    log(args, f"workload {wl.name}: {NL} layers, {len(wl.requests)} request(s), "
+              f"suffix {wl.total_suffix}, artifacts {[wl.art_len(r) for r in wl.requests]}")
+
+    # ---- inputs: one layer's seeded draws, one distinct device copy per layer ----
+    t0 = time.time()
+    w0 = sd.layer_weights(wl, 0)
+    wqkv0 = bf16_to_device(np.concatenate([w0["wq"], w0["wk"], w0["wv"]]), dev)
+    a0, b0 = bf16_to_device(w0["a"], dev), bf16_to_device(w0["b"], dev)
+    gq, gk = bf16_to_device(w0["gamma_q"], dev), bf16_to_device(w0["gamma_k"], dev)
+    x0 = bf16_to_device(np.concatenate([sd.suffix_hidden(wl, r, 0) for r in range(len(wl.requests))]), dev)
+    wqkv = [wqkv0.clone() for _ in range(NL)]
+    a_l = [a0.clone() for _ in range(NL)]
+    b_l = [b0.clone() for _ in range(NL)]
+    x_l = [x0.clone() for _ in range(NL)]
+    T = x0.shape[0]
+    nq, nkv = s.q_dim, s.kv_dim
+    n_out = nq + 2 * nkv
+    qkv = [torch.empty(T, n_out, dtype=torch.bfloat16, device=dev) for _ in range(NL)]
+    o_l = [torch.empty(T, s.n_q_heads, s.head_dim, dtype=torch.bfloat16, device=dev) for _ in range(NL)]
+
+    used = sorted({a for r in wl.requests for a in r.artifact_ids})
+    pages = sum(math.ceil(wl.artifact_lengths[a] / 16) for a in used)
+    cfg = ModelCfg(n_layers=NL, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
+                   head_dim=s.head_dim, rope_theta=s.rope_theta, rms_eps=s.rms_eps)
+    ctx = Context(cfg, pool_pages=pages)
+    ids = {}
+    for a in used:
+        k, v = sd.artifact_kv(wl, a, 0)
+        kd = bf16_to_device(np.ascontiguousarray(k.transpose(1, 0, 2)), dev)
+        vd = bf16_to_device(np.ascontiguousarray(v.transpose(1, 0, 2)), dev)
+        ids[a] = ctx.store_artifact(kd.unsqueeze(0).expand(NL, -1, -1, -1).contiguous(),
+                                    vd.unsqueeze(0).expand(NL, -1, -1, -1).contiguous())
+    requests = [[ids[a] for a in r.artifact_ids] for r in wl.requests]
+    suffix_cap = [r.suffix_len for r in wl.requests]
+    n_entries, rows = ctx.assemble_plan(requests, suffix_cap)
+    block_table = torch.empty(n_entries * 4, dtype=torch.int32, device=dev)
+    req_kv = torch.empty(NL * 2 * s.n_kv_heads * rows * s.head_dim, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    log(args, f"inputs resident in HBM ({time.time() - t0:.1f} s): pool {pages} pages, cache rows {rows}, "
+              f"block table {n_entries} entries")
+
+    # ---- marshalled argument tuples of every C call of a step ----------------
+    ptr = [0]
+    flat = []
+    for r in requests:
+        flat += r
+        ptr.append(len(flat))
+    i32 = lambda v: (C.c_int32 * max(1, len(v)))(*v)
+    c_ptr, c_ids, c_cap = i32(ptr), i32(flat), i32(suffix_cap)
+    cu_ctx_arr = (C.c_int32 * (len(requests) + 1))()
+    art_arr = (C.c_int32 * max(1, len(requests)))()
+    h = ctx._h
+    assemble_args = (h, len(requests), c_ptr, c_ids, c_cap, block_table.data_ptr(), cu_ctx_arr, art_arr,
+                     req_kv.data_ptr(), rows, sp)
+    rc = lib.attuner_assemble_kv(*assemble_args)
+    assert rc == 0, lib.attuner_last_error()
+    torch.cuda.synchronize()
+    cu_ctx, art_len = list(cu_ctx_arr), list(art_arr)[:len(requests)]
+    cu_q = [0]
+    for r in wl.requests:
+        cu_q.append(cu_q[-1] + r.suffix_len)
+    pos0 = [wl.pos0(r) for r in wl.requests]
+    c_cuq, c_cuctx, c_art, c_pos = i32(cu_q), i32(cu_ctx), i32(art_len), i32(pos0)
+    qproj_args, norm_args, attn_args = [], [], []
+    for l in range(NL):
+        base = qkv[l].data_ptr()
+        qproj_args.append((h, T, x_l[l].data_ptr(), wqkv[l].data_ptr(), n_out, a_l[l].data_ptr(), b_l[l].data_ptr(),
+                           wl.rank, wl.scale, nq, base, sp))
+        norm_args.append((h, l, len(requests), c_cuq, c_cuctx, c_art, c_pos, base, n_out, base + 2 * nq,
+                          base + 2 * (nq + nkv), n_out, gq.data_ptr(), gk.data_ptr(), o_l[l].data_ptr(),
+                          req_kv.data_ptr(), rows, sp))
+        attn_args.append((h, l, len(requests), c_cuq, c_cuctx, c_art, o_l[l].data_ptr(), req_kv.data_ptr(), rows,
+                          o_l[l].data_ptr(), None, sp))
+
+    # per-category events: gather, qproj, norm, attention
+    cats = ("gather", "qproj", "norm", "attn")
+    per_step = {"gather": 1, "qproj": NL, "norm": NL, "attn": NL}
+
+    def make_events(n_steps):
+        return {c: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    for _ in range(per_step[c] * n_steps)] for c in cats}
+
+    def run_step(evs, idx):
+        def call(cat, j, fn, a):
+            if evs is not None:
+                evs[cat][j][0].record(stream)
+            rc_ = fn(*a)
+            if rc_ != 0:
+                raise RuntimeError(f"{fn.__name__}: {lib.attuner_last_error().decode()}")
+            if evs is not None:
+                evs[cat][j][1].record(stream)
+        call("gather", idx, lib.attuner_assemble_kv, assemble_args)
+        for l in range(NL):
+            call("qproj", idx * NL + l, lib.attuner_qproj_lora, qproj_args[l])
+            call("norm", idx * NL + l, lib.attuner_qk_norm_rope, norm_args[l])
+            call("attn", idx * NL + l, lib.attuner_attention, attn_args[l])
+
+    log(args, f"warmup {args.warmup} steps")
+    for i in range(args.warmup):
+        run_step(None, 0)
+    torch.cuda.synchronize()
+
+    evs = make_events(args.steps)
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(args.steps):
+        run_step(evs, i)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    kern_ms = {c: sum(a.elapsed_time(b) for a, b in evs[c]) / len(evs[c]) for c in cats}
+    log(args, f"timed {args.steps} steps: {ms_step:.3f} ms/step (host wall {1e3 * wall / args.steps:.3f} ms/step); "
+              f"per launch ms: " + ", ".join(f"{c} {kern_ms[c]:.4f}" for c in cats))
+
+    # ---- algorithmic rates -----------------------------------------------------
+    reqs_shape = [(wl.art_len(r), r.suffix_len) for r in wl.requests]
+    attn_f = attention_flops(s, reqs_shape)
+    gemm_f = gemm_flops(s, T, wl.rank)
+    g_bytes = gather_bytes(s, sum(L for L, _ in reqs_shape), NL)
+    attn_tflops = attn_f / (kern_ms["attn"] * 1e-3) / 1e12
+    gemm_tflops = gemm_f / (kern_ms["qproj"] * 1e-3) / 1e12
+    gather_gbps = g_bytes / (kern_ms["gather"] * 1e-3) / 1e9
+    norm_bytes = T * (nq + 2 * nkv) * 2 * 2
+    norm_gbps = norm_bytes / (kern_ms["norm"] * 1e-3) / 1e9
+    tokens_s = wl.total_suffix / (ms_step * 1e-3)
+
+    # ---- full prefill on the same kernels ----------------------------------------
+    full = None
+    if args.full_steps > 0:
+        N = wl.art_len(wl.requests[0]) + wl.requests[0].suffix_len
+        if len(wl.requests) > 1:
+            N = None
+        if N is not None:
+            xf0 = bf16_to_device(sd.prefill_hidden(wl, 0, 0), dev)
+            xf = [xf0.clone() for _ in range(NL)]
+            of = torch.empty(N, s.n_q_heads, s.head_dim, dtype=torch.bfloat16, device=dev)
+            kf = [torch.empty(s.n_kv_heads, N, s.head_dim, dtype=torch.bfloat16, device=dev) for _ in range(NL)]
+            vf = [torch.empty(s.n_kv_heads, N, s.head_dim, dtype=torch.bfloat16, device=dev) for _ in range(NL)]
+            fargs = [(h, N, 0, xf[l].data_ptr(), wqkv[l].data_ptr(), None, None, 0, 0.0, gq.data_ptr(),
+                      gk.data_ptr(), of.data_ptr(), kf[l].data_ptr(), vf[l].data_ptr(), None, sp) for l in range(NL)]
+
+            def full_pass():
+                for l in range(NL):
+                    rc_ = lib.attuner_full_prefill(*fargs[l])
+                    if rc_ != 0:
+                        raise RuntimeError(lib.attuner_last_error().decode())
+            full_pass()
+            torch.cuda.synchronize()
+            f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            f0.record(stream)
+            for _ in range(args.full_steps):
+                full_pass()
+            f1.record(stream)
+            torch.cuda.synchronize()
+            full_ms = f0.elapsed_time(f1) / args.full_steps
+            full_attn_f = attention_flops(s, [(0, N)]) * NL
+            full = {"ms": full_ms, "tokens": N, "speedup": full_ms / ms_step,
+                    "attention_plus_gemm_tflops": (full_attn_f + gemm_flops(s, N, 0) * NL) / (full_ms * 1e-3) / 1e12}
+            log(args, f"full prefill of {N} tokens x {NL} layers: {full_ms:.2f} ms -> speedup {full_ms / ms_step:.2f}x")
+            del xf, kf, vf, of
+
+    # ---- CPU baseline ---------------------------------------------------------------
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(wl, args.cpu_seconds, args)
+
+    traffic = kernel_traffic("k_attention.hip", args.workload)
+    achieved = attn_tflops
+    out = {
+        "metric": METRIC,
+        "value": round(tokens_s, 2),
+        "unit": "suffix tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1)/N(0,0.02) bf16 draws of one layer, copied to a distinct buffer per layer)",
+        "config": {"workload": wl.name, "layers": NL, "hidden": s.hidden, "q_heads": s.n_q_heads,
+                   "kv_heads": s.n_kv_heads, "head_dim": s.head_dim, "requests": len(wl.requests),
+                   "artifact_tokens": [L for L, _ in reqs_shape], "suffix_tokens": [S for _, S in reqs_shape],
+                   "lora_rank": wl.rank, "page_tokens": 16},
+        "roofline": {"bound": "mfma", "kernel": "attention_kernel", "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic, "flops_per_launch": attn_f, "launch_ms": round(kern_ms["attn"], 5)},
+        "kernels": {
+            "attention": {"tflops": round(attn_tflops, 2), "mfma_frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                          "ms_per_layer": round(kern_ms["attn"], 5)},
+            "qproj_lora_gemm": {"tflops": round(gemm_tflops, 2), "mfma_frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
+                                "ms_per_layer": round(kern_ms["qproj"], 5), "flops_per_layer": gemm_f},
+            "kv_gather": {"gbps": round(gather_gbps, 1), "hbm_frac": round(gather_gbps / PEAK_HBM_GBPS, 4),
+                          "ms_per_step": round(kern_ms["gather"], 5), "bytes_per_step": g_bytes},
+            "qk_norm_rope": {"gbps": round(norm_gbps, 1), "ms_per_layer": round(kern_ms["norm"], 5)},
+        },
+        "full_prefill": full,
+        "speedup_vs_full_prefill": round(full["speedup"], 3) if full else None,
+        "paper_context": PAPER_CONTEXT,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    ctx.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -145,7 +145,7 @@ struct attuner_ctx {
   int32_t next_id = 0;
 
   DeviceBuf ws_pages;   // page list of the artifact being stored
-  DeviceBuf ws_lora;    // t_hi, t_lo of the LoRA-down pass
+  DeviceBuf ws_lora;    // LoRA-down slice partials
   DeviceBuf ws_part;    // split-KV partials
   DeviceBuf ws_qkv;     // full prefill: fused projection output
   DeviceBuf rope;       // (cos, sin) table [rope_pos][64]
@@ -286,7 +286,6 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
     p.part_ml = reinterpret_cast<float*>(static_cast<char*>(c->ws_part.ptr) + po);
   }
   HIP_TRY(launch_attention(p, stream));
-  if (n_split > 1) HIP_TRY(launch_attn_combine(p, stream));
   return ATTUNER_OK;
 }
 
@@ -351,18 +350,16 @@ attuner_status qproj_impl(attuner_ctx* c, int32_t n_tok, const void* x, const vo
     return fail(ATTUNER_EINVAL, "x, w, a and out must be 16-byte aligned");
   const int hidden = c->cfg.hidden;
   const int r_pad = rank > 0 && lora_cols > 0 ? (rank + 15) / 16 * 16 : 0;
-  uint16_t* t_hi = nullptr;
-  uint16_t* t_lo = nullptr;
+  float* t_part = nullptr;
   if (r_pad > 0) {
-    const size_t bytes = (size_t)n_tok * r_pad * sizeof(uint16_t);
-    HIP_TRY(c->ws_lora.ensure(2 * bytes));
-    t_hi = static_cast<uint16_t*>(c->ws_lora.ptr);
-    t_lo = t_hi + (size_t)n_tok * r_pad;
+    const size_t part_bytes = (size_t)lora_down_slices(hidden) * n_tok * r_pad * sizeof(float);
+    HIP_TRY(c->ws_lora.ensure(part_bytes));
+    t_part = static_cast<float*>(c->ws_lora.ptr);
     HIP_TRY(launch_lora_down(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(a), n_tok, hidden, rank,
-                             r_pad, scale, t_hi, t_lo, stream));
+                             r_pad, scale, t_part, stream));
   }
   HIP_TRY(launch_gemm_lora(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), n_tok, n_out, hidden,
-                           static_cast<const uint16_t*>(b), rank, r_pad, lora_cols, t_hi, t_lo,
+                           static_cast<const uint16_t*>(b), rank, r_pad, lora_cols, t_part,
                            static_cast<uint16_t*>(out), stream));
   return ATTUNER_OK;
 }

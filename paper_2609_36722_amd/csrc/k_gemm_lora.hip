@@ -1,20 +1,24 @@
 // K2: bf16 MFMA projection GEMM with the rank-r LoRA update fused into its
 // epilogue (query-side adaptation, section 4 eq. 4):
 //   out[i][n] = x[i] . w[n]  +  (n < lora_cols ? t[i] . b[n] : 0),
-//   t = scale * x A^T  (computed first by lora_down_kernel).
+//   t = scale * x A^T  (lora_down_kernel, run first).
 //
 // The GEMM is computed as C^T = W x^T so that the MFMA accumulator of a lane
 // holds four consecutive output features of one token (8-byte stores).  Both
 // operands are K-contiguous in memory ([rows][hidden]), so tiles go to LDS
 // without a transpose.  Workgroup tile BN (features) x BM (tokens) x 64 (k),
-// four waves in a 2 x 2 grid, 32x32x16 MFMAs, fp32 accumulation, LDS double
-// buffered with register prefetch of the next k-tile.  LDS rows are 128 bytes
-// (eight 16-byte chunks); chunk c of row r is stored at c ^ (r & 7) so that
-// the 32 rows an MFMA operand read touches spread over all banks.
+// four waves in a 2 x 2 grid, 32x32x16 MFMAs, fp32 accumulation.  The k-loop
+// keeps NS k-tiles in flight in a register ring (the small-token shapes of
+// suffix prefill are latency-bound, not bandwidth-bound) and double-buffers
+// LDS.  LDS rows are 128 bytes (eight 16-byte chunks); chunk c of row r is
+// stored at c ^ ((r >> 1) & 7), so the 16 rows one operand read touches in a
+// cycle land on 16 distinct bank groups.
 //
 // The LoRA term enters as extra MFMA k-steps after the main loop: A operand
-// = rows of B (rank padded to 16 with zeros), B operand = t as a bf16 hi/lo
-// pair, so t keeps ~16 significant bits and the update stays in fp32.
+// = rows of B (rank padded to 16 with zeros), B operand = t rounded to a
+// bf16 hi/lo pair, so t keeps ~16 significant bits and the update is summed
+// in fp32.  lora_down_kernel leaves t as fp32 partial sums over 256-wide
+// slices of the hidden dimension; the epilogue adds the slices in order.
 
 #include "common.h"
 #include "kernels.h"
@@ -25,16 +29,16 @@ namespace {
 
 constexpr int BK = 64;
 constexpr int kChunksPerRow = BK / 8;  // 16-byte chunks per LDS row
+constexpr int kLoraSlice = 256;        // hidden elements per lora_down workgroup
 
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 7); }
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-template <int BM, int BN>
+template <int BM, int BN, int NS>
 __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w,
                                                            int M, int N, int K, const bf16_t* __restrict__ b,
                                                            int rank, int r_pad, int lora_cols,
-                                                           const bf16_t* __restrict__ t_hi,
-                                                           const bf16_t* __restrict__ t_lo, bf16_t* __restrict__ out,
-                                                           int n_mt, int n_nt) {
+                                                           const float* __restrict__ t_part, int n_slice,
+                                                           bf16_t* __restrict__ out, int n_mt, int n_nt) {
   constexpr int FN = BN / 64;  // 32-row MFMA blocks per wave along features
   constexpr int FM = BM / 64;  // along tokens
   constexpr int ROWS = BN + BM;
@@ -43,11 +47,12 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
 
   __shared__ u32x4 lds[2][ROWS * kChunksPerRow];
 
-  // XCD-aware tile order: consecutive workgroups land on different XCDs, so
-  // give each XCD a contiguous run of tiles that share weight rows.
+  // XCD-aware tile order: workgroup i runs on XCD i % 8, so give each XCD a
+  // contiguous run of tiles; consecutive tiles share weight rows.
   const int total = n_mt * n_nt;
+  const int per_xcd = total >> 3;
   int lin = blockIdx.x;
-  if ((total & 7) == 0) lin = (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3);
+  if (lin < 8 * per_xcd) lin = (lin & 7) * per_xcd + (lin >> 3);
   const int nt = lin / n_mt;
   const int mt = lin - nt * n_mt;
   const int n0 = nt * BN;
@@ -61,7 +66,6 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
   const int l32 = lane & 31;
   const int hi = lane >> 5;
 
-  // global source of each of this thread's chunks
   const u32x4* src[LOADS];
   int dst[LOADS];
 #pragma unroll
@@ -87,54 +91,87 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
 #pragma unroll
     for (int j = 0; j < FM; ++j) acc[i][j] = f32x16{};
 
-  u32x4 pre[LOADS];
+  const int n_kt = K / BK;
+  u32x4 ring[NS][LOADS];
 #pragma unroll
-  for (int i = 0; i < LOADS; ++i) pre[i] = src[i][0];
+  for (int s = 0; s < NS; ++s)
+    if (s < n_kt) {
 #pragma unroll
-  for (int i = 0; i < LOADS; ++i) lds[0][dst[i]] = pre[i];
+      for (int i = 0; i < LOADS; ++i) ring[s][i] = src[i][s * kChunksPerRow];
+    }
+#pragma unroll
+  for (int i = 0; i < LOADS; ++i) lds[0][dst[i]] = ring[0][i];
   __syncthreads();
 
-  const int n_kt = K / BK;
-  for (int kt = 0; kt < n_kt; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < n_kt) {
+  for (int kt0 = 0; kt0 < n_kt; kt0 += NS) {
 #pragma unroll
-      for (int i = 0; i < LOADS; ++i) pre[i] = src[i][(kt + 1) * kChunksPerRow];
-    }
+    for (int u = 0; u < NS; ++u) {
+      const int kt = kt0 + u;
+      if (kt >= n_kt) break;
+      // ring[u] (tile kt) is already in LDS: refill it with tile kt + NS
+      if (kt + NS < n_kt) {
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int ch = 2 * ks + hi;
-      bf16x8 af[FN], bfr[FM];
-#pragma unroll
-      for (int i = 0; i < FN; ++i) {
-        const int row = wn * (BN / 2) + i * 32 + l32;
-        af[i] = as_bf16x8(lds[cur][row * kChunksPerRow + swz(row, ch)]);
+        for (int i = 0; i < LOADS; ++i) ring[u][i] = src[i][(kt + NS) * kChunksPerRow];
       }
+      const int cur = kt & 1;
 #pragma unroll
-      for (int j = 0; j < FM; ++j) {
-        const int row = BN + wm * (BM / 2) + j * 32 + l32;
-        bfr[j] = as_bf16x8(lds[cur][row * kChunksPerRow + swz(row, ch)]);
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        const int ch = 2 * ks + hi;
+        bf16x8 af[FN], bfr[FM];
+#pragma unroll
+        for (int i = 0; i < FN; ++i) {
+          const int row = wn * (BN / 2) + i * 32 + l32;
+          af[i] = as_bf16x8(lds[cur][row * kChunksPerRow + swz(row, ch)]);
+        }
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+          const int row = BN + wm * (BM / 2) + j * 32 + l32;
+          bfr[j] = as_bf16x8(lds[cur][row * kChunksPerRow + swz(row, ch)]);
+        }
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+          for (int j = 0; j < FM; ++j) acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
       }
+      if (kt + 1 < n_kt) {
+        const int nx = (u + 1) % NS;
 #pragma unroll
-      for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
+        for (int i = 0; i < LOADS; ++i) lds[cur ^ 1][dst[i]] = ring[nx][i];
+      }
+      __syncthreads();
     }
-    if (kt + 1 < n_kt) {
-#pragma unroll
-      for (int i = 0; i < LOADS; ++i) lds[cur ^ 1][dst[i]] = pre[i];
-    }
-    __syncthreads();
   }
 
   // ---- fused low-rank epilogue: acc += B[n][:] . t[m][:] --------------------
-  if (r_pad > 0) {
+  if (r_pad > 0 && n0 < lora_cols) {
+    const int64_t slice_stride = (int64_t)M * r_pad;
+    for (int ks = 0; ks < r_pad; ks += 16) {
+      bf16x8 th[FM], tl[FM];
 #pragma unroll
-    for (int i = 0; i < FN; ++i) {
-      const int nb = n0 + wn * (BN / 2) + i * 32;
-      if (nb >= lora_cols) continue;  // lora_cols is a multiple of 32
-      const int n = nb + l32;
-      for (int ks = 0; ks < r_pad; ks += 16) {
+      for (int j = 0; j < FM; ++j) {
+        int m = m0 + wm * (BM / 2) + j * 32 + l32;
+        m = m < M ? m : M - 1;
+        const float* tp = t_part + (int64_t)m * r_pad + ks + 8 * hi;
+        f32x4 s0 = f32x4{}, s1 = f32x4{};
+        for (int z = 0; z < n_slice; ++z) {
+          s0 += *reinterpret_cast<const f32x4*>(tp + z * slice_stride);
+          s1 += *reinterpret_cast<const f32x4*>(tp + z * slice_stride + 4);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const __bf16 h0 = static_cast<__bf16>(s0[e]);
+          const __bf16 h1 = static_cast<__bf16>(s1[e]);
+          th[j][e] = h0;
+          th[j][e + 4] = h1;
+          tl[j][e] = static_cast<__bf16>(s0[e] - static_cast<float>(h0));
+          tl[j][e + 4] = static_cast<__bf16>(s1[e] - static_cast<float>(h1));
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < FN; ++i) {
+        const int nb = n0 + wn * (BN / 2) + i * 32;
+        if (nb >= lora_cols) continue;  // lora_cols is a multiple of 32
+        const int n = nb + l32;
         bf16x8 a;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -144,13 +181,8 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
         }
 #pragma unroll
         for (int j = 0; j < FM; ++j) {
-          int m = m0 + wm * (BM / 2) + j * 32 + l32;
-          m = m < M ? m : M - 1;
-          const int64_t off = (int64_t)m * r_pad + ks + 8 * hi;
-          const bf16x8 th = as_bf16x8(*reinterpret_cast<const u32x4*>(t_hi + off));
-          const bf16x8 tl = as_bf16x8(*reinterpret_cast<const u32x4*>(t_lo + off));
-          acc[i][j] = mfma32(a, th, acc[i][j]);
-          acc[i][j] = mfma32(a, tl, acc[i][j]);
+          acc[i][j] = mfma32(a, th[j], acc[i][j]);
+          acc[i][j] = mfma32(a, tl[j], acc[i][j]);
         }
       }
     }
@@ -176,78 +208,86 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
   }
 }
 
-// t = scale * x A^T for one token per wave; each lane accumulates its slice of
-// the hidden dimension for every rank, then the wave reduces.
-
+// t = scale * x A^T with MFMAs, as fp32 partial sums per 256-wide slice of the
+// hidden dimension: workgroup (32-token block, slice), each wave multiplies a
+// 64-wide part of the slice and the four waves are summed through LDS.
+// t_part[slice][token][r_pad]; ranks rank .. r_pad-1 come out zero.
 __global__ __launch_bounds__(256) void lora_down_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ a,
                                                         int n_tok, int hidden, int rank, int r_pad, float scale,
-                                                        bf16_t* __restrict__ t_hi, bf16_t* __restrict__ t_lo) {
-  const int lane = threadIdx.x & 63;
-  const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (tok >= n_tok) return;
-  const bf16_t* xr = x + (int64_t)tok * hidden;
-  for (int j0 = 0; j0 < r_pad; j0 += 16) {
-    float accj[16];
+                                                        float* __restrict__ t_part) {
+  __shared__ float red[4][2][16][64];
+  const int mb = blockIdx.x, kz = blockIdx.y;
+  const int m0 = mb * 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, hf = lane >> 5;
+  const int nblk = (r_pad + 31) / 32;
+  const int m = min(m0 + l32, n_tok - 1);
+  const bf16_t* xr = x + (int64_t)m * hidden;
+
+  u32x4 xa[4], ab[4][2];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) accj[j] = 0.f;
-    for (int k = lane * 8; k < hidden; k += 64 * 8) {
-      const u32x4 xv = *reinterpret_cast<const u32x4*>(xr + k);
-      float xf[8];
+  for (int st = 0; st < 4; ++st) {
+    const int k = kz * kLoraSlice + wave * 64 + st * 16 + 8 * hf;
+    const bool kin = k < hidden;
+    xa[st] = kin ? *reinterpret_cast<const u32x4*>(xr + k) : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        xf[2 * e] = bf16_to_f32((bf16_t)(xv[e] & 0xFFFFu));
-        xf[2 * e + 1] = bf16_to_f32((bf16_t)(xv[e] >> 16));
-      }
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        if (j0 + j < rank) {
-          const u32x4 av = *reinterpret_cast<const u32x4*>(a + (int64_t)(j0 + j) * hidden + k);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            accj[j] = fmaf(xf[2 * e], bf16_to_f32((bf16_t)(av[e] & 0xFFFFu)), accj[j]);
-            accj[j] = fmaf(xf[2 * e + 1], bf16_to_f32((bf16_t)(av[e] >> 16)), accj[j]);
-          }
-        }
-      }
+    for (int nb = 0; nb < 2; ++nb) {
+      const int n = 32 * nb + l32;
+      ab[st][nb] = (kin && nb < nblk && n < rank) ? *reinterpret_cast<const u32x4*>(a + (int64_t)n * hidden + k)
+                                                 : u32x4{0u, 0u, 0u, 0u};
     }
+  }
+  f32x16 acc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const float s = wave_sum(accj[j]) * scale;
-      if (lane == j) {
-        const bf16_t h = (j0 + j < rank) ? f32_to_bf16(s) : (bf16_t)0;
-        const bf16_t l = (j0 + j < rank) ? f32_to_bf16(s - bf16_to_f32(h)) : (bf16_t)0;
-        t_hi[(int64_t)tok * r_pad + j0 + j] = h;
-        t_lo[(int64_t)tok * r_pad + j0 + j] = l;
-      }
-    }
+  for (int st = 0; st < 4; ++st)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+      if (nb < nblk) acc[nb] = mfma32(as_bf16x8(xa[st]), as_bf16x8(ab[st][nb]), acc[nb]);
+  // acc[nb][v] = C[token 8(v/4) + 4hf + v%4][rank 32nb + l32]
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) red[wave][nb][v][lane] = acc[nb][v];
+  __syncthreads();
+
+  for (int e = tid; e < nblk * 1024; e += 256) {
+    const int nb = e >> 10, v = (e >> 6) & 15, ln = e & 63;
+    const int tok = m0 + 8 * (v >> 2) + 4 * (ln >> 5) + (v & 3);
+    const int rk = 32 * nb + (ln & 31);
+    if (tok < n_tok && rk < r_pad)
+      t_part[((int64_t)kz * n_tok + tok) * r_pad + rk] =
+          scale * (red[0][nb][v][ln] + red[1][nb][v][ln] + red[2][nb][v][ln] + red[3][nb][v][ln]);
   }
 }
 
 }  // namespace
 
+int lora_down_slices(int hidden) { return (hidden + kLoraSlice - 1) / kLoraSlice; }
+
 hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int hidden, int rank, int r_pad,
-                            float scale, uint16_t* t_hi, uint16_t* t_lo, hipStream_t stream) {
+                            float scale, float* t_part, hipStream_t stream) {
   if (n_tok == 0 || r_pad == 0) return hipSuccess;
-  hipLaunchKernelGGL(lora_down_kernel, dim3((n_tok + 3) / 4), dim3(256), 0, stream, x, a, n_tok, hidden, rank, r_pad,
-                     scale, t_hi, t_lo);
+  hipLaunchKernelGGL(lora_down_kernel, dim3((n_tok + 31) / 32, lora_down_slices(hidden)), dim3(256), 0, stream, x, a,
+                     n_tok, hidden, rank, r_pad, scale, t_part);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
-                            const uint16_t* b, int rank, int r_pad, int lora_cols, const uint16_t* t_hi,
-                            const uint16_t* t_lo, uint16_t* out, hipStream_t stream) {
+                            const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
+                            uint16_t* out, hipStream_t stream) {
   if (n_tok == 0) return hipSuccess;
   constexpr int BN = 128;
   const int n_nt = n_out / BN;
+  const int n_slice = lora_down_slices(hidden);
   // Prefer 128-token tiles once they alone give every CU two workgroups.
   const int n_mt128 = (n_tok + 127) / 128;
   if ((int64_t)n_mt128 * n_nt >= 512) {
-    hipLaunchKernelGGL((gemm_lora_kernel<128, BN>), dim3(n_mt128 * n_nt), dim3(256), 0, stream, x, w, n_tok, n_out,
-                       hidden, b, rank, r_pad, lora_cols, t_hi, t_lo, out, n_mt128, n_nt);
+    hipLaunchKernelGGL((gemm_lora_kernel<128, BN, 3>), dim3(n_mt128 * n_nt), dim3(256), 0, stream, x, w, n_tok,
+                       n_out, hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, n_mt128, n_nt);
   } else {
     const int n_mt = (n_tok + 63) / 64;
-    hipLaunchKernelGGL((gemm_lora_kernel<64, BN>), dim3(n_mt * n_nt), dim3(256), 0, stream, x, w, n_tok, n_out,
-                       hidden, b, rank, r_pad, lora_cols, t_hi, t_lo, out, n_mt, n_nt);
+    hipLaunchKernelGGL((gemm_lora_kernel<64, BN, 4>), dim3(n_mt * n_nt), dim3(256), 0, stream, x, w, n_tok, n_out,
+                       hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, n_mt, n_nt);
   }
   return hipGetLastError();
 }

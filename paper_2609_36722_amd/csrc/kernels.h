@@ -27,16 +27,18 @@ hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint
 
 // ---- a3: LoRA-down and the projection GEMM --------------------------------
 
-// t = scale * x a^T, stored as bf16 hi/lo pairs: t_hi[i][j] = bf16(t),
-// t_lo[i][j] = bf16(t - t_hi); columns rank .. r_pad-1 are zero.
+// t = scale * x a^T as fp32 partial sums over 256-wide slices of the hidden
+// dimension: t_part[lora_down_slices(hidden)][n_tok][r_pad]; ranks rank ..
+// r_pad-1 are zero.
+int lora_down_slices(int hidden);
 hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int hidden, int rank, int r_pad,
-                            float scale, uint16_t* t_hi, uint16_t* t_lo, hipStream_t stream);
+                            float scale, float* t_part, hipStream_t stream);
 
-// out[i][n] = x[i] . w[n] + (n < lora_cols ? t[i] . b[n] : 0), with t given as
-// hi/lo bf16 pairs [n_tok][r_pad] (r_pad = 0: no adapter).
+// out[i][n] = x[i] . w[n] + (n < lora_cols ? t[i] . b[n] : 0) with t the sum
+// of the slices of t_part (r_pad = 0: no adapter).
 hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
-                            const uint16_t* b, int rank, int r_pad, int lora_cols, const uint16_t* t_hi,
-                            const uint16_t* t_lo, uint16_t* out, hipStream_t stream);
+                            const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
+                            uint16_t* out, hipStream_t stream);
 
 // ---- a4: QK-RMSNorm + RoPE ------------------------------------------------
 
@@ -97,7 +99,7 @@ struct AttnParams {
   AttnReq req[kMaxReq];
 };
 
+// Attention, plus the split-KV merge kernel when n_split > 1.
 hipError_t launch_attention(const AttnParams& p, hipStream_t stream);
-hipError_t launch_attn_combine(const AttnParams& p, hipStream_t stream);
 
 }  // namespace attuner
