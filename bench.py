@@ -53,6 +53,10 @@ def parse():
     ap.add_argument("--workload", default="c2", choices=["c2", "c3", "c5", "c1", "c4"])
     ap.add_argument("--full-steps", type=int, default=3, help="timed full-prefill passes (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline (0: skip)")
+    ap.add_argument("--no-graph", action="store_true", help="launch the per-layer loop eagerly instead of "
+                    "replaying it as a captured HIP graph")
+    ap.add_argument("--copy-probe-mb", type=int, default=0, help="run one device copy of this many MiB first "
+                    "(a known-size reference for hardware byte counters)")
     ap.add_argument("--quiet", action="store_true")
     return ap.parse_args()
 
@@ -264,32 +268,88 @@ def main():
             call("norm", idx * NL + l, lib.attuner_qk_norm_rope, norm_args[l])
             call("attn", idx * NL + l, lib.attuner_attention, attn_args[l])
 
+    if args.copy_probe_mb > 0:
+        nbytes = args.copy_probe_mb << 20
+        a_src = torch.empty(nbytes // 2, dtype=torch.int16, device=dev).fill_(1)
+        a_dst = torch.empty_like(a_src)
+        torch.cuda.synchronize()
+        torch.add(a_src, 1, out=a_dst)  # one elementwise kernel: reads and writes nbytes
+        torch.cuda.synchronize()
+        log(args, f"copy probe: {args.copy_probe_mb} MiB read + written by one elementwise kernel")
+        del a_src, a_dst
+
     log(args, f"warmup {args.warmup} steps")
     for i in range(args.warmup):
         run_step(None, 0)
     torch.cuda.synchronize()
 
-    evs = make_events(args.steps)
-    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # per-kernel times: eager steps with events around every call, and the
+    # library's launch tracer for each kernel on its own
+    n_ev = max(1, min(args.steps, 5))
+    evs = make_events(n_ev)
+    ctx.trace_begin()
+    for i in range(n_ev):
+        run_step(evs, i)
     torch.cuda.synchronize()
+    ktimes = ctx.trace_end()
+    kern_ms = {c: sum(a.elapsed_time(b) for a, b in evs[c]) / len(evs[c]) for c in cats}
+    per_kernel = {k: {"launches": n, "avg_ms": round(t / n, 5), "max_ms": round(mx, 5)}
+                  for k, (n, t, mx) in ktimes.items()}
+    attn_kernel_ms = ktimes["attention_kernel"][1] / ktimes["attention_kernel"][0]
+    log(args, "kernel avg ms: " + ", ".join(f"{k} {v['avg_ms']:.4f} (x{v['launches']})" for k, v in per_kernel.items()))
+
+    # the layer loop as one captured HIP graph (assembly stays eager: its block
+    # table is built on the host for each request)
+    graph = None
+    if not args.no_graph:
+        cap = torch.cuda.Stream()
+        csp = C.c_void_p(cap.cuda_stream)
+        g_qproj = [a[:-1] + (csp,) for a in qproj_args]
+        g_norm = [a[:-1] + (csp,) for a in norm_args]
+        g_attn = [a[:-1] + (csp,) for a in attn_args]
+        graph = torch.cuda.CUDAGraph()
+        cap.wait_stream(stream)
+        with torch.cuda.graph(graph, stream=cap):
+            for l in range(NL):
+                for fn, a in ((lib.attuner_qproj_lora, g_qproj[l]), (lib.attuner_qk_norm_rope, g_norm[l]),
+                              (lib.attuner_attention, g_attn[l])):
+                    rc_ = fn(*a)
+                    if rc_ != 0:
+                        raise RuntimeError(f"capture: {lib.attuner_last_error().decode()}")
+        torch.cuda.synchronize()
+
+    def timed_step():
+        rc_ = lib.attuner_assemble_kv(*assemble_args)
+        if rc_ != 0:
+            raise RuntimeError(lib.attuner_last_error().decode())
+        if graph is not None:
+            graph.replay()
+        else:
+            run_step(None, 0)
+
+    for i in range(2):
+        timed_step()
+    torch.cuda.synchronize()
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     wall0 = time.perf_counter()
     t_start.record(stream)
     for i in range(args.steps):
-        run_step(evs, i)
+        timed_step()
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_step = t_start.elapsed_time(t_end) / args.steps
-    kern_ms = {c: sum(a.elapsed_time(b) for a, b in evs[c]) / len(evs[c]) for c in cats}
-    log(args, f"timed {args.steps} steps: {ms_step:.3f} ms/step (host wall {1e3 * wall / args.steps:.3f} ms/step); "
-              f"per launch ms: " + ", ".join(f"{c} {kern_ms[c]:.4f}" for c in cats))
+    log(args, f"timed {args.steps} steps ({'graph' if graph is not None else 'eager'} layer loop): "
+              f"{ms_step:.3f} ms/step (host wall {1e3 * wall / args.steps:.3f} ms/step); per launch ms "
+              f"(eager, events): " + ", ".join(f"{c} {kern_ms[c]:.4f}" for c in cats))
 
     # ---- algorithmic rates -----------------------------------------------------
     reqs_shape = [(wl.art_len(r), r.suffix_len) for r in wl.requests]
     attn_f = attention_flops(s, reqs_shape)
     gemm_f = gemm_flops(s, T, wl.rank)
     g_bytes = gather_bytes(s, sum(L for L, _ in reqs_shape), NL)
-    attn_tflops = attn_f / (kern_ms["attn"] * 1e-3) / 1e12
+    attn_tflops = attn_f / (attn_kernel_ms * 1e-3) / 1e12          # attention_kernel alone
+    attn_call_tflops = attn_f / (kern_ms["attn"] * 1e-3) / 1e12   # attuner_attention call (+ split merge)
     gemm_tflops = gemm_f / (kern_ms["qproj"] * 1e-3) / 1e12
     gather_gbps = g_bytes / (kern_ms["gather"] * 1e-3) / 1e9
     norm_bytes = T * (nq + 2 * nkv) * 2 * 2
@@ -355,18 +415,21 @@ def main():
                    "kv_heads": s.n_kv_heads, "head_dim": s.head_dim, "requests": len(wl.requests),
                    "artifact_tokens": [L for L, _ in reqs_shape], "suffix_tokens": [S for _, S in reqs_shape],
                    "lora_rank": wl.rank, "page_tokens": 16},
+        "layer_loop": "hip_graph" if graph is not None else "eager",
         "roofline": {"bound": "mfma", "kernel": "attention_kernel", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic, "flops_per_launch": attn_f, "launch_ms": round(kern_ms["attn"], 5)},
+                     "traffic": traffic, "flops_per_launch": attn_f, "launch_ms": round(attn_kernel_ms, 5)},
         "kernels": {
             "attention": {"tflops": round(attn_tflops, 2), "mfma_frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-                          "ms_per_layer": round(kern_ms["attn"], 5)},
+                          "kernel_ms": round(attn_kernel_ms, 5), "call_ms_with_split_merge": round(kern_ms["attn"], 5),
+                          "call_tflops": round(attn_call_tflops, 2)},
             "qproj_lora_gemm": {"tflops": round(gemm_tflops, 2), "mfma_frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
                                 "ms_per_layer": round(kern_ms["qproj"], 5), "flops_per_layer": gemm_f},
             "kv_gather": {"gbps": round(gather_gbps, 1), "hbm_frac": round(gather_gbps / PEAK_HBM_GBPS, 4),
                           "ms_per_step": round(kern_ms["gather"], 5), "bytes_per_step": g_bytes},
             "qk_norm_rope": {"gbps": round(norm_gbps, 1), "ms_per_layer": round(kern_ms["norm"], 5)},
         },
+        "kernel_avg_ms": per_kernel,
         "full_prefill": full,
         "speedup_vs_full_prefill": round(full["speedup"], 3) if full else None,
         "paper_context": PAPER_CONTEXT,

@@ -241,6 +241,28 @@ attuner_status attuner_full_prefill(attuner_ctx* ctx, int32_t n_tok, int32_t pos
                                     float scale, const void* gamma_q, const void* gamma_k, void* o,
                                     void* k_out, void* v_out, float* lse, void* stream);
 
+/* --------------------------------------------------------------------------
+ * Kernel timing.  Between attuner_trace_begin and attuner_trace_end, every
+ * kernel this library launches from the calling thread is bracketed by a
+ * pair of HIP events on its stream.  attuner_trace_end waits for the
+ * recorded events and returns, per kernel name, the launch count, the summed
+ * and the largest event-to-event time, sorted by total time (host array of
+ * up to max_entries; *n_entries receives the number of kernels).  Do not
+ * trace while a stream is being captured into a graph.
+ * Errors: EINVAL (no trace open on this thread for ctx), ERANGE (max_entries
+ * too small; *n_entries still set), EDEVICE.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  char kernel[48];
+  int64_t launches;
+  double total_ms;
+  double max_ms;
+} attuner_kernel_time;
+
+attuner_status attuner_trace_begin(attuner_ctx* ctx);
+attuner_status attuner_trace_end(attuner_ctx* ctx, attuner_kernel_time* out, int32_t max_entries,
+                                 int32_t* n_entries);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,6 +23,10 @@ class ModelCfgC(C.Structure):
                 ("rope_theta", C.c_float), ("rms_eps", C.c_float)]
 
 
+class KernelTimeC(C.Structure):
+    _fields_ = [("kernel", C.c_char * 48), ("launches", C.c_int64), ("total_ms", C.c_double), ("max_ms", C.c_double)]
+
+
 _i32p = C.POINTER(C.c_int32)
 _i64p = C.POINTER(C.c_int64)
 _vp = C.c_void_p
@@ -48,6 +52,8 @@ SIGNATURES = {
                                       _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
     "attuner_full_prefill": (C.c_int, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, C.c_float, _vp, _vp, _vp, _vp,
                                        _vp, _vp, _vp]),
+    "attuner_trace_begin": (C.c_int, [_vp]),
+    "attuner_trace_end": (C.c_int, [_vp, C.POINTER(KernelTimeC), _i32, _i32p]),
 }
 
 _LIB = None

@@ -17,7 +17,7 @@ from typing import List, Optional, Sequence, Tuple
 import numpy as np
 import torch
 
-from ._lib import MAX_RANK, MAX_REQUESTS, STATUS, ModelCfgC, lib
+from ._lib import MAX_RANK, MAX_REQUESTS, STATUS, KernelTimeC, ModelCfgC, lib
 
 
 class AttunerError(RuntimeError):
@@ -241,6 +241,17 @@ class Context:
                                          _view_ptr(k_raw), _view_ptr(v_raw), int(ld_kv), _ptr(gamma_q), _ptr(gamma_k),
                                          _ptr(req_kv), int(cache_rows), _ptr(o), _ptr(lse, 4), _stream(stream)),
                "attuner_suffix_attn")
+
+    # ---- kernel timing ----------------------------------------------------------------
+    def trace_begin(self) -> None:
+        _check(lib().attuner_trace_begin(self._h), "attuner_trace_begin")
+
+    def trace_end(self, max_kernels: int = 64) -> dict:
+        """{kernel name: (launches, total_ms, max_ms)} of the launches since trace_begin."""
+        buf = (KernelTimeC * max_kernels)()
+        n = C.c_int32()
+        _check(lib().attuner_trace_end(self._h, buf, max_kernels, C.byref(n)), "attuner_trace_end")
+        return {buf[i].kernel.decode(): (buf[i].launches, buf[i].total_ms, buf[i].max_ms) for i in range(n.value)}
 
     def full_prefill(self, pos0: int, x, wqkv, a, b, rank: int, scale: float, gamma_q, gamma_k, o, k_out, v_out,
                      lse: Optional[torch.Tensor] = None, stream=None) -> None:

@@ -132,7 +132,64 @@ struct Artifact {
   int32_t n_tokens;
 };
 
+// Named HIP event pairs around kernel launches (attuner_trace_*).  Events
+// come from a pool that is reused from one trace to the next.
+struct Tracer {
+  struct Rec {
+    const char* name;
+    hipEvent_t start, stop;
+  };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  size_t pool_used = 0;
+  hipError_t err = hipSuccess;
+
+  hipEvent_t take() {
+    if (pool_used < pool.size()) return pool[pool_used++];
+    hipEvent_t e = nullptr;
+    // no system-scope fence at each record: the markers then perturb the
+    // kernels they bracket (and their caches) as little as possible
+    hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
+    if (r != hipSuccess) {
+      err = r;
+      return nullptr;
+    }
+    pool.push_back(e);
+    ++pool_used;
+    return e;
+  }
+  void release() {
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+    pool.clear();
+    recs.clear();
+    pool_used = 0;
+  }
+};
+
+thread_local Tracer* g_tracer = nullptr;
+
 }  // namespace
+
+namespace attuner {
+
+void trace_launch_begin(const char* kernel, hipStream_t stream) {
+  Tracer* t = g_tracer;
+  if (t == nullptr) return;
+  Tracer::Rec r{kernel, t->take(), t->take()};
+  if (r.start == nullptr || r.stop == nullptr) return;
+  hipError_t e = hipEventRecord(r.start, stream);
+  if (e != hipSuccess) t->err = e;
+  t->recs.push_back(r);
+}
+
+void trace_launch_end(const char* kernel, hipStream_t stream) {
+  Tracer* t = g_tracer;
+  if (t == nullptr || t->recs.empty() || t->recs.back().name != kernel) return;
+  hipError_t e = hipEventRecord(t->recs.back().stop, stream);
+  if (e != hipSuccess) t->err = e;
+}
+
+}  // namespace attuner
 
 struct attuner_ctx {
   attuner_model_cfg cfg;
@@ -151,6 +208,7 @@ struct attuner_ctx {
   DeviceBuf rope;       // (cos, sin) table [rope_pos][64]
   int64_t rope_pos = 0;
   Staging staging;
+  Tracer tracer;
 };
 
 namespace {
@@ -421,6 +479,8 @@ void attuner_destroy(attuner_ctx* c) {
   c->ws_part.release();
   c->ws_qkv.release();
   c->rope.release();
+  if (g_tracer == &c->tracer) g_tracer = nullptr;
+  c->tracer.release();
   if (c->pool) (void)hipFree(c->pool);
   delete c;
 }
@@ -684,6 +744,51 @@ attuner_status attuner_full_prefill(attuner_ctx* c, int32_t n_tok, int32_t pos0,
   if (st != ATTUNER_OK) return st;
   return run_attention(c, reqs, n_tok, o, static_cast<const uint16_t*>(k_out), static_cast<const uint16_t*>(v_out), hs,
                        o, lse, s);
+}
+
+attuner_status attuner_trace_begin(attuner_ctx* c) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (g_tracer != nullptr && g_tracer != &c->tracer) return fail(ATTUNER_EINVAL, "another context is tracing on this thread");
+  c->tracer.recs.clear();
+  c->tracer.pool_used = 0;
+  c->tracer.err = hipSuccess;
+  g_tracer = &c->tracer;
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_trace_end(attuner_ctx* c, attuner_kernel_time* out, int32_t max_entries, int32_t* n_entries) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (g_tracer != &c->tracer) return fail(ATTUNER_EINVAL, "this context is not tracing on this thread");
+  g_tracer = nullptr;
+  Tracer& t = c->tracer;
+  if (t.err != hipSuccess) return fail(ATTUNER_EDEVICE, "trace event: %s", hipGetErrorString(t.err));
+  DeviceGuard dg(c->device);
+  std::vector<attuner_kernel_time> agg;
+  for (const auto& r : t.recs) {
+    HIP_TRY(hipEventSynchronize(r.stop));
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, r.start, r.stop));
+    auto it = std::find_if(agg.begin(), agg.end(), [&](const attuner_kernel_time& k) { return strcmp(k.kernel, r.name) == 0; });
+    if (it == agg.end()) {
+      attuner_kernel_time k;
+      memset(&k, 0, sizeof k);
+      snprintf(k.kernel, sizeof k.kernel, "%s", r.name);
+      agg.push_back(k);
+      it = agg.end() - 1;
+    }
+    it->launches += 1;
+    it->total_ms += ms;
+    it->max_ms = std::max(it->max_ms, (double)ms);
+  }
+  t.recs.clear();
+  std::sort(agg.begin(), agg.end(),
+            [](const attuner_kernel_time& a, const attuner_kernel_time& b) { return a.total_ms > b.total_ms; });
+  if (n_entries) *n_entries = (int32_t)agg.size();
+  if (out) {
+    if (max_entries < (int32_t)agg.size()) return fail(ATTUNER_ERANGE, "max_entries %d < %zu kernels", max_entries, agg.size());
+    memcpy(out, agg.data(), agg.size() * sizeof(attuner_kernel_time));
+  }
+  return ATTUNER_OK;
 }
 
 }  // extern "C"

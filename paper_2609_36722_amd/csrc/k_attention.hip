@@ -309,11 +309,12 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
 
 hipError_t launch_attention(const AttnParams& p, hipStream_t stream) {
   if (p.n_units == 0) return hipSuccess;
-  hipLaunchKernelGGL(attention_kernel, dim3((unsigned)(p.n_units * p.n_kv_heads)), dim3(256), 0, stream, p);
+  ATTUNER_LAUNCH("attention_kernel", attention_kernel, dim3((unsigned)(p.n_units * p.n_kv_heads)), dim3(256), stream,
+                 p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_split == 1) return e;
   const int64_t rows = (int64_t)p.total_q * p.n_q_heads;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, p);
+  ATTUNER_LAUNCH("attn_combine_kernel", attn_combine_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), stream, p);
   return hipGetLastError();
 }
 

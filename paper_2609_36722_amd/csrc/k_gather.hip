@@ -8,7 +8,8 @@
 // One workgroup of 256 threads moves one page of one layer: thread t owns row
 // t / 16 and 16-byte chunk t % 16 of every slab, so each slab is read as one
 // contiguous 4 KiB span and written as n_valid contiguous 256-byte rows.
-// Eight slabs are in flight per thread before any store is issued.
+// All 16 slabs of a page (8 KV heads, K and V) are in flight per thread
+// before any store is issued.
 
 #include "common.h"
 #include "kernels.h"
@@ -18,6 +19,7 @@ namespace attuner {
 namespace {
 
 constexpr int kSlabBatch = 8;
+constexpr int kGatherBatch = 16;  // slabs in flight per thread: a whole page of 8 KV heads
 
 __global__ __launch_bounds__(256) void store_pages_kernel(const u32x4* __restrict__ k, const u32x4* __restrict__ v,
                                                           int n_tokens, const int32_t* __restrict__ pages,
@@ -65,20 +67,21 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ ta
   const int n_slab = 2 * n_kv;
   const int64_t src_base = ((int64_t)layer * pool_pages + ent.x) * n_slab;
   const int64_t dst_row = ent.z + rr;
-  for (int s0 = 0; s0 < n_slab; s0 += kSlabBatch) {
-    u32x4 buf[kSlabBatch];
+  for (int s0 = 0; s0 < n_slab; s0 += kGatherBatch) {
+    u32x4 buf[kGatherBatch];
 #pragma unroll
-    for (int i = 0; i < kSlabBatch; ++i) {
+    for (int i = 0; i < kGatherBatch; ++i) {
       const int s = s0 + i;
       if (s < n_slab) buf[i] = pool[((src_base + s) * kPageTokens + rr) * 16 + chunk];
     }
 #pragma unroll
-    for (int i = 0; i < kSlabBatch; ++i) {
+    for (int i = 0; i < kGatherBatch; ++i) {
       const int s = s0 + i;
       if (s < n_slab) {
-        // slab s = c * n_kv + g maps to cache plane (layer * 2 + c) * n_kv + g
+        // slab s = c * n_kv + g maps to cache plane (layer * 2 + c) * n_kv + g;
+        // streaming store: the gathered rows are read once, by a later kernel
         const int64_t plane = (int64_t)layer * n_slab + s;
-        req_kv[(plane * cache_rows + dst_row) * 16 + chunk] = buf[i];
+        __builtin_nontemporal_store(buf[i], req_kv + (plane * cache_rows + dst_row) * 16 + chunk);
       }
     }
   }
@@ -91,7 +94,7 @@ hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens
                               hipStream_t stream) {
   if (n_pages == 0) return hipSuccess;
   dim3 grid(n_pages, n_layers);
-  hipLaunchKernelGGL(store_pages_kernel, grid, dim3(256), 0, stream, reinterpret_cast<const u32x4*>(k),
+  ATTUNER_LAUNCH("store_pages_kernel", store_pages_kernel, grid, dim3(256), stream, reinterpret_cast<const u32x4*>(k),
                      reinterpret_cast<const u32x4*>(v), n_tokens, pages_dev, reinterpret_cast<u32x4*>(pool),
                      pool_pages, n_kv);
   return hipGetLastError();
@@ -101,7 +104,7 @@ hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint
                          int n_layers, int n_kv, uint16_t* req_kv, int64_t cache_rows, hipStream_t stream) {
   if (n_entries == 0) return hipSuccess;
   dim3 grid(static_cast<unsigned>(n_entries), n_layers);
-  hipLaunchKernelGGL(gather_kernel, grid, dim3(256), 0, stream, reinterpret_cast<const int4*>(table_dev),
+  ATTUNER_LAUNCH("gather_kernel", gather_kernel, grid, dim3(256), stream, reinterpret_cast<const int4*>(table_dev),
                      reinterpret_cast<const u32x4*>(pool), pool_pages, n_kv, reinterpret_cast<u32x4*>(req_kv),
                      cache_rows);
   return hipGetLastError();

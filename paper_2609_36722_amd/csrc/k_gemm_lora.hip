@@ -91,14 +91,15 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
 #pragma unroll
     for (int j = 0; j < FM; ++j) acc[i][j] = f32x16{};
 
+  // n_kt is a multiple of NS (the launcher picks NS so); every load and LDS
+  // store below is unconditional (tile indices clamped), which keeps the
+  // compiler's wait counting exact: only the oldest ring slot is waited for.
   const int n_kt = K / BK;
   u32x4 ring[NS][LOADS];
 #pragma unroll
   for (int s = 0; s < NS; ++s)
-    if (s < n_kt) {
 #pragma unroll
-      for (int i = 0; i < LOADS; ++i) ring[s][i] = src[i][s * kChunksPerRow];
-    }
+    for (int i = 0; i < LOADS; ++i) ring[s][i] = src[i][s * kChunksPerRow];
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) lds[0][dst[i]] = ring[0][i];
   __syncthreads();
@@ -107,12 +108,10 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
 #pragma unroll
     for (int u = 0; u < NS; ++u) {
       const int kt = kt0 + u;
-      if (kt >= n_kt) break;
       // ring[u] (tile kt) is already in LDS: refill it with tile kt + NS
-      if (kt + NS < n_kt) {
+      const int nxt = min(kt + NS, n_kt - 1);
 #pragma unroll
-        for (int i = 0; i < LOADS; ++i) ring[u][i] = src[i][(kt + NS) * kChunksPerRow];
-      }
+      for (int i = 0; i < LOADS; ++i) ring[u][i] = src[i][nxt * kChunksPerRow];
       const int cur = kt & 1;
 #pragma unroll
       for (int ks = 0; ks < BK / 16; ++ks) {
@@ -133,11 +132,10 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
 #pragma unroll
           for (int j = 0; j < FM; ++j) acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
       }
-      if (kt + 1 < n_kt) {
-        const int nx = (u + 1) % NS;
+      // tile kt + 1 (ring slot u + 1) into the other LDS buffer; after the last
+      // tile this stores a stale tile nobody reads
 #pragma unroll
-        for (int i = 0; i < LOADS; ++i) lds[cur ^ 1][dst[i]] = ring[nx][i];
-      }
+      for (int i = 0; i < LOADS; ++i) lds[cur ^ 1][dst[i]] = ring[(u + 1) % NS][i];
       __syncthreads();
     }
   }
@@ -267,8 +265,8 @@ int lora_down_slices(int hidden) { return (hidden + kLoraSlice - 1) / kLoraSlice
 hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int hidden, int rank, int r_pad,
                             float scale, float* t_part, hipStream_t stream) {
   if (n_tok == 0 || r_pad == 0) return hipSuccess;
-  hipLaunchKernelGGL(lora_down_kernel, dim3((n_tok + 31) / 32, lora_down_slices(hidden)), dim3(256), 0, stream, x, a,
-                     n_tok, hidden, rank, r_pad, scale, t_part);
+  ATTUNER_LAUNCH("lora_down_kernel", lora_down_kernel, dim3((n_tok + 31) / 32, lora_down_slices(hidden)), dim3(256),
+                 stream, x, a, n_tok, hidden, rank, r_pad, scale, t_part);
   return hipGetLastError();
 }
 
@@ -279,16 +277,23 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
   constexpr int BN = 128;
   const int n_nt = n_out / BN;
   const int n_slice = lora_down_slices(hidden);
-  // Prefer 128-token tiles once they alone give every CU two workgroups.
+  // Prefer 128-token tiles once they alone give every CU two workgroups.  The
+  // prefetch depth must divide the number of 64-wide k-tiles.
+  const int n_kt = hidden / BK;
   const int n_mt128 = (n_tok + 127) / 128;
+#define ATTUNER_GEMM(BM_, NS_, NMT_)                                                                           \
+  ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN, NS_>), dim3((NMT_) * n_nt), dim3(256), stream, x, w, \
+                 n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, (NMT_), n_nt)
   if ((int64_t)n_mt128 * n_nt >= 512) {
-    hipLaunchKernelGGL((gemm_lora_kernel<128, BN, 3>), dim3(n_mt128 * n_nt), dim3(256), 0, stream, x, w, n_tok,
-                       n_out, hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, n_mt128, n_nt);
+    if (n_kt % 2 == 0) ATTUNER_GEMM(128, 2, n_mt128);
+    else ATTUNER_GEMM(128, 1, n_mt128);
   } else {
     const int n_mt = (n_tok + 63) / 64;
-    hipLaunchKernelGGL((gemm_lora_kernel<64, BN, 4>), dim3(n_mt * n_nt), dim3(256), 0, stream, x, w, n_tok, n_out,
-                       hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, n_mt, n_nt);
+    if (n_kt % 4 == 0) ATTUNER_GEMM(64, 4, n_mt);
+    else if (n_kt % 2 == 0) ATTUNER_GEMM(64, 2, n_mt);
+    else ATTUNER_GEMM(64, 1, n_mt);
   }
+#undef ATTUNER_GEMM
   return hipGetLastError();
 }
 

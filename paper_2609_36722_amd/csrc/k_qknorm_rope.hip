@@ -60,7 +60,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
 hipError_t launch_qk_norm_rope(const NormRopeParams& p, hipStream_t stream) {
   if (p.total_q == 0) return hipSuccess;
   const int64_t waves = (int64_t)p.total_q * (p.n_q_heads + p.n_kv_heads);
-  hipLaunchKernelGGL(qk_norm_rope_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, stream, p);
+  ATTUNER_LAUNCH("qk_norm_rope_kernel", qk_norm_rope_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), stream, p);
   return hipGetLastError();
 }
 

@@ -12,6 +12,19 @@ constexpr int kMaxReq = 64;
 constexpr int kHeadDim = 128;    // the kernels are built for this head size
 constexpr int kPageTokens = 16;  // tokens per pool page
 
+// Launch tracing: while tracing is on for the calling thread (attuner_trace_*),
+// the runtime records a named HIP event pair on the launch stream around every
+// kernel launch; otherwise these are a pointer test.
+void trace_launch_begin(const char* kernel, hipStream_t stream);
+void trace_launch_end(const char* kernel, hipStream_t stream);
+
+#define ATTUNER_LAUNCH(name, kernel, grid, block, stream, ...)              \
+  do {                                                                      \
+    trace_launch_begin(name, stream);                                       \
+    hipLaunchKernelGGL(kernel, grid, block, 0, stream, __VA_ARGS__);        \
+    trace_launch_end(name, stream);                                         \
+  } while (0)
+
 // ---- a0 / a2: pool store and block-table gather ---------------------------
 
 // Copy one artifact (k, v: [n_layers][n_kv][n_tokens][128]) into its pages.
