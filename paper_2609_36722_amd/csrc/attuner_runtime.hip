@@ -308,25 +308,26 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c->cfg.head_dim));
   p.n_req = (int32_t)reqs.size();
 
-  // Split the keys of each query block when the blocks alone would not give
-  // every CU two workgroups; keep at least four 64-key tiles per split.
+  // Query blocks are 64 suffix tokens of one KV head (one 8-wave workgroup,
+  // one per CU).  Split the keys of each block when the blocks alone would
+  // not cover the 256 CUs; keep at least four 64-key tiles per split.
   int64_t blocks = 0;
   int64_t min_tiles = INT64_MAX;
   for (const auto& r : reqs) {
     if (r.q_len <= 0) continue;
-    blocks += (r.q_len + 31) / 32;
+    blocks += (r.q_len + 63) / 64;
     min_tiles = std::min<int64_t>(min_tiles, (r.art_len + r.q_len + 63) / 64);
   }
   const int64_t base = blocks * c->cfg.n_kv_heads;
   int n_split = 1;
-  if (base > 0 && base < 512) {
-    n_split = (int)std::min<int64_t>(16, (512 + base - 1) / base);
+  if (base > 0 && base < 256) {
+    n_split = (int)std::min<int64_t>(16, (256 + base - 1) / base);
     n_split = (int)std::max<int64_t>(1, std::min<int64_t>(n_split, min_tiles / 4));
   }
   p.n_split = n_split;
   int32_t units = 0;
   for (size_t r = 0; r < reqs.size(); ++r) {
-    const int nq = (reqs[r].q_len + 31) / 32;
+    const int nq = (reqs[r].q_len + 63) / 64;
     p.req[r].q_start = reqs[r].q_start;
     p.req[r].q_len = reqs[r].q_len;
     p.req[r].kv_start = reqs[r].kv_start;
@@ -338,9 +339,9 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   p.n_units = units;
   if (n_split > 1) {
     const size_t rows = (size_t)n_split * total_q * c->cfg.n_q_heads;
-    const size_t po = rows * c->cfg.head_dim * sizeof(float);
+    const size_t po = rows * c->cfg.head_dim * sizeof(uint16_t);
     HIP_TRY(c->ws_part.ensure(po + rows * 2 * sizeof(float)));
-    p.part_o = static_cast<float*>(c->ws_part.ptr);
+    p.part_o = static_cast<uint16_t*>(c->ws_part.ptr);
     p.part_ml = reinterpret_cast<float*>(static_cast<char*>(c->ws_part.ptr) + po);
   }
   HIP_TRY(launch_attention(p, stream));

@@ -4,36 +4,37 @@
 // i of a request sees cache keys 0 .. art_len + i: every artifact key and the
 // suffix causally.
 //
-// Work unit = (request, block of 32 suffix tokens, KV head g, key split).
-// The workgroup's four waves are the four query heads that share KV head g,
-// so every K/V tile staged in LDS serves 4 x 32 query rows.  Per 64-key tile:
+// Work unit = (request, block of 64 suffix tokens, KV head g, key split), one
+// workgroup of eight waves: the four query heads that share KV head g times
+// two 32-token halves, so every K/V tile staged in LDS serves 256 query rows.
+// K/V tiles (64 keys) are copied global -> LDS by the DMA form of the load
+// (global_load_lds, 16 bytes per lane) into a three-stage ring: while tile i
+// is consumed, tiles i+1 and i+2 are in flight, with no staging registers and
+// one barrier per tile.  Per tile and wave:
 //   S^T = K Q^T  (MFMA A = K rows from LDS, B = Q held in registers), so the
 //                accumulator of a lane holds 32 keys of ONE token and the row
 //                max / row sum are in-lane plus one exchange with lane ^ 32;
 //   online softmax in the log2 domain: p = 2^(s * log2(e)/sqrt(d) - m) as one
-//                FMA and one v_exp_f32; the O rescale is skipped when no row
-//                max of the wave moved;
+//                FMA and one v_exp_f32; the reference max m only moves when a
+//                tile exceeds it by 2^8, so the O rescale is rare;
 //   O^T += V^T P^T  (MFMA A = V^T, B = P^T straight from the S^T accumulator
 //                converted to bf16 in registers).
 // The S^T accumulator hands a lane the keys of each 16-key group in the order
 // (4hf + 0..3, 8 + 4hf + 0..3), hf = lane / 32; the V^T operand is read in that
 // same key order with the gfx950 LDS transpose read (ds_read_b64_tr_b16): a
 // 16-lane group pointing at a 4-key x 16-dim block of the natural [key][d]
-// tile receives one dimension per lane across the 4 keys.  So K and V both
-// sit in LDS in their natural layout, written with 16-byte stores.
-// LDS: K [2][64][16 chunks], V [2][64][16 chunks] (64 KiB per workgroup),
-// double buffered with a register prefetch of the next tile.  16-byte chunks
-// are XOR-swizzled by row (K: row & 15, for b128 operand reads of 16 rows;
-// V: 4 * (row & 3), for transpose reads of 4 rows x 2 chunks).
+// tile receives one dimension per lane across the 4 keys.  16-byte chunks are
+// XOR-swizzled by row (K: row & 15, for b128 operand reads of 16 rows; V:
+// 4 * (row & 3), for transpose reads of 4 rows x 2 chunks): no bank conflicts.
 //
 // Work units of one KV head go to blockIdx.x = unit * Hkv + g: with Hkv = 8
 // workgroups are dealt round-robin over the 8 XCDs, so each XCD's L2 serves a
 // single KV head.  Late (heavier, causal) query blocks are dispatched first.
 // With n_split > 1 the key range of a block is cut into n_split tile ranges;
-// each writes a normalised fp32 partial and its (max, sum), and a second
-// kernel merges them.  (Merging inside this kernel would need agent-scope
-// release/acquire between workgroups, which on gfx950 writes back and
-// invalidates the XCD's L2 and costs the other workgroups their K/V reuse.)
+// each writes its normalised partial (bf16) and (max, sum) (fp32), and a
+// second kernel merges them.  (Merging inside this kernel would need
+// agent-scope release/acquire between workgroups, which on gfx950 writes back
+// and invalidates the XCD's L2 and costs the other workgroups their K/V reuse.)
 
 #include "common.h"
 #include "kernels.h"
@@ -42,43 +43,98 @@ namespace attuner {
 
 namespace {
 
-constexpr int BQ = 32;
-constexpr int BKV = 64;
+constexpr int BQ = 64;       // suffix tokens per workgroup (two 32-token halves)
+constexpr int BKV = 64;      // keys per tile
+constexpr int NSTAGE = 3;    // K/V tiles resident in LDS: the current one + 2 in flight
 constexpr int D = kHeadDim;
-constexpr int CH = D / 8;  // 16-byte chunks per K/V row
+constexpr int CH = D / 8;    // 16-byte chunks per K/V row
+constexpr int NTHREADS = 512;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef __attribute__((address_space(3))) bf16_t lds_bf16;
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void glb_void;
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-struct TileRegs {
-  u32x4 k[4];
-  u32x4 v[4];
-};
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding and leaves the other counters alone (gfx9 layout:
+// vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int vmcnt_wait(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
 
-__device__ __forceinline__ void load_tile(TileRegs& t, const bf16_t* __restrict__ kb, const bf16_t* __restrict__ vb,
-                                          int kv0, int kv_len, int tid) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i;
-    const int row = c >> 4, ch = c & 15;
-    const int key = kv0 + row;
-    const bool ok = key < kv_len;
-    const int64_t off = (int64_t)key * D + ch * 8;
-    t.k[i] = ok ? *reinterpret_cast<const u32x4*>(kb + off) : u32x4{0u, 0u, 0u, 0u};
-    t.v[i] = ok ? *reinterpret_cast<const u32x4*>(vb + off) : u32x4{0u, 0u, 0u, 0u};
-  }
+// One 16-byte-per-lane global -> LDS copy (global_load_lds_dwordx4): lane i's
+// 16 bytes land at LDS byte lds_base + 16 i (lds_base wave-uniform, in M0).
+// Issued as inline assembly so the compiler does not track these LDS writes
+// (its tracking would add a full vmcnt(0) wait before every LDS read); the
+// caller orders them with an explicit vmcnt wait and a barrier.
+__device__ __forceinline__ void lds_dma16(const void* gaddr, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(gaddr), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+      : "memory", "m0");
 }
 
-__device__ __forceinline__ void store_tile(const TileRegs& t, u32x4* __restrict__ ks, u32x4* __restrict__ vs,
-                                           int tid) {
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
+}
+
+// Workgroup barrier without a memory fence: LDS DMA completion is covered by
+// the explicit vmcnt wait before it; the empty asm statements keep the
+// compiler from moving memory accesses across it.
+__device__ __forceinline__ void barrier_no_fence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Per-lane source offsets (elements within a 64-key tile) of the K/V tile
+// DMA.  Wave w moves 1 KiB blocks w and w + 8 of each 16 KiB tile; lane i of
+// a block lands at byte 16 i of it, i.e. row 4 * block + i / 16, physical
+// chunk i % 16, so the lane fetches the logical chunk the swizzle maps there
+// (K: chunk ^ (row & 15), V: chunk ^ 4 (row & 3)).
+struct DmaLane {
+  int row[2];
+  int koff[2], voff[2];
+};
+
+__device__ __forceinline__ DmaLane dma_lane(int wave, int lane) {
+  DmaLane d;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i;
-    const int row = c >> 4, ch = c & 15;
-    ks[row * CH + (ch ^ (row & 15))] = t.k[i];
-    vs[row * CH + (ch ^ ((row & 3) << 2))] = t.v[i];
+  for (int j = 0; j < 2; ++j) {
+    const int blk = wave + 8 * j;
+    const int row = 4 * blk + (lane >> 4);
+    const int phys = lane & 15;
+    d.row[j] = row;
+    d.koff[j] = row * D + 8 * (phys ^ (row & 15));
+    d.voff[j] = row * D + 8 * (phys ^ ((row & 3) << 2));
+  }
+  return d;
+}
+
+// Issue the DMA of one 64-key K and V tile (keys kv0 .. kv0+63 of the
+// request; rows past kv_len - 1 re-read row kv_len - 1, whose values the mask
+// discards) straight into LDS.  Exactly 4 loads per wave per tile.
+__device__ __forceinline__ void dma_tile(const bf16_t* __restrict__ kb, const bf16_t* __restrict__ vb, int kv0,
+                                         int kv_len, uint32_t k_dst, uint32_t v_dst, const DmaLane& d, int wave) {
+  if (kv0 + BKV <= kv_len) {
+    const int64_t base = (int64_t)kv0 * D;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t blk = wave + 8 * j;
+      lds_dma16(kb + base + d.koff[j], k_dst + 1024u * blk);
+      lds_dma16(vb + base + d.voff[j], v_dst + 1024u * blk);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t blk = wave + 8 * j;
+      const int shift = (min(kv0 + d.row[j], kv_len - 1) - d.row[j]) * D;  // clamp the row
+      lds_dma16(kb + (int64_t)shift + d.koff[j], k_dst + 1024u * blk);
+      lds_dma16(vb + (int64_t)shift + d.voff[j], v_dst + 1024u * blk);
+    }
   }
 }
 
@@ -100,9 +156,9 @@ __device__ __forceinline__ void store_output(const AttnParams& p, int64_t qrow, 
   if (p.lse != nullptr && hf == 0) p.lse[qrow * p.n_q_heads + h] = (m_log2 + __log2f(l)) * 0.69314718055994531f;
 }
 
-__global__ __launch_bounds__(256, 2) void attention_kernel(AttnParams p) {
-  __shared__ u32x4 k_lds[2][BKV * CH];
-  __shared__ u32x4 v_lds[2][BKV * CH];
+__global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
+  __shared__ u32x4 k_lds[NSTAGE][BKV * CH];
+  __shared__ u32x4 v_lds[NSTAGE][BKV * CH];
 
   const int hkv = p.n_kv_heads;
   const int g = blockIdx.x % hkv;
@@ -123,12 +179,13 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnParams p) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = tid >> 6;       // 0..7
   const int l32 = lane & 31;
   const int hf = lane >> 5;
-  const int h = g * 4 + wave;
-  const int t = t0 + l32;  // this lane's suffix token (index within the request)
-  const bool row_ok = l32 < blk_rows;
+  const int h = g * 4 + (wave & 3);
+  const int t0w = t0 + 32 * (wave >> 2);  // first token of this wave's half
+  const int t = t0w + l32;                // this lane's suffix token (index within the request)
+  const bool row_ok = t - t0 < blk_rows;
   const int64_t qrow = (int64_t)(rq.q_start + t);
 
   bf16x8 qf[8];
@@ -138,10 +195,13 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnParams p) {
     if (row_ok) v = *reinterpret_cast<const u32x4*>(p.q + (qrow * p.n_q_heads + h) * D + ks * 16 + hf * 8);
     qf[ks] = as_bf16x8(v);
   }
+  // Q is in registers before any K/V DMA is issued, so the compiler needs no
+  // vector-memory wait inside the tile loop
+  __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
 
-  // transpose-read addressing of the V^T operand (see the header): lane r of
-  // its 16-lane group points at key row (r >> 2) of a 4-key block and dims
-  // d0 + 4 (r & 3) .. +3, d0 = 32 db + 16 * group.
+  // transpose-read addressing of the V^T operand: lane r of its 16-lane group
+  // points at key row (r >> 2) of a 4-key block and dims d0 + 4 (r & 3) .. +3,
+  // d0 = 32 db + 16 * group.
   const int r16 = lane & 15;
   const int grp = (lane >> 4) & 1;
   const int vrow = r16 >> 2;  // == key & 3 of the row it reads
@@ -164,18 +224,32 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnParams p) {
   const int vis_lim = rq.art_len + t;  // last visible key of this row
 
   if (tb < te) {
-    TileRegs regs;
-    load_tile(regs, kb, vb, tb * BKV, kv_len, tid);
-    store_tile(regs, k_lds[0], v_lds[0], tid);
-    __syncthreads();
+    const uint32_t k_base = lds_addr(k_lds[0]), v_base = lds_addr(v_lds[0]);
+    constexpr uint32_t kStage = BKV * CH * 16;  // bytes per stage of K (and of V)
+    // prologue: tiles tb and tb + 1 in flight (indices clamped to te - 1, so
+    // every wave always has exactly 4 loads per tile outstanding)
+    const DmaLane dl = dma_lane(wave, lane);
+    dma_tile(kb, vb, tb * BKV, kv_len, k_base, v_base, dl, wave);
+    dma_tile(kb, vb, min(tb + 1, te - 1) * BKV, kv_len, k_base + kStage, v_base + kStage, dl, wave);
 
     for (int tile = tb; tile < te; ++tile) {
-      const int cur = (tile - tb) & 1;
+      const int it = tile - tb;
+      const int cur = it % NSTAGE;
+      // this wave's loads of `tile` done (those of tile + 1 may still fly),
+      // then everyone's: the tile is in LDS, and the buffer of tile - 1 is free
+      __builtin_amdgcn_s_waitcnt(vmcnt_wait(4));
+      barrier_no_fence();
+      {
+        const uint32_t nb = (uint32_t)((it + 2) % NSTAGE) * kStage;
+        dma_tile(kb, vb, min(tile + 2, te - 1) * BKV, kv_len, k_base + nb, v_base + nb, dl, wave);
+      }
       const int kv0 = tile * BKV;
-      if (tile + 1 < te) load_tile(regs, kb, vb, kv0 + BKV, kv_len, tid);
 
       // ---- S^T = K Q^T --------------------------------------------------
+      // (raised wave priority while issuing MFMAs: the other wave of the SIMD
+      // fills the matrix-core time with its softmax work)
       f32x16 s[2];
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh) {
         s[kh] = f32x16{};
@@ -186,9 +260,10 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnParams p) {
           s[kh] = mfma32(a, qf[ks], s[kh]);
         }
       }
+      __builtin_amdgcn_s_setprio(0);
 
       // ---- mask + online softmax (log2 domain) -----------------------------
-      if (kv0 + BKV - 1 > rq.art_len + t0) {
+      if (kv0 + BKV - 1 > rq.art_len + t0w) {
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
@@ -203,7 +278,11 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnParams p) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kh][v]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_i, mx * sc);
+      // Lazy reference max: keep m_i (and skip the O rescale) unless the tile
+      // max exceeds it by more than 8 in log2 units.  l and O accumulate
+      // against the same reference, so the result is unchanged; p <= 2^8.
+      const float m_tile = mx * sc;
+      const float m_new = m_tile > m_i + 8.0f ? m_tile : m_i;
       const float m_use = m_new == -INFINITY ? 0.f : m_new;
       const float alpha = __builtin_amdgcn_exp2f(m_i - m_use);
       float rs = 0.f;
@@ -236,26 +315,24 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnParams p) {
         pk[j] = as_bf16x8(w);
       }
       const lds_bf16* vbase = (const lds_bf16*)(v_lds[cur]);
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int row_a = 16 * j + 4 * hf + vrow;  // keys 16j + 4hf + 0..3
         const int row_b = row_a + 8;                // keys 16j + 8 + 4hf + 0..3
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
-          const v4i16 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_v4i16*)(vbase + row_a * D + vcol[db]));
-          const v4i16 vbv = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_v4i16*)(vbase + row_b * D + vcol[db]));
-          v4i16 lo = va, hi2 = vbv;
+          const v4i16 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vbase + row_a * D + vcol[db]));
+          const v4i16 vbv = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vbase + row_b * D + vcol[db]));
           typedef short v8i16 __attribute__((ext_vector_type(8)));
-          const v8i16 a8 = __builtin_shufflevector(lo, hi2, 0, 1, 2, 3, 4, 5, 6, 7);
+          const v8i16 a8 = __builtin_shufflevector(va, vbv, 0, 1, 2, 3, 4, 5, 6, 7);
           acc[db] = mfma32(__builtin_bit_cast(bf16x8, a8), pk[j], acc[db]);
         }
       }
-
-      if (tile + 1 < te) store_tile(regs, k_lds[cur ^ 1], v_lds[cur ^ 1], tid);
-      __syncthreads();
+      __builtin_amdgcn_s_setprio(0);
     }
+    // drain the two trailing (clamped) tile loads before the workgroup ends
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
   }
 
   const float inv_l = l_i > 0.f ? 1.0f / l_i : 0.f;
@@ -264,57 +341,64 @@ __global__ __launch_bounds__(256, 2) void attention_kernel(AttnParams p) {
     return;
   }
 
-  // ---- split-KV: publish the normalised partial and its (max, sum) --------
+  // ---- split-KV: publish the normalised partial (bf16) and its (max, sum) --
   if (!row_ok) return;
   const int64_t prow = (int64_t)split * p.total_q * p.n_q_heads + qrow * p.n_q_heads + h;
-  float* po = p.part_o + prow * D;
+  bf16_t* po = p.part_o + prow * D;
 #pragma unroll
   for (int db = 0; db < 4; ++db) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      f32x4 v;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = acc[db][4 * q + e] * inv_l;
-      *reinterpret_cast<f32x4*>(po + db * 32 + 8 * q + 4 * hf) = v;
+      u32x2 pr;
+      pr[0] = pack_bf16x2(acc[db][4 * q] * inv_l, acc[db][4 * q + 1] * inv_l);
+      pr[1] = pack_bf16x2(acc[db][4 * q + 2] * inv_l, acc[db][4 * q + 3] * inv_l);
+      *reinterpret_cast<u32x2*>(po + db * 32 + 8 * q + 4 * hf) = pr;
     }
   }
   if (hf == 0) *reinterpret_cast<f32x2*>(p.part_ml + prow * 2) = f32x2{m_i, l_i};
 }
 
-// Merge the n_split partials of one (token, head) per wave: weight of split s
-// is l_s * 2^(m_s - max_s m_s); lane j owns output dims 2j, 2j + 1.
+// Merge the n_split partials: weight of split s is l_s * 2^(m_s - max_s m_s).
+// A wave merges two (token, head) rows; lane j of a half owns dims 4j .. 4j+3.
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
   const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // token * Hq + head
+  const int64_t row = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 2 + (lane >> 5);  // token * Hq + head
+  const int d0 = 4 * (lane & 31);
   const int64_t stride = (int64_t)p.total_q * p.n_q_heads;
   if (row >= stride) return;
   float mmax = -INFINITY;
   for (int s = 0; s < p.n_split; ++s) mmax = fmaxf(mmax, p.part_ml[(s * stride + row) * 2]);
-  float wsum = 0.f, o0 = 0.f, o1 = 0.f;
+  float wsum = 0.f;
+  f32x4 o = f32x4{};
 #pragma unroll 4
   for (int s = 0; s < p.n_split; ++s) {
     const f32x2 ml = *reinterpret_cast<const f32x2*>(p.part_ml + (s * stride + row) * 2);
     const float w = (ml[0] == -INFINITY) ? 0.f : ml[1] * __builtin_amdgcn_exp2f(ml[0] - mmax);
-    const f32x2 v = *reinterpret_cast<const f32x2*>(p.part_o + (s * stride + row) * D + 2 * lane);
-    o0 = fmaf(w, v[0], o0);
-    o1 = fmaf(w, v[1], o1);
+    const u32x2 v = *reinterpret_cast<const u32x2*>(p.part_o + (s * stride + row) * D + d0);
+    o[0] = fmaf(w, bf16_to_f32((bf16_t)(v[0] & 0xFFFFu)), o[0]);
+    o[1] = fmaf(w, bf16_to_f32((bf16_t)(v[0] >> 16)), o[1]);
+    o[2] = fmaf(w, bf16_to_f32((bf16_t)(v[1] & 0xFFFFu)), o[2]);
+    o[3] = fmaf(w, bf16_to_f32((bf16_t)(v[1] >> 16)), o[3]);
     wsum += w;
   }
   const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
-  *reinterpret_cast<uint32_t*>(p.o + row * D + 2 * lane) = pack_bf16x2(o0 * inv, o1 * inv);
-  if (p.lse != nullptr && lane == 0) p.lse[row] = (mmax + __log2f(wsum)) * 0.69314718055994531f;
+  u32x2 pr;
+  pr[0] = pack_bf16x2(o[0] * inv, o[1] * inv);
+  pr[1] = pack_bf16x2(o[2] * inv, o[3] * inv);
+  *reinterpret_cast<u32x2*>(p.o + row * D + d0) = pr;
+  if (p.lse != nullptr && (lane & 31) == 0) p.lse[row] = (mmax + __log2f(wsum)) * 0.69314718055994531f;
 }
 
 }  // namespace
 
 hipError_t launch_attention(const AttnParams& p, hipStream_t stream) {
   if (p.n_units == 0) return hipSuccess;
-  ATTUNER_LAUNCH("attention_kernel", attention_kernel, dim3((unsigned)(p.n_units * p.n_kv_heads)), dim3(256), stream,
-                 p);
+  ATTUNER_LAUNCH("attention_kernel", attention_kernel, dim3((unsigned)(p.n_units * p.n_kv_heads)), dim3(NTHREADS),
+                 stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_split == 1) return e;
   const int64_t rows = (int64_t)p.total_q * p.n_q_heads;
-  ATTUNER_LAUNCH("attn_combine_kernel", attn_combine_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), stream, p);
+  ATTUNER_LAUNCH("attn_combine_kernel", attn_combine_kernel, dim3((unsigned)((rows + 7) / 8)), dim3(256), stream, p);
   return hipGetLastError();
 }
 

@@ -7,7 +7,8 @@
 // holds four consecutive output features of one token (8-byte stores).  Both
 // operands are K-contiguous in memory ([rows][hidden]), so tiles go to LDS
 // without a transpose.  Workgroup tile BN (features) x BM (tokens) x 64 (k),
-// four waves in a 2 x 2 grid, 32x32x16 MFMAs, fp32 accumulation.  The k-loop
+// four waves (WN along features x 4/WN along tokens), 32x32x16 MFMAs, fp32
+// accumulation.  The k-loop
 // keeps NS k-tiles in flight in a register ring (the small-token shapes of
 // suffix prefill are latency-bound, not bandwidth-bound) and double-buffers
 // LDS.  LDS rows are 128 bytes (eight 16-byte chunks); chunk c of row r is
@@ -33,14 +34,17 @@ constexpr int kLoraSlice = 256;        // hidden elements per lora_down workgrou
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-template <int BM, int BN, int NS>
+template <int BM, int BN, int WN, int NS>
 __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w,
                                                            int M, int N, int K, const bf16_t* __restrict__ b,
                                                            int rank, int r_pad, int lora_cols,
                                                            const float* __restrict__ t_part, int n_slice,
                                                            bf16_t* __restrict__ out, int n_mt, int n_nt) {
-  constexpr int FN = BN / 64;  // 32-row MFMA blocks per wave along features
-  constexpr int FM = BM / 64;  // along tokens
+  constexpr int WM = 4 / WN;            // waves along tokens (WN along features)
+  constexpr int TN = BN / WN, TM = BM / WM;  // wave tile
+  constexpr int FN = TN / 32;           // 32-row MFMA blocks per wave along features
+  constexpr int FM = TM / 32;           // along tokens
+  static_assert(FN >= 1 && FM >= 1 && WN * WM == 4, "bad wave layout");
   constexpr int ROWS = BN + BM;
   constexpr int LOADS = ROWS * kChunksPerRow / 256;  // 16-byte chunks per thread per k-tile
   static_assert(ROWS * kChunksPerRow % 256 == 0, "tile must split evenly over 256 threads");
@@ -61,8 +65,8 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wn = wave >> 1;  // feature half
-  const int wm = wave & 1;   // token half
+  const int wn = wave / WM;  // wave position along features
+  const int wm = wave % WM;  // along tokens
   const int l32 = lane & 31;
   const int hi = lane >> 5;
 
@@ -119,12 +123,12 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
         bf16x8 af[FN], bfr[FM];
 #pragma unroll
         for (int i = 0; i < FN; ++i) {
-          const int row = wn * (BN / 2) + i * 32 + l32;
+          const int row = wn * TN + i * 32 + l32;
           af[i] = as_bf16x8(lds[cur][row * kChunksPerRow + swz(row, ch)]);
         }
 #pragma unroll
         for (int j = 0; j < FM; ++j) {
-          const int row = BN + wm * (BM / 2) + j * 32 + l32;
+          const int row = BN + wm * TM + j * 32 + l32;
           bfr[j] = as_bf16x8(lds[cur][row * kChunksPerRow + swz(row, ch)]);
         }
 #pragma unroll
@@ -147,7 +151,7 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
       bf16x8 th[FM], tl[FM];
 #pragma unroll
       for (int j = 0; j < FM; ++j) {
-        int m = m0 + wm * (BM / 2) + j * 32 + l32;
+        int m = m0 + wm * TM + j * 32 + l32;
         m = m < M ? m : M - 1;
         const float* tp = t_part + (int64_t)m * r_pad + ks + 8 * hi;
         f32x4 s0 = f32x4{}, s1 = f32x4{};
@@ -167,7 +171,7 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
       }
 #pragma unroll
       for (int i = 0; i < FN; ++i) {
-        const int nb = n0 + wn * (BN / 2) + i * 32;
+        const int nb = n0 + wn * TN + i * 32;
         if (nb >= lora_cols) continue;  // lora_cols is a multiple of 32
         const int n = nb + l32;
         bf16x8 a;
@@ -189,11 +193,11 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
   // ---- store: lane holds features nb + 8q + 4*hi + (0..3) of token m --------
 #pragma unroll
   for (int j = 0; j < FM; ++j) {
-    const int m = m0 + wm * (BM / 2) + j * 32 + l32;
+    const int m = m0 + wm * TM + j * 32 + l32;
     if (m >= M) continue;
 #pragma unroll
     for (int i = 0; i < FN; ++i) {
-      const int nb = n0 + wn * (BN / 2) + i * 32;
+      const int nb = n0 + wn * TN + i * 32;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int n = nb + 8 * q + 4 * hi;
@@ -274,25 +278,35 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
                             const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
                             uint16_t* out, hipStream_t stream) {
   if (n_tok == 0) return hipSuccess;
-  constexpr int BN = 128;
-  const int n_nt = n_out / BN;
   const int n_slice = lora_down_slices(hidden);
-  // Prefer 128-token tiles once they alone give every CU two workgroups.  The
-  // prefetch depth must divide the number of 64-wide k-tiles.
+  // Tile choice (measured on gfx950 at hidden 2560, 6144 outputs): 128x128
+  // tiles once they alone give every CU two workgroups; 64 tokens x 128
+  // features with a 4-deep prefetch for mid-size suffixes; 64x64 tiles with an
+  // 8-deep prefetch when even that leaves most CUs idle (the weight stream is
+  // latency-bound there).  The prefetch depth must divide the number of
+  // 64-wide k-tiles; n_out is a multiple of 128.
   const int n_kt = hidden / BK;
   const int n_mt128 = (n_tok + 127) / 128;
-#define ATTUNER_GEMM(BM_, NS_, NMT_)                                                                           \
-  ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN, NS_>), dim3((NMT_) * n_nt), dim3(256), stream, x, w, \
-                 n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, (NMT_), n_nt)
-  if ((int64_t)n_mt128 * n_nt >= 512) {
-    if (n_kt % 2 == 0) ATTUNER_GEMM(128, 2, n_mt128);
-    else ATTUNER_GEMM(128, 1, n_mt128);
+  const int n_mt64 = (n_tok + 63) / 64;
+  const int n_nt128 = n_out / 128;
+#define ATTUNER_GEMM(BM_, BN_, WN_, NS_)                                                                          \
+  ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, NS_>),                                      \
+                 dim3(((n_tok + (BM_) - 1) / (BM_)) * (n_out / (BN_))), dim3(256), stream, x, w, n_tok, n_out,     \
+                 hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, (n_tok + (BM_) - 1) / (BM_), n_out / (BN_))
+#define ATTUNER_GEMM_NS(BM_, BN_, WN_, NSMAX_)          \
+  if (n_kt % (NSMAX_) == 0) ATTUNER_GEMM(BM_, BN_, WN_, NSMAX_);        \
+  else if (n_kt % 4 == 0) ATTUNER_GEMM(BM_, BN_, WN_, 4);               \
+  else if (n_kt % 2 == 0) ATTUNER_GEMM(BM_, BN_, WN_, 2);               \
+  else ATTUNER_GEMM(BM_, BN_, WN_, 1);
+  if ((int64_t)n_mt128 * n_nt128 >= 512) {
+    if (n_kt % 2 == 0) ATTUNER_GEMM(128, 128, 2, 2);
+    else ATTUNER_GEMM(128, 128, 2, 1);
+  } else if ((int64_t)n_mt64 * n_nt128 >= 128) {
+    ATTUNER_GEMM_NS(64, 128, 2, 4)
   } else {
-    const int n_mt = (n_tok + 63) / 64;
-    if (n_kt % 4 == 0) ATTUNER_GEMM(64, 4, n_mt);
-    else if (n_kt % 2 == 0) ATTUNER_GEMM(64, 2, n_mt);
-    else ATTUNER_GEMM(64, 1, n_mt);
+    ATTUNER_GEMM_NS(64, 64, 2, 8)
   }
+#undef ATTUNER_GEMM_NS
 #undef ATTUNER_GEMM
   return hipGetLastError();
 }

@@ -90,7 +90,7 @@ struct AttnReq {
   int32_t q_len;
   int32_t kv_start;  // cache row of key 0 of the request
   int32_t art_len;   // cached artifact keys; row i sees keys 0 .. art_len + i
-  int32_t n_qblk;    // ceil(q_len / 32)
+  int32_t n_qblk;    // ceil(q_len / 64)
   int32_t wg_start;  // first work unit of the request (units = qblocks * n_split)
 };
 
@@ -101,7 +101,7 @@ struct AttnParams {
   int64_t kv_head_stride;
   uint16_t* o;             // [T_q][Hq][128]
   float* lse;              // [T_q][Hq] or null
-  float* part_o;           // [n_split][T_q][Hq][128]   (n_split > 1)
+  uint16_t* part_o;        // [n_split][T_q][Hq][128] bf16, normalised (n_split > 1)
   float* part_ml;          // [n_split][T_q][Hq][2]      (n_split > 1)
   int32_t n_q_heads, n_kv_heads;
   int32_t total_q;
