@@ -52,4 +52,39 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// ---- direct global -> LDS copies ------------------------------------------
+
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding and leaves the other counters alone (gfx9 layout:
+// vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14, expcnt 6:4, lgkmcnt 11:8).
+__host__ __device__ constexpr int vmcnt_wait(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
+// One 16-byte-per-lane global -> LDS copy (global_load_lds_dwordx4): lane i's
+// 16 bytes land at LDS byte lds_base + 16 i (lds_base wave-uniform, in M0).
+// Issued as inline assembly so the compiler does not track these LDS writes
+// (its tracking would add a full vmcnt(0) wait before every LDS read); the
+// caller orders them with an explicit vmcnt wait and a barrier.
+__device__ __forceinline__ void lds_dma16(const void* gaddr, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(gaddr), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
+}
+
+// Workgroup barrier without a memory fence: LDS DMA completion is covered by
+// the explicit vmcnt wait before it; the empty asm statements keep the
+// compiler from moving memory accesses across it.
+__device__ __forceinline__ void barrier_no_fence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 }  // namespace attuner

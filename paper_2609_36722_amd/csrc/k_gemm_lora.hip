@@ -7,13 +7,13 @@
 // holds four consecutive output features of one token (8-byte stores).  Both
 // operands are K-contiguous in memory ([rows][hidden]), so tiles go to LDS
 // without a transpose.  Workgroup tile BN (features) x BM (tokens) x 64 (k),
-// four waves (WN along features x 4/WN along tokens), 32x32x16 MFMAs, fp32
-// accumulation.  The k-loop
-// keeps NS k-tiles in flight in a register ring (the small-token shapes of
-// suffix prefill are latency-bound, not bandwidth-bound) and double-buffers
-// LDS.  LDS rows are 128 bytes (eight 16-byte chunks); chunk c of row r is
-// stored at c ^ ((r >> 1) & 7), so the 16 rows one operand read touches in a
-// cycle land on 16 distinct bank groups.
+// WN x WM waves, 32x32x16 MFMAs, fp32 accumulation.  At suffix sizes the
+// kernel is bound by how fast CUs ingest operand tiles (measured on gfx950:
+// ~35-60 GB/s per CU, ~9 TB/s over the chip, with or without the MFMAs), so
+// the tile shape is chosen to minimise ingested bytes, M N K 2 (1/BM + 1/BN),
+// while keeping every CU busy.  LDS rows are 128 bytes (eight 16-byte
+// chunks); chunk c of row r is stored at c ^ ((r >> 1) & 7), so the 16 rows
+// one operand read touches in a cycle land on 16 distinct bank groups.
 //
 // The LoRA term enters as extra MFMA k-steps after the main loop: A operand
 // = rows of B (rank padded to 16 with zeros), B operand = t rounded to a
@@ -34,124 +34,22 @@ constexpr int kLoraSlice = 256;        // hidden elements per lora_down workgrou
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-template <int BM, int BN, int WN, int NS>
-__global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w,
-                                                           int M, int N, int K, const bf16_t* __restrict__ b,
-                                                           int rank, int r_pad, int lora_cols,
-                                                           const float* __restrict__ t_part, int n_slice,
-                                                           bf16_t* __restrict__ out, int n_mt, int n_nt) {
-  constexpr int WM = 4 / WN;            // waves along tokens (WN along features)
-  constexpr int TN = BN / WN, TM = BM / WM;  // wave tile
-  constexpr int FN = TN / 32;           // 32-row MFMA blocks per wave along features
-  constexpr int FM = TM / 32;           // along tokens
-  static_assert(FN >= 1 && FM >= 1 && WN * WM == 4, "bad wave layout");
-  constexpr int ROWS = BN + BM;
-  constexpr int LOADS = ROWS * kChunksPerRow / 256;  // 16-byte chunks per thread per k-tile
-  static_assert(ROWS * kChunksPerRow % 256 == 0, "tile must split evenly over 256 threads");
-
-  __shared__ u32x4 lds[2][ROWS * kChunksPerRow];
-
-  // XCD-aware tile order: workgroup i runs on XCD i % 8, so give each XCD a
-  // contiguous run of tiles; consecutive tiles share weight rows.
-  const int total = n_mt * n_nt;
-  const int per_xcd = total >> 3;
-  int lin = blockIdx.x;
-  if (lin < 8 * per_xcd) lin = (lin & 7) * per_xcd + (lin >> 3);
-  const int nt = lin / n_mt;
-  const int mt = lin - nt * n_mt;
-  const int n0 = nt * BN;
-  const int m0 = mt * BM;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wn = wave / WM;  // wave position along features
-  const int wm = wave % WM;  // along tokens
-  const int l32 = lane & 31;
-  const int hi = lane >> 5;
-
-  const u32x4* src[LOADS];
-  int dst[LOADS];
-#pragma unroll
-  for (int i = 0; i < LOADS; ++i) {
-    const int c = tid + 256 * i;
-    const int row = c / kChunksPerRow;
-    const int ch = c % kChunksPerRow;
-    const bf16_t* base;
-    if (row < BN) {
-      base = w + (int64_t)(n0 + row) * K;
-    } else {
-      int m = m0 + row - BN;
-      m = m < M ? m : M - 1;  // rows past the end are computed but never stored
-      base = x + (int64_t)m * K;
-    }
-    src[i] = reinterpret_cast<const u32x4*>(base) + ch;
-    dst[i] = row * kChunksPerRow + swz(row, ch);
-  }
-
-  f32x16 acc[FN][FM];
-#pragma unroll
-  for (int i = 0; i < FN; ++i)
-#pragma unroll
-    for (int j = 0; j < FM; ++j) acc[i][j] = f32x16{};
-
-  // n_kt is a multiple of NS (the launcher picks NS so); every load and LDS
-  // store below is unconditional (tile indices clamped), which keeps the
-  // compiler's wait counting exact: only the oldest ring slot is waited for.
-  const int n_kt = K / BK;
-  u32x4 ring[NS][LOADS];
-#pragma unroll
-  for (int s = 0; s < NS; ++s)
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) ring[s][i] = src[i][s * kChunksPerRow];
-#pragma unroll
-  for (int i = 0; i < LOADS; ++i) lds[0][dst[i]] = ring[0][i];
-  __syncthreads();
-
-  for (int kt0 = 0; kt0 < n_kt; kt0 += NS) {
-#pragma unroll
-    for (int u = 0; u < NS; ++u) {
-      const int kt = kt0 + u;
-      // ring[u] (tile kt) is already in LDS: refill it with tile kt + NS
-      const int nxt = min(kt + NS, n_kt - 1);
-#pragma unroll
-      for (int i = 0; i < LOADS; ++i) ring[u][i] = src[i][nxt * kChunksPerRow];
-      const int cur = kt & 1;
-#pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
-        const int ch = 2 * ks + hi;
-        bf16x8 af[FN], bfr[FM];
-#pragma unroll
-        for (int i = 0; i < FN; ++i) {
-          const int row = wn * TN + i * 32 + l32;
-          af[i] = as_bf16x8(lds[cur][row * kChunksPerRow + swz(row, ch)]);
-        }
-#pragma unroll
-        for (int j = 0; j < FM; ++j) {
-          const int row = BN + wm * TM + j * 32 + l32;
-          bfr[j] = as_bf16x8(lds[cur][row * kChunksPerRow + swz(row, ch)]);
-        }
-#pragma unroll
-        for (int i = 0; i < FN; ++i)
-#pragma unroll
-          for (int j = 0; j < FM; ++j) acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
-      }
-      // tile kt + 1 (ring slot u + 1) into the other LDS buffer; after the last
-      // tile this stores a stale tile nobody reads
-#pragma unroll
-      for (int i = 0; i < LOADS; ++i) lds[cur ^ 1][dst[i]] = ring[(u + 1) % NS][i];
-      __syncthreads();
-    }
-  }
-
-  // ---- fused low-rank epilogue: acc += B[n][:] . t[m][:] --------------------
-  if (r_pad > 0 && n0 < lora_cols) {
+// Fused low-rank epilogue and store of one wave's FN x FM blocks of C^T:
+// acc += B[n][:] . t[m][:] for features n < lora_cols, then bf16 stores (lane
+// holds features nb + 8q + 4*hi + (0..3) of token m).  n_base / m_base: the
+// wave tile's first feature / token.
+template <int FN, int FM>
+__device__ __forceinline__ void lora_epilogue_store(f32x16 (&acc)[FN][FM], int n_base, int m_base, int l32, int hi,
+                                                    int M, int N, const bf16_t* __restrict__ b, int rank, int r_pad,
+                                                    int lora_cols, const float* __restrict__ t_part, int n_slice,
+                                                    bf16_t* __restrict__ out) {
+  if (r_pad > 0 && n_base < lora_cols) {
     const int64_t slice_stride = (int64_t)M * r_pad;
     for (int ks = 0; ks < r_pad; ks += 16) {
       bf16x8 th[FM], tl[FM];
 #pragma unroll
       for (int j = 0; j < FM; ++j) {
-        int m = m0 + wm * TM + j * 32 + l32;
+        int m = m_base + j * 32 + l32;
         m = m < M ? m : M - 1;
         const float* tp = t_part + (int64_t)m * r_pad + ks + 8 * hi;
         f32x4 s0 = f32x4{}, s1 = f32x4{};
@@ -171,7 +69,7 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
       }
 #pragma unroll
       for (int i = 0; i < FN; ++i) {
-        const int nb = n0 + wn * TN + i * 32;
+        const int nb = n_base + i * 32;
         if (nb >= lora_cols) continue;  // lora_cols is a multiple of 32
         const int n = nb + l32;
         bf16x8 a;
@@ -190,14 +88,13 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
     }
   }
 
-  // ---- store: lane holds features nb + 8q + 4*hi + (0..3) of token m --------
 #pragma unroll
   for (int j = 0; j < FM; ++j) {
-    const int m = m0 + wm * TM + j * 32 + l32;
+    const int m = m_base + j * 32 + l32;
     if (m >= M) continue;
 #pragma unroll
     for (int i = 0; i < FN; ++i) {
-      const int nb = n0 + wn * TN + i * 32;
+      const int nb = n_base + i * 32;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int n = nb + 8 * q + 4 * hi;
@@ -208,6 +105,122 @@ __global__ __launch_bounds__(256, 2) void gemm_lora_kernel(const bf16_t* __restr
       }
     }
   }
+}
+
+// Both operand tiles are copied global -> LDS by the DMA form of the load
+// (16 bytes per lane, no staging registers) into an NST-stage ring, so NST - 1
+// k-tiles are in flight per workgroup while one is multiplied.  WN x WM waves;
+// one barrier per k-tile.  A k-tile stage is (BN + BM) rows of 128 bytes,
+// moved as 1 KiB blocks of 8 rows (lane i -> row 8 blk + i / 8, physical
+// chunk i % 8, holding the logical chunk the swizzle maps there).
+template <int BM, int BN, int WN, int WM, int NST>
+__global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t* __restrict__ x,
+                                                                   const bf16_t* __restrict__ w, int M, int N, int K,
+                                                                   const bf16_t* __restrict__ b, int rank, int r_pad,
+                                                                   int lora_cols, const float* __restrict__ t_part,
+                                                                   int n_slice, bf16_t* __restrict__ out, int n_mt,
+                                                                   int n_nt) {
+  constexpr int NW = WN * WM;
+  constexpr int TN = BN / WN, TM = BM / WM;
+  constexpr int FN = TN / 32, FM = TM / 32;
+  static_assert(FN >= 1 && FM >= 1 && TN % 32 == 0 && TM % 32 == 0, "bad wave layout");
+  constexpr int ROWS = BN + BM;
+  static_assert(ROWS % 8 == 0, "stage must be whole 1 KiB blocks");
+  constexpr int NBLK = ROWS / 8;
+  constexpr int PW = (NBLK + NW - 1) / NW;  // DMA instructions per wave per stage
+  constexpr int STAGE = ROWS * kChunksPerRow;
+  static_assert((NST - 2) * PW <= 63, "vmcnt range");
+  __shared__ u32x4 lds[NST * STAGE];
+
+  const int total = n_mt * n_nt;
+  const int per_xcd = total >> 3;
+  int lin = blockIdx.x;
+  if (lin < 8 * per_xcd) lin = (lin & 7) * per_xcd + (lin >> 3);
+  const int nt = lin / n_mt;
+  const int mt = lin - nt * n_mt;
+  const int n0 = nt * BN;
+  const int m0 = mt * BM;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wn = wave / WM;
+  const int wm = wave % WM;
+  const int l32 = lane & 31;
+  const int hi = lane >> 5;
+
+  // DMA sources of this lane (blocks past the stage repeat the last block:
+  // same bytes to the same place)
+  const int n_kt = K / BK;
+  const bf16_t* src[PW];
+  uint32_t doff[PW];
+#pragma unroll
+  for (int j = 0; j < PW; ++j) {
+    const int blk = min(wave + NW * j, NBLK - 1);
+    const int row = 8 * blk + (lane >> 3);
+    const int lg = swz(row, lane & 7);
+    const bf16_t* base;
+    if (row < BN) {
+      base = w + (int64_t)(n0 + row) * K;
+    } else {
+      const int m = min(m0 + row - BN, M - 1);  // rows past the end are computed, never stored
+      base = x + (int64_t)m * K;
+    }
+    src[j] = base + 8 * lg;
+    doff[j] = 1024u * blk;
+  }
+  const uint32_t lds0 = lds_addr(lds);
+
+#pragma unroll
+  for (int s = 0; s < NST - 1; ++s) {
+    const int kt = min(s, n_kt - 1);
+#pragma unroll
+    for (int j = 0; j < PW; ++j) lds_dma16(src[j] + kt * BK, lds0 + (uint32_t)(s * STAGE * 16) + doff[j]);
+  }
+
+  f32x16 acc[FN][FM];
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j) acc[i][j] = f32x16{};
+
+  int slot = 0, nslot = NST - 1;
+  for (int kt = 0; kt < n_kt; ++kt) {
+    // own copies of tile kt done, then everyone's; slot nslot (tile kt - 1) is free
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait((NST - 2) * PW));
+    barrier_no_fence();
+    const int nk = min(kt + NST - 1, n_kt - 1);
+#pragma unroll
+    for (int j = 0; j < PW; ++j) lds_dma16(src[j] + nk * BK, lds0 + (uint32_t)(nslot * STAGE * 16) + doff[j]);
+
+    const u32x4* cur = lds + slot * STAGE;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int ch = 2 * ks + hi;
+      bf16x8 af[FN], bfr[FM];
+#pragma unroll
+      for (int i = 0; i < FN; ++i) {
+        const int row = wn * TN + i * 32 + l32;
+        af[i] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+      }
+#pragma unroll
+      for (int j = 0; j < FM; ++j) {
+        const int row = BN + wm * TM + j * 32 + l32;
+        bfr[j] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+      }
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
+    }
+    slot = slot + 1 == NST ? 0 : slot + 1;
+    nslot = nslot + 1 == NST ? 0 : nslot + 1;
+  }
+  // the clamped copies of the last iterations must land before the workgroup
+  // ends (its LDS may be handed to the next workgroup)
+  __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+
+  lora_epilogue_store<FN, FM>(acc, n0 + wn * TN, m0 + wm * TM, l32, hi, M, N, b, rank, r_pad, lora_cols, t_part,
+                              n_slice, out);
 }
 
 // t = scale * x A^T with MFMAs, as fp32 partial sums per 256-wide slice of the
@@ -279,34 +292,25 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
                             uint16_t* out, hipStream_t stream) {
   if (n_tok == 0) return hipSuccess;
   const int n_slice = lora_down_slices(hidden);
-  // Tile choice (measured on gfx950 at hidden 2560, 6144 outputs): 128x128
-  // tiles once they alone give every CU two workgroups; 64 tokens x 128
-  // features with a 4-deep prefetch for mid-size suffixes; 64x64 tiles with an
-  // 8-deep prefetch when even that leaves most CUs idle (the weight stream is
-  // latency-bound there).  The prefetch depth must divide the number of
-  // 64-wide k-tiles; n_out is a multiple of 128.
-  const int n_kt = hidden / BK;
+  // Tile choice (measured on gfx950, hidden 2560, 6144 outputs): 128 x 256
+  // tiles with eight waves once they give >= 128 workgroups (the fewest
+  // ingested bytes; large batches); else 64 x 96 tiles when n_out allows and
+  // they give >= 128 workgroups (256 at a 256-token suffix); else 64 x 64
+  // (tiny suffixes: more workgroups pulling the weight stream).
   const int n_mt128 = (n_tok + 127) / 128;
   const int n_mt64 = (n_tok + 63) / 64;
-  const int n_nt128 = n_out / 128;
-#define ATTUNER_GEMM(BM_, BN_, WN_, NS_)                                                                          \
-  ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, NS_>),                                      \
-                 dim3(((n_tok + (BM_) - 1) / (BM_)) * (n_out / (BN_))), dim3(256), stream, x, w, n_tok, n_out,     \
-                 hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, (n_tok + (BM_) - 1) / (BM_), n_out / (BN_))
-#define ATTUNER_GEMM_NS(BM_, BN_, WN_, NSMAX_)          \
-  if (n_kt % (NSMAX_) == 0) ATTUNER_GEMM(BM_, BN_, WN_, NSMAX_);        \
-  else if (n_kt % 4 == 0) ATTUNER_GEMM(BM_, BN_, WN_, 4);               \
-  else if (n_kt % 2 == 0) ATTUNER_GEMM(BM_, BN_, WN_, 2);               \
-  else ATTUNER_GEMM(BM_, BN_, WN_, 1);
-  if ((int64_t)n_mt128 * n_nt128 >= 512) {
-    if (n_kt % 2 == 0) ATTUNER_GEMM(128, 128, 2, 2);
-    else ATTUNER_GEMM(128, 128, 2, 1);
-  } else if ((int64_t)n_mt64 * n_nt128 >= 128) {
-    ATTUNER_GEMM_NS(64, 128, 2, 4)
+#define ATTUNER_GEMM(BM_, BN_, WN_, WM_, NST_)                                                               \
+  ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, WM_, NST_>),                           \
+                 dim3(((n_tok + (BM_) - 1) / (BM_)) * (n_out / (BN_))), dim3(64 * (WN_) * (WM_)), stream, x, w, \
+                 n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, (n_tok + (BM_) - 1) / (BM_), \
+                 n_out / (BN_))
+  if (n_out % 256 == 0 && (int64_t)n_mt128 * (n_out / 256) >= 128) {
+    ATTUNER_GEMM(128, 256, 4, 2, 3);
+  } else if (n_out % 96 == 0 && (int64_t)n_mt64 * (n_out / 96) >= 128) {
+    ATTUNER_GEMM(64, 96, 3, 2, 5);
   } else {
-    ATTUNER_GEMM_NS(64, 64, 2, 8)
+    ATTUNER_GEMM(64, 64, 2, 2, 6);
   }
-#undef ATTUNER_GEMM_NS
 #undef ATTUNER_GEMM
   return hipGetLastError();
 }
