@@ -27,6 +27,8 @@ ARCH = "gfx950"
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result",
                 "-I", INCLUDE, "-I", CSRC]
+# Per-source extras (none at present).
+EXTRA_FLAGS = {}
 
 
 def _run(cmd):
@@ -50,7 +52,8 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
 
     def compile_one(pair):
         src, obj = pair
-        out = _run([HIPCC, *COMMON_FLAGS, *DEVICE_FLAGS, "-c", src, "-o", obj])
+        extra = EXTRA_FLAGS.get(os.path.basename(src), [])
+        out = _run([HIPCC, *COMMON_FLAGS, *DEVICE_FLAGS, *extra, "-c", src, "-o", obj])
         return src, out
 
     with cf.ThreadPoolExecutor(max_workers=max(1, min(jobs, len(srcs)))) as ex:

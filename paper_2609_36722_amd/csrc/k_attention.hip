@@ -193,22 +193,23 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   if (tb < te) {
     const uint32_t k_base = lds_addr(k_lds[0]), v_base = lds_addr(v_lds[0]);
     constexpr uint32_t kStage = BKV * CH * 16;  // bytes per stage of K (and of V)
-    // prologue: tiles tb and tb + 1 in flight (indices clamped to te - 1, so
-    // every wave always has exactly 4 loads per tile outstanding)
+    // prologue: tiles tb and tb + 1 in flight
     const DmaLane dl = dma_lane(wave, lane);
     dma_tile(kb, vb, tb * BKV, kv_len, k_base, v_base, dl, wave);
-    dma_tile(kb, vb, min(tb + 1, te - 1) * BKV, kv_len, k_base + kStage, v_base + kStage, dl, wave);
+    if (tb + 1 < te) dma_tile(kb, vb, (tb + 1) * BKV, kv_len, k_base + kStage, v_base + kStage, dl, wave);
 
     for (int tile = tb; tile < te; ++tile) {
       const int it = tile - tb;
       const int cur = it % NSTAGE;
-      // this wave's loads of `tile` done (those of tile + 1 may still fly),
-      // then everyone's: the tile is in LDS, and the buffer of tile - 1 is free
-      __builtin_amdgcn_s_waitcnt(vmcnt_wait(4));
+      // this wave's loads of `tile` done (those of tile + 1, if any, may
+      // still fly), then everyone's: the tile is in LDS, and the buffer of
+      // tile - 1 is free for tile + 2
+      if (tile + 1 < te) __builtin_amdgcn_s_waitcnt(vmcnt_wait(4));
+      else __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
       barrier_no_fence();
-      {
+      if (tile + 2 < te) {
         const uint32_t nb = (uint32_t)((it + 2) % NSTAGE) * kStage;
-        dma_tile(kb, vb, min(tile + 2, te - 1) * BKV, kv_len, k_base + nb, v_base + nb, dl, wave);
+        dma_tile(kb, vb, (tile + 2) * BKV, kv_len, k_base + nb, v_base + nb, dl, wave);
       }
       const int kv0 = tile * BKV;
 
@@ -298,8 +299,6 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
       }
       __builtin_amdgcn_s_setprio(0);
     }
-    // drain the two trailing (clamped) tile loads before the workgroup ends
-    __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
   }
 
   const float inv_l = l_i > 0.f ? 1.0f / l_i : 0.f;
