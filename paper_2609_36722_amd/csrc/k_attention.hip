@@ -325,34 +325,56 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
 }
 
 // Merge the n_split partials: weight of split s is l_s * 2^(m_s - max_s m_s).
-// A wave merges two (token, head) rows; lane j of a half owns dims 4j .. 4j+3.
+// Workgroup b serves KV head g = b % Hkv and 4 tokens: with Hkv = 8 it runs on
+// the XCD whose workgroups wrote those partials, so they are read from that
+// XCD's L2.  A wave merges the 4 query heads of one token; 16 lanes per
+// (token, head) row, lane owning dims 8 (lane % 16) .. +7; every split's data
+// is requested before any is used.
+constexpr int kMaxSplit = 16;
+
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
+  const int g = blockIdx.x % p.n_kv_heads;
+  const int t = (blockIdx.x / p.n_kv_heads) * 4 + (threadIdx.x >> 6);
+  if (t >= p.total_q) return;
   const int lane = threadIdx.x & 63;
-  const int64_t row = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 2 + (lane >> 5);  // token * Hq + head
-  const int d0 = 4 * (lane & 31);
+  const int h = g * 4 + (lane >> 4);
+  const int d0 = 8 * (lane & 15);
+  const int64_t row = (int64_t)t * p.n_q_heads + h;
   const int64_t stride = (int64_t)p.total_q * p.n_q_heads;
-  if (row >= stride) return;
+  const int ns = p.n_split;
+  f32x2 ml[kMaxSplit];
+  u32x4 v[kMaxSplit];
+#pragma unroll
+  for (int s = 0; s < kMaxSplit; ++s) {
+    if (s < ns) {
+      ml[s] = *reinterpret_cast<const f32x2*>(p.part_ml + (s * stride + row) * 2);
+      v[s] = *reinterpret_cast<const u32x4*>(p.part_o + (s * stride + row) * D + d0);
+    }
+  }
   float mmax = -INFINITY;
-  for (int s = 0; s < p.n_split; ++s) mmax = fmaxf(mmax, p.part_ml[(s * stride + row) * 2]);
+#pragma unroll
+  for (int s = 0; s < kMaxSplit; ++s)
+    if (s < ns) mmax = fmaxf(mmax, ml[s][0]);
   float wsum = 0.f;
-  f32x4 o = f32x4{};
-#pragma unroll 4
-  for (int s = 0; s < p.n_split; ++s) {
-    const f32x2 ml = *reinterpret_cast<const f32x2*>(p.part_ml + (s * stride + row) * 2);
-    const float w = (ml[0] == -INFINITY) ? 0.f : ml[1] * __builtin_amdgcn_exp2f(ml[0] - mmax);
-    const u32x2 v = *reinterpret_cast<const u32x2*>(p.part_o + (s * stride + row) * D + d0);
-    o[0] = fmaf(w, bf16_to_f32((bf16_t)(v[0] & 0xFFFFu)), o[0]);
-    o[1] = fmaf(w, bf16_to_f32((bf16_t)(v[0] >> 16)), o[1]);
-    o[2] = fmaf(w, bf16_to_f32((bf16_t)(v[1] & 0xFFFFu)), o[2]);
-    o[3] = fmaf(w, bf16_to_f32((bf16_t)(v[1] >> 16)), o[3]);
-    wsum += w;
+  float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < kMaxSplit; ++s) {
+    if (s < ns) {
+      const float w = (ml[s][0] == -INFINITY) ? 0.f : ml[s][1] * __builtin_amdgcn_exp2f(ml[s][0] - mmax);
+      wsum += w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[2 * e] = fmaf(w, __uint_as_float(v[s][e] << 16), o[2 * e]);
+        o[2 * e + 1] = fmaf(w, __uint_as_float(v[s][e] & 0xFFFF0000u), o[2 * e + 1]);
+      }
+    }
   }
   const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
-  u32x2 pr;
-  pr[0] = pack_bf16x2(o[0] * inv, o[1] * inv);
-  pr[1] = pack_bf16x2(o[2] * inv, o[3] * inv);
-  *reinterpret_cast<u32x2*>(p.o + row * D + d0) = pr;
-  if (p.lse != nullptr && (lane & 31) == 0) p.lse[row] = (mmax + __log2f(wsum)) * 0.69314718055994531f;
+  u32x4 pr;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) pr[e] = pack_bf16x2(o[2 * e] * inv, o[2 * e + 1] * inv);
+  *reinterpret_cast<u32x4*>(p.o + row * D + d0) = pr;
+  if (p.lse != nullptr && (lane & 15) == 0) p.lse[row] = (mmax + __log2f(wsum)) * 0.69314718055994531f;
 }
 
 }  // namespace
@@ -363,8 +385,9 @@ hipError_t launch_attention(const AttnParams& p, hipStream_t stream) {
                  stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_split == 1) return e;
-  const int64_t rows = (int64_t)p.total_q * p.n_q_heads;
-  ATTUNER_LAUNCH("attn_combine_kernel", attn_combine_kernel, dim3((unsigned)((rows + 7) / 8)), dim3(256), stream, p);
+  if (p.n_split > kMaxSplit || p.n_q_heads != 4 * p.n_kv_heads) return hipErrorInvalidValue;
+  const int64_t wgs = (int64_t)((p.total_q + 3) / 4) * p.n_kv_heads;
+  ATTUNER_LAUNCH("attn_combine_kernel", attn_combine_kernel, dim3((unsigned)wgs), dim3(256), stream, p);
   return hipGetLastError();
 }
 
