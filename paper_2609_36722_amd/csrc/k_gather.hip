@@ -8,8 +8,10 @@
 // One workgroup of 256 threads moves one page of one layer: thread t owns row
 // t / 16 and 16-byte chunk t % 16 of every slab, so each slab is read as one
 // contiguous 4 KiB span and written as n_valid contiguous 256-byte rows.
-// All 16 slabs of a page (8 KV heads, K and V) are in flight per thread
-// before any store is issued.
+// Loads and stores are both streaming (non-temporal: every byte is touched
+// once), two slabs in flight per thread at a time: on gfx950 a plain copy
+// reaches ~6.0 TB/s with 2-4 16-byte vectors per thread in flight and falls
+// to ~5.2-5.6 TB/s with 8-16.
 
 #include "common.h"
 #include "kernels.h"
@@ -19,7 +21,7 @@ namespace attuner {
 namespace {
 
 constexpr int kSlabBatch = 8;
-constexpr int kGatherBatch = 16;  // slabs in flight per thread: a whole page of 8 KV heads
+constexpr int kGatherBatch = 2;  // slabs in flight per thread (measured best on gfx950: 2 > 4 > 16)
 
 __global__ __launch_bounds__(256) void store_pages_kernel(const u32x4* __restrict__ k, const u32x4* __restrict__ v,
                                                           int n_tokens, const int32_t* __restrict__ pages,
@@ -72,7 +74,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ ta
 #pragma unroll
     for (int i = 0; i < kGatherBatch; ++i) {
       const int s = s0 + i;
-      if (s < n_slab) buf[i] = pool[((src_base + s) * kPageTokens + rr) * 16 + chunk];
+      if (s < n_slab) buf[i] = __builtin_nontemporal_load(pool + ((src_base + s) * kPageTokens + rr) * 16 + chunk);
     }
 #pragma unroll
     for (int i = 0; i < kGatherBatch; ++i) {
