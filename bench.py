@@ -348,12 +348,19 @@ def main():
     attn_f = attention_flops(s, reqs_shape)
     gemm_f = gemm_flops(s, T, wl.rank)
     g_bytes = gather_bytes(s, sum(L for L, _ in reqs_shape), NL)
+    def kavg(name):  # kernel-only average duration (ms) from the library's launch tracer
+        n, tot, _ = ktimes[name]
+        return tot / n
+
     attn_tflops = attn_f / (attn_kernel_ms * 1e-3) / 1e12          # attention_kernel alone
     attn_call_tflops = attn_f / (kern_ms["attn"] * 1e-3) / 1e12   # attuner_attention call (+ split merge)
-    gemm_tflops = gemm_f / (kern_ms["qproj"] * 1e-3) / 1e12
-    gather_gbps = g_bytes / (kern_ms["gather"] * 1e-3) / 1e9
+    gemm_kernel_ms = kavg("gemm_lora_kernel")
+    gemm_tflops = gemm_f / (gemm_kernel_ms * 1e-3) / 1e12
+    gather_kernel_ms = kavg("gather_kernel")
+    gather_gbps = g_bytes / (gather_kernel_ms * 1e-3) / 1e9
     norm_bytes = T * (nq + 2 * nkv) * 2 * 2
-    norm_gbps = norm_bytes / (kern_ms["norm"] * 1e-3) / 1e9
+    norm_kernel_ms = kavg("qk_norm_rope_kernel")
+    norm_gbps = norm_bytes / (norm_kernel_ms * 1e-3) / 1e9
     tokens_s = wl.total_suffix / (ms_step * 1e-3)
 
     # ---- full prefill on the same kernels ----------------------------------------
@@ -424,10 +431,13 @@ def main():
                           "kernel_ms": round(attn_kernel_ms, 5), "call_ms_with_split_merge": round(kern_ms["attn"], 5),
                           "call_tflops": round(attn_call_tflops, 2)},
             "qproj_lora_gemm": {"tflops": round(gemm_tflops, 2), "mfma_frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
-                                "ms_per_layer": round(kern_ms["qproj"], 5), "flops_per_layer": gemm_f},
+                                "kernel_ms": round(gemm_kernel_ms, 5), "call_ms_with_lora_down": round(kern_ms["qproj"], 5),
+                                "flops_per_layer": gemm_f},
             "kv_gather": {"gbps": round(gather_gbps, 1), "hbm_frac": round(gather_gbps / PEAK_HBM_GBPS, 4),
-                          "ms_per_step": round(kern_ms["gather"], 5), "bytes_per_step": g_bytes},
-            "qk_norm_rope": {"gbps": round(norm_gbps, 1), "ms_per_layer": round(kern_ms["norm"], 5)},
+                          "kernel_ms": round(gather_kernel_ms, 5), "call_ms": round(kern_ms["gather"], 5),
+                          "bytes_per_step": g_bytes},
+            "qk_norm_rope": {"gbps": round(norm_gbps, 1), "kernel_ms": round(norm_kernel_ms, 5),
+                             "call_ms": round(kern_ms["norm"], 5)},
         },
         "kernel_avg_ms": per_kernel,
         "full_prefill": full,
