@@ -8,9 +8,9 @@
 // workgroup of eight waves: the four query heads that share KV head g times
 // two 32-token halves, so every K/V tile staged in LDS serves 256 query rows.
 // K/V tiles (64 keys) are copied global -> LDS by the DMA form of the load
-// (global_load_lds, 16 bytes per lane) into a three-stage ring: while tile i
-// is consumed, tiles i+1 and i+2 are in flight, with no staging registers and
-// one barrier per tile.  Per tile and wave:
+// (global_load_lds, 16 bytes per lane) into a four-stage ring: while tile i
+// is multiplied and tile i - 1 finishes, tiles i+1 and i+2 are in flight, with
+// no staging registers and one barrier per tile.  Per tile and wave:
 //   S^T = K Q^T  (MFMA A = K rows from LDS, B = Q held in registers), so the
 //                accumulator of a lane holds 32 keys of ONE token and the row
 //                max / row sum are in-lane plus one exchange with lane ^ 32;
@@ -19,6 +19,11 @@
 //                tile exceeds it by 2^8, so the O rescale is rare;
 //   O^T += V^T P^T  (MFMA A = V^T, B = P^T straight from the S^T accumulator
 //                converted to bf16 in registers).
+// The loop is software-pipelined inside each wave: QK of tile i is issued
+// next to the exponentials of tile i - 1, and PV of tile i - 1 next to the row
+// max of tile i.  (On gfx950 the MFMA and vector-ALU work of one wave overlap;
+// those of two waves sharing a SIMD were measured not to.)  Tiles reaching
+// the causal diagonal take a plain masked step.
 // The S^T accumulator hands a lane the keys of each 16-key group in the order
 // (4hf + 0..3, 8 + 4hf + 0..3), hf = lane / 32; the V^T operand is read in that
 // same key order with the gfx950 LDS transpose read (ds_read_b64_tr_b16): a
@@ -45,7 +50,7 @@ namespace {
 
 constexpr int BQ = 64;       // suffix tokens per workgroup (two 32-token halves)
 constexpr int BKV = 64;      // keys per tile
-constexpr int NSTAGE = 3;    // K/V tiles resident in LDS: the current one + 2 in flight
+constexpr int NSTAGE = 4;    // K/V tiles in LDS: i - 1 (its PV), i (its QK), i + 1 and i + 2 in flight
 constexpr int D = kHeadDim;
 constexpr int CH = D / 8;    // 16-byte chunks per K/V row
 constexpr int NTHREADS = 512;
@@ -102,6 +107,107 @@ __device__ __forceinline__ void dma_tile(const bf16_t* __restrict__ kb, const bf
       lds_dma16(kb + (int64_t)shift + d.koff[j], k_dst + 1024u * blk);
       lds_dma16(vb + (int64_t)shift + d.voff[j], v_dst + 1024u * blk);
     }
+  }
+}
+
+// ---- per-wave phases of one 64-key tile (32 query rows per wave) -----------
+
+// S^T = K Q^T: MFMA A = K rows from LDS, B = Q in registers; the accumulator
+// of a lane holds keys 32 kh + 8 (v / 4) + 4 hf + v % 4 of ONE token.
+__device__ __forceinline__ void qk_tile(const u32x4* kt, const bf16x8 (&qf)[8], int l32, int hf, f32x16 (&s)[2]) {
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh) {
+    s[kh] = f32x16{};
+    const int row = kh * 32 + l32;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      const bf16x8 a = as_bf16x8(kt[row * CH + ((2 * ks + hf) ^ (row & 15))]);
+      s[kh] = mfma32(a, qf[ks], s[kh]);
+    }
+  }
+}
+
+__device__ __forceinline__ void mask_tile(f32x16 (&s)[2], int kv0, int vis_lim, int hf) {
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int key = kv0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
+      if (key > vis_lim) s[kh][v] = -INFINITY;
+    }
+}
+
+// Row max, lazy reference update (the reference m only moves when the tile
+// max exceeds it by more than 8 in log2 units: l and O accumulate against the
+// same reference, so the result is unchanged and p <= 2^8), l *= alpha, and
+// the scores turned into exponents s * log2(e)/sqrt(d) - m.  Returns alpha.
+__device__ __forceinline__ float max_tile(f32x16 (&s)[2], float sc, float& m_i, float& l_i) {
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kh][v]);
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_tile = mx * sc;
+  const float m_new = m_tile > m_i + 8.0f ? m_tile : m_i;
+  const float m_use = m_new == -INFINITY ? 0.f : m_new;
+  const float alpha = __builtin_amdgcn_exp2f(m_i - m_use);
+  l_i *= alpha;
+  m_i = m_new;
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s[kh][v] = fmaf(s[kh][v], sc, -m_use);
+  return alpha;
+}
+
+// p = 2^(exponent), l += row sum, and the bf16 P^T operand (16-key groups j).
+__device__ __forceinline__ void exp_tile(f32x16 (&s)[2], float& l_i, bf16x8 (&pk)[4]) {
+  float rs = 0.f;
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      s[kh][v] = __builtin_amdgcn_exp2f(s[kh][v]);
+      rs += s[kh][v];
+    }
+  l_i += rs + __shfl_xor(rs, 32, 64);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    u32x4 w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w[e] = pack_bf16x2(s[j >> 1][(j & 1) * 8 + 2 * e], s[j >> 1][(j & 1) * 8 + 2 * e + 1]);
+    pk[j] = as_bf16x8(w);
+  }
+}
+
+// O^T += V^T P^T.  The S^T accumulator hands a lane the keys of each 16-key
+// group in the order (4hf + 0..3, 8 + 4hf + 0..3); V^T is read in that key
+// order with the LDS transpose read.
+__device__ __forceinline__ void pv_tile(const lds_bf16* vt, const bf16x8 (&pk)[4], int hf, int vrow,
+                                        const int (&vcol)[4], f32x16 (&acc)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row_a = 16 * j + 4 * hf + vrow;  // keys 16j + 4hf + 0..3
+    const int row_b = row_a + 8;                // keys 16j + 8 + 4hf + 0..3
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+      const v4i16 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vt + row_a * D + vcol[db]));
+      const v4i16 vbv = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vt + row_b * D + vcol[db]));
+      typedef short v8i16 __attribute__((ext_vector_type(8)));
+      const v8i16 a8 = __builtin_shufflevector(va, vbv, 0, 1, 2, 3, 4, 5, 6, 7);
+      acc[db] = mfma32(__builtin_bit_cast(bf16x8, a8), pk[j], acc[db]);
+    }
+  }
+}
+
+__device__ __forceinline__ void rescale(f32x16 (&acc)[4], float alpha) {
+  if (__any(alpha != 1.0f)) {
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[db][v] *= alpha;
   }
 }
 
@@ -190,115 +296,78 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   const float sc = p.score_scale;
   const int vis_lim = rq.art_len + t;  // last visible key of this row
 
-  if (tb < te) {
-    const uint32_t k_base = lds_addr(k_lds[0]), v_base = lds_addr(v_lds[0]);
-    constexpr uint32_t kStage = BKV * CH * 16;  // bytes per stage of K (and of V)
-    // prologue: tiles tb and tb + 1 in flight
-    const DmaLane dl = dma_lane(wave, lane);
-    dma_tile(kb, vb, tb * BKV, kv_len, k_base, v_base, dl, wave);
-    if (tb + 1 < te) dma_tile(kb, vb, (tb + 1) * BKV, kv_len, k_base + kStage, v_base + kStage, dl, wave);
+  const int mask_from = rq.art_len + t0w;  // tiles ending past this key need the mask
+  // tiles before tp end at or before the diagonal of every row of the wave
+  const int tp = min(max((mask_from + 1) / BKV, tb), te);
 
-    for (int tile = tb; tile < te; ++tile) {
-      const int it = tile - tb;
-      const int cur = it % NSTAGE;
-      // this wave's loads of `tile` done (those of tile + 1, if any, may
-      // still fly), then everyone's: the tile is in LDS, and the buffer of
-      // tile - 1 is free for tile + 2
-      if (tile + 1 < te) __builtin_amdgcn_s_waitcnt(vmcnt_wait(4));
-      else __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
-      barrier_no_fence();
-      if (tile + 2 < te) {
-        const uint32_t nb = (uint32_t)((it + 2) % NSTAGE) * kStage;
-        dma_tile(kb, vb, (tile + 2) * BKV, kv_len, k_base + nb, v_base + nb, dl, wave);
-      }
-      const int kv0 = tile * BKV;
+  const uint32_t k_base = lds_addr(k_lds[0]), v_base = lds_addr(v_lds[0]);
+  constexpr uint32_t kStage = BKV * CH * 16;  // bytes per stage of K (and of V)
+  const DmaLane dl = dma_lane(wave, lane);
+  // prologue: tiles tb and tb + 1 in flight
+  if (tb < te) dma_tile(kb, vb, tb * BKV, kv_len, k_base, v_base, dl, wave);
+  if (tb + 1 < te) dma_tile(kb, vb, (tb + 1) * BKV, kv_len, k_base + kStage, v_base + kStage, dl, wave);
 
-      // ---- S^T = K Q^T --------------------------------------------------
-      // (raised wave priority while issuing MFMAs: the other wave of the SIMD
-      // fills the matrix-core time with its softmax work)
-      f32x16 s[2];
-      __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-      for (int kh = 0; kh < 2; ++kh) {
-        s[kh] = f32x16{};
-        const int row = kh * 32 + l32;
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-          const bf16x8 a = as_bf16x8(k_lds[cur][row * CH + ((2 * ks + hf) ^ (row & 15))]);
-          s[kh] = mfma32(a, qf[ks], s[kh]);
-        }
-      }
-      __builtin_amdgcn_s_setprio(0);
-
-      // ---- mask + online softmax (log2 domain) -----------------------------
-      if (kv0 + BKV - 1 > rq.art_len + t0w) {
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int key = kv0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-            if (key > vis_lim) s[kh][v] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kh][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      // Lazy reference max: keep m_i (and skip the O rescale) unless the tile
-      // max exceeds it by more than 8 in log2 units.  l and O accumulate
-      // against the same reference, so the result is unchanged; p <= 2^8.
-      const float m_tile = mx * sc;
-      const float m_new = m_tile > m_i + 8.0f ? m_tile : m_i;
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_i - m_use);
-      float rs = 0.f;
-#pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(s[kh][v], sc, -m_use));
-          s[kh][v] = e;
-          rs += e;
-        }
-      rs += __shfl_xor(rs, 32, 64);
-      l_i = l_i * alpha + rs;
-      m_i = m_new;
-      if (__any(alpha != 1.0f)) {
-#pragma unroll
-        for (int db = 0; db < 4; ++db)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) acc[db][v] *= alpha;
-      }
-
-      // ---- O^T += V^T P^T -------------------------------------------------
-      bf16x8 pk[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        u32x4 w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          w[e] = pack_bf16x2(s[j >> 1][(j & 1) * 8 + 2 * e], s[j >> 1][(j & 1) * 8 + 2 * e + 1]);
-        pk[j] = as_bf16x8(w);
-      }
-      const lds_bf16* vbase = (const lds_bf16*)(v_lds[cur]);
-      __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row_a = 16 * j + 4 * hf + vrow;  // keys 16j + 4hf + 0..3
-        const int row_b = row_a + 8;                // keys 16j + 8 + 4hf + 0..3
-#pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          const v4i16 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vbase + row_a * D + vcol[db]));
-          const v4i16 vbv = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vbase + row_b * D + vcol[db]));
-          typedef short v8i16 __attribute__((ext_vector_type(8)));
-          const v8i16 a8 = __builtin_shufflevector(va, vbv, 0, 1, 2, 3, 4, 5, 6, 7);
-          acc[db] = mfma32(__builtin_bit_cast(bf16x8, a8), pk[j], acc[db]);
-        }
-      }
-      __builtin_amdgcn_s_setprio(0);
+  // Start of tile `tile`: this wave's copies of it done (those of tile + 1,
+  // if any, may still fly), then everyone's; the stage of tile - 2 is free
+  // and receives tile + 2.
+  auto tile_sync = [&](int tile) __attribute__((always_inline)) {
+    if (tile + 1 < te) __builtin_amdgcn_s_waitcnt(vmcnt_wait(4));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+    barrier_no_fence();
+    if (tile + 2 < te) {
+      const uint32_t nb = (uint32_t)((tile - tb + 2) & (NSTAGE - 1)) * kStage;
+      dma_tile(kb, vb, (tile + 2) * BKV, kv_len, k_base + nb, v_base + nb, dl, wave);
     }
+  };
+  auto kst = [&](int tile) __attribute__((always_inline)) { return k_lds[(tile - tb) & (NSTAGE - 1)]; };
+  auto vst = [&](int tile) __attribute__((always_inline)) {
+    return (const lds_bf16*)v_lds[(tile - tb) & (NSTAGE - 1)];
+  };
+
+  // Unmasked tiles, software-pipelined inside the wave: QK of `tile` is
+  // issued alongside the exponentials of tile - 1, and PV of tile - 1
+  // alongside the row max of `tile` (MFMA and vector-ALU work of one wave
+  // overlap on gfx950; those of two waves sharing a SIMD do not).  S^T
+  // alternates between sa and sb.
+  if (tb < tp) {
+    f32x16 sa[2], sb[2];
+    bf16x8 pk[4];
+    tile_sync(tb);
+    qk_tile(kst(tb), qf, l32, hf, sa);
+    max_tile(sa, sc, m_i, l_i);
+    auto step = [&](f32x16 (&sn)[2], f32x16 (&so)[2], int tile) __attribute__((always_inline)) {
+      tile_sync(tile);
+      qk_tile(kst(tile), qf, l32, hf, sn);
+      exp_tile(so, l_i, pk);
+      pv_tile(vst(tile - 1), pk, hf, vrow, vcol, acc);
+      const float alpha = max_tile(sn, sc, m_i, l_i);
+      rescale(acc, alpha);  // after PV(tile - 1), before PV(tile)
+    };
+    int tile = tb + 1;
+    for (; tile + 1 < tp; tile += 2) {
+      step(sb, sa, tile);
+      step(sa, sb, tile + 1);
+    }
+    if (tile < tp) {
+      step(sb, sa, tile);
+      exp_tile(sb, l_i, pk);
+    } else {
+      exp_tile(sa, l_i, pk);
+    }
+    pv_tile(vst(tp - 1), pk, hf, vrow, vcol, acc);
+  }
+
+  // tiles reaching the diagonal: plain masked steps
+  for (int tile = tp; tile < te; ++tile) {
+    f32x16 s[2];
+    bf16x8 pk[4];
+    tile_sync(tile);
+    const int kv0 = tile * BKV;
+    qk_tile(kst(tile), qf, l32, hf, s);
+    if (kv0 + BKV - 1 > mask_from) mask_tile(s, kv0, vis_lim, hf);
+    rescale(acc, max_tile(s, sc, m_i, l_i));
+    exp_tile(s, l_i, pk);
+    pv_tile(vst(tile), pk, hf, vrow, vcol, acc);
   }
 
   const float inv_l = l_i > 0.f ? 1.0f / l_i : 0.f;
