@@ -185,7 +185,8 @@ attuner_status attuner_qproj_lora(attuner_ctx* ctx, int32_t n_tok, const void* x
  * rope pairs dimension j with j + 64 and turns it by (pos) * theta^(-2j/128)
  * (angles from an fp64 host table, stored fp32).
  * q_raw: device, row stride ld_q, Hq*d columns; k_raw, v_raw: device, row
- * stride ld_kv, Hkv*d columns; gamma_q, gamma_k: device [head_dim].
+ * stride ld_kv, Hkv*d columns; gamma_q, gamma_k: device [head_dim].  All five
+ * 16-byte aligned and ld_q, ld_kv multiples of 8 (else ATTUNER_EINVAL).
  * q_hat: device [T_q][Hq][d].  k_hat and v of request r's token i are written
  * to cache row cu_ctx[r] + art_len[r] + i of layer `layer` of req_kv
  * (layout of attuner_assemble_kv).  Requires art_len[r] + (cu_q[r+1] -
@@ -234,7 +235,8 @@ attuner_status attuner_suffix_attn(attuner_ctx* ctx, int32_t layer, int32_t n_re
  * o: device [n_tok][Hq][d]; k_out, v_out: device [n_kv_heads][n_tok][d]
  * (normalised/rotated keys and raw values: with pos0 = 0 on an artifact
  * alone, the K/V attuner_store_artifact expects for one layer);
- * lse: device [n_tok][Hq] fp32 or NULL.  Uses context workspaces.
+ * lse: device [n_tok][Hq] fp32 or NULL.  o, k_out, v_out, gamma_q and gamma_k
+ * must be 16-byte aligned (else ATTUNER_EINVAL).  Uses context workspaces.
  * ------------------------------------------------------------------------ */
 attuner_status attuner_full_prefill(attuner_ctx* ctx, int32_t n_tok, int32_t pos0, const void* x,
                                     const void* wqkv, const void* a, const void* b, int32_t rank,

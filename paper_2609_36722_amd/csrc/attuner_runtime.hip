@@ -643,6 +643,9 @@ static attuner_status check_norm_args(const void* q_raw, int64_t ld_q, const voi
                                       int64_t ld_kv, const void* gamma_q, const void* gamma_k, const attuner_ctx* c) {
   if (!q_raw || !k_raw || !v_raw || !gamma_q || !gamma_k) return fail(ATTUNER_EINVAL, "null q/k/v or gamma");
   if (ld_q < q_dim(c) || ld_kv < kv_dim(c)) return fail(ATTUNER_EINVAL, "ld_q %lld / ld_kv %lld too small", (long long)ld_q, (long long)ld_kv);
+  if (ld_q % 8 != 0 || ld_kv % 8 != 0 || !aligned16(q_raw) || !aligned16(k_raw) || !aligned16(v_raw) ||
+      !aligned16(gamma_q) || !aligned16(gamma_k))
+    return fail(ATTUNER_EINVAL, "q/k/v rows (ld_q, ld_kv multiples of 8) and gamma must be 16-byte aligned");
   return ATTUNER_OK;
 }
 
@@ -725,7 +728,8 @@ attuner_status attuner_full_prefill(attuner_ctx* c, int32_t n_tok, int32_t pos0,
   if (n_tok < 0 || pos0 < 0) return fail(ATTUNER_EINVAL, "negative n_tok or pos0");
   if (n_tok == 0) return ATTUNER_OK;
   if (!gamma_q || !gamma_k || !o || !k_out || !v_out) return fail(ATTUNER_EINVAL, "null gamma or output");
-  if (!aligned16(o) || !aligned16(k_out) || !aligned16(v_out)) return fail(ATTUNER_EINVAL, "outputs must be 16-byte aligned");
+  if (!aligned16(o) || !aligned16(k_out) || !aligned16(v_out) || !aligned16(gamma_q) || !aligned16(gamma_k))
+    return fail(ATTUNER_EINVAL, "outputs and gamma must be 16-byte aligned");
   DeviceGuard dg(c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nq = q_dim(c), nkv = kv_dim(c), n_out = nq + 2 * nkv;

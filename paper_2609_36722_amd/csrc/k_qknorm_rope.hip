@@ -2,11 +2,13 @@
 // query passes through the model's own query normalisation and RoPE), and the
 // write of the suffix keys and values into their request-cache rows.
 //
-// One wave per (token, head slot); slots 0..Hq-1 are query heads, Hq..Hq+Hkv-1
-// are KV heads (normalise + rotate k, copy v).  Lane j holds the rotary pair
-// (j, j + 64) of the head, so the rotation needs no data exchange and the
-// RMS is one wave reduction.  Angles come from a host-built table of
-// (cos, sin) of pos * theta^(-2j/128), evaluated in fp64 and stored fp32.
+// Eight lanes per (token, head slot); slots 0..Hq-1 are query heads,
+// Hq..Hq+Hkv-1 are KV heads (normalise + rotate k, copy v).  Lane j of a group
+// holds dimensions 8j..8j+7 and their rotary partners 64+8j..64+8j+7 (two
+// 16-byte loads), so the rotation needs no data exchange and the RMS is an
+// in-lane sum plus three exchanges within the group.  Angles come from a
+// host-built table of (cos, sin) of pos * theta^(-2j/128), evaluated in fp64
+// and stored fp32.  Rows, gamma and outputs are 16-byte aligned.
 
 #include "common.h"
 #include "kernels.h"
@@ -16,12 +18,12 @@ namespace attuner {
 namespace {
 
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
-  const int lane = threadIdx.x & 63;
-  const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane8 = threadIdx.x & 7;
+  const int64_t grp = (int64_t)blockIdx.x * 32 + (threadIdx.x >> 3);
   const int n_slots = p.n_q_heads + p.n_kv_heads;
-  const int tok = (int)(wid / n_slots);
-  const int slot = (int)(wid - (int64_t)tok * n_slots);
-  if (tok >= p.total_q) return;
+  const int tok = (int)(grp / n_slots);
+  const int slot = (int)(grp - (int64_t)tok * n_slots);
+  if (tok >= p.total_q) return;  // whole 8-lane groups leave together
 
   int r = 0;
   while (r + 1 < p.n_req && tok >= p.req[r + 1].q_start) ++r;
@@ -36,22 +38,55 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
   const bf16_t* gam = is_q ? p.gamma_q : p.gamma_k;
   bf16_t* dst = is_q ? p.q_hat + ((int64_t)tok * p.n_q_heads + slot) * kHeadDim
                      : p.k_cache + g * p.kv_head_stride + (int64_t)(rq.kv_row0 + i) * kHeadDim;
+  const int j0 = 8 * lane8;
 
-  const float x0 = bf16_to_f32(src[lane]);
-  const float x1 = bf16_to_f32(src[lane + 64]);
-  const float ms = wave_sum(x0 * x0 + x1 * x1) * (1.0f / kHeadDim);
-  const float inv = 1.0f / sqrtf(ms + p.eps);
-  const float y0 = x0 * inv * bf16_to_f32(gam[lane]);
-  const float y1 = x1 * inv * bf16_to_f32(gam[lane + 64]);
-  const float2 cs = p.rope[(int64_t)pos * 64 + lane];
-  dst[lane] = f32_to_bf16(y0 * cs.x - y1 * cs.y);
-  dst[lane + 64] = f32_to_bf16(y1 * cs.x + y0 * cs.y);
+  const u32x4 xa = *reinterpret_cast<const u32x4*>(src + j0);
+  const u32x4 xb = *reinterpret_cast<const u32x4*>(src + 64 + j0);
+  const u32x4 ga = *reinterpret_cast<const u32x4*>(gam + j0);
+  const u32x4 gb = *reinterpret_cast<const u32x4*>(gam + 64 + j0);
+  float x0[8], x1[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x0[2 * e] = __uint_as_float(xa[e] << 16);
+    x0[2 * e + 1] = __uint_as_float(xa[e] & 0xFFFF0000u);
+    x1[2 * e] = __uint_as_float(xb[e] << 16);
+    x1[2 * e + 1] = __uint_as_float(xb[e] & 0xFFFF0000u);
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ss += x0[e] * x0[e] + x1[e] * x1[e];
+  ss += __shfl_xor(ss, 1, 8);
+  ss += __shfl_xor(ss, 2, 8);
+  ss += __shfl_xor(ss, 4, 8);
+  const float inv = 1.0f / sqrtf(ss * (1.0f / kHeadDim) + p.eps);
+  const f32x4* cs4 = reinterpret_cast<const f32x4*>(p.rope + (int64_t)pos * 64 + j0);
+  u32x4 oa, ob;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const f32x4 cs = cs4[e];  // (cos, sin) of pairs j0 + 2e and j0 + 2e + 1
+    float o0[2], o1[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int k = 2 * e + u;
+      const float g0 = __uint_as_float(u ? (ga[e] & 0xFFFF0000u) : (ga[e] << 16));
+      const float g1 = __uint_as_float(u ? (gb[e] & 0xFFFF0000u) : (gb[e] << 16));
+      const float y0 = x0[k] * inv * g0;
+      const float y1 = x1[k] * inv * g1;
+      const float c = cs[2 * u], sn = cs[2 * u + 1];
+      o0[u] = y0 * c - y1 * sn;
+      o1[u] = y1 * c + y0 * sn;
+    }
+    oa[e] = pack_bf16x2(o0[0], o0[1]);
+    ob[e] = pack_bf16x2(o1[0], o1[1]);
+  }
+  *reinterpret_cast<u32x4*>(dst + j0) = oa;
+  *reinterpret_cast<u32x4*>(dst + 64 + j0) = ob;
 
   if (!is_q) {
     const bf16_t* vs = p.v_raw + (int64_t)tok * p.ld_kv + g * kHeadDim;
     bf16_t* vd = p.v_cache + g * p.kv_head_stride + (int64_t)(rq.kv_row0 + i) * kHeadDim;
-    vd[lane] = vs[lane];
-    vd[lane + 64] = vs[lane + 64];
+    *reinterpret_cast<u32x4*>(vd + j0) = *reinterpret_cast<const u32x4*>(vs + j0);
+    *reinterpret_cast<u32x4*>(vd + 64 + j0) = *reinterpret_cast<const u32x4*>(vs + 64 + j0);
   }
 }
 
@@ -59,8 +94,9 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
 
 hipError_t launch_qk_norm_rope(const NormRopeParams& p, hipStream_t stream) {
   if (p.total_q == 0) return hipSuccess;
-  const int64_t waves = (int64_t)p.total_q * (p.n_q_heads + p.n_kv_heads);
-  ATTUNER_LAUNCH("qk_norm_rope_kernel", qk_norm_rope_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), stream, p);
+  const int64_t groups = (int64_t)p.total_q * (p.n_q_heads + p.n_kv_heads);  // 8 lanes each
+  ATTUNER_LAUNCH("qk_norm_rope_kernel", qk_norm_rope_kernel, dim3((unsigned)((groups + 31) / 32)), dim3(256), stream,
+                 p);
   return hipGetLastError();
 }
 
