@@ -292,21 +292,27 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
                             uint16_t* out, hipStream_t stream) {
   if (n_tok == 0) return hipSuccess;
   const int n_slice = lora_down_slices(hidden);
-  // Tile choice (measured on gfx950, hidden 2560, 6144 outputs): 128 x 256
-  // tiles with eight waves once they give >= 128 workgroups (the fewest
-  // ingested bytes; large batches); else 64 x 96 tiles when n_out allows and
-  // they give >= 128 workgroups (256 at a 256-token suffix); else 64 x 64
-  // (tiny suffixes: more workgroups pulling the weight stream).
-  const int n_mt128 = (n_tok + 127) / 128;
-  const int n_mt64 = (n_tok + 63) / 64;
+  // Tile choice: the largest tile (fewest ingested bytes, M N K 2 (1/BM +
+  // 1/BN)) that still gives at least 180 workgroups for the 256 CUs, in the
+  // order 256x256, 128x256, 128x128, 64x96, 64x64 (tokens x features; measured
+  // on gfx950 at hidden 2560/4096 with 6144 outputs: T = 8448 -> 256x256,
+  // 1024 -> 128x256, 512 -> 128x128, 256 -> 64x96, 64 -> 64x64).
+  auto wgs = [&](int bm, int bn) -> int64_t {
+    return n_out % bn != 0 ? 0 : (int64_t)((n_tok + bm - 1) / bm) * (n_out / bn);
+  };
+  constexpr int64_t kMinWgs = 180;
 #define ATTUNER_GEMM(BM_, BN_, WN_, WM_, NST_)                                                               \
   ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, WM_, NST_>),                           \
                  dim3(((n_tok + (BM_) - 1) / (BM_)) * (n_out / (BN_))), dim3(64 * (WN_) * (WM_)), stream, x, w, \
                  n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, (n_tok + (BM_) - 1) / (BM_), \
                  n_out / (BN_))
-  if (n_out % 256 == 0 && (int64_t)n_mt128 * (n_out / 256) >= 128) {
+  if (wgs(256, 256) >= kMinWgs) {
+    ATTUNER_GEMM(256, 256, 2, 4, 2);
+  } else if (wgs(128, 256) >= kMinWgs) {
     ATTUNER_GEMM(128, 256, 4, 2, 3);
-  } else if (n_out % 96 == 0 && (int64_t)n_mt64 * (n_out / 96) >= 128) {
+  } else if (wgs(128, 128) >= kMinWgs) {
+    ATTUNER_GEMM(128, 128, 2, 2, 4);
+  } else if (wgs(64, 96) >= kMinWgs) {
     ATTUNER_GEMM(64, 96, 3, 2, 5);
   } else {
     ATTUNER_GEMM(64, 64, 2, 2, 6);
