@@ -409,8 +409,10 @@ attuner_status qproj_impl(attuner_ctx* c, int32_t n_tok, const void* x, const vo
     return fail(ATTUNER_EINVAL, "x, w, a and out must be 16-byte aligned");
   const int hidden = c->cfg.hidden;
   const int r_pad = rank > 0 && lora_cols > 0 ? (rank + 15) / 16 * 16 : 0;
+  // ranks up to kGemmFusedLoraMaxRank: the GEMM computes t = scale * x A^T
+  // itself; larger ranks take a separate down-projection kernel first
   float* t_part = nullptr;
-  if (r_pad > 0) {
+  if (r_pad > kGemmFusedLoraMaxRank) {
     const size_t part_bytes = (size_t)lora_down_slices(hidden) * n_tok * r_pad * sizeof(float);
     HIP_TRY(c->ws_lora.ensure(part_bytes));
     t_part = static_cast<float*>(c->ws_lora.ptr);
@@ -418,8 +420,8 @@ attuner_status qproj_impl(attuner_ctx* c, int32_t n_tok, const void* x, const vo
                              r_pad, scale, t_part, stream));
   }
   HIP_TRY(launch_gemm_lora(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), n_tok, n_out, hidden,
-                           static_cast<const uint16_t*>(b), rank, r_pad, lora_cols, t_part,
-                           static_cast<uint16_t*>(out), stream));
+                           static_cast<const uint16_t*>(a), scale, static_cast<const uint16_t*>(b), rank, r_pad,
+                           lora_cols, t_part, static_cast<uint16_t*>(out), stream));
   return ATTUNER_OK;
 }
 

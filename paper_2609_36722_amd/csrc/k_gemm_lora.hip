@@ -21,6 +21,8 @@
 // in fp32.  lora_down_kernel leaves t as fp32 partial sums over 256-wide
 // slices of the hidden dimension; the epilogue adds the slices in order.
 
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -31,6 +33,7 @@ namespace {
 constexpr int BK = 64;
 constexpr int kChunksPerRow = BK / 8;  // 16-byte chunks per LDS row
 constexpr int kLoraSlice = 256;        // hidden elements per lora_down workgroup
+constexpr int kLoraRows = 32;          // A rows staged per k-tile when the down-projection is fused
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
@@ -39,23 +42,34 @@ __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >>
 // holds features nb + 8q + 4*hi + (0..3) of token m).  n_base / m_base: the
 // wave tile's first feature / token.
 template <int FN, int FM>
-__device__ __forceinline__ void lora_epilogue_store(f32x16 (&acc)[FN][FM], int n_base, int m_base, int l32, int hi,
-                                                    int M, int N, const bf16_t* __restrict__ b, int rank, int r_pad,
-                                                    int lora_cols, const float* __restrict__ t_part, int n_slice,
-                                                    bf16_t* __restrict__ out) {
+__device__ __forceinline__ void lora_epilogue_store(f32x16 (&acc)[FN][FM], int n_base, int m_base, int ml_base,
+                                                    int l32, int hi, int M, int N, const bf16_t* __restrict__ b,
+                                                    int rank, int r_pad, int lora_cols,
+                                                    const float* __restrict__ t_part, int n_slice,
+                                                    const float* t_lds, bf16_t* __restrict__ out) {
   if (r_pad > 0 && n_base < lora_cols) {
     const int64_t slice_stride = (int64_t)M * r_pad;
     for (int ks = 0; ks < r_pad; ks += 16) {
       bf16x8 th[FM], tl[FM];
 #pragma unroll
       for (int j = 0; j < FM; ++j) {
-        int m = m_base + j * 32 + l32;
-        m = m < M ? m : M - 1;
-        const float* tp = t_part + (int64_t)m * r_pad + ks + 8 * hi;
         f32x4 s0 = f32x4{}, s1 = f32x4{};
-        for (int z = 0; z < n_slice; ++z) {
-          s0 += *reinterpret_cast<const f32x4*>(tp + z * slice_stride);
-          s1 += *reinterpret_cast<const f32x4*>(tp + z * slice_stride + 4);
+        if (t_lds != nullptr) {
+          // fused: t[token][rank] staged in LDS by this workgroup
+          const float* tr = t_lds + (ml_base + j * 32 + l32) * (kLoraRows + 1) + ks + 8 * hi;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            s0[e] = tr[e];
+            s1[e] = tr[4 + e];
+          }
+        } else {
+          int m = m_base + j * 32 + l32;
+          m = m < M ? m : M - 1;
+          const float* tp = t_part + (int64_t)m * r_pad + ks + 8 * hi;
+          for (int z = 0; z < n_slice; ++z) {
+            s0 += *reinterpret_cast<const f32x4*>(tp + z * slice_stride);
+            s1 += *reinterpret_cast<const f32x4*>(tp + z * slice_stride + 4);
+          }
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -116,6 +130,7 @@ __device__ __forceinline__ void lora_epilogue_store(f32x16 (&acc)[FN][FM], int n
 template <int BM, int BN, int WN, int WM, int NST>
 __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t* __restrict__ x,
                                                                    const bf16_t* __restrict__ w, int M, int N, int K,
+                                                                   const bf16_t* __restrict__ a, float scale,
                                                                    const bf16_t* __restrict__ b, int rank, int r_pad,
                                                                    int lora_cols, const float* __restrict__ t_part,
                                                                    int n_slice, bf16_t* __restrict__ out, int n_mt,
@@ -124,12 +139,12 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
   constexpr int TN = BN / WN, TM = BM / WM;
   constexpr int FN = TN / 32, FM = TM / 32;
   static_assert(FN >= 1 && FM >= 1 && TN % 32 == 0 && TM % 32 == 0, "bad wave layout");
-  constexpr int ROWS = BN + BM;
-  static_assert(ROWS % 8 == 0, "stage must be whole 1 KiB blocks");
-  constexpr int NBLK = ROWS / 8;
-  constexpr int PW = (NBLK + NW - 1) / NW;  // DMA instructions per wave per stage
+  // stage rows: W rows [0, BN), x rows [BN, BN + BM), and (fused LoRA) the
+  // kLoraRows rows of A [BN + BM, BN + BM + kLoraRows)
+  constexpr int ROWS = BN + BM + kLoraRows;
+  static_assert((BN + BM) % 8 == 0, "stage must be whole 1 KiB blocks");
   constexpr int STAGE = ROWS * kChunksPerRow;
-  static_assert((NST - 2) * PW <= 63, "vmcnt range");
+  static_assert(BM * (kLoraRows + 1) * 4 <= STAGE * 16, "t staging must fit one stage");
   __shared__ u32x4 lds[NST * STAGE];
 
   const int total = n_mt * n_nt;
@@ -147,35 +162,8 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
   const int wm = wave % WM;
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-
-  // DMA sources of this lane (blocks past the stage repeat the last block:
-  // same bytes to the same place)
   const int n_kt = K / BK;
-  const bf16_t* src[PW];
-  uint32_t doff[PW];
-#pragma unroll
-  for (int j = 0; j < PW; ++j) {
-    const int blk = min(wave + NW * j, NBLK - 1);
-    const int row = 8 * blk + (lane >> 3);
-    const int lg = swz(row, lane & 7);
-    const bf16_t* base;
-    if (row < BN) {
-      base = w + (int64_t)(n0 + row) * K;
-    } else {
-      const int m = min(m0 + row - BN, M - 1);  // rows past the end are computed, never stored
-      base = x + (int64_t)m * K;
-    }
-    src[j] = base + 8 * lg;
-    doff[j] = 1024u * blk;
-  }
   const uint32_t lds0 = lds_addr(lds);
-
-#pragma unroll
-  for (int s = 0; s < NST - 1; ++s) {
-    const int kt = min(s, n_kt - 1);
-#pragma unroll
-    for (int j = 0; j < PW; ++j) lds_dma16(src[j] + kt * BK, lds0 + (uint32_t)(s * STAGE * 16) + doff[j]);
-  }
 
   f32x16 acc[FN][FM];
 #pragma unroll
@@ -183,44 +171,116 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
 #pragma unroll
     for (int j = 0; j < FM; ++j) acc[i][j] = f32x16{};
 
-  int slot = 0, nslot = NST - 1;
-  for (int kt = 0; kt < n_kt; ++kt) {
-    // own copies of tile kt done, then everyone's; slot nslot (tile kt - 1) is free
-    __builtin_amdgcn_s_waitcnt(vmcnt_wait((NST - 2) * PW));
-    barrier_no_fence();
-    const int nk = min(kt + NST - 1, n_kt - 1);
+  // Fused down-projection (t_part == null): this workgroup needs t for its
+  // tokens, so the k-loop also stages A's rows and the waves with wn == 0
+  // accumulate t^T = A x^T next to their main MFMAs (the x fragments are
+  // shared).  t then goes through LDS to the epilogue.
+  const bool fused = t_part == nullptr && r_pad > 0 && n0 < lora_cols;
+  f32x16 tacc[FM];
 #pragma unroll
-    for (int j = 0; j < PW; ++j) lds_dma16(src[j] + nk * BK, lds0 + (uint32_t)(nslot * STAGE * 16) + doff[j]);
+  for (int j = 0; j < FM; ++j) tacc[j] = f32x16{};
 
-    const u32x4* cur = lds + slot * STAGE;
+  auto kloop = [&](auto la_tag) __attribute__((always_inline)) {
+    constexpr bool LA = decltype(la_tag)::value;
+    constexpr int NBLK = (BN + BM + (LA ? kLoraRows : 0)) / 8;
+    constexpr int PW = (NBLK + NW - 1) / NW;  // DMA instructions per wave per stage
+    static_assert((NST - 2) * PW <= 63, "vmcnt range");
+    // DMA sources of this lane (blocks past the stage repeat the last block:
+    // same bytes to the same place)
+    const bf16_t* src[PW];
+    uint32_t doff[PW];
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int ch = 2 * ks + hi;
-      bf16x8 af[FN], bfr[FM];
-#pragma unroll
-      for (int i = 0; i < FN; ++i) {
-        const int row = wn * TN + i * 32 + l32;
-        af[i] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+    for (int j = 0; j < PW; ++j) {
+      const int blk = min(wave + NW * j, NBLK - 1);
+      const int row = 8 * blk + (lane >> 3);
+      const int lg = swz(row, lane & 7);
+      const bf16_t* base;
+      if (row < BN) {
+        base = w + (int64_t)(n0 + row) * K;
+      } else if (row < BN + BM) {
+        const int m = min(m0 + row - BN, M - 1);  // rows past the end are computed, never stored
+        base = x + (int64_t)m * K;
+      } else {
+        // A rows past rank repeat row rank - 1: finite, and met by zero B columns
+        base = a + (int64_t)min(row - BN - BM, rank - 1) * K;
       }
+      src[j] = base + 8 * lg;
+      doff[j] = 1024u * blk;
+    }
+#pragma unroll
+    for (int st = 0; st < NST - 1; ++st) {
+      const int kt = min(st, n_kt - 1);
+#pragma unroll
+      for (int j = 0; j < PW; ++j) lds_dma16(src[j] + kt * BK, lds0 + (uint32_t)(st * STAGE * 16) + doff[j]);
+    }
+    const bool t_wave = LA && wn == 0;
+    int slot = 0, nslot = NST - 1;
+    for (int kt = 0; kt < n_kt; ++kt) {
+      // own copies of tile kt done, then everyone's; slot nslot (tile kt - 1) is free
+      __builtin_amdgcn_s_waitcnt(vmcnt_wait((NST - 2) * PW));
+      barrier_no_fence();
+      const int nk = min(kt + NST - 1, n_kt - 1);
+#pragma unroll
+      for (int j = 0; j < PW; ++j) lds_dma16(src[j] + nk * BK, lds0 + (uint32_t)(nslot * STAGE * 16) + doff[j]);
+
+      const u32x4* cur = lds + slot * STAGE;
+#pragma unroll
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        const int ch = 2 * ks + hi;
+        bf16x8 af[FN], bfr[FM];
+#pragma unroll
+        for (int i = 0; i < FN; ++i) {
+          const int row = wn * TN + i * 32 + l32;
+          af[i] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+        }
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+          const int row = BN + wm * TM + j * 32 + l32;
+          bfr[j] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+        }
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+          for (int j = 0; j < FM; ++j) acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
+        if (t_wave) {
+          const int row = BN + BM + l32;
+          const bf16x8 ar = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+#pragma unroll
+          for (int j = 0; j < FM; ++j) tacc[j] = mfma32(ar, bfr[j], tacc[j]);
+        }
+      }
+      slot = slot + 1 == NST ? 0 : slot + 1;
+      nslot = nslot + 1 == NST ? 0 : nslot + 1;
+    }
+    // the clamped copies of the last iterations must land before the LDS is
+    // reused or the workgroup ends (its LDS may be handed to the next one)
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+  };
+
+  const float* t_lds = nullptr;
+  if (fused) {
+    kloop(std::integral_constant<bool, true>{});
+    // t^T accumulator: lane holds ranks 8 (v / 4) + 4 hi + v % 4 of token
+    // l32 of each 32-token block; staged as fp32 t[token][rank], row stride
+    // kLoraRows + 1
+    float* ts = reinterpret_cast<float*>(lds);
+    barrier_no_fence();
+    if (wn == 0) {
 #pragma unroll
       for (int j = 0; j < FM; ++j) {
-        const int row = BN + wm * TM + j * 32 + l32;
-        bfr[j] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+        const int ml = wm * TM + j * 32 + l32;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) ts[ml * (kLoraRows + 1) + 8 * (v >> 2) + 4 * hi + (v & 3)] = scale * tacc[j][v];
       }
-#pragma unroll
-      for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
     }
-    slot = slot + 1 == NST ? 0 : slot + 1;
-    nslot = nslot + 1 == NST ? 0 : nslot + 1;
+    __syncthreads();
+    t_lds = ts;
+  } else {
+    kloop(std::integral_constant<bool, false>{});
   }
-  // the clamped copies of the last iterations must land before the workgroup
-  // ends (its LDS may be handed to the next workgroup)
-  __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
 
-  lora_epilogue_store<FN, FM>(acc, n0 + wn * TN, m0 + wm * TM, l32, hi, M, N, b, rank, r_pad, lora_cols, t_part,
-                              n_slice, out);
+  lora_epilogue_store<FN, FM>(acc, n0 + wn * TN, m0 + wm * TM, wm * TM, l32, hi, M, N, b, rank, r_pad, lora_cols,
+                              t_part, n_slice, t_lds, out);
 }
 
 // t = scale * x A^T with MFMAs, as fp32 partial sums per 256-wide slice of the
@@ -288,8 +348,8 @@ hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int
 }
 
 hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
-                            const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
-                            uint16_t* out, hipStream_t stream) {
+                            const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad, int lora_cols,
+                            const float* t_part, uint16_t* out, hipStream_t stream) {
   if (n_tok == 0) return hipSuccess;
   const int n_slice = lora_down_slices(hidden);
   // Tile choice: the largest tile (fewest ingested bytes, M N K 2 (1/BM +
@@ -304,8 +364,8 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
 #define ATTUNER_GEMM(BM_, BN_, WN_, WM_, NST_)                                                               \
   ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, WM_, NST_>),                           \
                  dim3(((n_tok + (BM_) - 1) / (BM_)) * (n_out / (BN_))), dim3(64 * (WN_) * (WM_)), stream, x, w, \
-                 n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, n_slice, out, (n_tok + (BM_) - 1) / (BM_), \
-                 n_out / (BN_))
+                 n_tok, n_out, hidden, a, scale, b, rank, r_pad, lora_cols, t_part, n_slice, out,                  \
+                 (n_tok + (BM_) - 1) / (BM_), n_out / (BN_))
   if (wgs(256, 256) >= kMinWgs) {
     ATTUNER_GEMM(256, 256, 2, 4, 2);
   } else if (wgs(128, 256) >= kMinWgs) {

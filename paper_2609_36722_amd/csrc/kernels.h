@@ -47,11 +47,14 @@ int lora_down_slices(int hidden);
 hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int hidden, int rank, int r_pad,
                             float scale, float* t_part, hipStream_t stream);
 
-// out[i][n] = x[i] . w[n] + (n < lora_cols ? t[i] . b[n] : 0) with t the sum
-// of the slices of t_part (r_pad = 0: no adapter).
+// out[i][n] = x[i] . w[n] + (n < lora_cols ? t[i] . b[n] : 0) (r_pad = 0: no
+// adapter).  t is the sum of the slices of t_part when t_part is given;
+// with t_part null (and r_pad <= kGemmFusedLoraMaxRank) the kernel computes
+// t = scale * x a^T itself.
+constexpr int kGemmFusedLoraMaxRank = 32;
 hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
-                            const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
-                            uint16_t* out, hipStream_t stream);
+                            const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad, int lora_cols,
+                            const float* t_part, uint16_t* out, hipStream_t stream);
 
 // ---- a4: QK-RMSNorm + RoPE ------------------------------------------------
 
