@@ -62,51 +62,54 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void glb_void;
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-// Per-lane source offsets (elements within a 64-key tile) of the K/V tile
-// DMA.  Wave w moves 1 KiB blocks w and w + 8 of each 16 KiB tile; lane i of
-// a block lands at byte 16 i of it, i.e. row 4 * block + i / 16, physical
-// chunk i % 16, so the lane fetches the logical chunk the swizzle maps there
-// (K: chunk ^ (row & 15), V: chunk ^ 4 (row & 3)).
+// One 16-byte-per-lane global -> LDS copy with a wave-uniform 64-bit base in
+// SGPRs and a per-lane 32-bit byte offset (the saddr form): the offsets stay
+// fixed from tile to tile, only the scalar base moves.
+__device__ __forceinline__ void lds_dma16_s(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      :
+      : "v"(voff), "s"(sbase), "s"(lds_base)
+      : "memory");
+}
+
+// Per-lane byte offsets (within a 64-key tile) of the K/V tile DMA.  Wave w
+// moves 1 KiB blocks w and w + 8 of each 16 KiB tile; lane i of a block lands
+// at byte 16 i of it, i.e. row 4 * block + i / 16, physical chunk i % 16, so
+// the lane fetches the logical chunk the swizzle maps there (K: chunk ^
+// (row & 15), V: chunk ^ 4 (row & 3); the same for both blocks of a lane).
 struct DmaLane {
-  int row[2];
-  int koff[2], voff[2];
+  int row0;                 // tile row of block w (block w + 8: row0 + 32)
+  uint32_t kchunk, vchunk;  // byte offset of the fetched chunk within its row
 };
 
 __device__ __forceinline__ DmaLane dma_lane(int wave, int lane) {
   DmaLane d;
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int blk = wave + 8 * j;
-    const int row = 4 * blk + (lane >> 4);
-    const int phys = lane & 15;
-    d.row[j] = row;
-    d.koff[j] = row * D + 8 * (phys ^ (row & 15));
-    d.voff[j] = row * D + 8 * (phys ^ ((row & 3) << 2));
-  }
+  d.row0 = 4 * wave + (lane >> 4);
+  const int phys = lane & 15;
+  d.kchunk = 16u * (phys ^ (d.row0 & 15));
+  d.vchunk = 16u * (phys ^ ((d.row0 & 3) << 2));
   return d;
 }
 
 // Issue the DMA of one 64-key K and V tile (keys kv0 .. kv0+63 of the
 // request; rows past kv_len - 1 re-read row kv_len - 1, whose values the mask
 // discards) straight into LDS.  Exactly 4 loads per wave per tile.
-__device__ __forceinline__ void dma_tile(const bf16_t* __restrict__ kb, const bf16_t* __restrict__ vb, int kv0,
-                                         int kv_len, uint32_t k_dst, uint32_t v_dst, const DmaLane& d, int wave) {
-  if (kv0 + BKV <= kv_len) {
-    const int64_t base = (int64_t)kv0 * D;
+__device__ __forceinline__ void dma_tile(const bf16_t* kb, const bf16_t* vb, int kv0, int kv_len, uint32_t k_dst,
+                                         uint32_t v_dst, const DmaLane& d, int wave) {
+  const bf16_t* ks = kb + (int64_t)kv0 * D;
+  const bf16_t* vs = vb + (int64_t)kv0 * D;
+  const bool full = kv0 + BKV <= kv_len;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const uint32_t blk = wave + 8 * j;
-      lds_dma16(kb + base + d.koff[j], k_dst + 1024u * blk);
-      lds_dma16(vb + base + d.voff[j], v_dst + 1024u * blk);
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const uint32_t blk = wave + 8 * j;
-      const int shift = (min(kv0 + d.row[j], kv_len - 1) - d.row[j]) * D;  // clamp the row
-      lds_dma16(kb + (int64_t)shift + d.koff[j], k_dst + 1024u * blk);
-      lds_dma16(vb + (int64_t)shift + d.voff[j], v_dst + 1024u * blk);
-    }
+  for (int j = 0; j < 2; ++j) {
+    const int row = d.row0 + 32 * j;
+    const int src = full ? row : min(kv0 + row, kv_len - 1) - kv0;
+    const uint32_t roff = (uint32_t)src * (D * 2);
+    const uint32_t blk = (uint32_t)(wave + 8 * j);
+    lds_dma16_s(ks, roff + d.kchunk, k_dst + 1024u * blk);
+    lds_dma16_s(vs, roff + d.vchunk, v_dst + 1024u * blk);
   }
 }
 
@@ -252,7 +255,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;       // 0..7
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // 0..7, kept in SGPRs
   const int l32 = lane & 31;
   const int hf = lane >> 5;
   const int h = g * 4 + (wave & 3);
