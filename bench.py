@@ -9,8 +9,8 @@ stack, with all inputs resident in HBM before timing starts:
                                layer's artifact K/V into the request cache
   per layer:
   a3     attuner_qproj_lora    fused [W_q; W_k; W_v] projection + rank-r LoRA on q
-  a4     attuner_qk_norm_rope  q/k RMSNorm + RoPE, suffix k/v into the cache
-  a5     attuner_attention     multi-segment GQA attention -> O
+  a4+a5  attuner_suffix_attn   q/k RMSNorm + RoPE, suffix k/v into the cache;
+                               multi-segment GQA attention -> O
 The same kernels then run the full-context prefill of the whole request
 (attuner_full_prefill, every layer, no adapter) for the speedup.
 
@@ -234,20 +234,21 @@ def main():
         cu_q.append(cu_q[-1] + r.suffix_len)
     pos0 = [wl.pos0(r) for r in wl.requests]
     c_cuq, c_cuctx, c_art, c_pos = i32(cu_q), i32(cu_ctx), i32(art_len), i32(pos0)
-    qproj_args, norm_args, attn_args = [], [], []
+    # per layer: attuner_qproj_lora (q|k|v rows, LoRA on the q columns), then
+    # attuner_suffix_attn (q/k norm + RoPE with the suffix k/v into the cache,
+    # attention, split merge)
+    qproj_args, attn_args = [], []
     for l in range(NL):
         base = qkv[l].data_ptr()
         qproj_args.append((h, T, x_l[l].data_ptr(), wqkv[l].data_ptr(), n_out, a_l[l].data_ptr(), b_l[l].data_ptr(),
                            wl.rank, wl.scale, nq, base, sp))
-        norm_args.append((h, l, len(requests), c_cuq, c_cuctx, c_art, c_pos, base, n_out, base + 2 * nq,
-                          base + 2 * (nq + nkv), n_out, gq.data_ptr(), gk.data_ptr(), o_l[l].data_ptr(),
-                          req_kv.data_ptr(), rows, sp))
-        attn_args.append((h, l, len(requests), c_cuq, c_cuctx, c_art, o_l[l].data_ptr(), req_kv.data_ptr(), rows,
+        attn_args.append((h, l, len(requests), c_cuq, c_cuctx, c_art, c_pos, base, n_out, base + 2 * nq,
+                          base + 2 * (nq + nkv), n_out, gq.data_ptr(), gk.data_ptr(), req_kv.data_ptr(), rows,
                           o_l[l].data_ptr(), None, sp))
 
-    # per-category events: gather, qproj, norm, attention
-    cats = ("gather", "qproj", "norm", "attn")
-    per_step = {"gather": 1, "qproj": NL, "norm": NL, "attn": NL}
+    # per-category events: gather, qproj, suffix attention
+    cats = ("gather", "qproj", "attn")
+    per_step = {"gather": 1, "qproj": NL, "attn": NL}
 
     def make_events(n_steps):
         return {c: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -265,8 +266,7 @@ def main():
         call("gather", idx, lib.attuner_assemble_kv, assemble_args)
         for l in range(NL):
             call("qproj", idx * NL + l, lib.attuner_qproj_lora, qproj_args[l])
-            call("norm", idx * NL + l, lib.attuner_qk_norm_rope, norm_args[l])
-            call("attn", idx * NL + l, lib.attuner_attention, attn_args[l])
+            call("attn", idx * NL + l, lib.attuner_suffix_attn, attn_args[l])
 
     if args.copy_probe_mb > 0:
         nbytes = args.copy_probe_mb << 20
@@ -305,14 +305,12 @@ def main():
         cap = torch.cuda.Stream()
         csp = C.c_void_p(cap.cuda_stream)
         g_qproj = [a[:-1] + (csp,) for a in qproj_args]
-        g_norm = [a[:-1] + (csp,) for a in norm_args]
         g_attn = [a[:-1] + (csp,) for a in attn_args]
         graph = torch.cuda.CUDAGraph()
         cap.wait_stream(stream)
         with torch.cuda.graph(graph, stream=cap):
             for l in range(NL):
-                for fn, a in ((lib.attuner_qproj_lora, g_qproj[l]), (lib.attuner_qk_norm_rope, g_norm[l]),
-                              (lib.attuner_attention, g_attn[l])):
+                for fn, a in ((lib.attuner_qproj_lora, g_qproj[l]), (lib.attuner_suffix_attn, g_attn[l])):
                     rc_ = fn(*a)
                     if rc_ != 0:
                         raise RuntimeError(f"capture: {lib.attuner_last_error().decode()}")
@@ -353,7 +351,7 @@ def main():
         return tot / n
 
     attn_tflops = attn_f / (attn_kernel_ms * 1e-3) / 1e12          # attention_kernel alone
-    attn_call_tflops = attn_f / (kern_ms["attn"] * 1e-3) / 1e12   # attuner_attention call (+ split merge)
+    attn_call_tflops = attn_f / (kern_ms["attn"] * 1e-3) / 1e12   # attuner_suffix_attn call (+ norm, merge)
     gemm_kernel_ms = kavg("gemm_lora_kernel")
     gemm_tflops = gemm_f / (gemm_kernel_ms * 1e-3) / 1e12
     gather_kernel_ms = kavg("gather_kernel")
@@ -428,16 +426,16 @@ def main():
                      "traffic": traffic, "flops_per_launch": attn_f, "launch_ms": round(attn_kernel_ms, 5)},
         "kernels": {
             "attention": {"tflops": round(attn_tflops, 2), "mfma_frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-                          "kernel_ms": round(attn_kernel_ms, 5), "call_ms_with_split_merge": round(kern_ms["attn"], 5),
+                          "kernel_ms": round(attn_kernel_ms, 5), "suffix_attn_call_ms": round(kern_ms["attn"], 5),
                           "call_tflops": round(attn_call_tflops, 2)},
             "qproj_lora_gemm": {"tflops": round(gemm_tflops, 2), "mfma_frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
-                                "kernel_ms": round(gemm_kernel_ms, 5), "call_ms_with_lora_down": round(kern_ms["qproj"], 5),
+                                "kernel_ms": round(gemm_kernel_ms, 5), "call_ms": round(kern_ms["qproj"], 5),
                                 "flops_per_layer": gemm_f},
             "kv_gather": {"gbps": round(gather_gbps, 1), "hbm_frac": round(gather_gbps / PEAK_HBM_GBPS, 4),
                           "kernel_ms": round(gather_kernel_ms, 5), "call_ms": round(kern_ms["gather"], 5),
                           "bytes_per_step": g_bytes},
             "qk_norm_rope": {"gbps": round(norm_gbps, 1), "kernel_ms": round(norm_kernel_ms, 5),
-                             "call_ms": round(kern_ms["norm"], 5)},
+                             "note": "inside attuner_suffix_attn"},
         },
         "kernel_avg_ms": per_kernel,
         "full_prefill": full,
