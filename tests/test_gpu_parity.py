@@ -211,6 +211,9 @@ def test_qk_norm_rope_parity(pos0, gamma):
     [(8192, 256)],                     # c2 layer: split-KV
     [(0, 300)],                        # plain causal, ragged block
     [(37, 1), (1000, 45), (0, 5), (2047, 64), (3, 130)],   # varlen batch, S = 1, tiny art
+    [(8192, 64)],                      # 8 blocks: 16 key splits, the most the merge takes
+    [(100, 7), (50, 0), (0, 0), (700, 33)],                # zero-length suffixes inside a batch
+    [(16 * (i % 5), 1 + (i % 3)) for i in range(64)],      # the maximum of 64 requests
 ])
 def test_attention_parity(reqs):
     _say(f"attention {reqs}")
@@ -233,6 +236,8 @@ def test_attention_parity(reqs):
         got, got_lse = host_f64(o), lse.cpu().numpy()
     qf, cf = oracle.decode_bf16(q), oracle.decode_bf16(cache)
     for r, (L, S) in enumerate(reqs):
+        if S == 0:
+            continue
         kk = cf[0, 0, :, cu_ctx[r]:cu_ctx[r] + L + S].transpose(1, 0, 2)
         vv = cf[0, 1, :, cu_ctx[r]:cu_ctx[r] + L + S].transpose(1, 0, 2)
         ref, ref_lse = oracle.attention(qf[cu_q[r]:cu_q[r + 1]], kk, vv, L, return_lse=True)
@@ -440,3 +445,14 @@ def test_error_codes():
         with pytest.raises(AttunerError) as e:
             ctx.attention(1, [0, 4], [0, rows], [1], q, kv, rows, q)
         assert e.value.status == -1
+        # q/k/v rows must be 16-byte aligned with row strides a multiple of 8
+        g = torch.ones(128, dtype=torch.bfloat16, device="cuda")
+        for ld, off in ((48 * 128 + 8, 1), (48 * 128 + 4, 0)):   # shifted start; row stride not a multiple of 8
+            qkv = torch.zeros(4, ld, dtype=torch.bfloat16, device="cuda")
+            q_raw, k_raw, v_raw = qkv[:, off:], qkv[:, 32 * 128:], qkv[:, 40 * 128:]
+            with pytest.raises(AttunerError) as e:
+                ctx.qk_norm_rope(0, [0, 4], [0, rows], [1], [1], q_raw, ld, k_raw, v_raw, ld, g, g, q, kv, rows)
+            assert e.value.status == -1
+            with pytest.raises(AttunerError) as e:
+                ctx.suffix_attn(0, [0, 4], [0, rows], [1], [1], q_raw, ld, k_raw, v_raw, ld, g, g, kv, rows, q)
+            assert e.value.status == -1
