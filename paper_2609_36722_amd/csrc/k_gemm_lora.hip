@@ -34,6 +34,7 @@ constexpr int BK = 64;
 constexpr int kChunksPerRow = BK / 8;  // 16-byte chunks per LDS row
 constexpr int kLoraSlice = 256;        // hidden elements per lora_down workgroup
 constexpr int kLoraRows = 32;          // A rows staged per k-tile when the down-projection is fused
+constexpr int kGroupM = 4;             // token tiles per group of the tile order
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
@@ -147,12 +148,20 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
   static_assert(BM * (kLoraRows + 1) * 4 <= STAGE * 16, "t staging must fit one stage");
   __shared__ u32x4 lds[NST * STAGE];
 
+  // Tile order.  Workgroup i runs on XCD i % 8: each XCD gets a contiguous
+  // run of the order below, so the ~32 workgroups one XCD runs at a time
+  // share operand panels in its L2.  The order walks groups of kGroupM token
+  // tiles across all feature tiles, token tile fastest: 32 concurrent
+  // workgroups cover about kGroupM x 8 tiles (kGroupM x-panels, 8 W-panels).
   const int total = n_mt * n_nt;
   const int per_xcd = total >> 3;
   int lin = blockIdx.x;
   if (lin < 8 * per_xcd) lin = (lin & 7) * per_xcd + (lin >> 3);
-  const int nt = lin / n_mt;
-  const int mt = lin - nt * n_mt;
+  const int in_group = kGroupM * n_nt;
+  const int first_m = (lin / in_group) * kGroupM;
+  const int gm = min(n_mt - first_m, kGroupM);
+  const int mt = first_m + (lin % in_group) % gm;
+  const int nt = (lin % in_group) / gm;
   const int n0 = nt * BN;
   const int m0 = mt * BM;
 
@@ -172,9 +181,9 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
     for (int j = 0; j < FM; ++j) acc[i][j] = f32x16{};
 
   // Fused down-projection (t_part == null): this workgroup needs t for its
-  // tokens, so the k-loop also stages A's rows and the waves with wn == 0
-  // accumulate t^T = A x^T next to their main MFMAs (the x fragments are
-  // shared).  t then goes through LDS to the epilogue.
+  // tokens, so the k-loop also stages A's rows and, for each 32-token block,
+  // one wave that holds its x fragments accumulates t^T = A x^T next to its
+  // main MFMAs.  t then goes through LDS to the epilogue.
   const bool fused = t_part == nullptr && r_pad > 0 && n0 < lora_cols;
   f32x16 tacc[FM];
 #pragma unroll
@@ -213,7 +222,9 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
 #pragma unroll
       for (int j = 0; j < PW; ++j) lds_dma16(src[j] + kt * BK, lds0 + (uint32_t)(st * STAGE * 16) + doff[j]);
     }
-    const bool t_wave = LA && wn == 0;
+    // t block j (32 tokens) is accumulated by the wave column wn == j % WN
+    // of the wave row that holds those tokens: the extra MFMAs spread over
+    // min(FM, WN) wave columns
     int slot = 0, nslot = NST - 1;
     for (int kt = 0; kt < n_kt; ++kt) {
       // own copies of tile kt done, then everyone's; slot nslot (tile kt - 1) is free
@@ -242,11 +253,12 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
         for (int i = 0; i < FN; ++i)
 #pragma unroll
           for (int j = 0; j < FM; ++j) acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
-        if (t_wave) {
+        if (LA && wn < FM) {
           const int row = BN + BM + l32;
           const bf16x8 ar = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
 #pragma unroll
-          for (int j = 0; j < FM; ++j) tacc[j] = mfma32(ar, bfr[j], tacc[j]);
+          for (int j = 0; j < FM; ++j)
+            if (j % WN == wn) tacc[j] = mfma32(ar, bfr[j], tacc[j]);
         }
       }
       slot = slot + 1 == NST ? 0 : slot + 1;
@@ -265,13 +277,12 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
     // kLoraRows + 1
     float* ts = reinterpret_cast<float*>(lds);
     barrier_no_fence();
-    if (wn == 0) {
 #pragma unroll
-      for (int j = 0; j < FM; ++j) {
-        const int ml = wm * TM + j * 32 + l32;
+    for (int j = 0; j < FM; ++j) {
+      if (j % WN != wn) continue;
+      const int ml = wm * TM + j * 32 + l32;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) ts[ml * (kLoraRows + 1) + 8 * (v >> 2) + 4 * hi + (v & 3)] = scale * tacc[j][v];
-      }
+      for (int v = 0; v < 16; ++v) ts[ml * (kLoraRows + 1) + 8 * (v >> 2) + 4 * hi + (v & 3)] = scale * tacc[j][v];
     }
     __syncthreads();
     t_lds = ts;
@@ -367,7 +378,7 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
                  n_tok, n_out, hidden, a, scale, b, rank, r_pad, lora_cols, t_part, n_slice, out,                  \
                  (n_tok + (BM_) - 1) / (BM_), n_out / (BN_))
   if (wgs(256, 256) >= kMinWgs) {
-    ATTUNER_GEMM(256, 256, 2, 4, 2);
+    ATTUNER_GEMM(256, 256, 4, 2, 2);
   } else if (wgs(128, 256) >= kMinWgs) {
     ATTUNER_GEMM(128, 256, 4, 2, 3);
   } else if (wgs(128, 128) >= kMinWgs) {
