@@ -214,24 +214,6 @@ __device__ __forceinline__ void rescale(f32x16 (&acc)[4], float alpha) {
   }
 }
 
-// O row (token qrow, head h) from the O^T accumulator: lane holds d =
-// 32 db + 8 q + 4 hf + (0..3); also the natural-log LSE of the row.
-__device__ __forceinline__ void store_output(const AttnParams& p, int64_t qrow, int h, int hf, const f32x16* acc,
-                                             float scale, float m_log2, float l) {
-  bf16_t* orow = p.o + (qrow * p.n_q_heads + h) * D;
-#pragma unroll
-  for (int db = 0; db < 4; ++db) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      u32x2 pr;
-      pr[0] = pack_bf16x2(acc[db][4 * q] * scale, acc[db][4 * q + 1] * scale);
-      pr[1] = pack_bf16x2(acc[db][4 * q + 2] * scale, acc[db][4 * q + 3] * scale);
-      *reinterpret_cast<u32x2*>(orow + db * 32 + 8 * q + 4 * hf) = pr;
-    }
-  }
-  if (p.lse != nullptr && hf == 0) p.lse[qrow * p.n_q_heads + h] = (m_log2 + __log2f(l)) * 0.69314718055994531f;
-}
-
 __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   __shared__ u32x4 k_lds[NSTAGE][BKV * CH];
   __shared__ u32x4 v_lds[NSTAGE][BKV * CH];
@@ -264,6 +246,15 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   const bool row_ok = t - t0 < blk_rows;
   const int64_t qrow = (int64_t)(rq.q_start + t);
 
+  const bf16_t* kb = p.k + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
+  const bf16_t* vb = p.v + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
+  const uint32_t k_base = lds_addr(k_lds[0]), v_base = lds_addr(v_lds[0]);
+  constexpr uint32_t kStage = BKV * CH * 16;  // bytes per stage of K (and of V)
+  const DmaLane dl = dma_lane(wave, lane);
+
+  // Prologue: the Q rows and the DMA of tile tb fly together and one wait
+  // covers both (Q is then in registers, so the compiler needs no
+  // vector-memory wait inside the tile loop); tile tb + 1 follows.
   bf16x8 qf[8];
 #pragma unroll
   for (int ks = 0; ks < 8; ++ks) {
@@ -271,8 +262,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
     if (row_ok) v = *reinterpret_cast<const u32x4*>(p.q + (qrow * p.n_q_heads + h) * D + ks * 16 + hf * 8);
     qf[ks] = as_bf16x8(v);
   }
-  // Q is in registers before any K/V DMA is issued, so the compiler needs no
-  // vector-memory wait inside the tile loop
+  if (tb < te) dma_tile(kb, vb, tb * BKV, kv_len, k_base, v_base, dl, wave);
   __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
 
   // transpose-read addressing of the V^T operand: lane r of its 16-lane group
@@ -288,9 +278,6 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
     vcol[db] = ((chunk ^ (vrow << 2)) << 3) + ((r16 & 1) << 2);
   }
 
-  const bf16_t* kb = p.k + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
-  const bf16_t* vb = p.v + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
-
   float m_i = -INFINITY, l_i = 0.f;
   f32x16 acc[4];
 #pragma unroll
@@ -303,11 +290,6 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   // tiles before tp end at or before the diagonal of every row of the wave
   const int tp = min(max((mask_from + 1) / BKV, tb), te);
 
-  const uint32_t k_base = lds_addr(k_lds[0]), v_base = lds_addr(v_lds[0]);
-  constexpr uint32_t kStage = BKV * CH * 16;  // bytes per stage of K (and of V)
-  const DmaLane dl = dma_lane(wave, lane);
-  // prologue: tiles tb and tb + 1 in flight
-  if (tb < te) dma_tile(kb, vb, tb * BKV, kv_len, k_base, v_base, dl, wave);
   if (tb + 1 < te) dma_tile(kb, vb, (tb + 1) * BKV, kv_len, k_base + kStage, v_base + kStage, dl, wave);
 
   // Start of tile `tile`: this wave's copies of it done (those of tile + 1,
@@ -373,16 +355,16 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
     pv_tile(vst(tile), pk, hf, vrow, vcol, acc);
   }
 
+  // ---- epilogue: O / l (the output, or with n_split > 1 this split's
+  // normalised partial) goes through LDS, so that each store below is 16
+  // bytes per lane of a whole 256-byte row.  The O^T accumulator holds, per
+  // lane, dims 32 db + 8 q + 4 hf + 0..3 of one token; rows are padded to 272
+  // bytes (16-byte aligned, at most 2-way bank conflicts on the 8-byte writes).
   const float inv_l = l_i > 0.f ? 1.0f / l_i : 0.f;
-  if (p.n_split == 1) {
-    if (row_ok) store_output(p, qrow, h, hf, acc, inv_l, m_i, l_i);
-    return;
-  }
-
-  // ---- split-KV: publish the normalised partial (bf16) and its (max, sum) --
-  if (!row_ok) return;
-  const int64_t prow = (int64_t)split * p.total_q * p.n_q_heads + qrow * p.n_q_heads + h;
-  bf16_t* po = p.part_o + prow * D;
+  constexpr int kRowBytes = D * 2 + 16;
+  static_assert(4 * 32 * kRowBytes <= (int)sizeof(k_lds), "epilogue staging must fit the K ring");
+  __syncthreads();  // every wave is done with the K/V ring
+  char* stage = reinterpret_cast<char*>(wave < 4 ? &k_lds[0][0] : &v_lds[0][0]) + (wave & 3) * 32 * kRowBytes;
 #pragma unroll
   for (int db = 0; db < 4; ++db) {
 #pragma unroll
@@ -390,10 +372,29 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
       u32x2 pr;
       pr[0] = pack_bf16x2(acc[db][4 * q] * inv_l, acc[db][4 * q + 1] * inv_l);
       pr[1] = pack_bf16x2(acc[db][4 * q + 2] * inv_l, acc[db][4 * q + 3] * inv_l);
-      *reinterpret_cast<u32x2*>(po + db * 32 + 8 * q + 4 * hf) = pr;
+      *reinterpret_cast<u32x2*>(stage + l32 * kRowBytes + (32 * db + 8 * q + 4 * hf) * 2) = pr;
     }
   }
-  if (hf == 0) *reinterpret_cast<f32x2*>(p.part_ml + prow * 2) = f32x2{m_i, l_i};
+  const int64_t head_rows = (int64_t)p.total_q * p.n_q_heads;  // rows of one split's partial
+  bf16_t* dst = p.n_split == 1 ? p.o : p.part_o + (int64_t)split * head_rows * D;
+  const int sub = lane >> 4;  // row within a group of 4; 16 lanes x 16 bytes per row
+  const int c16 = lane & 15;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int rr = 4 * j + sub;  // token t0w + rr
+    const u32x4 v = *reinterpret_cast<const u32x4*>(stage + rr * kRowBytes + c16 * 16);
+    if (t0w + rr - t0 < blk_rows) {
+      const int64_t orow = (int64_t)(rq.q_start + t0w + rr) * p.n_q_heads + h;
+      *reinterpret_cast<u32x4*>(dst + orow * D + c16 * 8) = v;
+    }
+  }
+  if (!row_ok || hf != 0) return;
+  const int64_t hrow = qrow * p.n_q_heads + h;
+  if (p.n_split == 1) {
+    if (p.lse != nullptr) p.lse[hrow] = (m_i + __log2f(l_i)) * 0.69314718055994531f;
+  } else {
+    *reinterpret_cast<f32x2*>(p.part_ml + ((int64_t)split * head_rows + hrow) * 2) = f32x2{m_i, l_i};
+  }
 }
 
 // Merge the n_split partials: weight of split s is l_s * 2^(m_s - max_s m_s).
