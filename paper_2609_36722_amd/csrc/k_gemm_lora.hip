@@ -50,6 +50,8 @@ __device__ __forceinline__ void lora_epilogue_store(f32x16 (&acc)[FN][FM], int n
                                                     const float* t_lds, bf16_t* __restrict__ out) {
   if (r_pad > 0 && n_base < lora_cols) {
     const int64_t slice_stride = (int64_t)M * r_pad;
+    // B rows as 16-byte loads when they are whole 16-byte runs
+    const bool b_vec = (rank & 7) == 0 && (reinterpret_cast<uintptr_t>(b) & 15) == 0;
     for (int ks = 0; ks < r_pad; ks += 16) {
       bf16x8 th[FM], tl[FM];
 #pragma unroll
@@ -88,11 +90,18 @@ __device__ __forceinline__ void lora_epilogue_store(f32x16 (&acc)[FN][FM], int n
         if (nb >= lora_cols) continue;  // lora_cols is a multiple of 32
         const int n = nb + l32;
         bf16x8 a;
+        const int j0 = ks + 8 * hi;  // this lane's 8 ranks j0 .. j0 + 7 of B row n
+        if (b_vec) {
+          // rank % 8 == 0: the 8 ranks are all below rank or all past it
+          u32x4 v = u32x4{0u, 0u, 0u, 0u};
+          if (j0 < rank) v = *reinterpret_cast<const u32x4*>(b + (int64_t)n * rank + j0);
+          a = as_bf16x8(v);
+        } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int jj = ks + 8 * hi + e;
-          const bf16_t bv = jj < rank ? b[(int64_t)n * rank + jj] : (bf16_t)0;
-          a[e] = __builtin_bit_cast(__bf16, bv);
+          for (int e = 0; e < 8; ++e) {
+            const bf16_t bv = j0 + e < rank ? b[(int64_t)n * rank + j0 + e] : (bf16_t)0;
+            a[e] = __builtin_bit_cast(__bf16, bv);
+          }
         }
 #pragma unroll
         for (int j = 0; j < FM; ++j) {
@@ -363,30 +372,42 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
                             const float* t_part, uint16_t* out, hipStream_t stream) {
   if (n_tok == 0) return hipSuccess;
   const int n_slice = lora_down_slices(hidden);
-  // Tile choice: the largest tile (fewest ingested bytes, M N K 2 (1/BM +
-  // 1/BN)) that still gives at least 180 workgroups for the 256 CUs, in the
-  // order 256x256, 128x256, 128x128, 64x96, 64x64 (tokens x features; measured
-  // on gfx950 at hidden 2560/4096 with 6144 outputs: T = 8448 -> 256x256,
-  // 1024 -> 128x256, 512 -> 128x128, 256 -> 64x96, 64 -> 64x64).
-  auto wgs = [&](int bm, int bn) -> int64_t {
-    return n_out % bn != 0 ? 0 : (int64_t)((n_tok + bm - 1) / bm) * (n_out / bn);
+  // Tile choice.  One workgroup per CU at a time, and a workgroup's k-loop
+  // runs at the CU's operand ingest rate, so a launch takes about
+  // ceil(workgroups / 256) rounds of (BM + BN) * hidden * 2 ingested bytes.
+  // Pick the tile (tokens x features) that minimises rounds * (BM + BN);
+  // ties go to the earlier entry.  Measured on gfx950 with 6144 outputs and
+  // hidden 2560 / 4096 this picks the fastest tile at T = 64 (64x64), 256
+  // (64x96), 512 (128x96), 1024 (256x96) and 8448 (256x256).
+  struct Tile {
+    int bm, bn;
   };
-  constexpr int64_t kMinWgs = 180;
+  constexpr Tile kTiles[] = {{256, 256}, {128, 256}, {256, 96}, {128, 128}, {128, 96}, {64, 96}, {64, 64}};
+  int best = -1;
+  int64_t best_cost = 0;
+  for (int i = 0; i < (int)(sizeof(kTiles) / sizeof(kTiles[0])); ++i) {
+    if (n_out % kTiles[i].bn != 0) continue;
+    const int64_t wgs = (int64_t)((n_tok + kTiles[i].bm - 1) / kTiles[i].bm) * (n_out / kTiles[i].bn);
+    const int64_t cost = (wgs + 255) / 256 * (kTiles[i].bm + kTiles[i].bn);
+    if (best < 0 || cost < best_cost) {
+      best = i;
+      best_cost = cost;
+    }
+  }
 #define ATTUNER_GEMM(BM_, BN_, WN_, WM_, NST_)                                                               \
   ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, WM_, NST_>),                           \
                  dim3(((n_tok + (BM_) - 1) / (BM_)) * (n_out / (BN_))), dim3(64 * (WN_) * (WM_)), stream, x, w, \
                  n_tok, n_out, hidden, a, scale, b, rank, r_pad, lora_cols, t_part, n_slice, out,                  \
                  (n_tok + (BM_) - 1) / (BM_), n_out / (BN_))
-  if (wgs(256, 256) >= kMinWgs) {
-    ATTUNER_GEMM(256, 256, 4, 2, 2);
-  } else if (wgs(128, 256) >= kMinWgs) {
-    ATTUNER_GEMM(128, 256, 4, 2, 3);
-  } else if (wgs(128, 128) >= kMinWgs) {
-    ATTUNER_GEMM(128, 128, 2, 2, 4);
-  } else if (wgs(64, 96) >= kMinWgs) {
-    ATTUNER_GEMM(64, 96, 3, 2, 5);
-  } else {
-    ATTUNER_GEMM(64, 64, 2, 2, 6);
+  switch (best) {
+    case 0: ATTUNER_GEMM(256, 256, 4, 2, 2); break;
+    case 1: ATTUNER_GEMM(128, 256, 4, 2, 3); break;
+    case 2: ATTUNER_GEMM(256, 96, 3, 4, 3); break;
+    case 3: ATTUNER_GEMM(128, 128, 2, 2, 4); break;
+    case 4: ATTUNER_GEMM(128, 96, 3, 2, 4); break;
+    case 5: ATTUNER_GEMM(64, 96, 3, 2, 5); break;
+    case 6: ATTUNER_GEMM(64, 64, 2, 2, 6); break;
+    default: return hipErrorInvalidValue;  // n_out is a multiple of 128: 64x64 always fits
   }
 #undef ATTUNER_GEMM
   return hipGetLastError();
