@@ -358,13 +358,16 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   // ---- epilogue: O / l (the output, or with n_split > 1 this split's
   // normalised partial) goes through LDS, so that each store below is 16
   // bytes per lane of a whole 256-byte row.  The O^T accumulator holds, per
-  // lane, dims 32 db + 8 q + 4 hf + 0..3 of one token; rows are padded to 272
-  // bytes (16-byte aligned, at most 2-way bank conflicts on the 8-byte writes).
+  // lane, dims 32 db + 8 q + 4 hf + 0..3 of one token: 8-byte slot 8 db + 2 q
+  // + hf of that token's row.  Slot s of row r is kept at s ^ r (rows of 32
+  // slots), so the 32 lanes of a half-wave, one row each, write 32 distinct
+  // slots (no bank conflicts); a 16-byte chunk c of row r then sits at chunk
+  // c ^ (r >> 1), its two halves swapped when r is odd.
   const float inv_l = l_i > 0.f ? 1.0f / l_i : 0.f;
-  constexpr int kRowBytes = D * 2 + 16;
-  static_assert(4 * 32 * kRowBytes <= (int)sizeof(k_lds), "epilogue staging must fit the K ring");
+  constexpr int kRowBytes = D * 2;
+  static_assert(8 * 32 * kRowBytes <= (int)sizeof(k_lds), "epilogue staging must fit the K ring");
   __syncthreads();  // every wave is done with the K/V ring
-  char* stage = reinterpret_cast<char*>(wave < 4 ? &k_lds[0][0] : &v_lds[0][0]) + (wave & 3) * 32 * kRowBytes;
+  char* stage = reinterpret_cast<char*>(&k_lds[0][0]) + wave * 32 * kRowBytes;
 #pragma unroll
   for (int db = 0; db < 4; ++db) {
 #pragma unroll
@@ -372,7 +375,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
       u32x2 pr;
       pr[0] = pack_bf16x2(acc[db][4 * q] * inv_l, acc[db][4 * q + 1] * inv_l);
       pr[1] = pack_bf16x2(acc[db][4 * q + 2] * inv_l, acc[db][4 * q + 3] * inv_l);
-      *reinterpret_cast<u32x2*>(stage + l32 * kRowBytes + (32 * db + 8 * q + 4 * hf) * 2) = pr;
+      const int slot = (8 * db + 2 * q + hf) ^ l32;
+      *reinterpret_cast<u32x2*>(stage + l32 * kRowBytes + slot * 8) = pr;
     }
   }
   const int64_t head_rows = (int64_t)p.total_q * p.n_q_heads;  // rows of one split's partial
@@ -382,7 +386,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int rr = 4 * j + sub;  // token t0w + rr
-    const u32x4 v = *reinterpret_cast<const u32x4*>(stage + rr * kRowBytes + c16 * 16);
+    u32x4 v = *reinterpret_cast<const u32x4*>(stage + rr * kRowBytes + (c16 ^ (rr >> 1)) * 16);
+    if (rr & 1) v = u32x4{v[2], v[3], v[0], v[1]};
     if (t0w + rr - t0 < blk_rows) {
       const int64_t orow = (int64_t)(rq.q_start + t0w + rr) * p.n_q_heads + h;
       *reinterpret_cast<u32x4*>(dst + orow * D + c16 * 8) = v;
