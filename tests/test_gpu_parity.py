@@ -123,6 +123,12 @@ def _gemm_case(M, H, N, rank, lora_cols, seed, b_std=0.01):
     (300, 1024, 1280, 32, 1024),   # several token tiles with a ragged tail
     (1024, 512, 512, 64, 512),     # 128-token tiles, maximum rank
     (130, 256, 256, 0, 0),         # no adapter (merged deployment form)
+    # token counts at which the launcher picks each larger tile (tokens x features)
+    (1000, 512, 6144, 32, 4096),   # 256 x 96, ragged last token tile
+    (500, 512, 6144, 16, 4096),    # 128 x 96
+    (2048, 256, 2560, 8, 2048),    # 128 x 256
+    (2100, 256, 6144, 16, 4096),   # 256 x 256, ragged
+    (1024, 256, 1280, 12, 1024),   # 128 x 128; rank 12 reads B element by element
 ])
 def test_qproj_lora_parity(M, H, N, rank, lora_cols):
     _say(f"qproj M={M} H={H} N={N} r={rank}")
