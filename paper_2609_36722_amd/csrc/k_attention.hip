@@ -21,9 +21,10 @@
 //                converted to bf16 in registers).
 // The loop is software-pipelined inside each wave: QK of tile i is issued
 // next to the exponentials of tile i - 1, and PV of tile i - 1 next to the row
-// max of tile i.  (On gfx950 the MFMA and vector-ALU work of one wave overlap;
-// those of two waves sharing a SIMD were measured not to.)  Tiles reaching
-// the causal diagonal take a plain masked step.
+// max of tile i, so that each MFMA has vector-ALU work beside it that does
+// not depend on it (gfx950 overlaps the two only in part, measured at about
+// 60% of the MFMA time).  Tiles reaching the causal diagonal take a plain
+// masked step.
 // The S^T accumulator hands a lane the keys of each 16-key group in the order
 // (4hf + 0..3, 8 + 4hf + 0..3), hf = lane / 32; the V^T operand is read in that
 // same key order with the gfx950 LDS transpose read (ds_read_b64_tr_b16): a
@@ -311,9 +312,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
 
   // Unmasked tiles, software-pipelined inside the wave: QK of `tile` is
   // issued alongside the exponentials of tile - 1, and PV of tile - 1
-  // alongside the row max of `tile` (MFMA and vector-ALU work of one wave
-  // overlap on gfx950; those of two waves sharing a SIMD do not).  S^T
-  // alternates between sa and sb.
+  // alongside the row max of `tile`.  S^T alternates between sa and sb.
   if (tb < tp) {
     f32x16 sa[2], sb[2];
     bf16x8 pk[4];
