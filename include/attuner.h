@@ -154,6 +154,33 @@ attuner_status attuner_assemble_kv(attuner_ctx* ctx, int32_t n_req, const int32_
                                    void* req_kv, int64_t cache_rows, void* stream);
 
 /* --------------------------------------------------------------------------
+ * a1 and a2 apart (same method and layout as attuner_assemble_kv, which is
+ * attuner_assemble_table followed by attuner_gather_layers over all layers).
+ *
+ * attuner_assemble_table plans the batch on the host and copies the block
+ * table to block_table on `stream`; it fills cu_ctx and art_len as
+ * attuner_assemble_kv does and copies no cache rows.
+ *
+ * attuner_gather_layers copies the pages of layers layer_begin ..
+ * layer_begin + n_layers - 1 into req_kv, leaving the other layers' rows
+ * untouched, so a caller can gather layer l on one stream while earlier
+ * layers compute on another (ordering the two with events).  block_table,
+ * n_entries and cache_rows must be the block table, entry count and cache
+ * rows of the last attuner_assemble_table call on this context, and the
+ * device table must not have been modified since (the copy trusts its
+ * entries); anything else is refused with EINVAL.  Errors: EINVAL (also a
+ * null or unaligned req_kv), ERANGE (layers outside [0, n_layers)).
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_assemble_table(attuner_ctx* ctx, int32_t n_req, const int32_t* req_ptr,
+                                      const int32_t* artifact_ids, const int32_t* suffix_cap,
+                                      int32_t* block_table, int32_t* cu_ctx, int32_t* art_len,
+                                      int64_t cache_rows, void* stream);
+
+attuner_status attuner_gather_layers(attuner_ctx* ctx, const int32_t* block_table, int64_t n_entries,
+                                     int32_t layer_begin, int32_t n_layers, void* req_kv,
+                                     int64_t cache_rows, void* stream);
+
+/* --------------------------------------------------------------------------
  * a3: LoRA-adapted projection (section 4, eq. 4; fused q/k/v weights).
  *
  *   out[i][n] = sum_k x[i][k] w[n][k]

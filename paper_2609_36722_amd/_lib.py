@@ -44,6 +44,8 @@ SIGNATURES = {
     "attuner_artifact_pages": (C.c_int, [_vp, _i32, _i32p, _i32, _i32p, _i32p]),
     "attuner_assemble_plan": (C.c_int, [_vp, _i32, _i32p, _i32p, _i32p, _i64p, _i64p]),
     "attuner_assemble_kv": (C.c_int, [_vp, _i32, _i32p, _i32p, _i32p, _vp, _i32p, _i32p, _vp, _i64, _vp]),
+    "attuner_assemble_table": (C.c_int, [_vp, _i32, _i32p, _i32p, _i32p, _vp, _i32p, _i32p, _i64, _vp]),
+    "attuner_gather_layers": (C.c_int, [_vp, _vp, _i64, _i32, _i32, _vp, _i64, _vp]),
     "attuner_qproj_lora": (C.c_int, [_vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, C.c_float, _i32, _vp, _vp]),
     "attuner_qk_norm_rope": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64,
                                        _vp, _vp, _vp, _vp, _i64, _vp]),

@@ -179,6 +179,29 @@ class Context:
                                          _ptr(req_kv), int(cache_rows), _stream(stream)), "attuner_assemble_kv")
         return list(cu), list(al)[:n]
 
+    def assemble_table(self, requests: Sequence[Sequence[int]], suffix_cap: Sequence[int],
+                       block_table: torch.Tensor, cache_rows: int, stream=None) -> Tuple[List[int], List[int]]:
+        """Returns (cu_ctx, art_len); fills block_table (int32 device) only."""
+        ne, _ = self.assemble_plan(requests, suffix_cap)
+        _need(block_table, 4 * ne, "block_table")
+        ptr, ids = self._csr(requests)
+        n = len(requests)
+        cu = (C.c_int32 * (n + 1))()
+        al = (C.c_int32 * max(1, n))()
+        _check(lib().attuner_assemble_table(self._h, n, _i32(ptr), _i32(ids), _i32(suffix_cap),
+                                            _ptr(block_table, 4) if block_table is not None else None, cu, al,
+                                            int(cache_rows), _stream(stream)), "attuner_assemble_table")
+        return list(cu), list(al)[:n]
+
+    def gather_layers(self, block_table: torch.Tensor, n_entries: int, layer_begin: int, n_layers: int,
+                      req_kv: torch.Tensor, cache_rows: int, stream=None) -> None:
+        c = self.cfg
+        _need(block_table, 4 * int(n_entries), "block_table")
+        _need(req_kv, c.n_layers * 2 * c.n_kv_heads * int(cache_rows) * c.head_dim, "req_kv")
+        _check(lib().attuner_gather_layers(self._h, _ptr(block_table, 4) if block_table is not None else None,
+                                           int(n_entries), int(layer_begin), int(n_layers), _ptr(req_kv),
+                                           int(cache_rows), _stream(stream)), "attuner_gather_layers")
+
     # ---- projection -----------------------------------------------------------
     def qproj_lora(self, x: torch.Tensor, w: torch.Tensor, a: Optional[torch.Tensor], b: Optional[torch.Tensor],
                    rank: int, scale: float, lora_cols: int, out: torch.Tensor, stream=None) -> None:

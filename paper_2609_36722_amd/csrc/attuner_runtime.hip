@@ -207,6 +207,10 @@ struct attuner_ctx {
   DeviceBuf ws_qkv;     // full prefill: fused projection output
   DeviceBuf rope;       // (cos, sin) table [rope_pos][64]
   int64_t rope_pos = 0;
+  // the block table the last attuner_assemble_table call wrote (the only one
+  // attuner_gather_layers accepts)
+  const int32_t* last_table = nullptr;
+  int64_t last_entries = -1, last_rows = -1;
   Staging staging;
   Tracer tracer;
 };
@@ -603,10 +607,12 @@ attuner_status attuner_assemble_plan(const attuner_ctx* c, int32_t n_req, const 
   return plan_impl(c, n_req, req_ptr, artifact_ids, suffix_cap, n_entries, cache_rows, nullptr, nullptr, nullptr);
 }
 
-attuner_status attuner_assemble_kv(attuner_ctx* c, int32_t n_req, const int32_t* req_ptr, const int32_t* artifact_ids,
-                                   const int32_t* suffix_cap, int32_t* block_table, int32_t* cu_ctx,
-                                   int32_t* art_len, void* req_kv, int64_t cache_rows, void* stream) {
+attuner_status attuner_assemble_table(attuner_ctx* c, int32_t n_req, const int32_t* req_ptr,
+                                      const int32_t* artifact_ids, const int32_t* suffix_cap, int32_t* block_table,
+                                      int32_t* cu_ctx, int32_t* art_len, int64_t cache_rows, void* stream) {
   if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  c->last_table = nullptr;
+  c->last_entries = c->last_rows = -1;
   std::vector<int32_t> table;
   std::vector<int32_t> cu(n_req > 0 ? n_req + 1 : 1), al(n_req > 0 ? n_req : 1);
   int64_t entries = 0, rows = 0;
@@ -619,18 +625,56 @@ attuner_status attuner_assemble_kv(attuner_ctx* c, int32_t n_req, const int32_t*
   }
   if (rows != cache_rows)
     return fail(ATTUNER_ERANGE, "cache_rows %lld does not match the plan (%lld)", (long long)cache_rows, (long long)rows);
-  if (entries > 0 && (!block_table || !req_kv)) return fail(ATTUNER_EINVAL, "null block_table or req_kv");
-  if (req_kv && !aligned16(req_kv)) return fail(ATTUNER_EINVAL, "req_kv must be 16-byte aligned");
+  if (entries > 0 && !block_table) return fail(ATTUNER_EINVAL, "null block_table");
   if (entries > INT32_MAX) return fail(ATTUNER_ERANGE, "block table of %lld entries", (long long)entries);
   if (cu_ctx) memcpy(cu_ctx, cu.data(), (size_t)(n_req + 1) * sizeof(int32_t));
   if (art_len && n_req > 0) memcpy(art_len, al.data(), (size_t)n_req * sizeof(int32_t));
-  if (entries == 0) return ATTUNER_OK;
-  DeviceGuard dg(c->device);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  HIP_TRY(c->staging.upload(table.data(), table.size() * sizeof(int32_t), block_table, s));
-  HIP_TRY(launch_gather(block_table, entries, c->pool, c->pool_pages, c->cfg.n_layers, c->cfg.n_kv_heads,
-                        static_cast<uint16_t*>(req_kv), cache_rows, s));
+  if (entries > 0) {
+    DeviceGuard dg(c->device);
+    HIP_TRY(c->staging.upload(table.data(), table.size() * sizeof(int32_t), block_table,
+                              static_cast<hipStream_t>(stream)));
+  }
+  c->last_table = block_table;
+  c->last_entries = entries;
+  c->last_rows = rows;
   return ATTUNER_OK;
+}
+
+attuner_status attuner_gather_layers(attuner_ctx* c, const int32_t* block_table, int64_t n_entries,
+                                     int32_t layer_begin, int32_t n_layers, void* req_kv, int64_t cache_rows,
+                                     void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (c->last_entries < 0 || block_table != c->last_table || n_entries != c->last_entries ||
+      cache_rows != c->last_rows)
+    return fail(ATTUNER_EINVAL, "block_table, n_entries and cache_rows must be those of the last "
+                                "attuner_assemble_table call");
+  if (layer_begin < 0 || n_layers < 0 || layer_begin > c->cfg.n_layers || n_layers > c->cfg.n_layers - layer_begin)
+    return fail(ATTUNER_ERANGE, "layers [%d, %d) outside [0, %d)", layer_begin, layer_begin + n_layers,
+                c->cfg.n_layers);
+  if (n_entries == 0 || n_layers == 0) return ATTUNER_OK;
+  if (!req_kv || !aligned16(req_kv)) return fail(ATTUNER_EINVAL, "req_kv must be non-null and 16-byte aligned");
+  DeviceGuard dg(c->device);
+  HIP_TRY(launch_gather(block_table, n_entries, c->pool, c->pool_pages, layer_begin, n_layers, c->cfg.n_kv_heads,
+                        static_cast<uint16_t*>(req_kv), cache_rows, static_cast<hipStream_t>(stream)));
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_assemble_kv(attuner_ctx* c, int32_t n_req, const int32_t* req_ptr, const int32_t* artifact_ids,
+                                   const int32_t* suffix_cap, int32_t* block_table, int32_t* cu_ctx,
+                                   int32_t* art_len, void* req_kv, int64_t cache_rows, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  int64_t entries = 0, rows = 0;
+  attuner_status st = plan_impl(c, n_req, req_ptr, artifact_ids, suffix_cap, &entries, &rows, nullptr, nullptr,
+                                nullptr);
+  if (st != ATTUNER_OK) return st;
+  if (rows != cache_rows)
+    return fail(ATTUNER_ERANGE, "cache_rows %lld does not match the plan (%lld)", (long long)cache_rows, (long long)rows);
+  if (entries > 0 && (!block_table || !req_kv)) return fail(ATTUNER_EINVAL, "null block_table or req_kv");
+  if (req_kv && !aligned16(req_kv)) return fail(ATTUNER_EINVAL, "req_kv must be 16-byte aligned");
+  st = attuner_assemble_table(c, n_req, req_ptr, artifact_ids, suffix_cap, block_table, cu_ctx, art_len, cache_rows,
+                              stream);
+  if (st != ATTUNER_OK) return st;
+  return attuner_gather_layers(c, block_table, entries, 0, c->cfg.n_layers, req_kv, cache_rows, stream);
 }
 
 attuner_status attuner_qproj_lora(attuner_ctx* c, int32_t n_tok, const void* x, const void* w, int32_t n_out,

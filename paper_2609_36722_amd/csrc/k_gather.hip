@@ -59,9 +59,9 @@ __global__ __launch_bounds__(256) void store_pages_kernel(const u32x4* __restric
 
 __global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ table, const u32x4* __restrict__ pool,
                                                      int64_t pool_pages, int n_kv, u32x4* __restrict__ req_kv,
-                                                     int64_t cache_rows) {
+                                                     int64_t cache_rows, int layer_begin) {
   const int64_t e = blockIdx.x;
-  const int layer = blockIdx.y;
+  const int layer = layer_begin + (int)blockIdx.y;
   const int4 ent = table[e];  // {page, n_valid, dst_row, request}
   const int rr = threadIdx.x >> 4;
   const int chunk = threadIdx.x & 15;
@@ -103,12 +103,13 @@ hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens
 }
 
 hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint16_t* pool, int64_t pool_pages,
-                         int n_layers, int n_kv, uint16_t* req_kv, int64_t cache_rows, hipStream_t stream) {
-  if (n_entries == 0) return hipSuccess;
+                         int layer_begin, int n_layers, int n_kv, uint16_t* req_kv, int64_t cache_rows,
+                         hipStream_t stream) {
+  if (n_entries == 0 || n_layers == 0) return hipSuccess;
   dim3 grid(static_cast<unsigned>(n_entries), n_layers);
   ATTUNER_LAUNCH("gather_kernel", gather_kernel, grid, dim3(256), stream, reinterpret_cast<const int4*>(table_dev),
                      reinterpret_cast<const u32x4*>(pool), pool_pages, n_kv, reinterpret_cast<u32x4*>(req_kv),
-                     cache_rows);
+                     cache_rows, layer_begin);
   return hipGetLastError();
 }
 

@@ -34,9 +34,11 @@ hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens
                               hipStream_t stream);
 
 // Copy every entry {page, n_valid, dst_row, request} of the block table, for
-// every layer, into req_kv [n_layers][2][n_kv][cache_rows][128].
+// layers layer_begin .. layer_begin + n_layers - 1, into req_kv
+// [model layers][2][n_kv][cache_rows][128].
 hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint16_t* pool, int64_t pool_pages,
-                         int n_layers, int n_kv, uint16_t* req_kv, int64_t cache_rows, hipStream_t stream);
+                         int layer_begin, int n_layers, int n_kv, uint16_t* req_kv, int64_t cache_rows,
+                         hipStream_t stream);
 
 // ---- a3: LoRA-down and the projection GEMM --------------------------------
 

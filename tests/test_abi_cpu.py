@@ -46,4 +46,6 @@ def test_null_context_is_an_error_not_a_crash():
     assert lib.attuner_release_artifact(None, 0) == -1
     assert lib.attuner_pool_info(None, None, None, None) == -1
     assert lib.attuner_qproj_lora(None, 1, None, None, 128, None, None, 0, 0.0, 0, None, None) == -1
+    assert lib.attuner_assemble_table(None, 0, None, None, None, None, None, None, 0, None) == -1
+    assert lib.attuner_gather_layers(None, None, 0, 0, 1, None, 0, None) == -1
     lib.attuner_destroy(None)

@@ -76,6 +76,58 @@ def test_gather_ragged_multilayer_multirequest_bit_exact():
         g.close()
 
 
+def test_gather_layers_split_from_table_bit_exact():
+    # a1 and a2 as separate calls: the table once, then layers gathered out of
+    # order on two streams; every artifact row bit-exact against the oracle's
+    # assembly, a one-layer gather touches no other layer, and a table other
+    # than the last one written is refused
+    _say("assemble_table + gather_layers")
+    cfg = ModelCfg(n_layers=3, hidden=256)
+    rng = np.random.default_rng(11)
+    lengths = {0: 17, 1: 40, 2: 1, 3: 16}
+    with Context(cfg, pool_pages=16) as ctx:
+        art_k, art_v, ids = {}, {}, {}
+        for a, L in lengths.items():
+            k = rng.integers(0, 2 ** 16, size=(3, 8, L, 128), dtype=np.uint16)
+            v = rng.integers(0, 2 ** 16, size=(3, 8, L, 128), dtype=np.uint16)
+            ids[a] = ctx.store_artifact(dev_bf16(k), dev_bf16(v))
+            art_k[a], art_v[a] = k.transpose(0, 2, 1, 3), v.transpose(0, 2, 1, 3)   # [layers][L][Hkv][d]
+        reqs = [([1, 0, 3], 5), ([], 3), ([2, 2, 1], 0)]
+        requests, caps = [[ids[a] for a in r] for r, _ in reqs], [c for _, c in reqs]
+        ne, rows = ctx.assemble_plan(requests, caps)
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        kv = torch.zeros(3 * 2 * 8 * rows * 128, dtype=torch.bfloat16, device="cuda")
+        cu, al = ctx.assemble_table(requests, caps, bt, rows)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        ctx.gather_layers(bt, ne, 2, 1, kv, rows, stream=side)
+        ctx.gather_layers(bt, ne, 0, 2, kv, rows)
+        torch.cuda.synchronize()
+        want, cu2 = oracle.assemble(art_k, art_v, reqs, 8, 128)
+        assert cu == cu2.tolist()
+        got = bf16_to_host(kv).reshape(3, 2, 8, rows, 128)
+        for r in range(len(reqs)):
+            lo, n = cu[r], al[r]
+            assert np.array_equal(got[:, :, :, lo:lo + n], want[:, :, :, lo:lo + n]), f"request {r} rows differ"
+        one = torch.zeros_like(kv)
+        ctx.gather_layers(bt, ne, 1, 1, one, rows)
+        torch.cuda.synchronize()
+        got1 = bf16_to_host(one).reshape(3, 2, 8, rows, 128)
+        assert not got1[0].any() and not got1[2].any()
+        assert np.array_equal(got1[1], got[1])
+        with pytest.raises(AttunerError) as e:
+            ctx.gather_layers(bt, ne, 2, 2, kv, rows)      # past the last layer
+        assert e.value.status == -5
+        other = torch.zeros_like(bt)
+        with pytest.raises(AttunerError) as e:
+            ctx.gather_layers(other, ne, 0, 1, kv, rows)   # not the table assemble_table wrote
+        assert e.value.status == -1
+        big = torch.zeros(3 * 2 * 8 * (rows + 1) * 128, dtype=torch.bfloat16, device="cuda")
+        with pytest.raises(AttunerError) as e:
+            ctx.gather_layers(bt, ne, 0, 1, big, rows + 1)  # other cache geometry
+        assert e.value.status == -1
+
+
 def test_pool_reuse_after_release_bit_exact():
     _say("pool release and reuse")
     shape = ModelShape(hidden=256)
