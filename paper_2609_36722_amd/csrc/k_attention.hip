@@ -409,7 +409,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
 // is requested before any is used.
 constexpr int kMaxSplit = 16;
 
-__global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
+template <int NS>
+__global__ __launch_bounds__(256, 2) void attn_combine_kernel(AttnParams p) {
   const int g = blockIdx.x % p.n_kv_heads;
   const int t = (blockIdx.x / p.n_kv_heads) * 4 + (threadIdx.x >> 6);
   if (t >= p.total_q) return;
@@ -418,32 +419,29 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p) {
   const int d0 = 8 * (lane & 15);
   const int64_t row = (int64_t)t * p.n_q_heads + h;
   const int64_t stride = (int64_t)p.total_q * p.n_q_heads;
-  const int ns = p.n_split;
-  f32x2 ml[kMaxSplit];
-  u32x4 v[kMaxSplit];
+  // the split count is a template constant: every load is issued before the
+  // first one is waited for
+  f32x2 ml[NS];
+  u32x4 v[NS];
 #pragma unroll
-  for (int s = 0; s < kMaxSplit; ++s) {
-    if (s < ns) {
-      ml[s] = *reinterpret_cast<const f32x2*>(p.part_ml + (s * stride + row) * 2);
-      v[s] = *reinterpret_cast<const u32x4*>(p.part_o + (s * stride + row) * D + d0);
-    }
+  for (int s = 0; s < NS; ++s) {
+    ml[s] = *reinterpret_cast<const f32x2*>(p.part_ml + (s * stride + row) * 2);
+    v[s] = *reinterpret_cast<const u32x4*>(p.part_o + (s * stride + row) * D + d0);
   }
+  __builtin_amdgcn_sched_barrier(0);  // keep every load ahead of the first use
   float mmax = -INFINITY;
 #pragma unroll
-  for (int s = 0; s < kMaxSplit; ++s)
-    if (s < ns) mmax = fmaxf(mmax, ml[s][0]);
+  for (int s = 0; s < NS; ++s) mmax = fmaxf(mmax, ml[s][0]);
   float wsum = 0.f;
   float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int s = 0; s < kMaxSplit; ++s) {
-    if (s < ns) {
-      const float w = (ml[s][0] == -INFINITY) ? 0.f : ml[s][1] * __builtin_amdgcn_exp2f(ml[s][0] - mmax);
-      wsum += w;
+  for (int s = 0; s < NS; ++s) {
+    const float w = (ml[s][0] == -INFINITY) ? 0.f : ml[s][1] * __builtin_amdgcn_exp2f(ml[s][0] - mmax);
+    wsum += w;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        o[2 * e] = fmaf(w, __uint_as_float(v[s][e] << 16), o[2 * e]);
-        o[2 * e + 1] = fmaf(w, __uint_as_float(v[s][e] & 0xFFFF0000u), o[2 * e + 1]);
-      }
+    for (int e = 0; e < 4; ++e) {
+      o[2 * e] = fmaf(w, __uint_as_float(v[s][e] << 16), o[2 * e]);
+      o[2 * e + 1] = fmaf(w, __uint_as_float(v[s][e] & 0xFFFF0000u), o[2 * e + 1]);
     }
   }
   const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
@@ -464,7 +462,17 @@ hipError_t launch_attention(const AttnParams& p, hipStream_t stream) {
   if (e != hipSuccess || p.n_split == 1) return e;
   if (p.n_split > kMaxSplit || p.n_q_heads != 4 * p.n_kv_heads) return hipErrorInvalidValue;
   const int64_t wgs = (int64_t)((p.total_q + 3) / 4) * p.n_kv_heads;
-  ATTUNER_LAUNCH("attn_combine_kernel", attn_combine_kernel, dim3((unsigned)wgs), dim3(256), stream, p);
+#define ATTUNER_COMBINE(NS_)                                                                                   \
+  case NS_:                                                                                                    \
+    ATTUNER_LAUNCH("attn_combine_kernel", attn_combine_kernel<NS_>, dim3((unsigned)wgs), dim3(256), stream, p); \
+    break;
+  switch (p.n_split) {
+    ATTUNER_COMBINE(2) ATTUNER_COMBINE(3) ATTUNER_COMBINE(4) ATTUNER_COMBINE(5) ATTUNER_COMBINE(6)
+    ATTUNER_COMBINE(7) ATTUNER_COMBINE(8) ATTUNER_COMBINE(9) ATTUNER_COMBINE(10) ATTUNER_COMBINE(11)
+    ATTUNER_COMBINE(12) ATTUNER_COMBINE(13) ATTUNER_COMBINE(14) ATTUNER_COMBINE(15) ATTUNER_COMBINE(16)
+    default: return hipErrorInvalidValue;
+  }
+#undef ATTUNER_COMBINE
   return hipGetLastError();
 }
 
