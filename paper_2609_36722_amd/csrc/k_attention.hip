@@ -402,11 +402,12 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
 }
 
 // Merge the n_split partials: weight of split s is l_s * 2^(m_s - max_s m_s).
-// Workgroup b serves KV head g = b % Hkv and 4 tokens: with Hkv = 8 it runs on
-// the XCD whose workgroups wrote those partials, so they are read from that
-// XCD's L2.  A wave merges the 4 query heads of one token; 16 lanes per
-// (token, head) row, lane owning dims 8 (lane % 16) .. +7; every split's data
-// is requested before any is used.
+// Workgroup b serves KV head g = b % Hkv and 4 tokens (with Hkv = 8, on the
+// XCD whose workgroups wrote those partials; the partials still come back
+// through the memory side, as the attention kernel's end writes its L2 back).
+// A wave merges the 4 query heads of one token; 16 lanes per (token, head)
+// row, lane owning dims 8 (lane % 16) .. +7; every split's data is requested
+// before any is used.
 constexpr int kMaxSplit = 16;
 
 template <int NS>
