@@ -25,9 +25,16 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
   const int slot = (int)(grp - (int64_t)tok * n_slots);
   if (tok >= p.total_q) return;  // whole 8-lane groups leave together
 
-  int r = 0;
-  while (r + 1 < p.n_req && tok >= p.req[r + 1].q_start) ++r;
-  const NormRopeReq rq = p.req[r];
+  // the request of this token: a constant-offset argument read (scalar) for a
+  // single request, a per-lane search otherwise
+  NormRopeReq rq;
+  if (p.n_req == 1) {
+    rq = p.req[0];
+  } else {
+    int r = 0;
+    while (r + 1 < p.n_req && tok >= p.req[r + 1].q_start) ++r;
+    rq = p.req[r];
+  }
   const int i = tok - rq.q_start;
   const int pos = rq.pos0 + i;
 
@@ -40,10 +47,22 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
                      : p.k_cache + g * p.kv_head_stride + (int64_t)(rq.kv_row0 + i) * kHeadDim;
   const int j0 = 8 * lane8;
 
+  // every load of the lane first (row, gamma, angles and, for a KV slot, the
+  // value row): one memory round trip
   const u32x4 xa = *reinterpret_cast<const u32x4*>(src + j0);
   const u32x4 xb = *reinterpret_cast<const u32x4*>(src + 64 + j0);
   const u32x4 ga = *reinterpret_cast<const u32x4*>(gam + j0);
   const u32x4 gb = *reinterpret_cast<const u32x4*>(gam + 64 + j0);
+  const f32x4* cs4 = reinterpret_cast<const f32x4*>(p.rope + (int64_t)pos * 64 + j0);
+  f32x4 cs[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) cs[e] = cs4[e];  // (cos, sin) of pairs j0 + 2e and j0 + 2e + 1
+  u32x4 va = u32x4{0u, 0u, 0u, 0u}, vb = u32x4{0u, 0u, 0u, 0u};
+  if (!is_q) {
+    const bf16_t* vs = p.v_raw + (int64_t)tok * p.ld_kv + g * kHeadDim;
+    va = *reinterpret_cast<const u32x4*>(vs + j0);
+    vb = *reinterpret_cast<const u32x4*>(vs + 64 + j0);
+  }
   float x0[8], x1[8];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -59,11 +78,9 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
   ss += __shfl_xor(ss, 2, 8);
   ss += __shfl_xor(ss, 4, 8);
   const float inv = 1.0f / sqrtf(ss * (1.0f / kHeadDim) + p.eps);
-  const f32x4* cs4 = reinterpret_cast<const f32x4*>(p.rope + (int64_t)pos * 64 + j0);
   u32x4 oa, ob;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const f32x4 cs = cs4[e];  // (cos, sin) of pairs j0 + 2e and j0 + 2e + 1
     float o0[2], o1[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -72,7 +89,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
       const float g1 = __uint_as_float(u ? (gb[e] & 0xFFFF0000u) : (gb[e] << 16));
       const float y0 = x0[k] * inv * g0;
       const float y1 = x1[k] * inv * g1;
-      const float c = cs[2 * u], sn = cs[2 * u + 1];
+      const float c = cs[e][2 * u], sn = cs[e][2 * u + 1];
       o0[u] = y0 * c - y1 * sn;
       o1[u] = y1 * c + y0 * sn;
     }
@@ -83,10 +100,9 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
   *reinterpret_cast<u32x4*>(dst + 64 + j0) = ob;
 
   if (!is_q) {
-    const bf16_t* vs = p.v_raw + (int64_t)tok * p.ld_kv + g * kHeadDim;
     bf16_t* vd = p.v_cache + g * p.kv_head_stride + (int64_t)(rq.kv_row0 + i) * kHeadDim;
-    *reinterpret_cast<u32x4*>(vd + j0) = *reinterpret_cast<const u32x4*>(vs + j0);
-    *reinterpret_cast<u32x4*>(vd + 64 + j0) = *reinterpret_cast<const u32x4*>(vs + 64 + j0);
+    *reinterpret_cast<u32x4*>(vd + j0) = va;
+    *reinterpret_cast<u32x4*>(vd + 64 + j0) = vb;
   }
 }
 
