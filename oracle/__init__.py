@@ -22,4 +22,9 @@ from .attuner_ref import (  # noqa: F401
     attention_probs,
     suffix_layer,
     full_prefill,
+    silu,
+    linear,
+    swiglu,
+    decoder_layer,
+    first_token,
 )

@@ -277,3 +277,62 @@ def full_prefill(x, wq, wk, wv, gamma_q, gamma_k, pos0: int, n_q_heads: int,
     empty = np.zeros((0, n_kv_heads, d))
     return suffix_layer(x, wq, wk, wv, a, b, scale, gamma_q, gamma_k, empty, empty,
                         pos0, n_q_heads, n_kv_heads, theta, eps, rows=rows)
+
+
+# ----------------------------------------------------------------------------
+# the decoder layer around the path (the base models of section 5.1 are
+# Qwen3 decoder stacks; the paper times prefill up to the greedy first token,
+# appendix A.2).  The layer structure is Qwen3's: pre-norm RMSNorm, attention,
+# residual, RMSNorm, SwiGLU MLP, residual; a final RMSNorm and the LM head.
+# ----------------------------------------------------------------------------
+
+def silu(z: np.ndarray) -> np.ndarray:
+    """silu(z) = z / (1 + e^-z) (the gate activation of the SwiGLU MLP)."""
+    z = np.asarray(z, np.float64)
+    with np.errstate(over="ignore"):
+        return z / (1.0 + np.exp(-z))
+
+
+def linear(x: np.ndarray, w: np.ndarray, residual: Optional[np.ndarray] = None) -> np.ndarray:
+    """x W^T (+ residual): o_proj and down_proj, with the residual connection."""
+    out = np.asarray(x, np.float64) @ np.asarray(w, np.float64).T
+    return out if residual is None else out + np.asarray(residual, np.float64)
+
+
+def swiglu(x: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray) -> np.ndarray:
+    """silu(x W_gate^T) * (x W_up^T): the MLP's gated hidden activation."""
+    return silu(linear(x, w_gate)) * linear(x, w_up)
+
+
+def decoder_layer(h, w: Dict[str, np.ndarray], k_art, v_art, pos0: int, n_q_heads: int,
+                  n_kv_heads: int, theta: float, eps: float, scale: float = 0.0) -> Dict[str, np.ndarray]:
+    """One decoder layer around the adapted attention of :func:`suffix_layer`.
+
+    h [S][H] is the residual stream of the suffix tokens; w holds wq, wk, wv,
+    a, b (or None), gamma_q, gamma_k (the path), gamma_in, wo, gamma_post,
+    w_gate, w_up, w_down:
+        x  = RMSNorm(h) * gamma_in
+        o  = attention of the suffix over the artifacts (suffix_layer on x)
+        h1 = h + o W_o^T
+        h2 = h1 + down(silu(x2 W_gate^T) * (x2 W_up^T)),  x2 = RMSNorm(h1) * gamma_post
+    Returns h2 and the pieces (x, o, h1, x2, mlp hidden, and the suffix K/V).
+    """
+    h = np.asarray(h, np.float64)
+    S = h.shape[0]
+    x = rms_norm_heads(h, w["gamma_in"], eps)
+    att = suffix_layer(x, w["wq"], w["wk"], w["wv"], w.get("a"), w.get("b"), scale, w["gamma_q"],
+                       w["gamma_k"], k_art, v_art, pos0, n_q_heads, n_kv_heads, theta, eps)
+    o = att["o"].reshape(S, -1)
+    h1 = linear(o, w["wo"], h)
+    x2 = rms_norm_heads(h1, w["gamma_post"], eps)
+    g = swiglu(x2, w["w_gate"], w["w_up"])
+    h2 = linear(g, w["w_down"], h1)
+    return {"x": x, "o": o, "h1": h1, "x2": x2, "mlp": g, "h": h2, "k_hat": att["k_hat"], "v": att["v"]}
+
+
+def first_token(h_last: np.ndarray, gamma_final: np.ndarray, w_lm: np.ndarray, eps: float):
+    """Greedy first token of each request: argmax over the vocabulary of
+    RMSNorm(h_last) * gamma_final W_lm^T (smallest index on ties).  h_last
+    [n][H] holds the last suffix token of each request.  Returns (ids, logits)."""
+    logits = linear(rms_norm_heads(h_last, gamma_final, eps), w_lm)
+    return np.argmax(logits, axis=-1), logits

@@ -18,6 +18,9 @@ from .workloads import (
     artifact_kv,
     suffix_hidden,
     prefill_hidden,
+    decoder_weights,
+    lm_weights,
+    suffix_tokens,
 )
 
 __all__ = [
@@ -33,4 +36,7 @@ __all__ = [
     "artifact_kv",
     "suffix_hidden",
     "prefill_hidden",
+    "decoder_weights",
+    "lm_weights",
+    "suffix_tokens",
 ]

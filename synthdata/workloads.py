@@ -29,7 +29,7 @@ import numpy as np
 from .bf16 import f32_to_bf16_bits
 
 # purposes (second seed word)
-_STRUCT, _WEIGHTS, _ARTIFACT, _SUFFIX, _PREFILL, _GAMMA = 0, 1, 2, 3, 4, 5
+_STRUCT, _WEIGHTS, _ARTIFACT, _SUFFIX, _PREFILL, _GAMMA, _DECODER, _LMHEAD, _TOKENS = 0, 1, 2, 3, 4, 5, 6, 7, 8
 
 
 @dataclass(frozen=True)
@@ -246,3 +246,44 @@ def prefill_hidden(wl: Workload, request_index: int, layer: int) -> np.ndarray:
     req = wl.requests[request_index]
     n = wl.art_len(req) + req.suffix_len
     return _normal_bf16(_rng(wl.index, _PREFILL, request_index, layer), (n, wl.shape.hidden), 1.0)
+
+
+# ----------------------------------------------------------------------------
+# the decoder layer around the path (o_proj, MLP, norms, embedding, LM head)
+# ----------------------------------------------------------------------------
+
+def _gamma(wl: Workload, n: int, *words: int) -> np.ndarray:
+    if wl.gamma == "ones":
+        return f32_to_bf16_bits(np.ones(n, np.float32))
+    return f32_to_bf16_bits(_rng(wl.index, _GAMMA, *words).uniform(0.5, 1.5, size=n).astype(np.float32))
+
+
+def decoder_weights(wl: Workload, layer: int, intermediate: int) -> Dict[str, np.ndarray]:
+    """bf16 bits of one layer's weights outside the attention path.
+
+    wo [hidden][q_dim], w_gate / w_up [intermediate][hidden], w_down
+    [hidden][intermediate], each ~ N(0, 1/sqrt(fan_in)) (N(0, 0.02) at the 4B
+    hidden size, and unit-scale activations at any test size); gamma_in,
+    gamma_post [hidden] as the workload's gamma setting.
+    """
+    s, H, I = wl.shape, wl.shape.hidden, int(intermediate)
+    d = lambda k, shape, fan: _normal_bf16(_rng(wl.index, _DECODER, layer, k), shape, 1.0 / float(np.sqrt(fan)))
+    return {"wo": d(0, (H, s.q_dim), s.q_dim), "w_gate": d(1, (I, H), H), "w_up": d(2, (I, H), H),
+            "w_down": d(3, (H, I), I), "gamma_in": _gamma(wl, H, 1000 + layer, 0),
+            "gamma_post": _gamma(wl, H, 1000 + layer, 1)}
+
+
+def lm_weights(wl: Workload, vocab: int) -> Dict[str, np.ndarray]:
+    """bf16 bits of the embedding table [vocab][hidden] ~ N(0, 1) (hidden states
+    of unit scale, as suffix_hidden draws them), the LM head [vocab][hidden] ~
+    N(0, 1/sqrt(hidden)) and the final norm's gamma [hidden]."""
+    H = wl.shape.hidden
+    return {"embed": _normal_bf16(_rng(wl.index, _LMHEAD, 0), (vocab, H), 1.0),
+            "w_lm": _normal_bf16(_rng(wl.index, _LMHEAD, 1), (vocab, H), 1.0 / float(np.sqrt(H))),
+            "gamma_final": _gamma(wl, H, 2000)}
+
+
+def suffix_tokens(wl: Workload, request_index: int, vocab: int) -> np.ndarray:
+    """Token ids of one request's suffix, uniform over the vocabulary (int32)."""
+    S = wl.requests[request_index].suffix_len
+    return _rng(wl.index, _TOKENS, request_index).integers(0, vocab, size=S).astype(np.int32)

@@ -507,3 +507,89 @@ def test_lora_delta_case_catches_a_dropped_update():
     ref = _run(wl, s, w, ka, va, x)
     assert not o_within(_run(wl, s, w, ka, va, x, scale=0.0)["o"], ref["o"])
     assert not o_within(_run(wl, s, w, ka, va, x, scale=wl.scale * 0.5)["o"], ref["o"])
+
+
+# ----------------------------------------------------------------------------
+# the decoder layer around the path
+# ----------------------------------------------------------------------------
+
+def test_silu_identity_limits_and_minimum():
+    z = np.linspace(-30.0, 30.0, 6001)
+    # silu(z) - silu(-z) = z, since sigma(-z) = 1 - sigma(z)
+    assert np.max(np.abs(oracle.silu(z) - oracle.silu(-z) - z)) <= 1e-12
+    assert oracle.silu(np.array([0.0]))[0] == 0.0
+    assert abs(oracle.silu(np.array([60.0]))[0] - 60.0) < 1e-20 * 60 + 1e-24
+    assert oracle.silu(np.array([-800.0]))[0] == 0.0          # e^800 overflows: the limit, no NaN
+    # the minimum sits at x* with 1 + e^x* = -x* (derivative zero), where silu(x*) = x* + 1;
+    # solve that fixed point by bisection and compare with a fine grid search of the oracle
+    lo, hi = -2.0, -1.0
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        if 1.0 + math.exp(mid) + mid > 0.0:
+            hi = mid
+        else:
+            lo = mid
+    x_star = 0.5 * (lo + hi)
+    grid = np.linspace(-1.5, -1.0, 500001)
+    vals = oracle.silu(grid)
+    i = int(np.argmin(vals))
+    assert abs(grid[i] - x_star) <= 2e-6
+    assert abs(vals[i] - (x_star + 1.0)) <= 1e-11
+
+
+def test_swiglu_brute_force():
+    rng = np.random.default_rng(21)
+    x, wg, wu = rng.standard_normal((3, 4)), rng.standard_normal((5, 4)), rng.standard_normal((5, 4))
+    got = oracle.swiglu(x, wg, wu)
+    for t in range(3):
+        for j in range(5):
+            g = sum(x[t, k] * wg[j, k] for k in range(4))
+            u = sum(x[t, k] * wu[j, k] for k in range(4))
+            assert abs(got[t, j] - g / (1.0 + math.exp(-g)) * u) <= 1e-12
+
+
+def _tiny_layer_weights(rng, H=256, I=128, Hq=32, Hkv=8, d=128):
+    f = lambda *s, std=1.0: rng.standard_normal(s) * std
+    return {"wq": f(Hq * d, H, std=0.02), "wk": f(Hkv * d, H, std=0.02), "wv": f(Hkv * d, H, std=0.02),
+            "a": None, "b": None, "gamma_q": 1.0 + 0.1 * f(d), "gamma_k": 1.0 + 0.1 * f(d),
+            "gamma_in": 1.0 + 0.1 * f(H), "wo": f(H, Hq * d, std=0.02), "gamma_post": 1.0 + 0.1 * f(H),
+            "w_gate": f(I, H, std=0.05), "w_up": f(I, H, std=0.05), "w_down": f(H, I, std=0.05)}
+
+
+def test_decoder_layer_residual_identities():
+    rng = np.random.default_rng(22)
+    w = _tiny_layer_weights(rng)
+    h = rng.standard_normal((5, 256))
+    k_art, v_art = rng.standard_normal((7, 8, 128)), rng.standard_normal((7, 8, 128))
+    args = (k_art, v_art, 7, 32, 8, 1e6, 1e-6)
+    # no attention output projection and no MLP output: the residual stream passes unchanged
+    w0 = dict(w, wo=np.zeros_like(w["wo"]), w_down=np.zeros_like(w["w_down"]))
+    assert np.array_equal(oracle.decoder_layer(h, w0, *args)["h"], h)
+    # a zero gate makes silu(0) = 0: the MLP adds nothing to h1
+    wg0 = dict(w, w_gate=np.zeros_like(w["w_gate"]))
+    r = oracle.decoder_layer(h, wg0, *args)
+    assert np.array_equal(r["h"], r["h1"]) and not r["mlp"].any()
+    # the attention part only enters through o W_o^T: scaling W_o by 2 doubles h1 - h
+    r1 = oracle.decoder_layer(h, w, *args)
+    r2 = oracle.decoder_layer(h, dict(w, wo=2.0 * w["wo"]), *args)
+    assert np.max(np.abs((r2["h1"] - h) - 2.0 * (r1["h1"] - h))) <= 1e-12
+
+
+def test_first_token_brute_force_and_ties():
+    rng = np.random.default_rng(23)
+    H, V = 16, 40
+    h = rng.standard_normal((3, H))
+    g = 1.0 + 0.1 * rng.standard_normal(H)
+    w = rng.standard_normal((V, H))
+    ids, logits = oracle.first_token(h, g, w, 1e-6)
+    for r in range(3):
+        x = [g[k] * h[r, k] / math.sqrt(sum(v * v for v in h[r]) / H + 1e-6) for k in range(H)]
+        lg = [sum(x[k] * w[v, k] for k in range(H)) for v in range(V)]
+        best = max(range(V), key=lambda v: (lg[v], -v))
+        assert ids[r] == best and abs(logits[r, best] - lg[best]) <= 1e-12
+    # two identical vocabulary rows at the top: the smaller index wins
+    w2 = w.copy()
+    top = int(ids[0])
+    w2[V - 1] = w2[top]
+    ids2, _ = oracle.first_token(h[:1], g, w2, 1e-6)
+    assert ids2[0] == min(top, V - 1)
