@@ -271,6 +271,61 @@ attuner_status attuner_full_prefill(attuner_ctx* ctx, int32_t n_tok, int32_t pos
                                     void* k_out, void* v_out, float* lse, void* stream);
 
 /* --------------------------------------------------------------------------
+ * The decoder layer around the path (the models the method adapts are Qwen3
+ * decoder stacks, section 5.1; the greedy first token ends the timed region
+ * of the paper's time-to-first-token, appendix A.2).  With
+ * these calls a caller chains real layers: h -> rms_norm -> (a3..a5) ->
+ * linear(o, W_o, residual h) -> rms_norm -> gate_up_swiglu -> linear(.,
+ * W_down, residual) -> next layer; then rms_norm of the last token of each
+ * request and lm_head_argmax.  All tensors are bf16 device buffers, 16-byte
+ * aligned, rows contiguous; errors EINVAL / ERANGE before any launch.
+ *
+ * attuner_embed: out[t] = table[token_ids[t]] for t < n_tok: the suffix
+ *   tokens' embedding rows, the residual stream entering layer 0.  token_ids:
+ *   host int32, each in [0, vocab) (else ERANGE); table: [vocab][hidden];
+ *   out: [n_tok][hidden].  Copies the ids through a context workspace.
+ *
+ * attuner_rms_norm: out[r] = x[rows[r]] / sqrt(mean(x[rows[r]]^2) + eps) * gamma
+ *   over the model's hidden size (<= 8192), fp32 arithmetic.  x holds
+ *   n_x_rows rows of stride ld_x (>= hidden, multiple of 8); rows (host int32,
+ *   n_rows entries, each in [0, n_x_rows)) or NULL for rows 0 .. n_rows - 1;
+ *   out: [n_rows][hidden].  eps is the context's rms_eps.
+ *
+ * attuner_linear: out[n_tok][n_out] = x[n_tok][k_dim] w[n_out][k_dim]^T
+ *   (+ residual[n_tok][n_out] when residual is not NULL; residual may be
+ *   out).  fp32 accumulation, one bf16 rounding.  k_dim and n_out: positive
+ *   multiples of 64.
+ *
+ * attuner_gate_up_swiglu: out[n_tok][n_inter] = silu(x W_gate^T) * (x W_up^T)
+ *   with silu(z) = z / (1 + e^-z) (the SwiGLU MLP).  w_gu: [2 n_inter][k_dim]
+ *   with gate row j at row 2j and up row j at row 2j + 1.  n_inter: a
+ *   positive multiple of 32; k_dim: a positive multiple of 64.
+ *
+ * attuner_lm_head_argmax: ids[r] = argmax_v x[r] . w_lm[v] over v < vocab
+ *   (fp32 logits; ties go to the smallest index), max_logit[r] = that logit
+ *   (max_logit may be NULL).  x: [n_rows][hidden]; w_lm: [vocab][hidden];
+ *   vocab a positive multiple of 64; ids (int32) and max_logit (fp32) on the
+ *   device.  Uses a context workspace of n_rows * vocab floats.
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_embed(attuner_ctx* ctx, int32_t n_tok, const int32_t* token_ids,
+                             const void* table, int32_t vocab, void* out, void* stream);
+
+attuner_status attuner_rms_norm(attuner_ctx* ctx, const void* x, int64_t n_x_rows, int64_t ld_x,
+                                const int32_t* rows, int32_t n_rows, const void* gamma, void* out,
+                                void* stream);
+
+attuner_status attuner_linear(attuner_ctx* ctx, int32_t n_tok, const void* x, int32_t k_dim,
+                              const void* w, int32_t n_out, const void* residual, void* out,
+                              void* stream);
+
+attuner_status attuner_gate_up_swiglu(attuner_ctx* ctx, int32_t n_tok, const void* x, int32_t k_dim,
+                                      const void* w_gu, int32_t n_inter, void* out, void* stream);
+
+attuner_status attuner_lm_head_argmax(attuner_ctx* ctx, int32_t n_rows, const void* x,
+                                      const void* w_lm, int32_t vocab, int32_t* ids,
+                                      float* max_logit, void* stream);
+
+/* --------------------------------------------------------------------------
  * Kernel timing.  Between attuner_trace_begin and attuner_trace_end, every
  * kernel this library launches from the calling thread is bracketed by a
  * pair of HIP events on its stream.  attuner_trace_end waits for the

@@ -216,6 +216,57 @@ class Context:
                                         int(rank), float(scale), int(lora_cols), _ptr(out), _stream(stream)),
                "attuner_qproj_lora")
 
+    # ---- the decoder layer around the path ------------------------------------------
+    def embed(self, token_ids: Sequence[int], table: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+        """out[t] = table[token_ids[t]]: the embedding rows of the suffix tokens."""
+        H = self.cfg.hidden
+        V = int(table.numel()) // H
+        n = len(token_ids)
+        _need(out, n * H, "out")
+        _check(lib().attuner_embed(self._h, n, _i32(token_ids), _ptr(table), V, _ptr(out), _stream(stream)),
+               "attuner_embed")
+
+    def rms_norm(self, x: torch.Tensor, gamma: torch.Tensor, out: torch.Tensor,
+                 rows: Optional[Sequence[int]] = None, stream=None) -> None:
+        """out[r] = RMSNorm(x[rows[r]]) * gamma over the hidden size (rows None: every row)."""
+        H = self.cfg.hidden
+        n_x = int(x.numel()) // H
+        n = n_x if rows is None else len(rows)
+        _need(gamma, H, "gamma")
+        _need(out, n * H, "out")
+        _check(lib().attuner_rms_norm(self._h, _ptr(x), n_x, H, _i32(rows) if rows is not None else None, n,
+                                      _ptr(gamma), _ptr(out), _stream(stream)), "attuner_rms_norm")
+
+    def linear(self, x: torch.Tensor, w: torch.Tensor, out: torch.Tensor, residual: Optional[torch.Tensor] = None,
+               stream=None) -> None:
+        """out = x w^T (+ residual); x [T][K], w [N][K], out and residual [T][N]."""
+        N, K = int(w.shape[0]), int(w.shape[1])
+        T = int(x.numel()) // K
+        _need(x, T * K, "x")
+        _need(out, T * N, "out")
+        _need(residual, T * N, "residual")
+        _check(lib().attuner_linear(self._h, T, _ptr(x), K, _ptr(w), N, _ptr(residual), _ptr(out), _stream(stream)),
+               "attuner_linear")
+
+    def gate_up_swiglu(self, x: torch.Tensor, w_gu: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+        """out = silu(x W_gate^T) * (x W_up^T); w_gu [2 I][K] with gate row j at 2j, up row j at 2j + 1."""
+        I2, K = int(w_gu.shape[0]), int(w_gu.shape[1])
+        T = int(x.numel()) // K
+        _need(out, T * (I2 // 2), "out")
+        _check(lib().attuner_gate_up_swiglu(self._h, T, _ptr(x), K, _ptr(w_gu), I2 // 2, _ptr(out), _stream(stream)),
+               "attuner_gate_up_swiglu")
+
+    def lm_head_argmax(self, x: torch.Tensor, w_lm: torch.Tensor, ids: torch.Tensor,
+                       max_logit: Optional[torch.Tensor] = None, stream=None) -> None:
+        """ids[r] = argmax over the vocabulary of x[r] w_lm^T (fp32 logits, smallest index on ties)."""
+        V, H = int(w_lm.shape[0]), self.cfg.hidden
+        n = int(x.numel()) // H
+        _need(ids, n, "ids")
+        _need(max_logit, n, "max_logit")
+        _check(lib().attuner_lm_head_argmax(self._h, n, _ptr(x), _ptr(w_lm), V, _ptr(ids, 4),
+                                            _ptr(max_logit, 4) if max_logit is not None else None,
+                                            _stream(stream)), "attuner_lm_head_argmax")
+
     # ---- norm + rope, attention ---------------------------------------------------
     def _check_cache(self, cu_q, cu_ctx, q_hat, req_kv, cache_rows, q_raw=None, ld_q=0, k_raw=None, v_raw=None,
                      ld_kv=0) -> None:

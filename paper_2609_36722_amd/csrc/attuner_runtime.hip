@@ -205,6 +205,8 @@ struct attuner_ctx {
   DeviceBuf ws_lora;    // LoRA-down slice partials
   DeviceBuf ws_part;    // split-KV partials
   DeviceBuf ws_qkv;     // full prefill: fused projection output
+  DeviceBuf ws_logits;  // LM-head logits (fp32)
+  DeviceBuf ws_rows;    // token ids of an embedding lookup / rows of a row-subset RMSNorm
   DeviceBuf rope;       // (cos, sin) table [rope_pos][64]
   int64_t rope_pos = 0;
   // the block table the last attuner_assemble_table call wrote (the only one
@@ -485,6 +487,8 @@ void attuner_destroy(attuner_ctx* c) {
   c->ws_lora.release();
   c->ws_part.release();
   c->ws_qkv.release();
+  c->ws_logits.release();
+  c->ws_rows.release();
   c->rope.release();
   if (g_tracer == &c->tracer) g_tracer = nullptr;
   c->tracer.release();
@@ -675,6 +679,112 @@ attuner_status attuner_assemble_kv(attuner_ctx* c, int32_t n_req, const int32_t*
                               stream);
   if (st != ATTUNER_OK) return st;
   return attuner_gather_layers(c, block_table, entries, 0, c->cfg.n_layers, req_kv, cache_rows, stream);
+}
+
+attuner_status attuner_rms_norm(attuner_ctx* c, const void* x, int64_t n_x_rows, int64_t ld_x, const int32_t* rows,
+                                int32_t n_rows, const void* gamma, void* out, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  const int dim = c->cfg.hidden;
+  if (n_rows < 0 || n_x_rows < 0) return fail(ATTUNER_EINVAL, "negative row count");
+  if (rows == nullptr && n_rows > n_x_rows) return fail(ATTUNER_ERANGE, "n_rows %d > n_x_rows %lld", n_rows, (long long)n_x_rows);
+  if (n_rows == 0) return ATTUNER_OK;
+  if (!x || !gamma || !out) return fail(ATTUNER_EINVAL, "null x, gamma or out");
+  if (ld_x < dim || ld_x % 8 != 0 || !aligned16(x) || !aligned16(gamma) || !aligned16(out))
+    return fail(ATTUNER_EINVAL, "ld_x %lld must be >= hidden and a multiple of 8; x, gamma, out 16-byte aligned",
+                (long long)ld_x);
+  if (dim > 8192) return fail(ATTUNER_EINVAL, "hidden %d: the norm kernel takes at most 8192", dim);
+  DeviceGuard dg(c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int32_t* rows_dev = nullptr;
+  if (rows != nullptr) {
+    for (int32_t i = 0; i < n_rows; ++i)
+      if (rows[i] < 0 || rows[i] >= n_x_rows)
+        return fail(ATTUNER_ERANGE, "rows[%d] = %d outside [0, %lld)", i, rows[i], (long long)n_x_rows);
+    HIP_TRY(c->ws_rows.ensure((size_t)n_rows * sizeof(int32_t)));
+    HIP_TRY(c->staging.upload(rows, (size_t)n_rows * sizeof(int32_t), c->ws_rows.ptr, s));
+    rows_dev = static_cast<const int32_t*>(c->ws_rows.ptr);
+  }
+  HIP_TRY(launch_rms_norm_rows(static_cast<const uint16_t*>(x), ld_x, rows_dev, n_rows, dim,
+                               static_cast<const uint16_t*>(gamma), c->cfg.rms_eps, static_cast<uint16_t*>(out), s));
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_embed(attuner_ctx* c, int32_t n_tok, const int32_t* token_ids, const void* table,
+                             int32_t vocab, void* out, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (n_tok < 0 || vocab <= 0) return fail(ATTUNER_EINVAL, "n_tok %d, vocab %d", n_tok, vocab);
+  if (n_tok == 0) return ATTUNER_OK;
+  if (!token_ids || !table || !out) return fail(ATTUNER_EINVAL, "null token_ids, table or out");
+  const int dim = c->cfg.hidden;
+  if (dim % 8 != 0 || !aligned16(table) || !aligned16(out))
+    return fail(ATTUNER_EINVAL, "hidden %d must be a multiple of 8; table and out 16-byte aligned", dim);
+  for (int32_t i = 0; i < n_tok; ++i)
+    if (token_ids[i] < 0 || token_ids[i] >= vocab)
+      return fail(ATTUNER_ERANGE, "token_ids[%d] = %d outside [0, %d)", i, token_ids[i], vocab);
+  DeviceGuard dg(c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(c->ws_rows.ensure((size_t)n_tok * sizeof(int32_t)));
+  HIP_TRY(c->staging.upload(token_ids, (size_t)n_tok * sizeof(int32_t), c->ws_rows.ptr, s));
+  HIP_TRY(launch_embed_rows(static_cast<const uint16_t*>(table), static_cast<const int32_t*>(c->ws_rows.ptr), n_tok,
+                            dim, static_cast<uint16_t*>(out), s));
+  return ATTUNER_OK;
+}
+
+static attuner_status check_gemm_args(int32_t n_tok, const void* x, int32_t k_dim, const void* w, int32_t n_out,
+                                      const void* out) {
+  if (n_tok < 0) return fail(ATTUNER_EINVAL, "n_tok < 0");
+  if (k_dim <= 0 || k_dim % 64 != 0) return fail(ATTUNER_EINVAL, "k_dim %d must be a positive multiple of 64", k_dim);
+  if (n_out <= 0 || n_out % 64 != 0) return fail(ATTUNER_EINVAL, "n_out %d must be a positive multiple of 64", n_out);
+  if (n_tok > 0 && (!x || !w || !out)) return fail(ATTUNER_EINVAL, "null x, w or out");
+  if (!aligned16(x) || !aligned16(w) || !aligned16(out)) return fail(ATTUNER_EINVAL, "x, w and out must be 16-byte aligned");
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_linear(attuner_ctx* c, int32_t n_tok, const void* x, int32_t k_dim, const void* w,
+                              int32_t n_out, const void* residual, void* out, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  attuner_status st = check_gemm_args(n_tok, x, k_dim, w, n_out, out);
+  if (st != ATTUNER_OK) return st;
+  if (residual && !aligned16(residual)) return fail(ATTUNER_EINVAL, "residual must be 16-byte aligned");
+  if (n_tok == 0) return ATTUNER_OK;
+  DeviceGuard dg(c->device);
+  const GemmEpi epi{residual ? kEpiResidual : kEpiBf16, static_cast<const uint16_t*>(residual), nullptr};
+  HIP_TRY(launch_gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), n_tok, n_out, k_dim, epi,
+                      static_cast<uint16_t*>(out), static_cast<hipStream_t>(stream)));
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_gate_up_swiglu(attuner_ctx* c, int32_t n_tok, const void* x, int32_t k_dim, const void* w_gu,
+                                      int32_t n_inter, void* out, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (n_inter <= 0 || n_inter % 32 != 0) return fail(ATTUNER_EINVAL, "n_inter %d must be a positive multiple of 32", n_inter);
+  attuner_status st = check_gemm_args(n_tok, x, k_dim, w_gu, 2 * n_inter, out);
+  if (st != ATTUNER_OK) return st;
+  if (n_tok == 0) return ATTUNER_OK;
+  DeviceGuard dg(c->device);
+  HIP_TRY(launch_gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_gu), n_tok, 2 * n_inter, k_dim,
+                      GemmEpi{kEpiSwiglu, nullptr, nullptr}, static_cast<uint16_t*>(out),
+                      static_cast<hipStream_t>(stream)));
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_lm_head_argmax(attuner_ctx* c, int32_t n_rows, const void* x, const void* w_lm, int32_t vocab,
+                                      int32_t* ids, float* max_logit, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  const int H = c->cfg.hidden;
+  if (vocab <= 0 || vocab % 64 != 0) return fail(ATTUNER_EINVAL, "vocab %d must be a positive multiple of 64", vocab);
+  attuner_status st = check_gemm_args(n_rows, x, H, w_lm, vocab, x);
+  if (st != ATTUNER_OK) return st;
+  if (n_rows == 0) return ATTUNER_OK;
+  if (!ids) return fail(ATTUNER_EINVAL, "null ids");
+  DeviceGuard dg(c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(c->ws_logits.ensure((size_t)n_rows * vocab * sizeof(float)));
+  float* logits = static_cast<float*>(c->ws_logits.ptr);
+  HIP_TRY(launch_gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_lm), n_rows, vocab, H,
+                      GemmEpi{kEpiF32, nullptr, logits}, nullptr, s));
+  HIP_TRY(launch_argmax_rows(logits, n_rows, vocab, ids, max_logit, s));
+  return ATTUNER_OK;
 }
 
 attuner_status attuner_qproj_lora(attuner_ctx* c, int32_t n_tok, const void* x, const void* w, int32_t n_out,

@@ -47,7 +47,7 @@ __device__ __forceinline__ void lora_epilogue_store(f32x16 (&acc)[FN][FM], int n
                                                     int l32, int hi, int M, int N, const bf16_t* __restrict__ b,
                                                     int rank, int r_pad, int lora_cols,
                                                     const float* __restrict__ t_part, int n_slice,
-                                                    const float* t_lds, bf16_t* __restrict__ out) {
+                                                    const float* t_lds, const GemmEpi& epi, bf16_t* out) {
   if (r_pad > 0 && n_base < lora_cols) {
     const int64_t slice_stride = (int64_t)M * r_pad;
     // B rows as 16-byte loads when they are whole 16-byte runs
@@ -121,10 +121,29 @@ __device__ __forceinline__ void lora_epilogue_store(f32x16 (&acc)[FN][FM], int n
       const int nb = n_base + i * 32;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int n = nb + 8 * q + 4 * hi;
+        const int n = nb + 8 * q + 4 * hi;  // features n .. n + 3 of token m
+        float c[4] = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        if (epi.mode == kEpiF32) {
+          *reinterpret_cast<f32x4*>(epi.out_f32 + (int64_t)m * N + n) = f32x4{c[0], c[1], c[2], c[3]};
+          continue;
+        }
+        if (epi.mode == kEpiSwiglu) {
+          // (gate, up) pairs (n, n + 1) and (n + 2, n + 3) -> outputs n / 2, n / 2 + 1
+          const float s0 = c[0] / (1.0f + __expf(-c[0])) * c[1];
+          const float s1 = c[2] / (1.0f + __expf(-c[2])) * c[3];
+          *reinterpret_cast<uint32_t*>(out + (int64_t)m * (N / 2) + n / 2) = pack_bf16x2(s0, s1);
+          continue;
+        }
+        if (epi.mode == kEpiResidual) {
+          const u32x2 r = *reinterpret_cast<const u32x2*>(epi.residual + (int64_t)m * N + n);
+          c[0] += __uint_as_float(r[0] << 16);
+          c[1] += __uint_as_float(r[0] & 0xFFFF0000u);
+          c[2] += __uint_as_float(r[1] << 16);
+          c[3] += __uint_as_float(r[1] & 0xFFFF0000u);
+        }
         u32x2 pk;
-        pk[0] = pack_bf16x2(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
-        pk[1] = pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+        pk[0] = pack_bf16x2(c[0], c[1]);
+        pk[1] = pack_bf16x2(c[2], c[3]);
         *reinterpret_cast<u32x2*>(out + (int64_t)m * N + n) = pk;
       }
     }
@@ -143,7 +162,7 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
                                                                    const bf16_t* __restrict__ a, float scale,
                                                                    const bf16_t* __restrict__ b, int rank, int r_pad,
                                                                    int lora_cols, const float* __restrict__ t_part,
-                                                                   int n_slice, bf16_t* __restrict__ out, int n_mt,
+                                                                   int n_slice, GemmEpi epi, bf16_t* out, int n_mt,
                                                                    int n_nt) {
   constexpr int NW = WN * WM;
   constexpr int TN = BN / WN, TM = BM / WM;
@@ -300,7 +319,7 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
   }
 
   lora_epilogue_store<FN, FM>(acc, n0 + wn * TN, m0 + wm * TM, wm * TM, l32, hi, M, N, b, rank, r_pad, lora_cols,
-                              t_part, n_slice, t_lds, out);
+                              t_part, n_slice, t_lds, epi, out);
 }
 
 // t = scale * x A^T with MFMAs, as fp32 partial sums per 256-wide slice of the
@@ -367,9 +386,11 @@ hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
-                            const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad, int lora_cols,
-                            const float* t_part, uint16_t* out, hipStream_t stream) {
+namespace {
+
+hipError_t launch_gemm_any(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden, const uint16_t* a,
+                           float scale, const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
+                           GemmEpi epi, uint16_t* out, hipStream_t stream) {
   if (n_tok == 0) return hipSuccess;
   const int n_slice = lora_down_slices(hidden);
   // Tile choice.  One workgroup per CU at a time, and a workgroup's k-loop
@@ -397,7 +418,7 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
 #define ATTUNER_GEMM(BM_, BN_, WN_, WM_, NST_)                                                               \
   ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, WM_, NST_>),                           \
                  dim3(((n_tok + (BM_) - 1) / (BM_)) * (n_out / (BN_))), dim3(64 * (WN_) * (WM_)), stream, x, w, \
-                 n_tok, n_out, hidden, a, scale, b, rank, r_pad, lora_cols, t_part, n_slice, out,                  \
+                 n_tok, n_out, hidden, a, scale, b, rank, r_pad, lora_cols, t_part, n_slice, epi, out,             \
                  (n_tok + (BM_) - 1) / (BM_), n_out / (BN_))
   switch (best) {
     case 0: ATTUNER_GEMM(256, 256, 4, 2, 2); break;
@@ -407,10 +428,24 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
     case 4: ATTUNER_GEMM(128, 96, 3, 2, 4); break;
     case 5: ATTUNER_GEMM(64, 96, 3, 2, 5); break;
     case 6: ATTUNER_GEMM(64, 64, 2, 2, 6); break;
-    default: return hipErrorInvalidValue;  // n_out is a multiple of 128: 64x64 always fits
+    default: return hipErrorInvalidValue;  // callers keep n_out a multiple of 64: 64x64 always fits
   }
 #undef ATTUNER_GEMM
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
+                            const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad, int lora_cols,
+                            const float* t_part, uint16_t* out, hipStream_t stream) {
+  return launch_gemm_any(x, w, n_tok, n_out, hidden, a, scale, b, rank, r_pad, lora_cols, t_part,
+                         GemmEpi{kEpiBf16, nullptr, nullptr}, out, stream);
+}
+
+hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, GemmEpi epi,
+                       uint16_t* out, hipStream_t stream) {
+  return launch_gemm_any(x, w, n_tok, n_out, k_dim, nullptr, 0.f, nullptr, 0, 0, 0, nullptr, epi, out, stream);
 }
 
 }  // namespace attuner

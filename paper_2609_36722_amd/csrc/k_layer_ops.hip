@@ -1,0 +1,161 @@
+// Row kernels of the decoder layer around the path: the embedding lookup of
+// the suffix tokens, the hidden-size RMSNorm (the layer's input and
+// post-attention norms and the final norm) and the greedy pick of the first
+// generated token over the vocabulary.
+//
+// embed_rows_kernel: one wave per token; out[t] = table[ids[t]] as 16-byte
+// copies (dim a multiple of 8).
+//
+// rms_norm_rows_kernel: one wave per row; lane l holds the 16-byte chunks l,
+// l + 64, ... of the row (all of it stays in registers), the sum of squares
+// is an in-lane sum plus a wave reduction, and the output is written from
+// the same registers.  dim is a multiple of 8 and at most 64 * 8 * kMaxPass.
+//
+// argmax_rows_kernel: one 1024-thread workgroup per row; thread t scans the
+// 16-byte groups t, t + 1024, ... keeping (largest value, smallest index),
+// then a wave reduction and one through LDS.
+
+#include "common.h"
+#include "kernels.h"
+
+namespace attuner {
+
+namespace {
+
+constexpr int kMaxPass = 16;  // dim <= 8192
+
+__global__ __launch_bounds__(256) void embed_rows_kernel(const bf16_t* __restrict__ table,
+                                                         const int32_t* __restrict__ ids, int n_tok, int dim,
+                                                         bf16_t* __restrict__ out) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= n_tok) return;
+  const int lane = threadIdx.x & 63;
+  const u32x4* src = reinterpret_cast<const u32x4*>(table + (int64_t)ids[t] * dim);
+  u32x4* dst = reinterpret_cast<u32x4*>(out + (int64_t)t * dim);
+  for (int c = lane; c < dim / 8; c += 64) dst[c] = src[c];
+}
+
+__global__ __launch_bounds__(256) void rms_norm_rows_kernel(const bf16_t* __restrict__ x, int64_t ld_x,
+                                                            const int32_t* __restrict__ rows, int n_rows, int dim,
+                                                            const bf16_t* __restrict__ gamma, float eps,
+                                                            bf16_t* __restrict__ out) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= n_rows) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t src_row = rows != nullptr ? rows[r] : r;
+  const bf16_t* xr = x + src_row * ld_x;
+  const int n_chunk = dim / 8;
+  u32x4 v[kMaxPass];
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < kMaxPass; ++k) {
+    const int c = lane + 64 * k;
+    v[k] = u32x4{0u, 0u, 0u, 0u};
+    if (c < n_chunk) v[k] = *reinterpret_cast<const u32x4*>(xr + 8 * c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __uint_as_float(v[k][e] << 16), hi = __uint_as_float(v[k][e] & 0xFFFF0000u);
+      ss += lo * lo + hi * hi;
+    }
+  }
+  ss = wave_sum(ss);
+  const float inv = 1.0f / sqrtf(ss / (float)dim + eps);
+  bf16_t* orow = out + (int64_t)r * dim;
+#pragma unroll
+  for (int k = 0; k < kMaxPass; ++k) {
+    const int c = lane + 64 * k;
+    if (c >= n_chunk) continue;
+    const u32x4 g = *reinterpret_cast<const u32x4*>(gamma + 8 * c);
+    u32x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __uint_as_float(v[k][e] << 16) * inv * __uint_as_float(g[e] << 16);
+      const float hi = __uint_as_float(v[k][e] & 0xFFFF0000u) * inv * __uint_as_float(g[e] & 0xFFFF0000u);
+      o[e] = pack_bf16x2(lo, hi);
+    }
+    *reinterpret_cast<u32x4*>(orow + 8 * c) = o;
+  }
+}
+
+// (value, index) order: larger value first, then smaller index
+__device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
+  return v > bv || (v == bv && i < bi);
+}
+
+__global__ __launch_bounds__(1024) void argmax_rows_kernel(const float* __restrict__ logits, int n,
+                                                           int32_t* __restrict__ ids, float* __restrict__ max_out) {
+  __shared__ float sv[16];
+  __shared__ int si[16];
+  const float* row = logits + (int64_t)blockIdx.x * n;
+  float bv = -INFINITY;
+  int bi = n;  // no element seen
+  const int n4 = n / 4;
+  for (int g = threadIdx.x; g < n4; g += 1024) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(row + 4 * g);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (better(v[e], 4 * g + e, bv, bi)) {
+        bv = v[e];
+        bi = 4 * g + e;
+      }
+  }
+  for (int i = 4 * n4 + threadIdx.x; i < n; i += 1024)
+    if (better(row[i], i, bv, bi)) {
+      bv = row[i];
+      bi = i;
+    }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ov = __shfl_xor(bv, off, 64);
+    const int oi = __shfl_xor(bi, off, 64);
+    if (better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sv[wave] = bv;
+    si[wave] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 16; ++w)
+      if (better(sv[w], si[w], bv, bi)) {
+        bv = sv[w];
+        bi = si[w];
+      }
+    ids[blockIdx.x] = bi < n ? bi : 0;  // a row of NaNs only: index 0
+    if (max_out != nullptr) max_out[blockIdx.x] = bv;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_embed_rows(const uint16_t* table, const int32_t* ids, int n_tok, int dim, uint16_t* out,
+                             hipStream_t stream) {
+  if (n_tok == 0) return hipSuccess;
+  if (dim % 8 != 0) return hipErrorInvalidValue;
+  ATTUNER_LAUNCH("embed_rows_kernel", embed_rows_kernel, dim3((unsigned)((n_tok + 3) / 4)), dim3(256), stream, table,
+                 ids, n_tok, dim, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_rms_norm_rows(const uint16_t* x, int64_t ld_x, const int32_t* rows, int n_rows, int dim,
+                                const uint16_t* gamma, float eps, uint16_t* out, hipStream_t stream) {
+  if (n_rows == 0) return hipSuccess;
+  if (dim % 8 != 0 || dim > 64 * 8 * kMaxPass) return hipErrorInvalidValue;
+  ATTUNER_LAUNCH("rms_norm_rows_kernel", rms_norm_rows_kernel, dim3((unsigned)((n_rows + 3) / 4)), dim3(256), stream,
+                 x, ld_x, rows, n_rows, dim, gamma, eps, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax_rows(const float* logits, int n_rows, int n, int32_t* ids, float* max_out,
+                              hipStream_t stream) {
+  if (n_rows == 0) return hipSuccess;
+  ATTUNER_LAUNCH("argmax_rows_kernel", argmax_rows_kernel, dim3((unsigned)n_rows), dim3(1024), stream, logits, n,
+                 ids, max_out);
+  return hipGetLastError();
+}
+
+}  // namespace attuner

@@ -58,6 +58,37 @@ hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int
                             const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad, int lora_cols,
                             const float* t_part, uint16_t* out, hipStream_t stream);
 
+// ---- the decoder layer around the path: plain GEMMs with other epilogues --
+
+// What the GEMM stores for C = x W^T ([n_tok][n_out], fp32 accumulate):
+//   kEpiBf16      out = C (bf16)
+//   kEpiResidual  out = C + residual (bf16; residual [n_tok][n_out], may be out)
+//   kEpiSwiglu    W rows interleave gate and up (row 2j = gate_j, 2j+1 = up_j):
+//                 out[i][j] = silu(C[i][2j]) * C[i][2j+1] (bf16, [n_tok][n_out/2])
+//   kEpiF32       out_f32 = C (fp32)
+enum GemmEpiMode : int { kEpiBf16 = 0, kEpiResidual = 1, kEpiSwiglu = 2, kEpiF32 = 3 };
+struct GemmEpi {
+  int mode;
+  const uint16_t* residual;
+  float* out_f32;
+};
+hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, GemmEpi epi,
+                       uint16_t* out, hipStream_t stream);
+
+// out[t] = table[ids[t]] (rows of dim bf16 elements; ids in range).
+hipError_t launch_embed_rows(const uint16_t* table, const int32_t* ids, int n_tok, int dim, uint16_t* out,
+                             hipStream_t stream);
+
+// out[r] = x[rows[r]] * rsqrt(mean(x[rows[r]]^2) + eps) * gamma over `dim`
+// elements (rows null: r itself); bf16 in and out, fp32 arithmetic.
+hipError_t launch_rms_norm_rows(const uint16_t* x, int64_t ld_x, const int32_t* rows, int n_rows, int dim,
+                                const uint16_t* gamma, float eps, uint16_t* out, hipStream_t stream);
+
+// ids[r] = the smallest index of the largest value of logits[r][0 .. n-1]
+// (fp32), max_out[r] = that value (max_out may be null).
+hipError_t launch_argmax_rows(const float* logits, int n_rows, int n, int32_t* ids, float* max_out,
+                              hipStream_t stream);
+
 // ---- a4: QK-RMSNorm + RoPE ------------------------------------------------
 
 struct NormRopeReq {

@@ -54,3 +54,21 @@ def lse_bar(q_hat, keys, n_q_heads, n_kv_heads) -> float:
         z = np.einsum("shd,nd->shn", q[:, g * G:(g + 1) * G, :], k[:, g, :]) / np.sqrt(q.shape[-1])
         zmax = max(zmax, float(np.abs(z).max()))
     return 2.0 ** -8 * zmax + 1e-3
+
+
+def assert_stack_close(got, ref, n_layers: int, what="stack output"):
+    """Bar on the residual stream after n_layers decoder layers run end to end
+    against an fp64 stack started from the same input.  Each layer stores h
+    to bf16 twice (after the attention residual and after the MLP residual),
+    and every stored rounding moves a value by at most 2^-9 relative; the
+    errors of earlier layers pass through later ones along the residual
+    connection, so they add: mean|err| <= 2 n_layers * 2^-9 * mean|ref|
+    (one layer: the single-step bar 2^-8).  max|err| stays within
+    1e-2 * max|ref|, as for one step."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    err = np.abs(got - ref)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    assert err.max() <= 1e-2 * np.abs(ref).max(), f"{what}: max|err| {err.max():.3e} vs max|ref| {np.abs(ref).max():.3e}"
+    bar = 2 * n_layers * 2.0 ** -9 * np.abs(ref).mean()
+    assert err.mean() <= bar, f"{what}: mean|err| {err.mean():.3e} > {bar:.3e} ({n_layers} layers)"

@@ -1,0 +1,258 @@
+"""GPU parity of the decoder layer around the suffix path (embedding rows,
+RMSNorm, o_proj / down_proj with the residual, the SwiGLU gate/up GEMM, the
+LM head with the greedy pick, and a two-layer stack chained through them)
+against the fp64 oracle, through the C ABI.
+
+Bars: the embedding lookup bit-exact; bf16-stored outputs of one step (and
+one layer run from the GPU's own input) within the intermediate bar
+(max|err| <= 1e-2 max|ref|, mean|err| <= 2^-8 mean|ref|); the stack run end to
+end from the embedding within L * 2^-8 mean|ref| after L layers (the errors
+of each layer's bf16 stores add along the residual stream);
+the greedy token by the rule for an argmax decided in floating point: the
+chosen id's exact logit is within the fp32 accumulation bound of the exact
+maximum, and equals the exact argmax wherever the exact top-two gap exceeds
+twice that bound.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synthdata as sd
+from synthdata.workloads import ModelShape, Request, custom_workload
+from tests._tol import assert_intermediate_close, assert_stack_close
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from tests._gpu import GpuWorkload, dev_bf16, host_f64
+    from paper_2609_36722_amd.api import AttunerError, Context, ModelCfg, bf16_to_host
+    from paper_2609_36722_amd.decoder import DecoderStack, LayerWeights, StackWeights
+
+
+def _say(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def _bits(rng, shape, std=1.0):
+    return sd.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32) * np.float32(std))
+
+
+def _fp32_bound(x, w):
+    """Bound on |fp32 dot - exact dot| for each output of x w^T with K terms:
+    K * 2^-24 * sum_k |x_k w_k| (one rounding per product-add, and a margin)."""
+    K = x.shape[-1]
+    return 2.0 * K * 2.0 ** -24 * (np.abs(x) @ np.abs(w).T)
+
+
+# ----------------------------------------------------------------------------
+# embedding rows (bit-exact) and RMSNorm rows
+# ----------------------------------------------------------------------------
+
+def test_embed_bit_exact():
+    _say("embed")
+    rng = np.random.default_rng(31)
+    V, H = 1000, 256
+    table = rng.integers(0, 2 ** 16, size=(V, H), dtype=np.uint16)
+    ids = np.concatenate([[0, V - 1, 5, 5], rng.integers(0, V, size=77)]).astype(np.int32)
+    with Context(ModelCfg(n_layers=1, hidden=H), pool_pages=0) as ctx:
+        out = torch.empty(len(ids), H, dtype=torch.bfloat16, device="cuda")
+        ctx.embed(ids.tolist(), dev_bf16(table), out)
+        torch.cuda.synchronize()
+        assert np.array_equal(bf16_to_host(out), table[ids])
+        with pytest.raises(AttunerError) as e:
+            ctx.embed([3, V], dev_bf16(table), out)
+        assert e.value.status == -5
+
+
+@pytest.mark.parametrize("H,n,rows", [(2560, 37, None), (4096, 300, None), (2560, 9, [8, 0, 5, 5, 1]),
+                                      (8192, 3, [2])])
+def test_rms_norm_rows(H, n, rows):
+    _say(f"rms_norm H={H} n={n} rows={rows}")
+    rng = np.random.default_rng(H + n)
+    x = _bits(rng, (n, H), 3.0)
+    g = sd.f32_to_bf16_bits(rng.uniform(0.5, 1.5, H).astype(np.float32))
+    m = n if rows is None else len(rows)
+    with Context(ModelCfg(n_layers=1, hidden=H), pool_pages=0) as ctx:
+        out = torch.empty(m, H, dtype=torch.bfloat16, device="cuda")
+        ctx.rms_norm(dev_bf16(x), dev_bf16(g), out, rows=rows)
+        torch.cuda.synchronize()
+        got = host_f64(out)
+    sel = np.arange(n) if rows is None else np.array(rows)
+    ref = oracle.rms_norm_heads(oracle.decode_bf16(x)[sel], oracle.decode_bf16(g), 1e-6)
+    assert_intermediate_close(got, ref, "rms_norm")
+
+
+# ----------------------------------------------------------------------------
+# plain GEMM epilogues: bf16, + residual (in place), SwiGLU, fp32 logits
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T,K,N,res", [
+    (1, 256, 64, "none"),
+    (37, 2560, 4096, "none"),
+    (300, 4096, 2560, "separate"),   # o_proj of the 4B stack (K = Hq d), ragged tokens
+    (256, 9728, 2560, "inplace"),    # down_proj of the 4B stack, residual read and written in place
+    (513, 12288, 4096, "inplace"),   # down_proj of the 8B stack
+])
+def test_linear_parity(T, K, N, res):
+    _say(f"linear T={T} K={K} N={N} residual={res}")
+    rng = np.random.default_rng(T + K + N)
+    x, w = _bits(rng, (T, K)), _bits(rng, (N, K), 1 / math.sqrt(K))
+    r = _bits(rng, (T, N)) if res != "none" else None
+    with Context(ModelCfg(n_layers=1, hidden=256), pool_pages=0) as ctx:
+        if res == "inplace":
+            out = dev_bf16(r)
+            ctx.linear(dev_bf16(x), dev_bf16(w), out, residual=out)
+        else:
+            out = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+            ctx.linear(dev_bf16(x), dev_bf16(w), out, residual=dev_bf16(r) if r is not None else None)
+        torch.cuda.synchronize()
+        got = host_f64(out)
+    ref = oracle.linear(oracle.decode_bf16(x), oracle.decode_bf16(w),
+                        oracle.decode_bf16(r) if r is not None else None)
+    assert_intermediate_close(got, ref, "linear")
+
+
+@pytest.mark.parametrize("T,K,I", [(1, 2560, 9728), (100, 2560, 9728), (513, 4096, 12288), (64, 256, 32)])
+def test_gate_up_swiglu_parity(T, K, I):
+    _say(f"gate_up_swiglu T={T} K={K} I={I}")
+    rng = np.random.default_rng(T + K + I)
+    x = _bits(rng, (T, K))
+    wg, wu = _bits(rng, (I, K), 1 / math.sqrt(K)), _bits(rng, (I, K), 1 / math.sqrt(K))
+    w_gu = np.stack([wg, wu], axis=1).reshape(2 * I, K)
+    with Context(ModelCfg(n_layers=1, hidden=256), pool_pages=0) as ctx:
+        out = torch.empty(T, I, dtype=torch.bfloat16, device="cuda")
+        ctx.gate_up_swiglu(dev_bf16(x), dev_bf16(np.ascontiguousarray(w_gu)), out)
+        torch.cuda.synchronize()
+        got = host_f64(out)
+    d = oracle.decode_bf16
+    assert_intermediate_close(got, oracle.swiglu(d(x), d(wg), d(wu)), "swiglu")
+
+
+def _check_pick(ids, max_logit, x, w):
+    """The greedy pick against the exact logits of the same bf16 x and w."""
+    exact = oracle.linear(x, w)
+    bound = _fp32_bound(x, w)
+    for r in range(exact.shape[0]):
+        top = int(np.argmax(exact[r]))
+        i = int(ids[r])
+        assert 0 <= i < w.shape[0]
+        assert exact[r, i] >= exact[r, top] - 2 * bound[r].max(), f"row {r}: id {i} is not a maximum"
+        assert abs(max_logit[r] - exact[r, i]) <= bound[r, i] + 1e-30
+        second = np.partition(exact[r], -2)[-2]
+        if exact[r, top] - second > 2 * bound[r].max():
+            assert i == top, f"row {r}: id {i}, exact argmax {top} with a clear gap"
+
+
+@pytest.mark.parametrize("n,H,V", [(1, 256, 1024), (5, 2560, 151936), (16, 512, 4096)])
+def test_lm_head_argmax(n, H, V):
+    _say(f"lm_head_argmax n={n} H={H} V={V}")
+    rng = np.random.default_rng(n + H + V)
+    x, w = _bits(rng, (n, H)), _bits(rng, (V, H), 1 / math.sqrt(H))
+    with Context(ModelCfg(n_layers=1, hidden=H), pool_pages=0) as ctx:
+        ids = torch.empty(n, dtype=torch.int32, device="cuda")
+        mx = torch.empty(n, dtype=torch.float32, device="cuda")
+        ctx.lm_head_argmax(dev_bf16(x), dev_bf16(w), ids, mx)
+        torch.cuda.synchronize()
+        _check_pick(ids.cpu().numpy(), mx.cpu().numpy().astype(np.float64), oracle.decode_bf16(x),
+                    oracle.decode_bf16(w))
+
+
+def test_lm_head_argmax_tie_takes_smallest_index():
+    # a copy of the winning vocabulary row at a smaller index gives the same
+    # fp32 logit (same products, same order): the smaller index must win
+    _say("lm_head_argmax tie")
+    rng = np.random.default_rng(33)
+    n, H, V = 3, 256, 2048
+    x, w = _bits(rng, (n, H)), _bits(rng, (V, H), 1 / math.sqrt(H))
+    exact = oracle.linear(oracle.decode_bf16(x), oracle.decode_bf16(w))
+    top = int(np.argmax(exact[0]))
+    dup = 7 if top > 7 else V - 1
+    w[dup] = w[top]
+    with Context(ModelCfg(n_layers=1, hidden=H), pool_pages=0) as ctx:
+        ids = torch.empty(n, dtype=torch.int32, device="cuda")
+        ctx.lm_head_argmax(dev_bf16(x), dev_bf16(w), ids)
+        torch.cuda.synchronize()
+        got = ids.cpu().numpy()
+    exact2 = oracle.linear(oracle.decode_bf16(x), oracle.decode_bf16(w))
+    gap = np.sort(exact2[0])[-1] - np.sort(exact2[0])[-3]   # the top two are the tie
+    assert gap > 2 * _fp32_bound(oracle.decode_bf16(x), oracle.decode_bf16(w))[0].max(), "seed gives no clear tie"
+    assert got[0] == min(top, dup)
+
+
+# ----------------------------------------------------------------------------
+# a two-layer stack chained through the calls
+# ----------------------------------------------------------------------------
+
+def _stack_case():
+    shape = ModelShape(hidden=256)
+    wl = custom_workload("stack", 92, shape, [40, 17, 64], [Request((0, 1), 20), Request((2, 0), 33)],
+                         n_layers=2, rank=16, scale=1.0, gamma="uniform")
+    return wl, 512, 1024     # intermediate, vocab
+
+
+def _oracle_weights(wl, l, I):
+    w = {k: oracle.decode_bf16(v) for k, v in sd.layer_weights(wl, l).items()}
+    w.update({k: oracle.decode_bf16(v) for k, v in sd.decoder_weights(wl, l, I).items()})
+    return w
+
+
+def test_decoder_stack_two_layers():
+    _say("decoder stack 2 layers")
+    wl, I, V = _stack_case()
+    s = wl.shape
+    g = GpuWorkload(wl, layers=[0, 1])
+    try:
+        layers = []
+        for l in range(2):
+            w, dw = sd.layer_weights(wl, l), sd.decoder_weights(wl, l, I)
+            layers.append(LayerWeights(
+                wqkv=dev_bf16(np.concatenate([w["wq"], w["wk"], w["wv"]])), gamma_q=dev_bf16(w["gamma_q"]),
+                gamma_k=dev_bf16(w["gamma_k"]), gamma_in=dev_bf16(dw["gamma_in"]), wo=dev_bf16(dw["wo"]),
+                gamma_post=dev_bf16(dw["gamma_post"]),
+                w_gu=dev_bf16(np.ascontiguousarray(np.stack([dw["w_gate"], dw["w_up"]], 1).reshape(2 * I, -1))),
+                w_down=dev_bf16(dw["w_down"]), a=dev_bf16(w["a"]), b=dev_bf16(w["b"])))
+        lm = sd.lm_weights(wl, V)
+        sw = StackWeights(embed=dev_bf16(lm["embed"]), gamma_final=dev_bf16(lm["gamma_final"]),
+                          w_lm=dev_bf16(lm["w_lm"]), layers=layers, rank=wl.rank, scale=wl.scale)
+        stack = DecoderStack(g.ctx, sw, [r.suffix_len for r in wl.requests])
+        tokens = [sd.suffix_tokens(wl, r, V) for r in range(len(wl.requests))]
+        stack.embed(np.concatenate(tokens).tolist())
+        hs = [host_f64(stack.h)]
+        for l in range(2):
+            stack.layers(g.cu_ctx, g.art_len, g.pos0, g.req_kv, g.rows, first=l, count=1)
+            torch.cuda.synchronize()
+            hs.append(host_f64(stack.h))
+        ids = stack.first_token().cpu().numpy()
+        mx = stack.max_logit.cpu().numpy().astype(np.float64)
+        x_last = host_f64(stack.x_last)
+        torch.cuda.synchronize()
+    finally:
+        g.close()
+
+    emb = oracle.decode_bf16(lm["embed"])
+    h0 = np.concatenate([emb[t] for t in tokens])
+    assert np.array_equal(hs[0], h0), "embedding rows"
+    ws = [_oracle_weights(wl, l, I) for l in range(2)]
+    h_e2e = []
+    for r, req in enumerate(wl.requests):
+        lo, hi = g.cu_q[r], g.cu_q[r + 1]
+        h = h0[lo:hi]
+        for l in range(2):
+            ka = np.concatenate([oracle.decode_bf16(g.art_k[a][l]) for a in req.artifact_ids])
+            va = np.concatenate([oracle.decode_bf16(g.art_v[a][l]) for a in req.artifact_ids])
+            args = (ka, va, wl.pos0(req), s.n_q_heads, s.n_kv_heads, s.rope_theta, s.rms_eps, wl.scale)
+            # each layer from the GPU's own input, then the whole stack from the embedding
+            one = oracle.decoder_layer(hs[l][lo:hi], ws[l], *args)
+            assert_intermediate_close(hs[l + 1][lo:hi], one["h"], f"request {r} layer {l} h")
+            h = oracle.decoder_layer(h, ws[l], *args)["h"]
+        h_e2e.append(h)
+    assert_stack_close(hs[2], np.concatenate(h_e2e), 2, "two-layer stack h")
+    # final norm of the last token of each request, then the greedy pick
+    last = [g.cu_q[r + 1] - 1 for r in range(len(wl.requests))]
+    gf = oracle.decode_bf16(lm["gamma_final"])
+    assert_intermediate_close(x_last, oracle.rms_norm_heads(hs[2][last], gf, s.rms_eps), "final norm")
+    _check_pick(ids, mx, x_last, oracle.decode_bf16(lm["w_lm"]))
