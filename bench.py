@@ -14,6 +14,14 @@ stack, with all inputs resident in HBM before timing starts:
 The same kernels then run the full-context prefill of the whole request
 (attuner_full_prefill, every layer, no adapter) for the speedup.
 
+With --model the step is instead the whole Qwen3-shaped decoder stack up to
+the greedy first token (the time-to-first-token of the paper's measurements):
+the assembly, the embedding rows of the suffix, per layer input RMSNorm ->
+q/k/v projection + LoRA -> suffix attention -> o_proj + residual -> post
+RMSNorm -> gate/up SwiGLU -> down_proj + residual, then the final RMSNorm of
+each request's last token, the LM head and the argmax; the full prefill runs
+all of the request's tokens through the same stack.
+
 Default workload: the Qwen3-4B-shaped 36-layer stack (8 artifacts x 1024
 tokens, 256-token suffix, LoRA rank 16).  One layer's seeded inputs are drawn
 and copied into a distinct device buffer per layer, so every layer reads its
@@ -60,6 +68,9 @@ def parse():
                     "replaying it as a captured HIP graph")
     ap.add_argument("--copy-probe-mb", type=int, default=0, help="run one device copy of this many MiB first "
                     "(a known-size reference for hardware byte counters)")
+    ap.add_argument("--model", action="store_true", help="time the whole Qwen3-shaped decoder stack instead "
+                    "(embedding, input norm, q/k/v projection + LoRA, suffix attention, o_proj, post norm, SwiGLU "
+                    "MLP, final norm, LM head, greedy first token) against a full prefill through the same stack")
     ap.add_argument("--quiet", action="store_true")
     return ap.parse_args()
 
@@ -157,6 +168,9 @@ def main():
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
+    if args.model:
+        model_main(args)
+        return
 
     import numpy as np
     import torch
@@ -485,6 +499,220 @@ def main():
         "speedup_vs_full_prefill": round(full["speedup"], 3) if full else None,
         "paper_context": PAPER_CONTEXT,
         "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    ctx.close()
+
+
+# ----------------------------------------------------------------------------
+# --model: the whole decoder stack up to the first token
+# ----------------------------------------------------------------------------
+
+# Qwen3 dimensions beyond the attention geometry: hidden -> (MLP intermediate, vocabulary)
+QWEN3_MLP_VOCAB = {2560: (9728, 151936), 4096: (12288, 151936)}
+MODEL_METRIC = "first-token prefill tokens/s (whole decoder stack), speedup vs full prefill"
+
+
+def model_main(args):
+    import numpy as np
+    import torch
+
+    import synthdata as sd
+    from paper_2609_36722_amd.api import Context, ModelCfg
+    from paper_2609_36722_amd.decoder import DecoderStack, LayerWeights, StackWeights
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = sd.make_workload(args.workload)
+    s, NL = wl.shape, wl.n_layers
+    I, V = QWEN3_MLP_VOCAB[s.hidden]
+    H, nq, nkv = s.hidden, s.q_dim, s.kv_dim
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    log(args, f"decoder stack {wl.name}: {NL} layers, hidden {H}, intermediate {I}, vocab {V}")
+
+    # ---- seeded device-side draws: every layer its own weights ----------------
+    t0 = time.time()
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1000 + wl.index)
+
+    def randn(*shape, std=1.0):
+        t = torch.randn(*shape, generator=gen, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            t.mul_(std)
+        return t.to(torch.bfloat16)
+
+    ones_d = torch.ones(s.head_dim, dtype=torch.bfloat16, device=dev)
+    ones_h = torch.ones(H, dtype=torch.bfloat16, device=dev)
+    layers = []
+    for _ in range(NL):
+        layers.append(LayerWeights(
+            wqkv=randn(nq + 2 * nkv, H, std=wl.w_std), gamma_q=ones_d, gamma_k=ones_d, gamma_in=ones_h,
+            wo=randn(H, nq, std=wl.w_std), gamma_post=ones_h, w_gu=randn(2 * I, H, std=wl.w_std),
+            w_down=randn(H, I, std=wl.w_std), a=randn(wl.rank, H, std=wl.a_std), b=randn(nq, wl.rank, std=wl.b_std)))
+    sw = StackWeights(embed=randn(V, H), gamma_final=ones_h, w_lm=randn(V, H, std=wl.w_std), layers=layers,
+                      rank=wl.rank, scale=wl.scale)
+    weight_bytes = sum(t.numel() * 2 for lw in layers for t in (lw.wqkv, lw.wo, lw.w_gu, lw.w_down)) + V * H * 2
+
+    used = sorted({a for r in wl.requests for a in r.artifact_ids})
+    pages = sum(math.ceil(wl.artifact_lengths[a] / 16) for a in used)
+    cfg = ModelCfg(n_layers=NL, hidden=H, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads, head_dim=s.head_dim,
+                   rope_theta=s.rope_theta, rms_eps=s.rms_eps)
+    ctx = Context(cfg, pool_pages=pages)
+    ids = {}
+    for a in used:
+        L = wl.artifact_lengths[a]
+        ids[a] = ctx.store_artifact(randn(NL, s.n_kv_heads, L, s.head_dim), randn(NL, s.n_kv_heads, L, s.head_dim))
+    requests = [[ids[a] for a in r.artifact_ids] for r in wl.requests]
+    caps = [r.suffix_len for r in wl.requests]
+    n_entries, rows = ctx.assemble_plan(requests, caps)
+    bt = torch.zeros(max(1, n_entries) * 4, dtype=torch.int32, device=dev)
+    req_kv = torch.zeros(NL * 2 * s.n_kv_heads * rows * s.head_dim, dtype=torch.bfloat16, device=dev)
+    tokens = np.concatenate([sd.suffix_tokens(wl, r, V) for r in range(len(wl.requests))]).tolist()
+    pos0 = [wl.pos0(r) for r in wl.requests]
+    stack = DecoderStack(ctx, sw, caps)
+    torch.cuda.synchronize()
+    log(args, f"weights {weight_bytes / 1e9:.2f} GB and artifacts resident ({time.time() - t0:.1f} s)")
+
+    def make_step(stk, reqs, cps, table, kv, n_rows, toks, p0):
+        """One step: assembly, embedding, the layer loop (a graph once captured), first token."""
+        state = {"graph": None, "cu": None, "al": None}
+
+        def assemble():
+            state["cu"], state["al"] = ctx.assemble_kv(reqs, cps, table, kv, n_rows)
+
+        def layer_loop(mark=None):
+            stk.layers(state["cu"], state["al"], p0, kv, n_rows, mark=mark)
+
+        def step():
+            assemble()
+            stk.embed(toks)
+            if state["graph"] is not None:
+                state["graph"].replay()
+            else:
+                layer_loop()
+            stk.first_token()
+
+        def capture():
+            cap = torch.cuda.Stream()
+            cap.wait_stream(stream)
+            g = torch.cuda.CUDAGraph()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=cap):
+                layer_loop()
+            torch.cuda.synchronize()
+            state["graph"] = g
+
+        return step, capture, assemble, layer_loop
+
+    step, capture, assemble, layer_loop = make_step(stack, requests, caps, bt, req_kv, rows, tokens, pos0)
+    log(args, f"warmup {args.warmup} steps")
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+
+    # ---- one instrumented eager step: events around every call ----------------
+    ev = []
+
+    def mark(name):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        ev.append((name, e))
+
+    ctx.trace_begin()
+    mark("assemble_kv")
+    assemble()
+    mark("embed")
+    stack.embed(tokens)
+    layer_loop(mark=mark)
+    mark("final_norm_lm_head")
+    stack.first_token()
+    mark(None)
+    torch.cuda.synchronize()
+    ktimes = ctx.trace_end()
+    breakdown = {}
+    for (name, e0), (_, e1) in zip(ev[:-1], ev[1:]):
+        if name is not None:
+            breakdown[name] = breakdown.get(name, 0.0) + e0.elapsed_time(e1)
+    per_kernel = {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t, _) in ktimes.items()}
+
+    if not args.no_graph:
+        capture()
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for _ in range(args.steps):
+        step()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    first_ids = stack.ids.cpu().tolist()
+    log(args, f"timed {args.steps} steps: {ms_step:.3f} ms to the first token; breakdown (eager) " +
+        ", ".join(f"{k} {v:.3f}" for k, v in breakdown.items()))
+
+    # ---- GEMM rates over the step (eager call times summed over the layers) -----
+    T = wl.total_suffix
+    gemm_work = {"qkv_proj": (H, nq + 2 * nkv), "o_proj": (nq, H), "gate_up": (H, 2 * I), "down_proj": (I, H)}
+    gemms = {}
+    for name, (K, N) in gemm_work.items():
+        ms = breakdown[name]
+        gemms[name] = {"ms_per_step": round(ms, 4), "tflops": round(2.0 * T * K * N * NL / (ms * 1e-3) / 1e12, 1),
+                       "weight_gbps": round(2.0 * K * N * NL / (ms * 1e-3) / 1e9, 1)}
+
+    # ---- full prefill of every token of the request through the same stack -----
+    full = None
+    if args.full_steps > 0 and len(wl.requests) == 1:
+        N = wl.art_len(wl.requests[0]) + wl.requests[0].suffix_len
+        ne_f, rows_f = ctx.assemble_plan([[]], [N])
+        bt_f = torch.zeros(max(1, ne_f) * 4, dtype=torch.int32, device=dev)
+        kv_f = torch.zeros(NL * 2 * s.n_kv_heads * rows_f * s.head_dim, dtype=torch.bfloat16, device=dev)
+        toks_f = np.random.default_rng(wl.index).integers(0, V, size=N).tolist()
+        stack_f = DecoderStack(ctx, sw, [N])
+        step_f, capture_f, _, _ = make_step(stack_f, [[]], [N], bt_f, kv_f, rows_f, toks_f, [0])
+        step_f()
+        if not args.no_graph:
+            capture_f()
+        step_f()
+        torch.cuda.synchronize()
+        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        f0.record(stream)
+        for _ in range(args.full_steps):
+            step_f()
+        f1.record(stream)
+        torch.cuda.synchronize()
+        full_ms = f0.elapsed_time(f1) / args.full_steps
+        full = {"ms": round(full_ms, 3), "tokens": N, "speedup": round(full_ms / ms_step, 3)}
+        log(args, f"full prefill of {N} tokens through the stack: {full_ms:.2f} ms -> speedup {full_ms / ms_step:.2f}x")
+        del stack_f, kv_f
+
+    out = {
+        "metric": MODEL_METRIC,
+        "value": round(T / (ms_step * 1e-3), 2),
+        "unit": "suffix tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded device-side N(0,1) / N(0,0.02) bf16 draws, distinct weights per layer)",
+        "config": {"workload": wl.name + "+decoder_stack", "layers": NL, "hidden": H, "intermediate": I,
+                   "vocab": V, "q_heads": s.n_q_heads, "kv_heads": s.n_kv_heads, "head_dim": s.head_dim,
+                   "requests": len(wl.requests), "artifact_tokens": [wl.art_len(r) for r in wl.requests],
+                   "suffix_tokens": [r.suffix_len for r in wl.requests], "lora_rank": wl.rank},
+        "layer_loop": "hip_graph" if not args.no_graph else "eager",
+        "breakdown_ms_per_step_eager": {k: round(v, 4) for k, v in breakdown.items()},
+        "gemms": gemms,
+        "weight_bytes": weight_bytes,
+        "kernel_avg_ms": per_kernel,
+        "first_token_ids": first_ids,
+        "full_prefill": full,
+        "speedup_vs_full_prefill": full["speedup"] if full else None,
+        "paper_context": PAPER_CONTEXT,
     }
     print(json.dumps(out), flush=True)
     ctx.close()

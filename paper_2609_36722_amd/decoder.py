@@ -25,7 +25,7 @@ row j at row 2j + 1 (see interleave_gate_up).
 from __future__ import annotations
 
 from dataclasses import dataclass, field
-from typing import List, Optional, Sequence
+from typing import Callable, List, Optional, Sequence
 
 import torch
 
@@ -104,26 +104,40 @@ class DecoderStack:
             raise ValueError(f"{len(token_ids)} token ids for {self.cu_q[-1]} suffix tokens")
         self.ctx.embed(token_ids, self.w.embed, self.h, stream=stream)
 
+    STEPS = ("input_norm", "qkv_proj", "suffix_attn", "o_proj", "post_norm", "gate_up", "down_proj")
+
     def layers(self, cu_ctx, art_len, pos0, req_kv: torch.Tensor, cache_rows: int, stream=None,
-               first: int = 0, count: Optional[int] = None) -> None:
+               first: int = 0, count: Optional[int] = None,
+               mark: Optional[Callable[[Optional[str]], None]] = None) -> None:
         """Decoder layers first .. first + count - 1 (default: all) over h, in
         place.  cu_ctx / art_len / pos0 as attuner_suffix_attn takes them (from
         the cache assembly).  Makes no host-to-device copy, so a caller may
-        capture it into a graph."""
+        capture it into a graph.  mark, if given, is called with the name of
+        each step (one of STEPS) before its call and with None after the last
+        (e.g. to record timing events)."""
         c, w, ld = self.ctx, self.w, self.nq + 2 * self.nkv
         q, k, v = self.qkv[:, :self.nq], self.qkv[:, self.nq:self.nq + self.nkv], self.qkv[:, self.nq + self.nkv:]
         count = len(w.layers) - first if count is None else count
+        m = mark if mark is not None else (lambda name: None)
         for l in range(first, first + count):
             lw = w.layers[l]
+            m("input_norm")
             c.rms_norm(self.h, lw.gamma_in, self.x, stream=stream)
+            m("qkv_proj")
             c.qproj_lora(self.x, lw.wqkv, lw.a, lw.b, w.rank if lw.a is not None else 0, w.scale, self.nq, self.qkv,
                          stream=stream)
+            m("suffix_attn")
             c.suffix_attn(l, self.cu_q, cu_ctx, art_len, pos0, q, ld, k, v, ld, lw.gamma_q, lw.gamma_k, req_kv,
                           cache_rows, self.o, stream=stream)
+            m("o_proj")
             c.linear(self.o.view(-1, self.nq), lw.wo, self.h, residual=self.h, stream=stream)
+            m("post_norm")
             c.rms_norm(self.h, lw.gamma_post, self.x, stream=stream)
+            m("gate_up")
             c.gate_up_swiglu(self.x, lw.w_gu, self.g, stream=stream)
+            m("down_proj")
             c.linear(self.g, lw.w_down, self.h, residual=self.h, stream=stream)
+        m(None)
 
     def first_token(self, stream=None) -> torch.Tensor:
         """ids[r] = greedy first token of request r from the final h (device int32)."""
