@@ -271,6 +271,32 @@ attuner_status attuner_full_prefill(attuner_ctx* ctx, int32_t n_tok, int32_t pos
                                     void* k_out, void* v_out, float* lse, void* stream);
 
 /* --------------------------------------------------------------------------
+ * Decode with the adapted queries: every generated token keeps the adapted
+ * query projection (section 4: the adapter acts on all online tokens), and
+ * attends to its request's whole assembled context (eq. 3 with one query
+ * row).  One new token per request; its q/k/v rows come from
+ * attuner_qproj_lora on those tokens (row r = request r).
+ *
+ * Request r has ctx_len[r] keys already in its cache rows cu_ctx[r] ..
+ * (artifacts, suffix and earlier generated tokens, as attuner_assemble_kv and
+ * earlier calls left them).  The call normalises and rotates the new q and k
+ * at position pos[r] (NULL: ctx_len[r]), writes k_hat and v into cache row
+ * cu_ctx[r] + ctx_len[r] of layer `layer`, and writes
+ * o[r][h][:] = sum_j softmax_j(q_hat . k_j / sqrt(d)) v_j over the
+ * ctx_len[r] + 1 keys j = 0 .. ctx_len[r].  Requires ctx_len[r] + 1 <=
+ * cu_ctx[r+1] - cu_ctx[r] (the suffix capacity given to the assembly must
+ * cover the generated tokens) and n_q_heads = 4 n_kv_heads.  q_raw/k_raw/
+ * v_raw/ld_q/ld_kv/gamma as in attuner_qk_norm_rope; o: device [n_req][Hq][d]
+ * bf16 (also stages the normalised queries).  Long contexts are split into
+ * key chunks merged in fp32 (context workspace).
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_decode_attn(attuner_ctx* ctx, int32_t layer, int32_t n_req, const int32_t* cu_ctx,
+                                   const int32_t* ctx_len, const int32_t* pos, const void* q_raw,
+                                   int64_t ld_q, const void* k_raw, const void* v_raw, int64_t ld_kv,
+                                   const void* gamma_q, const void* gamma_k, void* req_kv,
+                                   int64_t cache_rows, void* o, void* stream);
+
+/* --------------------------------------------------------------------------
  * The decoder layer around the path (the models the method adapts are Qwen3
  * decoder stacks, section 5.1; the greedy first token ends the timed region
  * of the paper's time-to-first-token, appendix A.2).  With

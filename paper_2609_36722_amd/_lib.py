@@ -52,6 +52,8 @@ SIGNATURES = {
     "attuner_attention": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _vp, _vp, _i64, _vp, _vp, _vp]),
     "attuner_suffix_attn": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64,
                                       _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "attuner_decode_attn": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64, _vp, _vp,
+                                      _vp, _i64, _vp, _vp]),
     "attuner_embed": (C.c_int, [_vp, _i32, _i32p, _vp, _i32, _vp, _vp]),
     "attuner_rms_norm": (C.c_int, [_vp, _vp, _i64, _i64, _i32p, _i32, _vp, _vp, _vp]),
     "attuner_linear": (C.c_int, [_vp, _i32, _vp, _i32, _vp, _i32, _vp, _vp, _vp]),

@@ -316,6 +316,18 @@ class Context:
                                          _ptr(req_kv), int(cache_rows), _ptr(o), _ptr(lse, 4), _stream(stream)),
                "attuner_suffix_attn")
 
+    def decode_attn(self, layer: int, cu_ctx, ctx_len, pos, q_raw, ld_q: int, k_raw, v_raw, ld_kv: int,
+                    gamma_q, gamma_k, req_kv, cache_rows: int, o, stream=None) -> None:
+        """One new token per request (row r = request r) over its ctx_len[r] cached keys and its own."""
+        n = len(ctx_len)
+        cu_q = list(range(n + 1))
+        self._check_cache(cu_q, cu_ctx, o, req_kv, cache_rows, q_raw, ld_q, k_raw, v_raw, ld_kv)
+        _check(lib().attuner_decode_attn(self._h, int(layer), n, _i32(cu_ctx), _i32(ctx_len),
+                                         _i32(pos) if pos is not None else None, _view_ptr(q_raw), int(ld_q),
+                                         _view_ptr(k_raw), _view_ptr(v_raw), int(ld_kv), _ptr(gamma_q), _ptr(gamma_k),
+                                         _ptr(req_kv), int(cache_rows), _ptr(o), _stream(stream)),
+               "attuner_decode_attn")
+
     # ---- kernel timing ----------------------------------------------------------------
     def trace_begin(self) -> None:
         _check(lib().attuner_trace_begin(self._h), "attuner_trace_begin")

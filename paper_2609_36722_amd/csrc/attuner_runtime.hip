@@ -354,6 +354,49 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   return ATTUNER_OK;
 }
 
+// One new token per request (reqs[r].q_len == 1, row r): attention over the
+// request's art_len + 1 keys, cut into equal chunks so that the launch has
+// about four workgroups per CU.
+attuner_status run_decode(attuner_ctx* c, const std::vector<ReqDesc>& reqs, const void* q, const uint16_t* k_plane,
+                          const uint16_t* v_plane, int64_t head_stride, void* o, hipStream_t stream) {
+  DecodeParams p;
+  memset(&p, 0, sizeof p);
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = k_plane;
+  p.v = v_plane;
+  p.kv_head_stride = head_stride;
+  p.o = static_cast<uint16_t*>(o);
+  p.n_q_heads = c->cfg.n_q_heads;
+  p.n_kv_heads = c->cfg.n_kv_heads;
+  p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c->cfg.head_dim));
+  p.n_req = (int32_t)reqs.size();
+  int64_t keys = 0;
+  for (const auto& r : reqs) keys += (int64_t)r.art_len + 1;
+  // chunks of a multiple of 128 keys (one step of the 32 key groups x 4)
+  const int64_t want = (keys * c->cfg.n_kv_heads + 1023) / 1024;
+  p.chunk = (int32_t)std::max<int64_t>(128, (want + 127) / 128 * 128);
+  int32_t splits = 0;
+  for (size_t r = 0; r < reqs.size(); ++r) {
+    const int32_t n_keys = reqs[r].art_len + 1;
+    p.req[r].q_row = reqs[r].q_start;
+    p.req[r].kv_start = reqs[r].kv_start;
+    p.req[r].n_keys = n_keys;
+    p.req[r].split0 = splits;
+    p.req[r].n_split = (n_keys + p.chunk - 1) / p.chunk;
+    splits += p.req[r].n_split;
+  }
+  p.total_splits = splits;
+  if (splits > (int32_t)reqs.size()) {
+    const size_t rows = (size_t)splits * c->cfg.n_q_heads;
+    const size_t po = rows * c->cfg.head_dim * sizeof(float);
+    HIP_TRY(c->ws_part.ensure(po + rows * 2 * sizeof(float)));
+    p.part_o = static_cast<float*>(c->ws_part.ptr);
+    p.part_ml = reinterpret_cast<float*>(static_cast<char*>(c->ws_part.ptr) + po);
+  }
+  HIP_TRY(launch_decode_attention(p, stream));
+  return ATTUNER_OK;
+}
+
 // Validate the per-request host arrays of a norm/attention call against a cache.
 attuner_status build_reqs(const attuner_ctx* c, int32_t n_req, const int32_t* cu_q, const int32_t* cu_ctx,
                           const int32_t* art_len, const int32_t* pos0, int64_t cache_rows,
@@ -874,6 +917,38 @@ attuner_status attuner_suffix_attn(attuner_ctx* c, int32_t layer, int32_t n_req,
   st = run_norm_rope(c, reqs, total_q, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, o, kp, vp, hs, s);
   if (st != ATTUNER_OK) return st;
   return run_attention(c, reqs, total_q, o, kp, vp, hs, o, lse, s);
+}
+
+attuner_status attuner_decode_attn(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_ctx,
+                                   const int32_t* ctx_len, const int32_t* pos, const void* q_raw, int64_t ld_q,
+                                   const void* k_raw, const void* v_raw, int64_t ld_kv, const void* gamma_q,
+                                   const void* gamma_k, void* req_kv, int64_t cache_rows, void* o, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  attuner_status st = check_layer(c, layer);
+  if (st != ATTUNER_OK) return st;
+  if (n_req < 0 || n_req > ATTUNER_MAX_REQUESTS)
+    return fail(ATTUNER_ERANGE, "n_req %d outside [0, %d]", n_req, ATTUNER_MAX_REQUESTS);
+  if (n_req == 0) return ATTUNER_OK;
+  if (c->cfg.n_q_heads != 4 * c->cfg.n_kv_heads)
+    return fail(ATTUNER_EINVAL, "the decode kernel is built for 4 query heads per KV head");
+  std::vector<int32_t> cu_q(n_req + 1);
+  for (int32_t r = 0; r <= n_req; ++r) cu_q[r] = r;
+  std::vector<ReqDesc> reqs;
+  int32_t total_q = 0;
+  st = build_reqs(c, n_req, cu_q.data(), cu_ctx, ctx_len, pos, cache_rows, &reqs, &total_q);
+  if (st != ATTUNER_OK) return st;
+  st = check_norm_args(q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, c);
+  if (st != ATTUNER_OK) return st;
+  if (!req_kv || !o || !aligned16(req_kv) || !aligned16(o))
+    return fail(ATTUNER_EINVAL, "req_kv and o must be non-null and 16-byte aligned");
+  DeviceGuard dg(c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t hs = cache_rows * c->cfg.head_dim;
+  uint16_t* kp = cache_plane(req_kv, c, layer, 0, cache_rows);
+  uint16_t* vp = cache_plane(req_kv, c, layer, 1, cache_rows);
+  st = run_norm_rope(c, reqs, total_q, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, o, kp, vp, hs, s);
+  if (st != ATTUNER_OK) return st;
+  return run_decode(c, reqs, o, kp, vp, hs, o, s);
 }
 
 attuner_status attuner_full_prefill(attuner_ctx* c, int32_t n_tok, int32_t pos0, const void* x, const void* wqkv,

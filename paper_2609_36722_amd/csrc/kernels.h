@@ -151,4 +151,33 @@ struct AttnParams {
 // Attention, plus the split-KV merge kernel when n_split > 1.
 hipError_t launch_attention(const AttnParams& p, hipStream_t stream);
 
+// ---- decode: one new token per request over its whole cache ----------------
+
+struct DecodeReq {
+  int32_t q_row;     // row of the request's token in q / o
+  int32_t kv_start;  // cache row of key 0 of the request
+  int32_t n_keys;    // keys it attends to (its own, already in the cache, is the last)
+  int32_t split0;    // first key chunk of the request in the launch
+  int32_t n_split;   // chunks of the request (ceil(n_keys / chunk))
+};
+
+struct DecodeParams {
+  const uint16_t* q;       // [rows][Hq][128]
+  const uint16_t* k;       // K head 0; head stride kv_head_stride
+  const uint16_t* v;
+  int64_t kv_head_stride;
+  uint16_t* o;             // [rows][Hq][128]
+  float* part_o;           // [total_splits][Hq][128] fp32, unnormalised
+  float* part_ml;          // [total_splits][Hq][2] (max in log2 units, sum)
+  int32_t n_q_heads, n_kv_heads;
+  int32_t chunk;           // keys per chunk
+  float score_scale;       // log2(e) / sqrt(d)
+  int32_t n_req;
+  int32_t total_splits;
+  DecodeReq req[kMaxReq];
+};
+
+// Decode attention, plus the chunk merge when a request has several chunks.
+hipError_t launch_decode_attention(const DecodeParams& p, hipStream_t stream);
+
 }  // namespace attuner

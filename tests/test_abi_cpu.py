@@ -49,6 +49,8 @@ def test_null_context_is_an_error_not_a_crash():
     assert lib.attuner_assemble_table(None, 0, None, None, None, None, None, None, 0, None) == -1
     assert lib.attuner_gather_layers(None, None, 0, 0, 1, None, 0, None) == -1
     assert lib.attuner_embed(None, 1, None, None, 8, None, None) == -1
+    assert lib.attuner_decode_attn(None, 0, 1, None, None, None, None, 0, None, None, 0, None, None, None, 0, None,
+                                   None) == -1
     assert lib.attuner_rms_norm(None, None, 1, 256, None, 1, None, None, None) == -1
     assert lib.attuner_linear(None, 1, None, 64, None, 64, None, None, None) == -1
     assert lib.attuner_gate_up_swiglu(None, 1, None, 64, None, 32, None, None) == -1

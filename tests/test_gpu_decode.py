@@ -1,0 +1,159 @@
+"""GPU parity of decode with the adapted queries (one new token per request
+over its whole assembled context) against the fp64 oracle, through the C ABI.
+
+The cache holds the assembled artifacts (gathered from the pool) and, after
+them, rows of earlier tokens (seeded bf16 bits written straight into the
+cache: inputs, as the suffix prefill or earlier decode steps would leave
+them).  The new token's q/k/v rows are seeded bf16 bits as the projection
+would give them.  The oracle normalises and rotates q and k at the token's
+position and attends over the prior keys plus the new one.  Bar: the O bar
+(max|err| <= 1e-2 max|ref|, mean|err| <= 1e-3) over each batch; each request
+of a batch within it or, for a context of a few keys whose outputs are of
+unit size, within the relative bar of a bf16-stored value.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synthdata as sd
+from tests._tol import assert_o_close, assert_o_close_per_request
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from tests._gpu import dev_bf16, host_f64
+    from paper_2609_36722_amd.api import AttunerError, Context, ModelCfg, bf16_to_host
+
+HQ, HKV, D = 32, 8, 128
+
+
+def _say(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def _bits(rng, shape, std=1.0):
+    return sd.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32) * np.float32(std))
+
+
+def _run_decode(seed, art_lengths, reqs, n_layers=1, layer=0, pos=None, gamma="uniform"):
+    """reqs: [(artifact ids, prior rows)]; returns (GPU o [n][Hq][d], oracle o)."""
+    rng = np.random.default_rng(seed)
+    n = len(reqs)
+    cfg = ModelCfg(n_layers=n_layers, hidden=256)
+    pages = sum(math.ceil(L / 16) for L in art_lengths)
+    with Context(cfg, pool_pages=max(1, pages)) as ctx:
+        art_k, art_v, ids = {}, {}, {}
+        for a, L in enumerate(art_lengths):
+            k, v = _bits(rng, (n_layers, HKV, L, D)), _bits(rng, (n_layers, HKV, L, D))
+            ids[a] = ctx.store_artifact(dev_bf16(k), dev_bf16(v))
+            art_k[a], art_v[a] = k, v
+        requests = [[ids[a] for a in arts] for arts, _ in reqs]
+        caps = [prior + 1 for _, prior in reqs]
+        ne, rows = ctx.assemble_plan(requests, caps)
+        bt = torch.zeros(max(1, ne) * 4, dtype=torch.int32, device="cuda")
+        kv = torch.zeros(n_layers * 2 * HKV * rows * D, dtype=torch.bfloat16, device="cuda")
+        cu, al = ctx.assemble_kv(requests, caps, bt, kv, rows)
+        kv5 = kv.view(n_layers, 2, HKV, rows, D)
+        prior_k, prior_v = [], []
+        for r, (_, prior) in enumerate(reqs):
+            pk, pv = _bits(rng, (HKV, prior, D)), _bits(rng, (HKV, prior, D))
+            lo = cu[r] + al[r]
+            kv5[layer, 0, :, lo:lo + prior] = dev_bf16(pk)
+            kv5[layer, 1, :, lo:lo + prior] = dev_bf16(pv)
+            prior_k.append(pk)
+            prior_v.append(pv)
+        ctx_len = [al[r] + reqs[r][1] for r in range(n)]
+        qkv = _bits(rng, (n, HQ * D + 2 * HKV * D))
+        if gamma == "uniform":
+            gq = sd.f32_to_bf16_bits(rng.uniform(0.5, 1.5, D).astype(np.float32))
+            gk = sd.f32_to_bf16_bits(rng.uniform(0.5, 1.5, D).astype(np.float32))
+        else:
+            gq = gk = sd.f32_to_bf16_bits(np.ones(D, np.float32))
+        qd = dev_bf16(qkv)
+        o = torch.empty(n, HQ, D, dtype=torch.bfloat16, device="cuda")
+        ld = qkv.shape[1]
+        ctx.decode_attn(layer, cu, ctx_len, pos, qd[:, :HQ * D], ld, qd[:, HQ * D:HQ * D + HKV * D],
+                        qd[:, HQ * D + HKV * D:], ld, dev_bf16(gq), dev_bf16(gk), kv, rows, o)
+        torch.cuda.synchronize()
+        got = host_f64(o)
+        # the new key and value sit right after the prior rows
+        new_kv = bf16_to_host(kv).reshape(n_layers, 2, HKV, rows, D)
+    q_all = oracle.decode_bf16(qkv)
+    ref = np.empty((n, HQ, D))
+    for r, (arts, prior) in enumerate(reqs):
+        p = ctx_len[r] if pos is None else pos[r]
+        q = oracle.rope(oracle.rms_norm_heads(q_all[r:r + 1, :HQ * D].reshape(1, HQ, D), oracle.decode_bf16(gq), 1e-6),
+                        np.array([p]), 1e6)
+        k_new = oracle.rope(oracle.rms_norm_heads(q_all[r:r + 1, HQ * D:HQ * D + HKV * D].reshape(1, HKV, D),
+                                                  oracle.decode_bf16(gk), 1e-6), np.array([p]), 1e6)
+        v_new = q_all[r:r + 1, HQ * D + HKV * D:].reshape(1, HKV, D)
+        ks = [oracle.decode_bf16(art_k[a][layer]).transpose(1, 0, 2) for a in arts]
+        vs = [oracle.decode_bf16(art_v[a][layer]).transpose(1, 0, 2) for a in arts]
+        ks += [oracle.decode_bf16(prior_k[r]).transpose(1, 0, 2), k_new]
+        vs += [oracle.decode_bf16(prior_v[r]).transpose(1, 0, 2), v_new]
+        keys, vals = np.concatenate(ks), np.concatenate(vs)
+        ref[r] = oracle.attention(q, keys, vals, art_len=ctx_len[r])[0]
+        # the value row written into the cache is the input's bits
+        row = cu[r] + ctx_len[r]
+        assert np.array_equal(new_kv[layer, 1, :, row], qkv[r, HQ * D + HKV * D:].reshape(HKV, D))
+    return got, ref
+
+
+def test_decode_ragged_batch():
+    # an empty request (its own key only: O = its value), artifacts of one
+    # token, chunk-straddling lengths, duplicates
+    _say("decode ragged batch")
+    got, ref = _run_decode(41, [300, 17, 1, 1024, 1024, 900],
+                           [((0,), 5), ((), 0), ((1, 2), 1), ((3, 4, 5), 37), ((2, 2, 2), 0), ((1,), 250)])
+    assert_o_close(got, ref, "batch")
+    for r in range(got.shape[0]):
+        assert_o_close_per_request(got[r], ref[r], f"request {r}")
+
+
+def test_decode_single_key_is_value():
+    _say("decode single key")
+    got, ref = _run_decode(42, [16], [((), 0)], gamma="ones")
+    assert_o_close(got, ref)
+
+
+def test_decode_c2_context_one_request():
+    # the c2 request's context: 8 x 1024 artifact keys + 256 suffix keys, then the new token
+    _say("decode c2 context")
+    got, ref = _run_decode(43, [1024] * 8, [(tuple(range(8)), 256)])
+    assert_o_close(got, ref)
+
+
+def test_decode_batch16_long_second_layer_and_positions():
+    # sixteen requests of ~1-9k keys on layer 1 of a two-layer cache, explicit positions
+    _say("decode batch 16, layer 1")
+    rng = np.random.default_rng(44)
+    lengths = [int(v) for v in rng.integers(256, 1537, size=12)]
+    reqs = []
+    for i in range(16):
+        k = int(rng.integers(1, 7))
+        reqs.append((tuple(int(a) for a in rng.choice(12, size=k, replace=False)), int(rng.integers(0, 300))))
+    pos = [int(v) for v in rng.integers(0, 20000, size=16)]
+    got, ref = _run_decode(45, lengths, reqs, n_layers=2, layer=1, pos=pos)
+    assert_o_close(got, ref, "batch")
+    for r in range(16):
+        assert_o_close_per_request(got[r], ref[r], f"request {r}")
+
+
+def test_decode_capacity_error():
+    _say("decode capacity error")
+    cfg = ModelCfg(n_layers=1, hidden=256)
+    with Context(cfg, pool_pages=1) as ctx:
+        kv = torch.zeros(2 * HKV * 8 * D, dtype=torch.bfloat16, device="cuda")
+        q = torch.zeros(1, HQ * D + 2 * HKV * D, dtype=torch.bfloat16, device="cuda")
+        g = torch.ones(D, dtype=torch.bfloat16, device="cuda")
+        ld = q.shape[1]
+        with pytest.raises(AttunerError) as e:
+            # 8 cache rows, 8 keys already there: no row for the new one
+            ctx.decode_attn(0, [0, 8], [8], None, q[:, :HQ * D], ld, q[:, HQ * D:HQ * D + HKV * D],
+                            q[:, HQ * D + HKV * D:], ld, g, g, kv, 8, torch.empty(1, HQ, D, dtype=torch.bfloat16,
+                                                                                  device="cuda"))
+        assert e.value.status == -1
