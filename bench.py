@@ -14,6 +14,11 @@ stack, with all inputs resident in HBM before timing starts:
 The same kernels then run the full-context prefill of the whole request
 (attuner_full_prefill, every layer, no adapter) for the speedup.
 
+With --decode the step is one generated token per request after the suffix:
+per layer the projection + LoRA of the new tokens and attuner_decode_attn
+(norm + RoPE of the new q/k, the new k/v into the cache, split-KV attention
+over the whole context); its roofline is HBM (the cached K/V read once).
+
 With --model the step is instead the whole Qwen3-shaped decoder stack up to
 the greedy first token (the time-to-first-token of the paper's measurements):
 the assembly, the embedding rows of the suffix, per layer input RMSNorm ->
@@ -71,6 +76,9 @@ def parse():
     ap.add_argument("--model", action="store_true", help="time the whole Qwen3-shaped decoder stack instead "
                     "(embedding, input norm, q/k/v projection + LoRA, suffix attention, o_proj, post norm, SwiGLU "
                     "MLP, final norm, LM head, greedy first token) against a full prefill through the same stack")
+    ap.add_argument("--decode", action="store_true", help="time one decode step per request instead: every "
+                    "layer's q/k/v projection + LoRA of the new tokens and attuner_decode_attn over the whole "
+                    "assembled context (the suffix already prefilled)")
     ap.add_argument("--quiet", action="store_true")
     return ap.parse_args()
 
@@ -170,6 +178,9 @@ def main():
         sys.exit(2)
     if args.model:
         model_main(args)
+        return
+    if args.decode:
+        decode_main(args)
         return
 
     import numpy as np
@@ -713,6 +724,169 @@ def model_main(args):
         "full_prefill": full,
         "speedup_vs_full_prefill": full["speedup"] if full else None,
         "paper_context": PAPER_CONTEXT,
+    }
+    print(json.dumps(out), flush=True)
+    ctx.close()
+
+
+# ----------------------------------------------------------------------------
+# --decode: one generated token per request over the whole context
+# ----------------------------------------------------------------------------
+
+DECODE_METRIC = "decode tokens/s (adapted queries, every layer) + decode attention HBM GB/s (% of peak)"
+
+
+def decode_main(args):
+    import numpy as np
+    import torch
+
+    import synthdata as sd
+    from paper_2609_36722_amd.api import Context, ModelCfg
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = sd.make_workload(args.workload)
+    s, NL = wl.shape, wl.n_layers
+    H, nq, nkv = s.hidden, s.q_dim, s.kv_dim
+    n_out = nq + 2 * nkv
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2000 + wl.index)
+
+    def randn(*shape, std=1.0):
+        t = torch.randn(*shape, generator=gen, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            t.mul_(std)
+        return t.to(torch.bfloat16)
+
+    n_req = len(wl.requests)
+    log(args, f"decode {wl.name}: {NL} layers, {n_req} request(s), contexts "
+              f"{[wl.art_len(r) + r.suffix_len for r in wl.requests]} keys before the new token")
+    wqkv = [randn(n_out, H, std=wl.w_std) for _ in range(NL)]
+    a_l = [randn(wl.rank, H, std=wl.a_std) for _ in range(NL)]
+    b_l = [randn(nq, wl.rank, std=wl.b_std) for _ in range(NL)]
+    ones = torch.ones(s.head_dim, dtype=torch.bfloat16, device=dev)
+    x_new = randn(n_req, H)
+    qkv = [torch.empty(n_req, n_out, dtype=torch.bfloat16, device=dev) for _ in range(NL)]
+    o = torch.empty(n_req, s.n_q_heads, s.head_dim, dtype=torch.bfloat16, device=dev)
+
+    used = sorted({a for r in wl.requests for a in r.artifact_ids})
+    pages = sum(math.ceil(wl.artifact_lengths[a] / 16) for a in used)
+    cfg = ModelCfg(n_layers=NL, hidden=H, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads, head_dim=s.head_dim,
+                   rope_theta=s.rope_theta, rms_eps=s.rms_eps)
+    ctx = Context(cfg, pool_pages=pages)
+    ids = {}
+    for a in used:
+        L = wl.artifact_lengths[a]
+        ids[a] = ctx.store_artifact(randn(NL, s.n_kv_heads, L, s.head_dim), randn(NL, s.n_kv_heads, L, s.head_dim))
+    requests = [[ids[a] for a in r.artifact_ids] for r in wl.requests]
+    caps = [r.suffix_len + 1 for r in wl.requests]
+    n_entries, rows = ctx.assemble_plan(requests, caps)
+    bt = torch.zeros(max(1, n_entries) * 4, dtype=torch.int32, device=dev)
+    req_kv = torch.zeros(NL * 2 * s.n_kv_heads * rows * s.head_dim, dtype=torch.bfloat16, device=dev)
+    cu_ctx, art_len = ctx.assemble_kv(requests, caps, bt, req_kv, rows)
+    # the suffix rows of every layer: seeded keys/values standing in for the prefilled suffix
+    kv5 = req_kv.view(NL, 2, s.n_kv_heads, rows, s.head_dim)
+    for r, req in enumerate(wl.requests):
+        lo = cu_ctx[r] + art_len[r]
+        kv5[:, :, :, lo:lo + req.suffix_len] = randn(NL, 2, s.n_kv_heads, req.suffix_len, s.head_dim)
+    ctx_len = [art_len[r] + wl.requests[r].suffix_len for r in range(n_req)]
+    torch.cuda.synchronize()
+
+    def layer_loop(mark=None):
+        for l in range(NL):
+            if mark:
+                mark("qkv_proj")
+            ctx.qproj_lora(x_new, wqkv[l], a_l[l], b_l[l], wl.rank, wl.scale, nq, qkv[l])
+            if mark:
+                mark("decode_attn")
+            q = qkv[l]
+            ctx.decode_attn(l, cu_ctx, ctx_len, None, q[:, :nq], n_out, q[:, nq:nq + nkv], q[:, nq + nkv:], n_out,
+                            ones, ones, req_kv, rows, o)
+        if mark:
+            mark(None)
+
+    for _ in range(max(1, args.warmup)):
+        layer_loop()
+    torch.cuda.synchronize()
+    ev = []
+
+    def mark(name):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        ev.append((name, e))
+
+    ctx.trace_begin()
+    for _ in range(3):
+        layer_loop(mark)
+    torch.cuda.synchronize()
+    ktimes = ctx.trace_end()
+    breakdown = {}
+    for (name, e0), (_, e1) in zip(ev[:-1], ev[1:]):
+        if name is not None:
+            breakdown[name] = breakdown.get(name, 0.0) + e0.elapsed_time(e1) / 3
+    per_kernel = {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t, _) in ktimes.items()}
+
+    graph = None
+    if not args.no_graph:
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        graph = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap):
+            layer_loop()
+        torch.cuda.synchronize()
+
+    def step():
+        if graph is not None:
+            graph.replay()
+        else:
+            layer_loop()
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+
+    n_keys = [c + 1 for c in ctx_len]
+    kv_bytes = sum(n_keys) * s.n_kv_heads * s.head_dim * 2 * 2          # K and V of every visible key, per layer
+    io_bytes = n_req * s.n_q_heads * s.head_dim * 2 * 2                  # q_hat in, O out
+    attn_ms = per_kernel["decode_attention_kernel"]["avg_ms"]
+    attn_gbps = (kv_bytes + io_bytes) / (attn_ms * 1e-3) / 1e9
+    gemm_ms = per_kernel["gemm_lora_kernel"]["avg_ms"]
+    gemm_w_gbps = n_out * H * 2 / (gemm_ms * 1e-3) / 1e9
+    log(args, f"decode step {ms_step:.3f} ms ({n_req / (ms_step * 1e-3):.1f} tokens/s); decode attention "
+              f"{attn_ms * 1e3:.1f} us = {attn_gbps:.0f} GB/s; projection {gemm_ms * 1e3:.1f} us = "
+              f"{gemm_w_gbps:.0f} GB/s of weights")
+    out = {
+        "metric": DECODE_METRIC,
+        "value": round(n_req / (ms_step * 1e-3), 2),
+        "unit": "decode tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded device-side N(0,1) / N(0,0.02) bf16 draws, distinct weights per layer)",
+        "config": {"workload": wl.name + "+decode", "layers": NL, "hidden": H, "requests": n_req,
+                   "keys_per_request": n_keys, "lora_rank": wl.rank},
+        "layer_loop": "hip_graph" if graph is not None else "eager",
+        "roofline": {"bound": "hbm", "kernel": "decode_attention_kernel", "achieved": round(attn_gbps, 1),
+                     "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(attn_gbps / PEAK_HBM_GBPS, 4),
+                     "traffic": None, "bytes_per_launch": kv_bytes + io_bytes, "launch_ms": attn_ms},
+        "breakdown_ms_per_step_eager": {k: round(v, 4) for k, v in breakdown.items()},
+        "projection_weight_gbps": round(gemm_w_gbps, 1),
+        "kernel_avg_ms": per_kernel,
     }
     print(json.dumps(out), flush=True)
     ctx.close()

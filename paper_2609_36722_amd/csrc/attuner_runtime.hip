@@ -355,8 +355,7 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
 }
 
 // One new token per request (reqs[r].q_len == 1, row r): attention over the
-// request's art_len + 1 keys, cut into equal chunks so that the launch has
-// about four workgroups per CU.
+// request's art_len + 1 keys, cut into equal chunks.
 attuner_status run_decode(attuner_ctx* c, const std::vector<ReqDesc>& reqs, const void* q, const uint16_t* k_plane,
                           const uint16_t* v_plane, int64_t head_stride, void* o, hipStream_t stream) {
   DecodeParams p;
@@ -370,11 +369,17 @@ attuner_status run_decode(attuner_ctx* c, const std::vector<ReqDesc>& reqs, cons
   p.n_kv_heads = c->cfg.n_kv_heads;
   p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c->cfg.head_dim));
   p.n_req = (int32_t)reqs.size();
-  int64_t keys = 0;
-  for (const auto& r : reqs) keys += (int64_t)r.art_len + 1;
-  // chunks of a multiple of 128 keys (one step of the 32 key groups x 4)
-  const int64_t want = (keys * c->cfg.n_kv_heads + 1023) / 1024;
-  p.chunk = (int32_t)std::max<int64_t>(128, (want + 127) / 128 * 128);
+  // Chunks are a multiple of 64 keys (one step of the 32 key groups x 2),
+  // at least two steps.  Two workgroups fit a CU (VGPRs and LDS), so 512 run
+  // at once: take the smallest chunk whose workgroups fit that single round;
+  // past 32 steps per chunk, rounds of long workgroups are fine.
+  int32_t chunk = 128;
+  for (;; chunk += 64) {
+    int64_t wgs = 0;
+    for (const auto& r : reqs) wgs += ((int64_t)r.art_len + 1 + chunk - 1) / chunk;
+    if (wgs * c->cfg.n_kv_heads <= 512 || chunk >= 2048) break;
+  }
+  p.chunk = chunk;
   int32_t splits = 0;
   for (size_t r = 0; r < reqs.size(); ++r) {
     const int32_t n_keys = reqs[r].art_len + 1;

@@ -15,8 +15,9 @@
 // (bf16 pairs) and of the 4 output accumulators (fp32); a wave's K (and V)
 // load instruction covers 8 whole 128-byte lines of 8 consecutive keys.  Per
 // key: q . k as bf16 dot2 products, summed over the group's 8 lanes with
-// DPP; online softmax in the log2 domain per step of 4 keys; o += p v.  The
-// 32 groups then merge through LDS.  A request with one chunk writes O
+// DPP; online softmax in the log2 domain per step of 2 keys; o += p v; the
+// loads of the next step are in flight during the arithmetic of this one.
+// The 32 groups then merge through LDS.  A request with one chunk writes O
 // (bf16); otherwise each chunk writes its unnormalised O and (max, sum) in
 // fp32 and decode_combine_kernel merges the chunks of the request.
 
@@ -32,7 +33,7 @@ constexpr int G = 4;                // query heads per KV head
 constexpr int LPK = 8;              // lanes per key
 constexpr int NTH = 256;
 constexpr int GROUPS = NTH / LPK;   // keys per workgroup per sub-step
-constexpr int U = 4;                // keys per group per step
+constexpr int U = 2;                // keys per group per step
 constexpr float kNegBig = -1.0e30f;
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -88,18 +89,24 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
     for (int i = 0; i < 16; ++i) o[h][i] = 0.f;
   }
 
-  for (int key0 = k0 + grp; key0 < k1; key0 += GROUPS * U) {
+  // Steps of U keys per group, double-buffered: the loads of step i + 1 are
+  // issued before the arithmetic of step i.
+  struct Buf {
     u32x4 ka[U], kc[U], va[U], vc[U];
+  };
+  auto load = [&](int key0, Buf& b) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int key = min(key0 + u * GROUPS, k1 - 1);  // past the chunk: a valid row, masked below
       const bf16_t* kr = kbase + (int64_t)key * D;
       const bf16_t* vr = vbase + (int64_t)key * D;
-      ka[u] = *reinterpret_cast<const u32x4*>(kr + 8 * sub);
-      kc[u] = *reinterpret_cast<const u32x4*>(kr + 64 + 8 * sub);
-      va[u] = *reinterpret_cast<const u32x4*>(vr + 8 * sub);
-      vc[u] = *reinterpret_cast<const u32x4*>(vr + 64 + 8 * sub);
+      b.ka[u] = *reinterpret_cast<const u32x4*>(kr + 8 * sub);
+      b.kc[u] = *reinterpret_cast<const u32x4*>(kr + 64 + 8 * sub);
+      b.va[u] = *reinterpret_cast<const u32x4*>(vr + 8 * sub);
+      b.vc[u] = *reinterpret_cast<const u32x4*>(vr + 64 + 8 * sub);
     }
+  };
+  auto step = [&](int key0, const Buf& b) __attribute__((always_inline)) {
     float sc[U][G];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -108,9 +115,9 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
       for (int h = 0; h < G; ++h) {
         float acc = 0.f;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc = dot2(qa[h][e], ka[u][e], acc);
+        for (int e = 0; e < 4; ++e) acc = dot2(qa[h][e], b.ka[u][e], acc);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc = dot2(qb[h][e], kc[u][e], acc);
+        for (int e = 0; e < 4; ++e) acc = dot2(qb[h][e], b.kc[u][e], acc);
         acc = sum8(acc);
         sc[u][h] = valid ? acc * p.score_scale : kNegBig;
       }
@@ -133,10 +140,10 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
       float vf[16];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        vf[2 * e] = lo_f(va[u][e]);
-        vf[2 * e + 1] = hi_f(va[u][e]);
-        vf[8 + 2 * e] = lo_f(vc[u][e]);
-        vf[8 + 2 * e + 1] = hi_f(vc[u][e]);
+        vf[2 * e] = lo_f(b.va[u][e]);
+        vf[2 * e + 1] = hi_f(b.va[u][e]);
+        vf[8 + 2 * e] = lo_f(b.vc[u][e]);
+        vf[8 + 2 * e + 1] = hi_f(b.vc[u][e]);
       }
 #pragma unroll
       for (int h = 0; h < G; ++h) {
@@ -145,6 +152,23 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[h][i] = fmaf(pr, vf[i], o[h][i]);
       }
+    }
+  };
+
+  constexpr int STEP = GROUPS * U;
+  int key0 = k0 + grp;
+  if (key0 < k1) {
+    Buf b0, b1;
+    load(key0, b0);
+    while (true) {
+      if (key0 + STEP < k1) load(key0 + STEP, b1);
+      step(key0, b0);
+      key0 += STEP;
+      if (key0 >= k1) break;
+      if (key0 + STEP < k1) load(key0 + STEP, b0);
+      step(key0, b1);
+      key0 += STEP;
+      if (key0 >= k1) break;
     }
   }
 
@@ -185,27 +209,68 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
 }
 
 // Merge the chunks of each request with more than one: workgroup = (request,
-// KV head g), thread = (query head, 2 dims).
+// query head); its 256 threads are 8 chunk groups of 32 lanes (4 dims each),
+// group j merging chunks j, j + 8, ... with the loads of up to 8 chunks in
+// flight, then the 8 groups merge through LDS.
+constexpr int CG = 8;     // chunk groups per workgroup
+constexpr int CB = 8;     // chunks loaded per group before merging
+
 __global__ __launch_bounds__(NTH) void decode_combine_kernel(const DecodeParams p) {
-  const int g = blockIdx.x % p.n_kv_heads;
-  const DecodeReq rq = p.req[blockIdx.x / p.n_kv_heads];
+  __shared__ f32x4 s_o[CG][32];
+  __shared__ f32x2 s_ml[CG];
+  const int qh = blockIdx.x % p.n_q_heads;
+  const DecodeReq rq = p.req[blockIdx.x / p.n_q_heads];
   if (rq.n_split <= 1) return;
-  const int qh = g * G + (threadIdx.x >> 6);
-  const int d = 2 * (threadIdx.x & 63);
+  const int cg = threadIdx.x >> 5;
+  const int ln = threadIdx.x & 31;
+  float m = kNegBig, l = 0.f;
+  f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s0 = cg; s0 < rq.n_split; s0 += CG * CB) {
+    f32x2 ml[CB];
+    f32x4 ov[CB];
+#pragma unroll
+    for (int b = 0; b < CB; ++b) {
+      const int s = min(s0 + b * CG, rq.n_split - 1);
+      const int64_t row = (int64_t)(rq.split0 + s) * p.n_q_heads + qh;
+      ml[b] = *reinterpret_cast<const f32x2*>(p.part_ml + row * 2);
+      ov[b] = *reinterpret_cast<const f32x4*>(p.part_o + row * D + 4 * ln);
+    }
+    float mb = m;
+#pragma unroll
+    for (int b = 0; b < CB; ++b)
+      if (s0 + b * CG < rq.n_split) mb = fmaxf(mb, ml[b][0]);
+    const float alpha = exp2f(m - mb);
+    l *= alpha;
+    o *= alpha;
+#pragma unroll
+    for (int b = 0; b < CB; ++b) {
+      if (s0 + b * CG >= rq.n_split) continue;
+      const float w = exp2f(ml[b][0] - mb);
+      l = fmaf(w, ml[b][1], l);
+      o += w * ov[b];
+    }
+    m = mb;
+  }
+  s_o[cg][ln] = o;
+  if (ln == 0) s_ml[cg] = f32x2{m, l};
+  __syncthreads();
+  if (threadIdx.x >= 32) return;
   float mm = kNegBig;
-  for (int s = 0; s < rq.n_split; ++s) mm = fmaxf(mm, p.part_ml[((int64_t)(rq.split0 + s) * p.n_q_heads + qh) * 2]);
-  float ll = 0.f, o0 = 0.f, o1 = 0.f;
-  for (int s = 0; s < rq.n_split; ++s) {
-    const int64_t row = (int64_t)(rq.split0 + s) * p.n_q_heads + qh;
-    const f32x2 ml = *reinterpret_cast<const f32x2*>(p.part_ml + row * 2);
-    const f32x2 ov = *reinterpret_cast<const f32x2*>(p.part_o + row * D + d);
-    const float w = exp2f(ml[0] - mm);
-    ll = fmaf(w, ml[1], ll);
-    o0 = fmaf(w, ov[0], o0);
-    o1 = fmaf(w, ov[1], o1);
+#pragma unroll
+  for (int j = 0; j < CG; ++j) mm = fmaxf(mm, s_ml[j][0]);
+  float ll = 0.f;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < CG; ++j) {
+    const float w = exp2f(s_ml[j][0] - mm);
+    ll = fmaf(w, s_ml[j][1], ll);
+    acc += w * s_o[j][ln];
   }
   const float inv = 1.0f / ll;
-  *reinterpret_cast<uint32_t*>(p.o + ((int64_t)rq.q_row * p.n_q_heads + qh) * D + d) = pack_bf16x2(o0 * inv, o1 * inv);
+  u32x2 pk;
+  pk[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  pk[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+  *reinterpret_cast<u32x2*>(p.o + ((int64_t)rq.q_row * p.n_q_heads + qh) * D + 4 * ln) = pk;
 }
 
 }  // namespace
@@ -218,7 +283,7 @@ hipError_t launch_decode_attention(const DecodeParams& p, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.total_splits > p.n_req) {
-    ATTUNER_LAUNCH("decode_combine_kernel", decode_combine_kernel, dim3((unsigned)(p.n_req * p.n_kv_heads)), dim3(NTH),
+    ATTUNER_LAUNCH("decode_combine_kernel", decode_combine_kernel, dim3((unsigned)(p.n_req * p.n_q_heads)), dim3(NTH),
                    stream, p);
     e = hipGetLastError();
   }
