@@ -860,7 +860,10 @@ def decode_main(args):
     io_bytes = n_req * s.n_q_heads * s.head_dim * 2 * 2                  # q_hat in, O out
     attn_ms = per_kernel["decode_attention_kernel"]["avg_ms"]
     attn_gbps = (kv_bytes + io_bytes) / (attn_ms * 1e-3) / 1e9
-    gemm_ms = per_kernel["gemm_lora_kernel"]["avg_ms"]
+    # the projection of a few tokens: the weight-streaming GEMV (+ the LoRA
+    # down-projection kernel); more tokens take the MFMA GEMM
+    proj = [k for k in ("gemv_kernel", "lora_down_kernel", "gemm_lora_kernel") if k in per_kernel]
+    gemm_ms = sum(per_kernel[k]["avg_ms"] for k in proj)
     gemm_w_gbps = n_out * H * 2 / (gemm_ms * 1e-3) / 1e9
     log(args, f"decode step {ms_step:.3f} ms ({n_req / (ms_step * 1e-3):.1f} tokens/s); decode attention "
               f"{attn_ms * 1e3:.1f} us = {attn_gbps:.0f} GB/s; projection {gemm_ms * 1e3:.1f} us = "
@@ -886,6 +889,7 @@ def decode_main(args):
                      "traffic": None, "bytes_per_launch": kv_bytes + io_bytes, "launch_ms": attn_ms},
         "breakdown_ms_per_step_eager": {k: round(v, 4) for k, v in breakdown.items()},
         "projection_weight_gbps": round(gemm_w_gbps, 1),
+        "projection_kernels": proj,
         "kernel_avg_ms": per_kernel,
     }
     print(json.dumps(out), flush=True)

@@ -464,9 +464,10 @@ attuner_status qproj_impl(attuner_ctx* c, int32_t n_tok, const void* x, const vo
   const int hidden = c->cfg.hidden;
   const int r_pad = rank > 0 && lora_cols > 0 ? (rank + 15) / 16 * 16 : 0;
   // ranks up to kGemmFusedLoraMaxRank: the GEMM computes t = scale * x A^T
-  // itself; larger ranks take a separate down-projection kernel first
+  // itself; larger ranks, and the GEMV of a few tokens, take a separate
+  // down-projection kernel first
   float* t_part = nullptr;
-  if (r_pad > kGemmFusedLoraMaxRank) {
+  if (r_pad > kGemmFusedLoraMaxRank || (r_pad > 0 && n_tok <= kGemvMaxTok)) {
     const size_t part_bytes = (size_t)lora_down_slices(hidden) * n_tok * r_pad * sizeof(float);
     HIP_TRY(c->ws_lora.ensure(part_bytes));
     t_part = static_cast<float*>(c->ws_lora.ptr);

@@ -392,6 +392,8 @@ hipError_t launch_gemm_any(const uint16_t* x, const uint16_t* w, int n_tok, int 
                            float scale, const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
                            GemmEpi epi, uint16_t* out, hipStream_t stream) {
   if (n_tok == 0) return hipSuccess;
+  if (n_tok <= kGemvMaxTok) return launch_gemv(x, w, n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, epi, out,
+                                              stream);
   const int n_slice = lora_down_slices(hidden);
   // Tile choice.  One workgroup per CU at a time, and a workgroup's k-loop
   // runs at the CU's operand ingest rate, so a launch takes about

@@ -1,0 +1,159 @@
+// Projection for a few tokens (decode: one new token per request): out =
+// x W^T with the same epilogue modes and low-rank update as the GEMM, for
+// n_tok <= kGemvMaxTok.  With a handful of tokens each weight is used once
+// per token, so the launch streams W from HBM and an MFMA tile would be
+// mostly empty: every wave owns two consecutive output rows, its 64 lanes
+// read 16-byte chunks of both rows (consecutive lanes, consecutive chunks:
+// whole 128-byte lines) and of every token's x, accumulate bf16 dot2
+// products in fp32, and the rows' sums meet in a wave reduction.  The
+// low-rank term (rows below lora_cols) enters before the reduction: lane j
+// adds t[token][j] * B[row][j], t = scale * x A^T summed from the slice
+// partials of the down-projection kernel.  Lane t then stores token t.
+
+#include "common.h"
+#include "kernels.h"
+
+namespace attuner {
+
+namespace {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kChunkBatch = 4;  // 16-byte chunks per row and lane in flight
+
+// The operands go through scalar parameters: a bit cast applied to a vector
+// element expression directly reads element 0 whatever the index (seen with
+// this compiler).
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
+}
+
+__device__ __forceinline__ float dot8(u32x4 a, u32x4 b, float c) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) c = dot2(a[e], b[e], c);
+  return c;
+}
+
+template <int T>
+__global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w, int N,
+                                                   int K, const bf16_t* __restrict__ b, int rank, int r_pad,
+                                                   int lora_cols, const float* __restrict__ t_part, int n_slice,
+                                                   GemmEpi epi, bf16_t* out) {
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int n0 = (blockIdx.x * 4 + wave) * 2;
+  if (n0 >= N) return;
+  const bf16_t* w0 = w + (int64_t)n0 * K;
+  const bf16_t* w1 = w0 + K;
+  const int nc = K / 8;
+
+  float acc[2][T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) acc[0][t] = acc[1][t] = 0.f;
+
+  // whole batches of kChunkBatch chunks per lane (all loads issued, then the
+  // products), then the chunks left one at a time
+  int c = lane;
+  for (; c + 64 * (kChunkBatch - 1) < nc; c += 64 * kChunkBatch) {
+    u32x4 wa[kChunkBatch], wb[kChunkBatch], xv[kChunkBatch][T];
+#pragma unroll
+    for (int j = 0; j < kChunkBatch; ++j) {
+      const int cj = c + 64 * j;
+      wa[j] = *reinterpret_cast<const u32x4*>(w0 + 8 * cj);
+      wb[j] = *reinterpret_cast<const u32x4*>(w1 + 8 * cj);
+#pragma unroll
+      for (int t = 0; t < T; ++t) xv[j][t] = *reinterpret_cast<const u32x4*>(x + (int64_t)t * K + 8 * cj);
+    }
+#pragma unroll
+    for (int j = 0; j < kChunkBatch; ++j)
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        acc[0][t] = dot8(wa[j], xv[j][t], acc[0][t]);
+        acc[1][t] = dot8(wb[j], xv[j][t], acc[1][t]);
+      }
+  }
+  for (; c < nc; c += 64) {
+    const u32x4 wa = *reinterpret_cast<const u32x4*>(w0 + 8 * c);
+    const u32x4 wb = *reinterpret_cast<const u32x4*>(w1 + 8 * c);
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const u32x4 xv = *reinterpret_cast<const u32x4*>(x + (int64_t)t * K + 8 * c);
+      acc[0][t] = dot8(wa, xv, acc[0][t]);
+      acc[1][t] = dot8(wb, xv, acc[1][t]);
+    }
+  }
+
+  // rows below lora_cols (a multiple of 32, so both rows or neither)
+  if (r_pad > 0 && n0 < lora_cols && lane < rank) {
+    const float b0 = bf16_to_f32(b[(int64_t)n0 * rank + lane]);
+    const float b1 = bf16_to_f32(b[(int64_t)(n0 + 1) * rank + lane]);
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      float tv = 0.f;
+      for (int z = 0; z < n_slice; ++z) tv += t_part[((int64_t)z * T + t) * r_pad + lane];
+      acc[0][t] = fmaf(tv, b0, acc[0][t]);
+      acc[1][t] = fmaf(tv, b1, acc[1][t]);
+    }
+  }
+
+  float y0 = 0.f, y1 = 0.f;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const float s0 = wave_sum(acc[0][t]);
+    const float s1 = wave_sum(acc[1][t]);
+    if (lane == t) {
+      y0 = s0;
+      y1 = s1;
+    }
+  }
+  if (lane >= T) return;
+  const int t = lane;
+  if (epi.mode == kEpiF32) {
+    *reinterpret_cast<f32x2*>(epi.out_f32 + (int64_t)t * N + n0) = f32x2{y0, y1};
+    return;
+  }
+  if (epi.mode == kEpiSwiglu) {
+    // rows n0 (gate j) and n0 + 1 (up j), j = n0 / 2
+    out[(int64_t)t * (N / 2) + n0 / 2] = f32_to_bf16(y0 / (1.0f + __expf(-y0)) * y1);
+    return;
+  }
+  if (epi.mode == kEpiResidual) {
+    const uint32_t r = *reinterpret_cast<const uint32_t*>(epi.residual + (int64_t)t * N + n0);
+    y0 += __uint_as_float(r << 16);
+    y1 += __uint_as_float(r & 0xFFFF0000u);
+  }
+  *reinterpret_cast<uint32_t*>(out + (int64_t)t * N + n0) = pack_bf16x2(y0, y1);
+}
+
+}  // namespace
+
+hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, const uint16_t* b,
+                       int rank, int r_pad, int lora_cols, const float* t_part, GemmEpi epi, uint16_t* out,
+                       hipStream_t stream) {
+  if (n_tok == 0) return hipSuccess;
+  if (n_tok > kGemvMaxTok || n_out % 8 != 0 || k_dim % 8 != 0 || (r_pad > 0 && t_part == nullptr))
+    return hipErrorInvalidValue;
+  const int n_slice = lora_down_slices(k_dim);
+  const dim3 grid((unsigned)(n_out / 8));
+#define ATTUNER_GEMV(T_)                                                                                     \
+  case T_:                                                                                                   \
+    ATTUNER_LAUNCH("gemv_kernel", gemv_kernel<T_>, grid, dim3(256), stream, x, w, n_out, k_dim, b, rank, r_pad, \
+                   lora_cols, t_part, n_slice, epi, out);                                                     \
+    break;
+  switch (n_tok) {
+    ATTUNER_GEMV(1)
+    ATTUNER_GEMV(2)
+    ATTUNER_GEMV(3)
+    ATTUNER_GEMV(4)
+    ATTUNER_GEMV(5)
+    ATTUNER_GEMV(6)
+    ATTUNER_GEMV(7)
+    ATTUNER_GEMV(8)
+    default: return hipErrorInvalidValue;
+  }
+#undef ATTUNER_GEMV
+  return hipGetLastError();
+}
+
+}  // namespace attuner

@@ -52,7 +52,8 @@ hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int
 // out[i][n] = x[i] . w[n] + (n < lora_cols ? t[i] . b[n] : 0) (r_pad = 0: no
 // adapter).  t is the sum of the slices of t_part when t_part is given;
 // with t_part null (and r_pad <= kGemmFusedLoraMaxRank) the kernel computes
-// t = scale * x a^T itself.
+// t = scale * x a^T itself, except for n_tok <= kGemvMaxTok, which needs
+// t_part.
 constexpr int kGemmFusedLoraMaxRank = 32;
 hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
                             const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad, int lora_cols,
@@ -74,6 +75,15 @@ struct GemmEpi {
 };
 hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, GemmEpi epi,
                        uint16_t* out, hipStream_t stream);
+
+// The same product for at most kGemvMaxTok tokens as a weight-streaming
+// GEMV (any mode; the low-rank term needs t_part from launch_lora_down);
+// n_out and k_dim multiples of 8.  launch_gemm_lora and launch_gemm route
+// such token counts here.
+constexpr int kGemvMaxTok = 8;
+hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, const uint16_t* b,
+                       int rank, int r_pad, int lora_cols, const float* t_part, GemmEpi epi, uint16_t* out,
+                       hipStream_t stream);
 
 // out[t] = table[ids[t]] (rows of dim bf16 elements; ids in range).
 hipError_t launch_embed_rows(const uint16_t* table, const int32_t* ids, int n_tok, int dim, uint16_t* out,

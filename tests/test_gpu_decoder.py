@@ -256,3 +256,53 @@ def test_decoder_stack_two_layers():
     gf = oracle.decode_bf16(lm["gamma_final"])
     assert_intermediate_close(x_last, oracle.rms_norm_heads(hs[2][last], gf, s.rms_eps), "final norm")
     _check_pick(ids, mx, x_last, oracle.decode_bf16(lm["w_lm"]))
+
+
+# ----------------------------------------------------------------------------
+# the few-token path (at most 8 tokens: the weight-streaming GEMV) in every mode
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T,rank", [(1, 16), (2, 8), (3, 48), (5, 0), (8, 32), (7, 5)])
+def test_few_token_qproj_lora(T, rank):
+    _say(f"few-token qproj T={T} r={rank}")
+    rng = np.random.default_rng(100 + T + rank)
+    H, N, lora_cols = 2560, 6144, 4096
+    x, w = _bits(rng, (T, H)), _bits(rng, (N, H), 0.02)
+    a = _bits(rng, (max(rank, 1), H), 1 / math.sqrt(H))[:rank]
+    b = _bits(rng, (lora_cols, max(rank, 1)), 1.0)[:, :rank]     # B ~ N(0, 1): the update is visible
+    scale = 16.0 / max(rank, 1)
+    with Context(ModelCfg(n_layers=1, hidden=H), pool_pages=0) as ctx:
+        out = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+        ctx.qproj_lora(dev_bf16(x), dev_bf16(w), dev_bf16(np.ascontiguousarray(a)) if rank else None,
+                       dev_bf16(np.ascontiguousarray(b)) if rank else None, rank, scale, lora_cols, out)
+        torch.cuda.synchronize()
+        got = host_f64(out)
+    d = oracle.decode_bf16
+    ref = oracle.qproj_lora(d(x), d(w), d(a) if rank else None, d(b) if rank else None, scale, lora_cols)
+    assert_intermediate_close(got[:, :lora_cols], ref[:, :lora_cols], "q columns")
+    assert_intermediate_close(got[:, lora_cols:], ref[:, lora_cols:], "k/v columns")
+
+
+@pytest.mark.parametrize("T", [2, 4, 6, 8])
+def test_few_token_modes(T):
+    _say(f"few-token modes T={T}")
+    rng = np.random.default_rng(200 + T)
+    d = oracle.decode_bf16
+    with Context(ModelCfg(n_layers=1, hidden=512), pool_pages=0) as ctx:
+        # down projection with the residual in place (K = 9728)
+        g, wd, h = _bits(rng, (T, 9728)), _bits(rng, (512, 9728), 1 / math.sqrt(9728)), _bits(rng, (T, 512))
+        hd = dev_bf16(h)
+        ctx.linear(dev_bf16(g), dev_bf16(wd), hd, residual=hd)
+        # gate/up SwiGLU
+        x, wg, wu = _bits(rng, (T, 512)), _bits(rng, (1024, 512), 1 / math.sqrt(512)), _bits(rng, (1024, 512), 1 / math.sqrt(512))
+        sw = torch.empty(T, 1024, dtype=torch.bfloat16, device="cuda")
+        ctx.gate_up_swiglu(dev_bf16(x), dev_bf16(np.ascontiguousarray(np.stack([wg, wu], 1).reshape(2048, 512))), sw)
+        # greedy pick over fp32 logits
+        wl = _bits(rng, (4096, 512), 1 / math.sqrt(512))
+        ids = torch.empty(T, dtype=torch.int32, device="cuda")
+        mx = torch.empty(T, dtype=torch.float32, device="cuda")
+        ctx.lm_head_argmax(dev_bf16(x), dev_bf16(wl), ids, mx)
+        torch.cuda.synchronize()
+        assert_intermediate_close(host_f64(hd), oracle.linear(d(g), d(wd), d(h)), "down + residual")
+        assert_intermediate_close(host_f64(sw), oracle.swiglu(d(x), d(wg), d(wu)), "swiglu")
+        _check_pick(ids.cpu().numpy(), mx.cpu().numpy().astype(np.float64), d(x), d(wl))
