@@ -27,4 +27,6 @@ from .attuner_ref import (  # noqa: F401
     swiglu,
     decoder_layer,
     first_token,
+    interleaved_layer,
+    block_table_segments,
 )

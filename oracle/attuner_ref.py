@@ -336,3 +336,101 @@ def first_token(h_last: np.ndarray, gamma_final: np.ndarray, w_lm: np.ndarray, e
     [n][H] holds the last suffix token of each request.  Returns (ids, logits)."""
     logits = linear(rms_norm_heads(h_last, gamma_final, eps), w_lm)
     return np.argmax(logits, axis=-1), logits
+
+
+# ----------------------------------------------------------------------------
+# interleaved online spans (appendix A.3, the request layouts: system text,
+# headers, separators and the question sit between and around the cached
+# artifacts and are computed online; appendix A.5: attention with the causal
+# mask over the assembled context and its position ids)
+# ----------------------------------------------------------------------------
+
+def interleaved_layer(segments, x, wq, wk, wv, a, b, scale, gamma_q, gamma_k, art_k, art_v,
+                      n_q_heads: int, n_kv_heads: int, theta: float, eps: float) -> Dict[str, np.ndarray]:
+    """One layer of online prefill for a prompt that interleaves cached
+    artifacts with online spans.
+
+    segments: the prompt in order; an entry >= 0 is a cached artifact id
+    (art_k[id], art_v[id]: [L][Hkv][d], frozen, normalised and rotated at
+    their own local positions), an entry -n < 0 is an online span of n tokens.
+    x [n_online][H]: the hidden states of all online tokens, spans in order.
+    An online token at assembled position p (its offset in the whole prompt)
+    gets the adapted query and unadapted key/value projections, the per-head
+    norms and RoPE at position p, and attends to every assembled key at a
+    position <= p (cached keys as stored, online keys as just computed).
+    Returns o [n_online][Hq][d], q_hat, k_hat, v, the position of every online
+    token and the assembled keys/values [n_pos][Hkv][d].
+    """
+    x = np.asarray(x, np.float64)
+    d = np.asarray(gamma_q).shape[0]
+    pos = []
+    p = 0
+    for s in segments:
+        if s >= 0:
+            p += np.asarray(art_k[s]).shape[0]
+        else:
+            pos.extend(range(p, p - s))
+            p -= s
+    pos = np.asarray(pos, dtype=np.int64)
+    n = x.shape[0]
+    assert n == len(pos), "x must hold one row per online token"
+    q = qproj_lora(x, wq, a, b, scale).reshape(n, n_q_heads, d)
+    k = qproj_lora(x, wk).reshape(n, n_kv_heads, d)
+    v = qproj_lora(x, wv).reshape(n, n_kv_heads, d)
+    q_hat = rope(rms_norm_heads(q, gamma_q, eps), pos, theta)
+    k_hat = rope(rms_norm_heads(k, gamma_k, eps), pos, theta)
+    keys, vals = [], []
+    t = 0
+    for s in segments:
+        if s >= 0:
+            keys.append(np.asarray(art_k[s], np.float64))
+            vals.append(np.asarray(art_v[s], np.float64))
+        else:
+            keys.append(k_hat[t:t - s])
+            vals.append(v[t:t - s])
+            t -= s
+    keys = np.concatenate(keys) if keys else np.zeros((0, n_kv_heads, d))
+    vals = np.concatenate(vals) if vals else np.zeros((0, n_kv_heads, d))
+    G = n_q_heads // n_kv_heads
+    visible = np.arange(keys.shape[0])[None, :] <= pos[:, None]
+    o = np.empty((n, n_q_heads, d))
+    for h in range(n_q_heads):
+        z = (q_hat[:, h, :] @ keys[:, h // G, :].T) / math.sqrt(d)
+        z = np.where(visible, z, -np.inf)
+        e = np.exp(z - z.max(axis=1, keepdims=True))
+        o[:, h, :] = (e / e.sum(axis=1, keepdims=True)) @ vals[:, h // G, :]
+    return {"o": o, "q_hat": q_hat, "k_hat": k_hat, "v": v, "pos": pos, "keys": keys, "vals": vals}
+
+
+def block_table_segments(artifact_lengths: Sequence[int], requests: Sequence[Sequence[int]], page_tokens: int):
+    """Logical block table of a batch whose prompts interleave cached
+    artifacts with online spans (appendix A.3: cached KV is put together in
+    the original prompt order; the text between and around the artifacts is
+    computed online).
+
+    Each request is a list of segments: an entry >= 0 is an artifact id, an
+    entry -n < 0 an online span of n tokens.  Request r owns rows [cu_ctx[r],
+    cu_ctx[r+1]) holding its whole prompt in order: artifact pages where the
+    artifacts sit, and rows left for the online spans where they sit.
+
+    Returns (entries, cu_ctx, spans): entries as in :func:`block_table`
+    (artifact_id, page_index, n_valid, request, dst_row); spans an int64 array
+    of rows (request, offset of the span in its request, length), in request
+    and prompt order.
+    """
+    entries, spans = [], []
+    cu_ctx = [0]
+    for r, segs in enumerate(requests):
+        base = cu_ctx[-1]
+        off = 0
+        for s in segs:
+            if s >= 0:
+                for p, nv in enumerate(page_valid_counts(int(artifact_lengths[s]), page_tokens)):
+                    entries.append((int(s), p, nv, r, base + off))
+                    off += nv
+            else:
+                spans.append((r, off, -int(s)))
+                off += -int(s)
+        cu_ctx.append(base + off)
+    return (np.asarray(entries, dtype=np.int64).reshape(-1, 5), np.asarray(cu_ctx, dtype=np.int64),
+            np.asarray(spans, dtype=np.int64).reshape(-1, 3))

@@ -593,3 +593,118 @@ def test_first_token_brute_force_and_ties():
     w2[V - 1] = w2[top]
     ids2, _ = oracle.first_token(h[:1], g, w2, 1e-6)
     assert ids2[0] == min(top, V - 1)
+
+
+# ----------------------------------------------------------------------------
+# interleaved online spans
+# ----------------------------------------------------------------------------
+
+def test_block_table_segments_worked_example():
+    # prompt of request 0: 3 online | artifact 0 (20 tokens: pages of 16 and 4) |
+    # 2 online | artifact 1 (5) | 4 online; request 1: artifact 1 alone.
+    # Offsets by hand: art0 at 3 (rows 3..18, 19..22), span at 23, art1 at 25,
+    # span at 30; request 0 spans 34 rows, request 1 rows 34..38.
+    e, cu, sp = oracle.block_table_segments([20, 5], [[-3, 0, -2, 1, -4], [1]], 16)
+    assert e.tolist() == [[0, 0, 16, 0, 3], [0, 1, 4, 0, 19], [1, 0, 5, 0, 25], [1, 0, 5, 1, 34]]
+    assert cu.tolist() == [0, 34, 39]
+    assert sp.tolist() == [[0, 0, 3], [0, 23, 2], [0, 30, 4]]
+
+
+def test_block_table_segments_trailing_span_is_the_suffix_layout():
+    lengths = [17, 40, 1, 16]
+    reqs = [([1, 0, 3], 5), ([], 3), ([2, 2, 1], 0)]
+    segs = [ids + ([-cap] if cap else []) for ids, cap in reqs]
+    e, cu, sp = oracle.block_table_segments(lengths, segs, 16)
+    e2, cu2 = oracle.block_table(lengths, reqs, 16)
+    assert np.array_equal(e, e2) and np.array_equal(cu, cu2)
+    assert sp.tolist() == [[0, 73, 5], [1, 0, 3]]
+
+
+def _tiny_interleaved(seed, segments, lengths, H=16, Hq=4, Hkv=2, d=8):
+    rng = np.random.default_rng(seed)
+    n_online = sum(-s for s in segments if s < 0)
+    w = {"wq": rng.standard_normal((Hq * d, H)) * 0.3, "wk": rng.standard_normal((Hkv * d, H)) * 0.3,
+         "wv": rng.standard_normal((Hkv * d, H)), "a": rng.standard_normal((2, H)) * 0.3,
+         "b": rng.standard_normal((Hq * d, 2)) * 0.3, "gq": rng.uniform(0.5, 1.5, d), "gk": rng.uniform(0.5, 1.5, d)}
+    art_k = {i: rng.standard_normal((L, Hkv, d)) for i, L in enumerate(lengths)}
+    art_v = {i: rng.standard_normal((L, Hkv, d)) for i, L in enumerate(lengths)}
+    x = rng.standard_normal((n_online, H))
+    return w, art_k, art_v, x, (Hq, Hkv)
+
+
+def _run_interleaved(segments, w, art_k, art_v, x, heads, scale=0.7):
+    return oracle.interleaved_layer(segments, x, w["wq"], w["wk"], w["wv"], w["a"], w["b"], scale, w["gq"], w["gk"],
+                                    art_k, art_v, heads[0], heads[1], 1e4, 1e-6)
+
+
+def test_interleaved_trailing_span_equals_suffix_layer():
+    segs = [1, 0, -6]
+    w, ak, av, x, heads = _tiny_interleaved(61, segs, [5, 9])
+    got = _run_interleaved(segs, w, ak, av, x, heads)
+    ref = oracle.suffix_layer(x, w["wq"], w["wk"], w["wv"], w["a"], w["b"], 0.7, w["gq"], w["gk"],
+                              np.concatenate([ak[1], ak[0]]), np.concatenate([av[1], av[0]]), 14, heads[0],
+                              heads[1], 1e4, 1e-6)
+    assert np.max(np.abs(got["o"] - ref["o"])) <= 1e-12
+    assert got["pos"].tolist() == list(range(14, 20))
+
+
+def test_interleaved_single_span_without_artifacts_equals_full_prefill():
+    w, ak, av, x, heads = _tiny_interleaved(62, [-7], [])
+    got = _run_interleaved([-7], w, ak, av, x, heads)
+    ref = oracle.full_prefill(x, w["wq"], w["wk"], w["wv"], w["gq"], w["gk"], 0, heads[0], heads[1], 1e4, 1e-6,
+                              a=w["a"], b=w["b"], scale=0.7)
+    assert np.max(np.abs(got["o"] - ref["o"])) <= 1e-12
+
+
+def test_interleaved_split_span_is_invariant():
+    w, ak, av, x, heads = _tiny_interleaved(63, [-3, 0, -5], [6])
+    one = _run_interleaved([-3, 0, -5], w, ak, av, x, heads)
+    two = _run_interleaved([-3, 0, -2, -3], w, ak, av, x, heads)
+    assert np.max(np.abs(one["o"] - two["o"])) <= 1e-12
+
+
+def test_interleaved_brute_force_mask_and_order():
+    # the test lays the prompt out itself (its own walk over the segments) and
+    # runs a per-row math.exp softmax over the keys each online token may see
+    segs = [-2, 1, -3, 0, 0, -1]
+    lengths = [3, 4]
+    w, ak, av, x, heads = _tiny_interleaved(64, segs, lengths)
+    out = _run_interleaved(segs, w, ak, av, x, heads)
+    Hq, Hkv = heads
+    G, d = Hq // Hkv, 8
+    keys, vals, qpos = [], [], []
+    t = 0
+    for s in segs:
+        if s >= 0:
+            for i in range(lengths[s]):
+                keys.append(ak[s][i])
+                vals.append(av[s][i])
+        else:
+            for _ in range(-s):
+                qpos.append(len(keys))
+                keys.append(out["k_hat"][t])
+                vals.append(out["v"][t])
+                t += 1
+    for r, p in enumerate(qpos):
+        for h in range(Hq):
+            g = h // G
+            sc = [sum(out["q_hat"][r, h, j] * keys[kk][g, j] for j in range(d)) / math.sqrt(d) for kk in range(p + 1)]
+            mx = max(sc)
+            e = [math.exp(z - mx) for z in sc]
+            den = sum(e)
+            want = [sum(e[kk] * vals[kk][g, j] for kk in range(p + 1)) / den for j in range(d)]
+            assert np.max(np.abs(out["o"][r, h] - np.array(want))) <= 1e-12
+
+
+def test_interleaved_causality_and_leading_token():
+    segs = [-4, 0, -3]
+    w, ak, av, x, heads = _tiny_interleaved(65, segs, [5])
+    base = _run_interleaved(segs, w, ak, av, x, heads)
+    av2 = {0: av[0] + 1.0}
+    moved = _run_interleaved(segs, w, ak, av2, x, heads)
+    # the artifact sits after the first span: that span cannot see it, the last one does
+    assert np.array_equal(base["o"][:4], moved["o"][:4])
+    assert np.max(np.abs(base["o"][4:] - moved["o"][4:])) > 1e-3
+    # the first online token sees only its own key: O = its value (GQA repeat)
+    G = heads[0] // heads[1]
+    assert np.max(np.abs(base["o"][0] - np.repeat(base["v"][0], G, axis=0))) <= 1e-12
