@@ -181,6 +181,36 @@ attuner_status attuner_gather_layers(attuner_ctx* ctx, const int32_t* block_tabl
                                      int64_t cache_rows, void* stream);
 
 /* --------------------------------------------------------------------------
+ * Prompts that interleave cached artifacts with online spans (appendix A.3:
+ * system text, headers, separators and the question sit between and around
+ * the cached artifacts and are computed online, while the artifacts' KV is
+ * put together in the original prompt order; appendix A.5: attention with
+ * the causal mask and the position ids of the assembled context).
+ *
+ * Request r is the segment list segments[req_ptr[r] .. req_ptr[r+1]) in
+ * prompt order: an entry >= 0 is an artifact id, an entry -n < 0 an online
+ * span of n tokens.  Request r owns cache rows [cu_ctx[r], cu_ctx[r+1]): its
+ * whole prompt, artifact pages where the artifacts sit and rows left for the
+ * online spans where they sit (same cache layout as attuner_assemble_kv).
+ * attuner_assemble_segments_plan returns n_entries, cache_rows and the
+ * number of online spans.  attuner_assemble_segments builds the block table
+ * (entries as in attuner_assemble_kv, copied to block_table on `stream`),
+ * gathers every layer into req_kv, fills cu_ctx (host, n_req + 1) and spans
+ * (host, n_spans x 3: request, offset of the span inside its request,
+ * length; in request and prompt order), and records the table for
+ * attuner_gather_layers.  Online rows are not written.
+ * Errors: EINVAL, ENOENT (unknown id), ERANGE (n_req > ATTUNER_MAX_REQUESTS,
+ * cache_rows does not match the plan).
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_assemble_segments_plan(const attuner_ctx* ctx, int32_t n_req, const int32_t* req_ptr,
+                                              const int32_t* segments, int64_t* n_entries,
+                                              int64_t* cache_rows, int32_t* n_spans);
+
+attuner_status attuner_assemble_segments(attuner_ctx* ctx, int32_t n_req, const int32_t* req_ptr,
+                                         const int32_t* segments, int32_t* block_table, int32_t* cu_ctx,
+                                         int32_t* spans, void* req_kv, int64_t cache_rows, void* stream);
+
+/* --------------------------------------------------------------------------
  * a3: LoRA-adapted projection (section 4, eq. 4; fused q/k/v weights).
  *
  *   out[i][n] = sum_k x[i][k] w[n][k]
@@ -269,6 +299,30 @@ attuner_status attuner_full_prefill(attuner_ctx* ctx, int32_t n_tok, int32_t pos
                                     const void* wqkv, const void* a, const void* b, int32_t rank,
                                     float scale, const void* gamma_q, const void* gamma_k, void* o,
                                     void* k_out, void* v_out, float* lse, void* stream);
+
+/* --------------------------------------------------------------------------
+ * a4 + a5 for online spans at any offsets (the interleaved prompts above;
+ * the suffix of attuner_suffix_attn is the case of one span at the end).
+ *
+ * Span s (host arrays of n_spans <= ATTUNER_MAX_REQUESTS entries, cu_q of
+ * n_spans + 1): its tokens are rows cu_q[s] .. cu_q[s+1]-1 of q_raw/k_raw/
+ * v_raw/o; its request's cache rows start at kv_start[s] and the span sits
+ * offset[s] rows into them; token i has position pos0[s] + i (pos0 NULL:
+ * offset[s] + i, the assembled position).  The call normalises and rotates
+ * q and k, writes k_hat and v to rows kv_start[s] + offset[s] + i of layer
+ * `layer` (every span's rows first), then token i of span s attends to rows
+ * kv_start[s] .. kv_start[s] + offset[s] + i: everything before it in its
+ * prompt (artifact keys as stored, earlier spans' keys as just written) and
+ * its own span causally.  Requires kv_start[s] + offset[s] + (cu_q[s+1] -
+ * cu_q[s]) <= cache_rows.  q_raw/k_raw/v_raw/ld/gamma as in
+ * attuner_qk_norm_rope; o: device [T][Hq][d] (also stages the normalised
+ * queries); lse: device [T][Hq] fp32 or NULL.
+ * ------------------------------------------------------------------------ */
+attuner_status attuner_span_attn(attuner_ctx* ctx, int32_t layer, int32_t n_spans, const int32_t* cu_q,
+                                 const int32_t* kv_start, const int32_t* offset, const int32_t* pos0,
+                                 const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                 int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                 int64_t cache_rows, void* o, float* lse, void* stream);
 
 /* --------------------------------------------------------------------------
  * Decode with the adapted queries: every generated token keeps the adapted

@@ -52,6 +52,10 @@ SIGNATURES = {
     "attuner_attention": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _vp, _vp, _i64, _vp, _vp, _vp]),
     "attuner_suffix_attn": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64,
                                       _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "attuner_assemble_segments_plan": (C.c_int, [_vp, _i32, _i32p, _i32p, _i64p, _i64p, _i32p]),
+    "attuner_assemble_segments": (C.c_int, [_vp, _i32, _i32p, _i32p, _vp, _i32p, _i32p, _vp, _i64, _vp]),
+    "attuner_span_attn": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64, _vp, _vp,
+                                    _vp, _i64, _vp, _vp, _vp]),
     "attuner_decode_attn": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64, _vp, _vp,
                                       _vp, _i64, _vp, _vp]),
     "attuner_embed": (C.c_int, [_vp, _i32, _i32p, _vp, _i32, _vp, _vp]),

@@ -179,6 +179,34 @@ class Context:
                                          _ptr(req_kv), int(cache_rows), _stream(stream)), "attuner_assemble_kv")
         return list(cu), list(al)[:n]
 
+    # ---- prompts interleaving artifacts with online spans ------------------------------
+    def assemble_segments_plan(self, segments: Sequence[Sequence[int]]) -> Tuple[int, int, int]:
+        """segments[r]: request r's prompt in order, artifact ids (>= 0) and online spans (-n).
+        Returns (n_entries, cache_rows, n_spans)."""
+        ptr, flat = self._csr(segments)
+        ne, rows, ns = C.c_int64(), C.c_int64(), C.c_int32()
+        _check(lib().attuner_assemble_segments_plan(self._h, len(segments), _i32(ptr), _i32(flat), C.byref(ne),
+                                                    C.byref(rows), C.byref(ns)), "attuner_assemble_segments_plan")
+        return ne.value, rows.value, ns.value
+
+    def assemble_segments(self, segments: Sequence[Sequence[int]], block_table: torch.Tensor, req_kv: torch.Tensor,
+                          cache_rows: int, stream=None) -> Tuple[List[int], List[Tuple[int, int, int]]]:
+        """Returns (cu_ctx, spans [(request, offset, length)]); fills block_table and req_kv."""
+        ne, rows, ns = self.assemble_segments_plan(segments)
+        c = self.cfg
+        _need(block_table, 4 * ne, "block_table")
+        _need(req_kv, c.n_layers * 2 * c.n_kv_heads * int(cache_rows) * c.head_dim, "req_kv")
+        ptr, flat = self._csr(segments)
+        n = len(segments)
+        cu = (C.c_int32 * (n + 1))()
+        sp = (C.c_int32 * max(3, 3 * ns))()
+        _check(lib().attuner_assemble_segments(self._h, n, _i32(ptr), _i32(flat),
+                                               _ptr(block_table, 4) if block_table is not None else None, cu, sp,
+                                               _ptr(req_kv), int(cache_rows), _stream(stream)),
+               "attuner_assemble_segments")
+        spans = [(sp[3 * i], sp[3 * i + 1], sp[3 * i + 2]) for i in range(ns)]
+        return list(cu), spans
+
     def assemble_table(self, requests: Sequence[Sequence[int]], suffix_cap: Sequence[int],
                        block_table: torch.Tensor, cache_rows: int, stream=None) -> Tuple[List[int], List[int]]:
         """Returns (cu_ctx, art_len); fills block_table (int32 device) only."""
@@ -315,6 +343,20 @@ class Context:
                                          _view_ptr(k_raw), _view_ptr(v_raw), int(ld_kv), _ptr(gamma_q), _ptr(gamma_k),
                                          _ptr(req_kv), int(cache_rows), _ptr(o), _ptr(lse, 4), _stream(stream)),
                "attuner_suffix_attn")
+
+    def span_attn(self, layer: int, cu_q, kv_start, offset, pos0, q_raw, ld_q: int, k_raw, v_raw, ld_kv: int,
+                  gamma_q, gamma_k, req_kv, cache_rows: int, o, lse: Optional[torch.Tensor] = None,
+                  stream=None) -> None:
+        """Online spans at any offsets: span s = rows cu_q[s] .. cu_q[s+1]-1, its request's cache rows
+        start at kv_start[s] and it sits offset[s] rows into them."""
+        n = len(kv_start)
+        self._check_cache(cu_q, [0] * (n + 1), o, req_kv, cache_rows, q_raw, ld_q, k_raw, v_raw, ld_kv)
+        _need(lse, int(cu_q[-1]) * self.cfg.n_q_heads, "lse")
+        _check(lib().attuner_span_attn(self._h, int(layer), n, _i32(cu_q), _i32(kv_start), _i32(offset),
+                                       _i32(pos0) if pos0 is not None else None, _view_ptr(q_raw), int(ld_q),
+                                       _view_ptr(k_raw), _view_ptr(v_raw), int(ld_kv), _ptr(gamma_q), _ptr(gamma_k),
+                                       _ptr(req_kv), int(cache_rows), _ptr(o), _ptr(lse, 4), _stream(stream)),
+               "attuner_span_attn")
 
     def decode_attn(self, layer: int, cu_ctx, ctx_len, pos, q_raw, ld_q: int, k_raw, v_raw, ld_kv: int,
                     gamma_q, gamma_k, req_kv, cache_rows: int, o, stream=None) -> None:

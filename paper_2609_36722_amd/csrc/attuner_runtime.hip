@@ -730,6 +730,112 @@ attuner_status attuner_assemble_kv(attuner_ctx* c, int32_t n_req, const int32_t*
   return attuner_gather_layers(c, block_table, entries, 0, c->cfg.n_layers, req_kv, cache_rows, stream);
 }
 
+// Prompts that interleave cached artifacts with online spans: segments[j]
+// >= 0 is an artifact id, -n < 0 an online span of n tokens.  Request r
+// owns rows [cu_ctx[r], cu_ctx[r+1]) holding its prompt in order; spans get
+// (request, offset in the request, length).
+static attuner_status plan_segments_impl(const attuner_ctx* c, int32_t n_req, const int32_t* req_ptr,
+                                         const int32_t* segments, int64_t* n_entries, int64_t* cache_rows,
+                                         int32_t* n_spans, std::vector<int32_t>* table, int32_t* cu_ctx,
+                                         std::vector<int32_t>* spans) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (n_req < 0 || n_req > ATTUNER_MAX_REQUESTS)
+    return fail(ATTUNER_ERANGE, "n_req %d outside [0, %d]", n_req, ATTUNER_MAX_REQUESTS);
+  if (n_req > 0 && !req_ptr) return fail(ATTUNER_EINVAL, "null req_ptr");
+  if (n_req > 0 && req_ptr[0] != 0) return fail(ATTUNER_EINVAL, "req_ptr[0] must be 0");
+  int64_t entries = 0, row = 0;
+  int32_t ns = 0;
+  if (cu_ctx) cu_ctx[0] = 0;
+  for (int r = 0; r < n_req; ++r) {
+    if (req_ptr[r + 1] < req_ptr[r]) return fail(ATTUNER_EINVAL, "req_ptr not monotone at %d", r);
+    if (req_ptr[r + 1] > req_ptr[r] && !segments) return fail(ATTUNER_EINVAL, "null segments");
+    int64_t off = 0;
+    for (int32_t j = req_ptr[r]; j < req_ptr[r + 1]; ++j) {
+      const int32_t sg = segments[j];
+      if (sg < 0) {
+        if (sg == INT32_MIN) return fail(ATTUNER_EINVAL, "request %d: segment %d out of range", r, j);
+        if (spans) {
+          spans->push_back(r);
+          spans->push_back((int32_t)off);
+          spans->push_back(-sg);
+        }
+        off += -(int64_t)sg;
+        ++ns;
+        continue;
+      }
+      auto it = c->artifacts.find(sg);
+      if (it == c->artifacts.end()) return fail(ATTUNER_ENOENT, "request %d: unknown artifact id %d", r, sg);
+      const Artifact& a = it->second;
+      if (table) {
+        int32_t left = a.n_tokens;
+        for (int32_t pg : a.pages) {
+          const int32_t nv = std::min(left, kPageTokens);
+          table->push_back(pg);
+          table->push_back(nv);
+          table->push_back((int32_t)(row + off));
+          table->push_back(r);
+          off += nv;
+          left -= nv;
+        }
+      } else {
+        off += a.n_tokens;
+      }
+      entries += (int64_t)a.pages.size();
+      if (row + off > INT32_MAX) return fail(ATTUNER_ERANGE, "cache rows exceed 2^31");
+    }
+    row += off;
+    if (row > INT32_MAX) return fail(ATTUNER_ERANGE, "cache rows exceed 2^31");
+    if (cu_ctx) cu_ctx[r + 1] = (int32_t)row;
+  }
+  if (n_entries) *n_entries = entries;
+  if (cache_rows) *cache_rows = row;
+  if (n_spans) *n_spans = ns;
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_assemble_segments_plan(const attuner_ctx* c, int32_t n_req, const int32_t* req_ptr,
+                                              const int32_t* segments, int64_t* n_entries, int64_t* cache_rows,
+                                              int32_t* n_spans) {
+  return plan_segments_impl(c, n_req, req_ptr, segments, n_entries, cache_rows, n_spans, nullptr, nullptr, nullptr);
+}
+
+attuner_status attuner_assemble_segments(attuner_ctx* c, int32_t n_req, const int32_t* req_ptr,
+                                         const int32_t* segments, int32_t* block_table, int32_t* cu_ctx,
+                                         int32_t* spans, void* req_kv, int64_t cache_rows, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  c->last_table = nullptr;
+  c->last_entries = c->last_rows = -1;
+  std::vector<int32_t> table, sp;
+  std::vector<int32_t> cu(n_req > 0 ? n_req + 1 : 1);
+  int64_t entries = 0, rows = 0;
+  int32_t ns = 0;
+  try {
+    attuner_status st = plan_segments_impl(c, n_req, req_ptr, segments, &entries, &rows, &ns, &table, cu.data(), &sp);
+    if (st != ATTUNER_OK) return st;
+  } catch (const std::bad_alloc&) {
+    return fail(ATTUNER_ENOMEM, "host allocation");
+  }
+  if (rows != cache_rows)
+    return fail(ATTUNER_ERANGE, "cache_rows %lld does not match the plan (%lld)", (long long)cache_rows, (long long)rows);
+  if (entries > 0 && !block_table) return fail(ATTUNER_EINVAL, "null block_table");
+  if (entries > INT32_MAX) return fail(ATTUNER_ERANGE, "block table of %lld entries", (long long)entries);
+  if (ns > 0 && !spans) return fail(ATTUNER_EINVAL, "null spans");
+  if (entries > 0 && (!req_kv || !aligned16(req_kv))) return fail(ATTUNER_EINVAL, "null or unaligned req_kv");
+  if (cu_ctx) memcpy(cu_ctx, cu.data(), (size_t)(n_req + 1) * sizeof(int32_t));
+  if (ns > 0) memcpy(spans, sp.data(), sp.size() * sizeof(int32_t));
+  if (entries > 0) {
+    DeviceGuard dg(c->device);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(c->staging.upload(table.data(), table.size() * sizeof(int32_t), block_table, s));
+    HIP_TRY(launch_gather(block_table, entries, c->pool, c->pool_pages, 0, c->cfg.n_layers, c->cfg.n_kv_heads,
+                          static_cast<uint16_t*>(req_kv), cache_rows, s));
+  }
+  c->last_table = block_table;
+  c->last_entries = entries;
+  c->last_rows = rows;
+  return ATTUNER_OK;
+}
+
 attuner_status attuner_rms_norm(attuner_ctx* c, const void* x, int64_t n_x_rows, int64_t ld_x, const int32_t* rows,
                                 int32_t n_rows, const void* gamma, void* out, void* stream) {
   if (!c) return fail(ATTUNER_EINVAL, "null ctx");
@@ -910,6 +1016,50 @@ attuner_status attuner_suffix_attn(attuner_ctx* c, int32_t layer, int32_t n_req,
   int32_t total_q = 0;
   st = build_reqs(c, n_req, cu_q, cu_ctx, art_len, pos0, cache_rows, &reqs, &total_q);
   if (st != ATTUNER_OK) return st;
+  if (total_q == 0) return ATTUNER_OK;
+  st = check_norm_args(q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, c);
+  if (st != ATTUNER_OK) return st;
+  if (!req_kv || !o || !aligned16(req_kv) || !aligned16(o))
+    return fail(ATTUNER_EINVAL, "req_kv and o must be non-null and 16-byte aligned");
+  DeviceGuard dg(c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t hs = cache_rows * c->cfg.head_dim;
+  uint16_t* kp = cache_plane(req_kv, c, layer, 0, cache_rows);
+  uint16_t* vp = cache_plane(req_kv, c, layer, 1, cache_rows);
+  st = run_norm_rope(c, reqs, total_q, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, o, kp, vp, hs, s);
+  if (st != ATTUNER_OK) return st;
+  return run_attention(c, reqs, total_q, o, kp, vp, hs, o, lse, s);
+}
+
+attuner_status attuner_span_attn(attuner_ctx* c, int32_t layer, int32_t n_spans, const int32_t* cu_q,
+                                 const int32_t* kv_start, const int32_t* offset, const int32_t* pos0,
+                                 const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                 int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                 int64_t cache_rows, void* o, float* lse, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  attuner_status st = check_layer(c, layer);
+  if (st != ATTUNER_OK) return st;
+  if (n_spans < 0 || n_spans > ATTUNER_MAX_REQUESTS)
+    return fail(ATTUNER_ERANGE, "n_spans %d outside [0, %d]", n_spans, ATTUNER_MAX_REQUESTS);
+  if (n_spans == 0) return ATTUNER_OK;
+  if (!cu_q || !kv_start || !offset) return fail(ATTUNER_EINVAL, "null span array");
+  if (cu_q[0] != 0) return fail(ATTUNER_EINVAL, "cu_q[0] must be 0");
+  std::vector<ReqDesc> reqs;
+  for (int s = 0; s < n_spans; ++s) {
+    ReqDesc d;
+    d.q_start = cu_q[s];
+    d.q_len = cu_q[s + 1] - cu_q[s];
+    d.kv_start = kv_start[s];
+    d.art_len = offset[s];
+    d.pos0 = pos0 ? pos0[s] : offset[s];
+    if (d.q_len < 0 || d.kv_start < 0 || d.art_len < 0 || d.pos0 < 0)
+      return fail(ATTUNER_EINVAL, "span %d: negative length, start, offset or position", s);
+    if ((int64_t)d.kv_start + d.art_len + d.q_len > cache_rows)
+      return fail(ATTUNER_EINVAL, "span %d: rows %d + %d + %d exceed cache_rows %lld", s, d.kv_start, d.art_len,
+                  d.q_len, (long long)cache_rows);
+    reqs.push_back(d);
+  }
+  const int32_t total_q = cu_q[n_spans];
   if (total_q == 0) return ATTUNER_OK;
   st = check_norm_args(q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, c);
   if (st != ATTUNER_OK) return st;

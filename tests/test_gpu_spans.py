@@ -1,0 +1,127 @@
+"""GPU parity of prompts that interleave cached artifacts with online spans
+(system text, separators, questions between and around the artifacts),
+through the C ABI: the segment block table and gathered artifact rows
+bit-exact against the oracle; the online spans' normalised keys within the
+intermediate bar and their values bit-exact; O within the O bar over the
+batch (each request within it or the relative bar of a bf16-stored value).
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synthdata as sd
+from tests._tol import assert_intermediate_close, assert_o_close, assert_o_close_per_request
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from tests._gpu import dev_bf16, host_f64
+    from paper_2609_36722_amd.api import AttunerError, Context, ModelCfg, bf16_to_host
+
+HQ, HKV, D = 32, 8, 128
+
+
+def _say(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def _bits(rng, shape, std=1.0):
+    return sd.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32) * np.float32(std))
+
+
+@pytest.mark.parametrize("H,rank,layer", [(512, 16, 1), (2560, 8, 0)])
+def test_interleaved_spans(H, rank, layer):
+    _say(f"interleaved spans H={H} r={rank} layer={layer}")
+    rng = np.random.default_rng(70 + H + rank)
+    n_layers = 2
+    lengths = [40, 17, 64, 1, 300]
+    # prompts in order: artifacts by index, online spans as -n
+    prompts = [[-7, 0, -3, 1, -20], [2, -5], [-9], [3, 3, -1, 0], [4, -64, 2, -70]]
+    scale = 16.0 / rank
+    with Context(ModelCfg(n_layers=n_layers, hidden=H), pool_pages=sum(math.ceil(L / 16) for L in lengths)) as ctx:
+        art_k, art_v, ids = {}, {}, {}
+        for a, L in enumerate(lengths):
+            k, v = _bits(rng, (n_layers, HKV, L, D)), _bits(rng, (n_layers, HKV, L, D))
+            ids[a] = ctx.store_artifact(dev_bf16(k), dev_bf16(v))
+            art_k[a], art_v[a] = k, v
+        segs = [[ids[s] if s >= 0 else s for s in p] for p in prompts]
+        ne, rows, ns = ctx.assemble_segments_plan(segs)
+        bt = torch.zeros(max(1, ne) * 4, dtype=torch.int32, device="cuda")
+        kv = torch.zeros(n_layers * 2 * HKV * rows * D, dtype=torch.bfloat16, device="cuda")
+        cu, spans = ctx.assemble_segments(segs, bt, kv, rows)
+        assert len(spans) == ns
+
+        # the plan against the oracle's segment table (physical pages mapped in)
+        e, cu_ref, sp_ref = oracle.block_table_segments(lengths, prompts, 16)
+        phys = {a: ctx.artifact_pages(ids[a])[0] for a in ids}
+        want = np.array([[phys[a][p], nv, dst, r] for a, p, nv, r, dst in e.tolist()], np.int32).reshape(-1, 4)
+        assert np.array_equal(bt.cpu().numpy().reshape(-1, 4)[:len(want)], want)
+        assert cu == cu_ref.tolist() and [list(s) for s in spans] == sp_ref.tolist()
+
+        n_on = sum(l for _, _, l in spans)
+        x = _bits(rng, (n_on, H))
+        wq, wk, wv = _bits(rng, (HQ * D, H), 0.02), _bits(rng, (HKV * D, H), 0.02), _bits(rng, (HKV * D, H), 0.02)
+        a, b = _bits(rng, (rank, H), 1 / math.sqrt(H)), _bits(rng, (HQ * D, rank), 0.01)
+        gq = sd.f32_to_bf16_bits(rng.uniform(0.5, 1.5, D).astype(np.float32))
+        gk = sd.f32_to_bf16_bits(rng.uniform(0.5, 1.5, D).astype(np.float32))
+        n_out = (HQ + 2 * HKV) * D
+        qkv = torch.empty(n_on, n_out, dtype=torch.bfloat16, device="cuda")
+        ctx.qproj_lora(dev_bf16(x), dev_bf16(np.concatenate([wq, wk, wv])), dev_bf16(a), dev_bf16(b), rank, scale,
+                       HQ * D, qkv)
+        cu_q = [0]
+        for _, _, l in spans:
+            cu_q.append(cu_q[-1] + l)
+        o = torch.empty(n_on, HQ, D, dtype=torch.bfloat16, device="cuda")
+        ctx.span_attn(layer, cu_q, [cu[r] for r, _, _ in spans], [off for _, off, _ in spans], None,
+                      qkv[:, :HQ * D], n_out, qkv[:, HQ * D:(HQ + HKV) * D], qkv[:, (HQ + HKV) * D:], n_out,
+                      dev_bf16(gq), dev_bf16(gk), kv, rows, o)
+        torch.cuda.synchronize()
+        got_o = host_f64(o)
+        cache = bf16_to_host(kv).reshape(n_layers, 2, HKV, rows, D)
+        qkv_bits = bf16_to_host(qkv)
+
+    # artifact rows bit-exact at their offsets, on every layer
+    for a_idx, p, nv, r, dst in e.tolist():
+        src = slice(16 * p, 16 * p + nv)
+        assert np.array_equal(cache[:, 0, :, dst:dst + nv], art_k[a_idx][:, :, src]), f"K rows of artifact {a_idx}"
+        assert np.array_equal(cache[:, 1, :, dst:dst + nv], art_v[a_idx][:, :, src]), f"V rows of artifact {a_idx}"
+
+    d = oracle.decode_bf16
+    refs, t0 = [], 0
+    for r, p in enumerate(prompts):
+        n_r = sum(-s for s in p if s < 0)
+        ak = {i: d(art_k[i][layer]).transpose(1, 0, 2) for i in range(len(lengths))}
+        av = {i: d(art_v[i][layer]).transpose(1, 0, 2) for i in range(len(lengths))}
+        ref = oracle.interleaved_layer(p, d(x[t0:t0 + n_r]), d(wq), d(wk), d(wv), d(a), d(b), scale, d(gq), d(gk),
+                                       ak, av, HQ, HKV, 1e6, 1e-6)
+        # the online rows of the cache: normalised keys and the projection's value bits
+        rows_r = cu[r] + ref["pos"]
+        assert_intermediate_close(d(cache[layer, 0][:, rows_r]).transpose(1, 0, 2), ref["k_hat"], f"request {r} k_hat")
+        v_bits = qkv_bits[t0:t0 + n_r, (HQ + HKV) * D:].reshape(n_r, HKV, D)
+        assert np.array_equal(cache[layer, 1][:, rows_r].transpose(1, 0, 2), v_bits), f"request {r} v rows"
+        assert_o_close_per_request(got_o[t0:t0 + n_r], ref["o"], f"request {r} O")
+        refs.append(ref["o"])
+        t0 += n_r
+    assert_o_close(got_o, np.concatenate(refs), "batch O")
+
+
+def test_span_errors():
+    _say("span errors")
+    with Context(ModelCfg(n_layers=1, hidden=256), pool_pages=1) as ctx:
+        with pytest.raises(AttunerError) as e:
+            ctx.assemble_segments_plan([[5]])          # unknown artifact id
+        assert e.value.status == -3
+        kv = torch.zeros(2 * HKV * 10 * D, dtype=torch.bfloat16, device="cuda")
+        q = torch.zeros(4, (HQ + 2 * HKV) * D, dtype=torch.bfloat16, device="cuda")
+        g = torch.ones(D, dtype=torch.bfloat16, device="cuda")
+        ld = q.shape[1]
+        with pytest.raises(AttunerError) as e:
+            # 10 cache rows; a span of 4 at offset 7 would end at row 11
+            ctx.span_attn(0, [0, 4], [0], [7], None, q[:, :HQ * D], ld, q[:, HQ * D:(HQ + HKV) * D],
+                          q[:, (HQ + HKV) * D:], ld, g, g, kv, 10, torch.empty(4, HQ, D, dtype=torch.bfloat16,
+                                                                                 device="cuda"))
+        assert e.value.status == -1
