@@ -10,6 +10,7 @@
 #include <cstring>
 #include <map>
 #include <new>
+#include <queue>
 #include <set>
 #include <string>
 #include <vector>
@@ -213,6 +214,10 @@ struct attuner_ctx {
   // attuner_gather_layers accepts)
   const int32_t* last_table = nullptr;
   int64_t last_entries = -1, last_rows = -1;
+  // key splits chosen for the last attention batch shape (q_len, art_len per
+  // request), reused while the shape repeats (every layer of a stack)
+  std::vector<int32_t> split_shape;
+  std::vector<int> split_plan;
   Staging staging;
   Tracer tracer;
 };
@@ -297,6 +302,77 @@ attuner_status run_norm_rope(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   return ATTUNER_OK;
 }
 
+// Key splits per request for one attention launch.  A workgroup serves one
+// 64-token query block of one KV head (one per CU at a time) over a range of
+// key tiles; workgroups start in launch order on whichever CU frees first.
+// The modelled finish time of a plan is that greedy schedule over 256 CUs,
+// with a workgroup costing its tiles plus kWgOverhead tiles (loading Q and
+// the first tile, the epilogue) and a plan with splits paying kMergeCost for
+// the merge launch.  Candidates cut the longest request into k = 1 .. 16
+// splits (split size tau = its tiles / k) and every request into
+// ceil(its tiles / tau); a candidate with more splits must be modelled 2%
+// faster to win.
+std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc>& reqs) {
+  std::vector<int32_t> shape;
+  shape.reserve(2 * reqs.size());
+  for (const auto& r : reqs) {
+    shape.push_back(r.q_len);
+    shape.push_back(r.art_len);
+  }
+  if (shape == c->split_shape) return c->split_plan;
+  constexpr double kWgOverhead = 4.0, kMergeCost = 3.0;
+  constexpr int kCUs = 256;
+  std::vector<int64_t> tiles(reqs.size(), 0);
+  int64_t longest = 0;
+  for (size_t r = 0; r < reqs.size(); ++r) {
+    if (reqs[r].q_len <= 0) continue;
+    tiles[r] = ((int64_t)reqs[r].art_len + reqs[r].q_len + 63) / 64;
+    longest = std::max(longest, tiles[r]);
+  }
+  std::vector<int> best(reqs.size(), 1), cand(reqs.size(), 1);
+  double best_t = -1.0;
+  int64_t prev_tau = -1;
+  for (int k = 1; k <= kMaxAttnSplit && longest > 0; ++k) {
+    const int64_t tau = std::max<int64_t>(4, (longest + k - 1) / k);
+    if (tau == prev_tau) continue;
+    prev_tau = tau;
+    bool any_split = false;
+    for (size_t r = 0; r < reqs.size(); ++r) {
+      cand[r] = (int)std::min<int64_t>(kMaxAttnSplit, std::max<int64_t>(1, (tiles[r] + tau - 1) / tau));
+      any_split |= cand[r] > 1;
+    }
+    std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+    for (int i = 0; i < kCUs; ++i) free_at.push(0.0);
+    double finish = 0.0;
+    for (size_t r = 0; r < reqs.size(); ++r) {
+      const int nq = (reqs[r].q_len + 63) / 64;
+      const int ns = cand[r];
+      for (int u = 0; u < nq * ns; ++u) {
+        const int split = u % ns, qb = nq - 1 - u / ns;
+        const int64_t t0 = 64LL * qb;
+        const int64_t n_t = ((int64_t)reqs[r].art_len + t0 + std::min<int64_t>(64, reqs[r].q_len - t0) + 63) / 64;
+        const int64_t per = (n_t + ns - 1) / ns;
+        const int64_t tb = std::min<int64_t>(n_t, split * per), te = std::min<int64_t>(n_t, tb + per);
+        const double dur = (double)(te - tb) + kWgOverhead;
+        for (int g = 0; g < c->cfg.n_kv_heads; ++g) {
+          const double t = free_at.top() + dur;
+          free_at.pop();
+          free_at.push(t);
+          finish = std::max(finish, t);
+        }
+      }
+    }
+    if (any_split) finish += kMergeCost;
+    if (best_t < 0.0 || finish < 0.98 * best_t) {
+      best_t = finish;
+      best = cand;
+    }
+  }
+  c->split_shape = shape;
+  c->split_plan = best;
+  return best;
+}
+
 attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int32_t total_q, const void* q,
                              const uint16_t* k_plane, const uint16_t* v_plane, int64_t head_stride, void* o,
                              float* lse, hipStream_t stream) {
@@ -314,34 +390,23 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c->cfg.head_dim));
   p.n_req = (int32_t)reqs.size();
 
-  // Query blocks are 64 suffix tokens of one KV head (one 8-wave workgroup,
-  // one per CU).  Split the keys of each block when the blocks alone would
-  // not cover the 256 CUs; keep at least four 64-key tiles per split.
-  int64_t blocks = 0;
-  int64_t min_tiles = INT64_MAX;
-  for (const auto& r : reqs) {
-    if (r.q_len <= 0) continue;
-    blocks += (r.q_len + 63) / 64;
-    min_tiles = std::min<int64_t>(min_tiles, (r.art_len + r.q_len + 63) / 64);
-  }
-  const int64_t base = blocks * c->cfg.n_kv_heads;
+  const std::vector<int> ns_plan = plan_attention_splits(c, reqs);
   int n_split = 1;
-  if (base > 0 && base < 256) {
-    n_split = (int)std::min<int64_t>(16, (256 + base - 1) / base);
-    n_split = (int)std::max<int64_t>(1, std::min<int64_t>(n_split, min_tiles / 4));
-  }
-  p.n_split = n_split;
   int32_t units = 0;
   for (size_t r = 0; r < reqs.size(); ++r) {
     const int nq = (reqs[r].q_len + 63) / 64;
+    const int ns = ns_plan[r];
+    n_split = std::max(n_split, ns);
     p.req[r].q_start = reqs[r].q_start;
     p.req[r].q_len = reqs[r].q_len;
     p.req[r].kv_start = reqs[r].kv_start;
     p.req[r].art_len = reqs[r].art_len;
     p.req[r].n_qblk = nq;
     p.req[r].wg_start = units;
-    units += nq * n_split;
+    p.req[r].n_split = ns;
+    units += nq * ns;
   }
+  p.n_split = n_split;
   p.n_units = units;
   if (n_split > 1) {
     const size_t rows = (size_t)n_split * total_q * c->cfg.n_q_heads;

@@ -36,9 +36,9 @@
 // Work units of one KV head go to blockIdx.x = unit * Hkv + g: with Hkv = 8
 // workgroups are dealt round-robin over the 8 XCDs, so each XCD's L2 serves a
 // single KV head.  Late (heavier, causal) query blocks are dispatched first.
-// With n_split > 1 the key range of a block is cut into n_split tile ranges;
-// each writes its normalised partial (bf16) and (max, sum) (fp32), and a
-// second kernel merges them.  (Merging inside this kernel would need
+// With key splits the key range of a block is cut into its request's n_split
+// tile ranges; each writes its normalised partial (bf16) and (max, sum)
+// (fp32), and a second kernel merges them.  (Merging inside this kernel would need
 // agent-scope release/acquire between workgroups, which on gfx950 writes back
 // and invalidates the XCD's L2 and costs the other workgroups their K/V reuse.)
 
@@ -226,13 +226,13 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   while (r + 1 < p.n_req && unit >= p.req[r + 1].wg_start) ++r;
   const AttnReq rq = p.req[r];
   unit -= rq.wg_start;
-  const int split = unit % p.n_split;
-  const int qb = rq.n_qblk - 1 - unit / p.n_split;
+  const int split = unit % rq.n_split;
+  const int qb = rq.n_qblk - 1 - unit / rq.n_split;
   const int t0 = qb * BQ;
   const int blk_rows = min(BQ, rq.q_len - t0);
   const int kv_len = rq.art_len + t0 + blk_rows;  // keys any row of the block sees
   const int n_tiles = (kv_len + BKV - 1) / BKV;
-  const int per = (n_tiles + p.n_split - 1) / p.n_split;
+  const int per = (n_tiles + rq.n_split - 1) / rq.n_split;
   const int tb = min(n_tiles, split * per);
   const int te = min(n_tiles, tb + per);
 
@@ -398,6 +398,10 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
     if (p.lse != nullptr) p.lse[hrow] = (m_i + __log2f(l_i)) * 0.69314718055994531f;
   } else {
     *reinterpret_cast<f32x2*>(p.part_ml + ((int64_t)split * head_rows + hrow) * 2) = f32x2{m_i, l_i};
+    // slices past this request's own split count: empty (the merge skips them)
+    if (split == 0)
+      for (int s = rq.n_split; s < p.n_split; ++s)
+        *reinterpret_cast<f32x2*>(p.part_ml + ((int64_t)s * head_rows + hrow) * 2) = f32x2{-INFINITY, 0.f};
   }
 }
 
@@ -408,7 +412,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
 // A wave merges the 4 query heads of one token; 16 lanes per (token, head)
 // row, lane owning dims 8 (lane % 16) .. +7; every split's data is requested
 // before any is used.
-constexpr int kMaxSplit = 16;
+constexpr int kMaxSplit = kMaxAttnSplit;
 
 template <int NS>
 __global__ __launch_bounds__(256, 2) void attn_combine_kernel(AttnParams p) {
@@ -437,12 +441,17 @@ __global__ __launch_bounds__(256, 2) void attn_combine_kernel(AttnParams p) {
   float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
-    const float w = (ml[s][0] == -INFINITY) ? 0.f : ml[s][1] * __builtin_amdgcn_exp2f(ml[s][0] - mmax);
+    // an empty slice (no keys, or past its request's split count) holds no
+    // partial worth reading: its values are skipped, not weighted by zero
+    const bool empty = ml[s][0] == -INFINITY;
+    const float w = empty ? 0.f : ml[s][1] * __builtin_amdgcn_exp2f(ml[s][0] - mmax);
     wsum += w;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      o[2 * e] = fmaf(w, __uint_as_float(v[s][e] << 16), o[2 * e]);
-      o[2 * e + 1] = fmaf(w, __uint_as_float(v[s][e] & 0xFFFF0000u), o[2 * e + 1]);
+      const float lo = fmaf(w, __uint_as_float(v[s][e] << 16), o[2 * e]);
+      const float hi = fmaf(w, __uint_as_float(v[s][e] & 0xFFFF0000u), o[2 * e + 1]);
+      o[2 * e] = empty ? o[2 * e] : lo;
+      o[2 * e + 1] = empty ? o[2 * e + 1] : hi;
     }
   }
   const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;

@@ -138,6 +138,7 @@ struct AttnReq {
   int32_t art_len;   // cached artifact keys; row i sees keys 0 .. art_len + i
   int32_t n_qblk;    // ceil(q_len / 64)
   int32_t wg_start;  // first work unit of the request (units = qblocks * n_split)
+  int32_t n_split;   // key splits of the request's blocks (<= AttnParams::n_split)
 };
 
 struct AttnParams {
@@ -151,14 +152,16 @@ struct AttnParams {
   float* part_ml;          // [n_split][T_q][Hq][2]      (n_split > 1)
   int32_t n_q_heads, n_kv_heads;
   int32_t total_q;
-  int32_t n_split;
+  int32_t n_split;         // largest split count of any request: partial slices
   int32_t n_units;         // work units per KV head
   float score_scale;       // log2(e) / sqrt(d)
   int32_t n_req;
   AttnReq req[kMaxReq];
 };
 
-// Attention, plus the split-KV merge kernel when n_split > 1.
+// Attention, plus the split-KV merge kernel when n_split > 1 (at most
+// kMaxAttnSplit splits).
+constexpr int kMaxAttnSplit = 16;
 hipError_t launch_attention(const AttnParams& p, hipStream_t stream);
 
 // ---- decode: one new token per request over its whole cache ----------------
