@@ -79,6 +79,10 @@ def parse():
     ap.add_argument("--decode", action="store_true", help="time one decode step per request instead: every "
                     "layer's q/k/v projection + LoRA of the new tokens and attuner_decode_attn over the whole "
                     "assembled context (the suffix already prefilled)")
+    ap.add_argument("--spans", type=int, default=0, metavar="SEP",
+                    help="time prompts that interleave the artifacts with online spans instead: a 32-token system "
+                         "span first, SEP online tokens between consecutive artifacts, the suffix last "
+                         "(attuner_assemble_segments + per layer attuner_qproj_lora and attuner_span_attn)")
     ap.add_argument("--quiet", action="store_true")
     return ap.parse_args()
 
@@ -181,6 +185,9 @@ def main():
         return
     if args.decode:
         decode_main(args)
+        return
+    if args.spans > 0:
+        spans_main(args)
         return
 
     import numpy as np
@@ -890,6 +897,156 @@ def decode_main(args):
         "breakdown_ms_per_step_eager": {k: round(v, 4) for k, v in breakdown.items()},
         "projection_weight_gbps": round(gemm_w_gbps, 1),
         "projection_kernels": proj,
+        "kernel_avg_ms": per_kernel,
+    }
+    print(json.dumps(out), flush=True)
+    ctx.close()
+
+
+# ----------------------------------------------------------------------------
+# --spans SEP: prompts with online spans between and around the artifacts
+# ----------------------------------------------------------------------------
+
+SPANS_METRIC = "interleaved-prompt online tokens/s + attention TFLOP/s (% MFMA peak)"
+SYSTEM_SPAN = 32
+
+
+def spans_main(args):
+    import numpy as np
+    import torch
+
+    import synthdata as sd
+    from paper_2609_36722_amd.api import Context, ModelCfg
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = sd.make_workload(args.workload)
+    s, NL = wl.shape, wl.n_layers
+    H, nq, nkv = s.hidden, s.q_dim, s.kv_dim
+    n_out = nq + 2 * nkv
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(3000 + wl.index)
+
+    def randn(*shape, std=1.0):
+        t = torch.randn(*shape, generator=gen, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            t.mul_(std)
+        return t.to(torch.bfloat16)
+
+    used = sorted({a for r in wl.requests for a in r.artifact_ids})
+    pages = sum(math.ceil(wl.artifact_lengths[a] / 16) for a in used)
+    cfg = ModelCfg(n_layers=NL, hidden=H, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads, head_dim=s.head_dim,
+                   rope_theta=s.rope_theta, rms_eps=s.rms_eps)
+    ctx = Context(cfg, pool_pages=pages)
+    ids = {}
+    for a in used:
+        L = wl.artifact_lengths[a]
+        ids[a] = ctx.store_artifact(randn(NL, s.n_kv_heads, L, s.head_dim), randn(NL, s.n_kv_heads, L, s.head_dim))
+    prompts = []
+    for r in wl.requests:
+        p = [-SYSTEM_SPAN]
+        for j, a in enumerate(r.artifact_ids):
+            if j > 0:
+                p.append(-args.spans)
+            p.append(ids[a])
+        p.append(-r.suffix_len)
+        prompts.append(p)
+    ne, rows, ns = ctx.assemble_segments_plan(prompts)
+    bt = torch.zeros(max(1, ne) * 4, dtype=torch.int32, device=dev)
+    req_kv = torch.zeros(NL * 2 * s.n_kv_heads * rows * s.head_dim, dtype=torch.bfloat16, device=dev)
+    cu, spans = ctx.assemble_segments(prompts, bt, req_kv, rows)
+    T = sum(l for _, _, l in spans)
+    cu_q = [0]
+    for _, _, l in spans:
+        cu_q.append(cu_q[-1] + l)
+    kv_start = [cu[r] for r, _, _ in spans]
+    offset = [off for _, off, _ in spans]
+    log(args, f"spans {wl.name}: {NL} layers, {len(spans)} online spans, {T} online tokens, {rows} cache rows")
+    wqkv = [randn(n_out, H, std=wl.w_std) for _ in range(NL)]
+    a_l = [randn(wl.rank, H, std=wl.a_std) for _ in range(NL)]
+    b_l = [randn(nq, wl.rank, std=wl.b_std) for _ in range(NL)]
+    ones = torch.ones(s.head_dim, dtype=torch.bfloat16, device=dev)
+    x = [randn(T, H) for _ in range(NL)]
+    qkv = [torch.empty(T, n_out, dtype=torch.bfloat16, device=dev) for _ in range(NL)]
+    o = torch.empty(T, s.n_q_heads, s.head_dim, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+
+    def layer_loop():
+        for l in range(NL):
+            ctx.qproj_lora(x[l], wqkv[l], a_l[l], b_l[l], wl.rank, wl.scale, nq, qkv[l])
+            q = qkv[l]
+            ctx.span_attn(l, cu_q, kv_start, offset, None, q[:, :nq], n_out, q[:, nq:nq + nkv], q[:, nq + nkv:],
+                          n_out, ones, ones, req_kv, rows, o)
+
+    def assemble():
+        ctx.assemble_segments(prompts, bt, req_kv, rows)
+
+    for _ in range(max(1, args.warmup)):
+        assemble()
+        layer_loop()
+    torch.cuda.synchronize()
+    ctx.trace_begin()
+    for _ in range(3):
+        assemble()
+        layer_loop()
+    torch.cuda.synchronize()
+    ktimes = ctx.trace_end()
+    per_kernel = {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t, _) in ktimes.items()}
+    graph = None
+    if not args.no_graph:
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        graph = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap):
+            layer_loop()
+        torch.cuda.synchronize()
+
+    def step():
+        assemble()
+        if graph is not None:
+            graph.replay()
+        else:
+            layer_loop()
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    # attention work: span rows see offset + i + 1 keys
+    attn_f = sum(4 * s.head_dim * s.n_q_heads * (l * off + l * (l + 1) // 2) for _, off, l in spans)
+    attn_ms = per_kernel["attention_kernel"]["avg_ms"]
+    attn_tflops = attn_f / (attn_ms * 1e-3) / 1e12
+    log(args, f"step {ms_step:.3f} ms ({T / (ms_step * 1e-3):.0f} online tokens/s); attention {attn_ms * 1e3:.1f} us "
+              f"= {attn_tflops:.0f} TFLOP/s")
+    out = {
+        "metric": SPANS_METRIC,
+        "value": round(T / (ms_step * 1e-3), 2),
+        "unit": "online tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded device-side N(0,1) / N(0,0.02) bf16 draws, distinct weights per layer)",
+        "config": {"workload": wl.name + f"+spans(system {SYSTEM_SPAN}, separator {args.spans})", "layers": NL,
+                   "hidden": H, "online_spans": len(spans), "online_tokens": T, "cache_rows": rows,
+                   "lora_rank": wl.rank},
+        "layer_loop": "hip_graph" if graph is not None else "eager",
+        "roofline": {"bound": "mfma", "kernel": "attention_kernel", "achieved": round(attn_tflops, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "flops_per_launch": attn_f, "launch_ms": attn_ms},
         "kernel_avg_ms": per_kernel,
     }
     print(json.dumps(out), flush=True)
