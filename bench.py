@@ -83,6 +83,12 @@ def parse():
                     help="time prompts that interleave the artifacts with online spans instead: a 32-token system "
                          "span first, SEP online tokens between consecutive artifacts, the suffix last "
                          "(attuner_assemble_segments + per layer attuner_qproj_lora and attuner_span_attn)")
+    ap.add_argument("--host-cache", action="store_true",
+                    help="keep the artifact caches in pinned host memory (attuner_store_artifact_host): every step "
+                         "then gathers them over the host link into HBM, as the paper's timed TTFT does")
+    ap.add_argument("--merged", action="store_true",
+                    help="deployment form: merge each layer's adapter into W_q once before timing "
+                         "(attuner_merge_lora) and run the rank-0 projection in the step")
     ap.add_argument("--quiet", action="store_true")
     return ap.parse_args()
 
@@ -230,14 +236,17 @@ def main():
     pages = sum(math.ceil(wl.artifact_lengths[a] / 16) for a in used)
     cfg = ModelCfg(n_layers=NL, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
                    head_dim=s.head_dim, rope_theta=s.rope_theta, rms_eps=s.rms_eps)
-    ctx = Context(cfg, pool_pages=pages)
+    ctx = Context(cfg, pool_pages=0 if args.host_cache else pages)
+    if args.host_cache:
+        ctx.host_pool_create(pages)
+    store = ctx.store_artifact_host if args.host_cache else ctx.store_artifact
     ids = {}
     for a in used:
         k, v = sd.artifact_kv(wl, a, 0)
         kd = bf16_to_device(np.ascontiguousarray(k.transpose(1, 0, 2)), dev)
         vd = bf16_to_device(np.ascontiguousarray(v.transpose(1, 0, 2)), dev)
-        ids[a] = ctx.store_artifact(kd.unsqueeze(0).expand(NL, -1, -1, -1).contiguous(),
-                                    vd.unsqueeze(0).expand(NL, -1, -1, -1).contiguous())
+        ids[a] = store(kd.unsqueeze(0).expand(NL, -1, -1, -1).contiguous(),
+                       vd.unsqueeze(0).expand(NL, -1, -1, -1).contiguous())
     requests = [[ids[a] for a in r.artifact_ids] for r in wl.requests]
     suffix_cap = [r.suffix_len for r in wl.requests]
     n_entries, rows = ctx.assemble_plan(requests, suffix_cap)
@@ -276,10 +285,15 @@ def main():
     # attuner_suffix_attn (q/k norm + RoPE with the suffix k/v into the cache,
     # attention, split merge)
     qproj_args, attn_args = [], []
+    if args.merged:   # W_q + s B A in place, once, outside the timed region
+        for l in range(NL):
+            ctx.merge_lora(wqkv[l], a_l[l], b_l[l], wl.rank, wl.scale, nq, wqkv[l])
+        torch.cuda.synchronize()
+    step_rank = 0 if args.merged else wl.rank
     for l in range(NL):
         base = qkv[l].data_ptr()
         qproj_args.append((h, T, x_l[l].data_ptr(), wqkv[l].data_ptr(), n_out, a_l[l].data_ptr(), b_l[l].data_ptr(),
-                           wl.rank, wl.scale, nq, base, sp))
+                           step_rank, wl.scale, nq, base, sp))
         attn_args.append((h, l, len(requests), c_cuq, c_cuctx, c_art, c_pos, base, n_out, base + 2 * nq,
                           base + 2 * (nq + nkv), n_out, gq.data_ptr(), gk.data_ptr(), req_kv.data_ptr(), rows,
                           o_l[l].data_ptr(), None, sp))
@@ -418,7 +432,7 @@ def main():
     # ---- algorithmic rates -----------------------------------------------------
     reqs_shape = [(wl.art_len(r), r.suffix_len) for r in wl.requests]
     attn_f = attention_flops(s, reqs_shape)
-    gemm_f = gemm_flops(s, T, wl.rank)
+    gemm_f = gemm_flops(s, T, 0 if args.merged else wl.rank)
     g_bytes = gather_bytes(s, sum(L for L, _ in reqs_shape), NL)
     def kavg(name):  # kernel-only average duration (ms) from the library's launch tracer
         n, tot, _ = ktimes[name]
@@ -496,6 +510,8 @@ def main():
                    "lora_rank": wl.rank, "page_tokens": 16},
         "layer_loop": "hip_graph" if graph is not None else "eager",
         "gather_schedule": "per layer on a second stream beside the layer loop" if overlap else "all layers first",
+        "artifact_cache": "pinned host memory, gathered over the host link every step" if args.host_cache else "HBM",
+        "adapter": "merged into W_q (rank-0 projection)" if args.merged else "unmerged, fused into the projection",
         "roofline": {"bound": "mfma", "kernel": "attention_kernel", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "flops_per_launch": attn_f, "launch_ms": round(attn_kernel_ms, 5)},

@@ -112,11 +112,40 @@ attuner_status attuner_store_artifact(attuner_ctx* ctx, int32_t n_tokens, const 
  * Errors: ENOENT. */
 attuner_status attuner_release_artifact(attuner_ctx* ctx, int32_t artifact_id);
 
-/* Physical page ids of an artifact, in token order (host output of up to
- * max_pages entries), its page count and its token count.  Errors: ENOENT,
- * ERANGE (max_pages too small; *n_pages still set). */
+/* Physical page ids of an artifact as block tables carry them (host pool
+ * pages with ATTUNER_HOST_PAGE_FLAG set), in token order (host output of up
+ * to max_pages entries), its page count and its token count.  Errors:
+ * ENOENT, ERANGE (max_pages too small; *n_pages still set). */
 attuner_status attuner_artifact_pages(const attuner_ctx* ctx, int32_t artifact_id, int32_t* pages_out,
                                       int32_t max_pages, int32_t* n_pages, int32_t* n_tokens);
+
+/* --------------------------------------------------------------------------
+ * Artifact caches kept in CPU RAM: the paper stores the artifact caches in
+ * host memory and copies what a request uses to the GPU inside the timed
+ * region (appendix A.2: CPU RAM cache lookup and GPU transfer are timed).
+ *
+ * attuner_host_pool_create gives the context a second pool of host_pages
+ * pages (same page size and layout as the HBM pool) in pinned host memory
+ * mapped for the device (hipHostMalloc), released by attuner_destroy; once
+ * per context.  attuner_store_artifact_host stores an artifact there (k, v
+ * as for attuner_store_artifact, device memory; the copy runs on `stream`);
+ * its id is used like any other: every assembly call gathers its pages
+ * straight from host memory over the host link into the request cache (the
+ * same gather kernel; per layer with attuner_gather_layers, so a layer's
+ * transfer can overlap earlier layers' compute).  Block tables carry host
+ * pages as (page | ATTUNER_HOST_PAGE_FLAG).  attuner_release_artifact returns
+ * pages to the pool they came from.
+ * Errors: EINVAL (no host pool / a second one), ERANGE (host_pages outside
+ * [1, 2^30)), ENOMEM (pinned allocation, host pool full), EDEVICE.
+ * ------------------------------------------------------------------------ */
+#define ATTUNER_HOST_PAGE_FLAG (1 << 30)
+
+attuner_status attuner_host_pool_create(attuner_ctx* ctx, int64_t host_pages);
+
+attuner_status attuner_store_artifact_host(attuner_ctx* ctx, int32_t n_tokens, const void* k, const void* v,
+                                           void* stream, int32_t* artifact_id);
+
+attuner_status attuner_host_pool_info(const attuner_ctx* ctx, int64_t* host_pages, int64_t* free_pages);
 
 /* --------------------------------------------------------------------------
  * a1 + a2: assemble request caches (section 2, the PIC box; appendix A.3).
@@ -229,6 +258,18 @@ attuner_status attuner_assemble_segments(attuner_ctx* ctx, int32_t n_req, const 
 attuner_status attuner_qproj_lora(attuner_ctx* ctx, int32_t n_tok, const void* x, const void* w,
                                   int32_t n_out, const void* a, const void* b, int32_t rank, float scale,
                                   int32_t lora_cols, void* out, void* stream);
+
+/* Deployment form of the adapter (appendix A.5: the learned update is merged
+ * into the query projection, W_Q <- W_Q + (alpha/r) B A, for online
+ * inference; attuner_qproj_lora with rank 0 then runs the merged weights).
+ * w_out[n][k] = w[n][k] + scale * sum_j b[n][j] a[j][k] for rows n <
+ * lora_cols (fp32 sum, one bf16 rounding), w_out[n][k] = w[n][k] for the
+ * other rows.  w, w_out: device [n_out][k_dim] bf16 (w_out may be w); a:
+ * [rank][k_dim]; b: [lora_cols][rank].  k_dim a multiple of 8; 0 <= rank <=
+ * ATTUNER_MAX_RANK (rank 0: a copy).  Errors: EINVAL, ERANGE. */
+attuner_status attuner_merge_lora(attuner_ctx* ctx, const void* w, int32_t n_out, int32_t k_dim,
+                                  const void* a, const void* b, int32_t rank, float scale,
+                                  int32_t lora_cols, void* w_out, void* stream);
 
 /* --------------------------------------------------------------------------
  * a4: per-head QK-RMSNorm + RoPE of the suffix (section 4: the adapted query

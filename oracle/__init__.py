@@ -29,4 +29,5 @@ from .attuner_ref import (  # noqa: F401
     first_token,
     interleaved_layer,
     block_table_segments,
+    merge_lora,
 )

@@ -434,3 +434,12 @@ def block_table_segments(artifact_lengths: Sequence[int], requests: Sequence[Seq
         cu_ctx.append(base + off)
     return (np.asarray(entries, dtype=np.int64).reshape(-1, 5), np.asarray(cu_ctx, dtype=np.int64),
             np.asarray(spans, dtype=np.int64).reshape(-1, 3))
+
+
+def merge_lora(w: np.ndarray, a: np.ndarray, b: np.ndarray, scale: float, lora_cols: int) -> np.ndarray:
+    """Deployment form of the adapter (appendix A.5: the update is merged into
+    the query projection, W_Q <- W_Q + (alpha / r) B A): rows below lora_cols
+    get scale * B A added, the other rows (keys, values) are unchanged."""
+    w = np.array(w, np.float64)
+    w[:lora_cols] += scale * (np.asarray(b, np.float64) @ np.asarray(a, np.float64))
+    return w

@@ -134,6 +134,27 @@ class Context:
                "attuner_store_artifact")
         return out.value
 
+    # ---- artifact caches in CPU RAM (pinned host pool) ----------------------------------
+    def host_pool_create(self, host_pages: int) -> None:
+        _check(lib().attuner_host_pool_create(self._h, int(host_pages)), "attuner_host_pool_create")
+
+    def store_artifact_host(self, k: torch.Tensor, v: torch.Tensor, n_tokens: Optional[int] = None,
+                            stream=None) -> int:
+        """Like store_artifact, into the host pool."""
+        n = int(k.shape[-2]) if n_tokens is None else int(n_tokens)
+        c = self.cfg
+        _need(k, c.n_layers * c.n_kv_heads * n * c.head_dim, "k")
+        _need(v, c.n_layers * c.n_kv_heads * n * c.head_dim, "v")
+        out = C.c_int32()
+        _check(lib().attuner_store_artifact_host(self._h, n, _ptr(k), _ptr(v), _stream(stream), C.byref(out)),
+               "attuner_store_artifact_host")
+        return out.value
+
+    def host_pool_info(self) -> Tuple[int, int]:
+        pages, free = C.c_int64(), C.c_int64()
+        _check(lib().attuner_host_pool_info(self._h, C.byref(pages), C.byref(free)), "attuner_host_pool_info")
+        return pages.value, free.value
+
     def release_artifact(self, artifact_id: int) -> None:
         _check(lib().attuner_release_artifact(self._h, int(artifact_id)), "attuner_release_artifact")
 
@@ -243,6 +264,17 @@ class Context:
         _check(lib().attuner_qproj_lora(self._h, int(x.shape[0]), _ptr(x), _ptr(w), int(w.shape[0]), _ptr(a), _ptr(b),
                                         int(rank), float(scale), int(lora_cols), _ptr(out), _stream(stream)),
                "attuner_qproj_lora")
+
+    def merge_lora(self, w: torch.Tensor, a: Optional[torch.Tensor], b: Optional[torch.Tensor], rank: int,
+                   scale: float, lora_cols: int, w_out: torch.Tensor, stream=None) -> None:
+        """w_out = w + scale * B A on rows < lora_cols (the deployment form of the adapter)."""
+        N, K = int(w.shape[0]), int(w.shape[1])
+        _need(w_out, N * K, "w_out")
+        if rank:
+            _need(a, rank * K, "a")
+            _need(b, lora_cols * rank, "b")
+        _check(lib().attuner_merge_lora(self._h, _ptr(w), N, K, _ptr(a), _ptr(b), int(rank), float(scale),
+                                        int(lora_cols), _ptr(w_out), _stream(stream)), "attuner_merge_lora")
 
     # ---- the decoder layer around the path ------------------------------------------
     def embed(self, token_ids: Sequence[int], table: torch.Tensor, out: torch.Tensor, stream=None) -> None:

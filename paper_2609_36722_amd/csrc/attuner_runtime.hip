@@ -129,8 +129,11 @@ struct Staging {
 };
 
 struct Artifact {
-  std::vector<int32_t> pages;
+  std::vector<int32_t> pages;  // page indices in its pool
   int32_t n_tokens;
+  bool host = false;           // pages of the host pool
+  // the page id as block tables carry it
+  int32_t table_page(int32_t pg) const { return host ? (pg | kHostPageFlag) : pg; }
 };
 
 // Named HIP event pairs around kernel launches (attuner_trace_*).  Events
@@ -199,6 +202,11 @@ struct attuner_ctx {
   int64_t page_bytes = 0;  // one page, all layers
   uint16_t* pool = nullptr;
   std::set<int32_t> free_pages;
+  // host pool: pinned, mapped host memory (host pointer and its device alias)
+  int64_t host_pages = 0;
+  uint16_t* host_pool = nullptr;
+  uint16_t* host_pool_dev = nullptr;
+  std::set<int32_t> host_free;
   std::map<int32_t, Artifact> artifacts;
   int32_t next_id = 0;
 
@@ -607,6 +615,7 @@ void attuner_destroy(attuner_ctx* c) {
   if (g_tracer == &c->tracer) g_tracer = nullptr;
   c->tracer.release();
   if (c->pool) (void)hipFree(c->pool);
+  if (c->host_pool) (void)hipHostFree(c->host_pool);
   delete c;
 }
 
@@ -618,28 +627,33 @@ attuner_status attuner_pool_info(const attuner_ctx* c, int64_t* pool_pages, int6
   return ATTUNER_OK;
 }
 
-attuner_status attuner_store_artifact(attuner_ctx* c, int32_t n_tokens, const void* k, const void* v, void* stream,
-                                      int32_t* artifact_id) {
+static attuner_status store_impl(attuner_ctx* c, bool host, int32_t n_tokens, const void* k, const void* v,
+                                 void* stream, int32_t* artifact_id) {
   if (!c || !artifact_id) return fail(ATTUNER_EINVAL, "null ctx or artifact_id");
   if (n_tokens <= 0) return fail(ATTUNER_EINVAL, "an artifact holds at least one token (got %d)", n_tokens);
   if (!k || !v) return fail(ATTUNER_EINVAL, "null k or v");
   if (!aligned16(k) || !aligned16(v)) return fail(ATTUNER_EINVAL, "k and v must be 16-byte aligned");
+  if (host && !c->host_pool) return fail(ATTUNER_EINVAL, "no host pool (attuner_host_pool_create)");
+  std::set<int32_t>& free_set = host ? c->host_free : c->free_pages;
   const int64_t need = (n_tokens + kPageTokens - 1) / kPageTokens;
-  if (need > (int64_t)c->free_pages.size())
-    return fail(ATTUNER_ENOMEM, "pool full: artifact needs %lld pages, %zu free", (long long)need, c->free_pages.size());
+  if (need > (int64_t)free_set.size())
+    return fail(ATTUNER_ENOMEM, "%s pool full: artifact needs %lld pages, %zu free", host ? "host" : "HBM",
+                (long long)need, free_set.size());
   DeviceGuard dg(c->device);
   try {
     HIP_TRY(c->ws_pages.ensure((size_t)need * sizeof(int32_t)));
     Artifact art;
     art.n_tokens = n_tokens;
-    auto it = c->free_pages.begin();
+    art.host = host;
+    auto it = free_set.begin();
     for (int64_t i = 0; i < need; ++i) art.pages.push_back(*it++);
     hipStream_t s = static_cast<hipStream_t>(stream);
     HIP_TRY(c->staging.upload(art.pages.data(), art.pages.size() * sizeof(int32_t), c->ws_pages.ptr, s));
     HIP_TRY(launch_store_pages(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), n_tokens,
-                               static_cast<const int32_t*>(c->ws_pages.ptr), (int)need, c->pool, c->pool_pages,
+                               static_cast<const int32_t*>(c->ws_pages.ptr), (int)need,
+                               host ? c->host_pool_dev : c->pool, host ? c->host_pages : c->pool_pages,
                                c->cfg.n_layers, c->cfg.n_kv_heads, s));
-    for (int32_t pg : art.pages) c->free_pages.erase(pg);
+    for (int32_t pg : art.pages) free_set.erase(pg);
     const int32_t id = c->next_id++;
     c->artifacts.emplace(id, std::move(art));
     *artifact_id = id;
@@ -649,11 +663,55 @@ attuner_status attuner_store_artifact(attuner_ctx* c, int32_t n_tokens, const vo
   return ATTUNER_OK;
 }
 
+attuner_status attuner_store_artifact(attuner_ctx* c, int32_t n_tokens, const void* k, const void* v, void* stream,
+                                      int32_t* artifact_id) {
+  return store_impl(c, false, n_tokens, k, v, stream, artifact_id);
+}
+
+attuner_status attuner_host_pool_create(attuner_ctx* c, int64_t host_pages) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (c->host_pool) return fail(ATTUNER_EINVAL, "the context already has a host pool");
+  if (host_pages <= 0 || host_pages >= kHostPageFlag)
+    return fail(ATTUNER_ERANGE, "host_pages %lld outside [1, 2^30)", (long long)host_pages);
+  DeviceGuard dg(c->device);
+  void* h = nullptr;
+  hipError_t e = hipHostMalloc(&h, (size_t)(host_pages * c->page_bytes), hipHostMallocMapped | hipHostMallocPortable);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(ATTUNER_ENOMEM, "host pool of %lld pages (%lld bytes): %s", (long long)host_pages,
+                (long long)(host_pages * c->page_bytes), hipGetErrorString(e));
+  }
+  void* d = nullptr;
+  e = hipHostGetDevicePointer(&d, h, 0);
+  if (e != hipSuccess) {
+    (void)hipHostFree(h);
+    return fail(ATTUNER_EDEVICE, "hipHostGetDevicePointer: %s", hipGetErrorString(e));
+  }
+  c->host_pool = static_cast<uint16_t*>(h);
+  c->host_pool_dev = static_cast<uint16_t*>(d);
+  c->host_pages = host_pages;
+  for (int32_t p = 0; p < (int32_t)host_pages; ++p) c->host_free.insert(c->host_free.end(), p);
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_store_artifact_host(attuner_ctx* c, int32_t n_tokens, const void* k, const void* v,
+                                           void* stream, int32_t* artifact_id) {
+  return store_impl(c, true, n_tokens, k, v, stream, artifact_id);
+}
+
+attuner_status attuner_host_pool_info(const attuner_ctx* c, int64_t* host_pages, int64_t* free_pages) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (host_pages) *host_pages = c->host_pages;
+  if (free_pages) *free_pages = (int64_t)c->host_free.size();
+  return ATTUNER_OK;
+}
+
 attuner_status attuner_release_artifact(attuner_ctx* c, int32_t artifact_id) {
   if (!c) return fail(ATTUNER_EINVAL, "null ctx");
   auto it = c->artifacts.find(artifact_id);
   if (it == c->artifacts.end()) return fail(ATTUNER_ENOENT, "unknown artifact id %d", artifact_id);
-  for (int32_t pg : it->second.pages) c->free_pages.insert(pg);
+  std::set<int32_t>& free_set = it->second.host ? c->host_free : c->free_pages;
+  for (int32_t pg : it->second.pages) free_set.insert(pg);
   c->artifacts.erase(it);
   return ATTUNER_OK;
 }
@@ -668,7 +726,7 @@ attuner_status attuner_artifact_pages(const attuner_ctx* c, int32_t artifact_id,
   if (n_tokens) *n_tokens = it->second.n_tokens;
   if (pages_out) {
     if (max_pages < np) return fail(ATTUNER_ERANGE, "max_pages %d < %d pages", max_pages, np);
-    memcpy(pages_out, it->second.pages.data(), (size_t)np * sizeof(int32_t));
+    for (int32_t i = 0; i < np; ++i) pages_out[i] = it->second.table_page(it->second.pages[i]);
   }
   return ATTUNER_OK;
 }
@@ -697,7 +755,7 @@ static attuner_status plan_impl(const attuner_ctx* c, int32_t n_req, const int32
         int32_t left = a.n_tokens;
         for (int32_t pg : a.pages) {
           const int32_t nv = std::min(left, kPageTokens);
-          table->push_back(pg);
+          table->push_back(a.table_page(pg));
           table->push_back(nv);
           table->push_back((int32_t)(row + alen));
           table->push_back(r);
@@ -772,7 +830,8 @@ attuner_status attuner_gather_layers(attuner_ctx* c, const int32_t* block_table,
   if (n_entries == 0 || n_layers == 0) return ATTUNER_OK;
   if (!req_kv || !aligned16(req_kv)) return fail(ATTUNER_EINVAL, "req_kv must be non-null and 16-byte aligned");
   DeviceGuard dg(c->device);
-  HIP_TRY(launch_gather(block_table, n_entries, c->pool, c->pool_pages, layer_begin, n_layers, c->cfg.n_kv_heads,
+  HIP_TRY(launch_gather(block_table, n_entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages, layer_begin,
+                          n_layers, c->cfg.n_kv_heads,
                         static_cast<uint16_t*>(req_kv), cache_rows, static_cast<hipStream_t>(stream)));
   return ATTUNER_OK;
 }
@@ -835,7 +894,7 @@ static attuner_status plan_segments_impl(const attuner_ctx* c, int32_t n_req, co
         int32_t left = a.n_tokens;
         for (int32_t pg : a.pages) {
           const int32_t nv = std::min(left, kPageTokens);
-          table->push_back(pg);
+          table->push_back(a.table_page(pg));
           table->push_back(nv);
           table->push_back((int32_t)(row + off));
           table->push_back(r);
@@ -892,7 +951,8 @@ attuner_status attuner_assemble_segments(attuner_ctx* c, int32_t n_req, const in
     DeviceGuard dg(c->device);
     hipStream_t s = static_cast<hipStream_t>(stream);
     HIP_TRY(c->staging.upload(table.data(), table.size() * sizeof(int32_t), block_table, s));
-    HIP_TRY(launch_gather(block_table, entries, c->pool, c->pool_pages, 0, c->cfg.n_layers, c->cfg.n_kv_heads,
+    HIP_TRY(launch_gather(block_table, entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages, 0,
+                          c->cfg.n_layers, c->cfg.n_kv_heads,
                           static_cast<uint16_t*>(req_kv), cache_rows, s));
   }
   c->last_table = block_table;
@@ -1004,6 +1064,26 @@ attuner_status attuner_lm_head_argmax(attuner_ctx* c, int32_t n_rows, const void
   HIP_TRY(launch_gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_lm), n_rows, vocab, H,
                       GemmEpi{kEpiF32, nullptr, logits}, nullptr, s));
   HIP_TRY(launch_argmax_rows(logits, n_rows, vocab, ids, max_logit, s));
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_merge_lora(attuner_ctx* c, const void* w, int32_t n_out, int32_t k_dim, const void* a,
+                                  const void* b, int32_t rank, float scale, int32_t lora_cols, void* w_out,
+                                  void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (n_out < 0 || k_dim <= 0 || k_dim % 8 != 0)
+    return fail(ATTUNER_EINVAL, "n_out %d, k_dim %d (a positive multiple of 8)", n_out, k_dim);
+  if (rank < 0 || rank > ATTUNER_MAX_RANK) return fail(ATTUNER_ERANGE, "rank %d outside [0, %d]", rank, ATTUNER_MAX_RANK);
+  if (lora_cols < 0 || lora_cols > n_out) return fail(ATTUNER_EINVAL, "lora_cols %d outside [0, n_out]", lora_cols);
+  if (n_out == 0) return ATTUNER_OK;
+  if (!w || !w_out || (rank > 0 && lora_cols > 0 && (!a || !b)))
+    return fail(ATTUNER_EINVAL, "null w, w_out, a or b");
+  if (!aligned16(w) || !aligned16(w_out) || (rank > 0 && !aligned16(a)))
+    return fail(ATTUNER_EINVAL, "w, w_out and a must be 16-byte aligned");
+  DeviceGuard dg(c->device);
+  HIP_TRY(launch_merge_lora(static_cast<const uint16_t*>(w), n_out, k_dim, static_cast<const uint16_t*>(a),
+                            static_cast<const uint16_t*>(b), rank, scale, rank > 0 ? lora_cols : 0,
+                            static_cast<uint16_t*>(w_out), static_cast<hipStream_t>(stream)));
   return ATTUNER_OK;
 }
 

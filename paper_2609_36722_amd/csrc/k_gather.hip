@@ -1,5 +1,9 @@
 // K1: paged artifact pool -- store and block-table gather (bit-exact copies).
 //
+// Two pools with one layout: the HBM pool and, optionally, a host pool in
+// pinned host memory (the paper keeps artifact caches in CPU RAM and copies
+// them to the GPU per request, inside the timed region, appendix A.2); the
+// gather kernel reads host pages over the host link directly.
 // Pool layout: [n_layers][pool_pages][2 (K, V)][n_kv][16 tokens][128] bf16, so
 // one page of one layer is a contiguous 2 * n_kv * 4 KiB block and each
 // (K|V, head) slab of it is 4 KiB.  Request cache layout:
@@ -57,8 +61,9 @@ __global__ __launch_bounds__(256) void store_pages_kernel(const u32x4* __restric
   }
 }
 
-__global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ table, const u32x4* __restrict__ pool,
-                                                     int64_t pool_pages, int n_kv, u32x4* __restrict__ req_kv,
+__global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ table, const u32x4* __restrict__ dev_pool,
+                                                     int64_t dev_pages, const u32x4* __restrict__ host_pool,
+                                                     int64_t host_pages, int n_kv, u32x4* __restrict__ req_kv,
                                                      int64_t cache_rows, int layer_begin) {
   const int64_t e = blockIdx.x;
   const int layer = layer_begin + (int)blockIdx.y;
@@ -66,8 +71,11 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ ta
   const int rr = threadIdx.x >> 4;
   const int chunk = threadIdx.x & 15;
   if (rr >= ent.y) return;
+  const bool host = (ent.x & kHostPageFlag) != 0;
+  const u32x4* __restrict__ pool = host ? host_pool : dev_pool;
+  const int64_t pool_pages = host ? host_pages : dev_pages;
   const int n_slab = 2 * n_kv;
-  const int64_t src_base = ((int64_t)layer * pool_pages + ent.x) * n_slab;
+  const int64_t src_base = ((int64_t)layer * pool_pages + (ent.x & ~kHostPageFlag)) * n_slab;
   const int64_t dst_row = ent.z + rr;
   for (int s0 = 0; s0 < n_slab; s0 += kGatherBatch) {
     u32x4 buf[kGatherBatch];
@@ -103,13 +111,13 @@ hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens
 }
 
 hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint16_t* pool, int64_t pool_pages,
-                         int layer_begin, int n_layers, int n_kv, uint16_t* req_kv, int64_t cache_rows,
-                         hipStream_t stream) {
+                         const uint16_t* host_pool, int64_t host_pages, int layer_begin, int n_layers, int n_kv,
+                         uint16_t* req_kv, int64_t cache_rows, hipStream_t stream) {
   if (n_entries == 0 || n_layers == 0) return hipSuccess;
   dim3 grid(static_cast<unsigned>(n_entries), n_layers);
   ATTUNER_LAUNCH("gather_kernel", gather_kernel, grid, dim3(256), stream, reinterpret_cast<const int4*>(table_dev),
-                     reinterpret_cast<const u32x4*>(pool), pool_pages, n_kv, reinterpret_cast<u32x4*>(req_kv),
-                     cache_rows, layer_begin);
+                     reinterpret_cast<const u32x4*>(pool), pool_pages, reinterpret_cast<const u32x4*>(host_pool),
+                     host_pages, n_kv, reinterpret_cast<u32x4*>(req_kv), cache_rows, layer_begin);
   return hipGetLastError();
 }
 

@@ -159,3 +159,55 @@ hipError_t launch_argmax_rows(const float* logits, int n_rows, int n, int32_t* i
 }
 
 }  // namespace attuner
+
+namespace attuner {
+
+namespace {
+
+// Deployment form of the adapter: w_out[n] = w[n] + scale * sum_j b[n][j] a[j]
+// for rows n < lora_cols (one bf16 rounding of the fp32 sum), w_out[n] = w[n]
+// otherwise.  Workgroup = one row; thread = 16-byte chunks of it.
+__global__ __launch_bounds__(256) void merge_lora_kernel(const bf16_t* __restrict__ w, int k_dim,
+                                                         const bf16_t* __restrict__ a, const bf16_t* __restrict__ b,
+                                                         int rank, float scale, int lora_cols, bf16_t* w_out) {
+  const int n = blockIdx.x;
+  const bf16_t* wr = w + (int64_t)n * k_dim;
+  bf16_t* orow = w_out + (int64_t)n * k_dim;
+  const bool adapt = n < lora_cols;
+  for (int c = threadIdx.x; c < k_dim / 8; c += 256) {
+    const u32x4 wv = *reinterpret_cast<const u32x4*>(wr + 8 * c);
+    if (!adapt) {
+      *reinterpret_cast<u32x4*>(orow + 8 * c) = wv;
+      continue;
+    }
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < rank; ++j) {
+      const float bj = bf16_to_f32(b[(int64_t)n * rank + j]);
+      const u32x4 av = *reinterpret_cast<const u32x4*>(a + (int64_t)j * k_dim + 8 * c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] = fmaf(bj, __uint_as_float(av[e] << 16), acc[2 * e]);
+        acc[2 * e + 1] = fmaf(bj, __uint_as_float(av[e] & 0xFFFF0000u), acc[2 * e + 1]);
+      }
+    }
+    u32x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      o[e] = pack_bf16x2(__uint_as_float(wv[e] << 16) + scale * acc[2 * e],
+                         __uint_as_float(wv[e] & 0xFFFF0000u) + scale * acc[2 * e + 1]);
+    *reinterpret_cast<u32x4*>(orow + 8 * c) = o;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_merge_lora(const uint16_t* w, int n_out, int k_dim, const uint16_t* a, const uint16_t* b, int rank,
+                             float scale, int lora_cols, uint16_t* w_out, hipStream_t stream) {
+  if (n_out == 0) return hipSuccess;
+  if (k_dim % 8 != 0) return hipErrorInvalidValue;
+  ATTUNER_LAUNCH("merge_lora_kernel", merge_lora_kernel, dim3((unsigned)n_out), dim3(256), stream, w, k_dim, a, b,
+                 rank, scale, lora_cols, w_out);
+  return hipGetLastError();
+}
+
+}  // namespace attuner

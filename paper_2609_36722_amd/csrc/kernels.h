@@ -35,10 +35,13 @@ hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens
 
 // Copy every entry {page, n_valid, dst_row, request} of the block table, for
 // layers layer_begin .. layer_begin + n_layers - 1, into req_kv
-// [model layers][2][n_kv][cache_rows][128].
+// [model layers][2][n_kv][cache_rows][128].  A page with kHostPageFlag set
+// is page (page & ~kHostPageFlag) of the host pool (pinned host memory, same
+// layout, read by the kernel over the host link); others are HBM pool pages.
+constexpr int32_t kHostPageFlag = 1 << 30;
 hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint16_t* pool, int64_t pool_pages,
-                         int layer_begin, int n_layers, int n_kv, uint16_t* req_kv, int64_t cache_rows,
-                         hipStream_t stream);
+                         const uint16_t* host_pool, int64_t host_pages, int layer_begin, int n_layers, int n_kv,
+                         uint16_t* req_kv, int64_t cache_rows, hipStream_t stream);
 
 // ---- a3: LoRA-down and the projection GEMM --------------------------------
 
@@ -84,6 +87,11 @@ constexpr int kGemvMaxTok = 8;
 hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, const uint16_t* b,
                        int rank, int r_pad, int lora_cols, const float* t_part, GemmEpi epi, uint16_t* out,
                        hipStream_t stream);
+
+// w_out[n] = w[n] + scale * b[n] . a for n < lora_cols, w[n] otherwise
+// ([n_out][k_dim] bf16; w_out may be w).
+hipError_t launch_merge_lora(const uint16_t* w, int n_out, int k_dim, const uint16_t* a, const uint16_t* b, int rank,
+                             float scale, int lora_cols, uint16_t* w_out, hipStream_t stream);
 
 // out[t] = table[ids[t]] (rows of dim bf16 elements; ids in range).
 hipError_t launch_embed_rows(const uint16_t* table, const int32_t* ids, int n_tok, int dim, uint16_t* out,

@@ -49,6 +49,10 @@ def test_null_context_is_an_error_not_a_crash():
     assert lib.attuner_assemble_table(None, 0, None, None, None, None, None, None, 0, None) == -1
     assert lib.attuner_gather_layers(None, None, 0, 0, 1, None, 0, None) == -1
     assert lib.attuner_embed(None, 1, None, None, 8, None, None) == -1
+    assert lib.attuner_host_pool_create(None, 4) == -1
+    assert lib.attuner_merge_lora(None, None, 64, 64, None, None, 0, 0.0, 0, None, None) == -1
+    assert lib.attuner_store_artifact_host(None, 4, None, None, None, C.byref(out)) == -1
+    assert lib.attuner_host_pool_info(None, None, None) == -1
     assert lib.attuner_assemble_segments_plan(None, 0, None, None, None, None, None) == -1
     assert lib.attuner_assemble_segments(None, 0, None, None, None, None, None, None, 0, None) == -1
     assert lib.attuner_span_attn(None, 0, 1, None, None, None, None, None, 0, None, None, 0, None, None, None, 0, None,

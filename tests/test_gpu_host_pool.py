@@ -1,0 +1,160 @@
+"""Artifact caches kept in CPU RAM (the pinned host pool): assembly gathers
+host pages over the host link into the request cache, bit-exact against the
+oracle's assembly, mixed with HBM-pool artifacts, all layers at once and
+layer by layer, and in an interleaved prompt; pages are reused after a
+release."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from tests._gpu import dev_bf16
+    from paper_2609_36722_amd.api import AttunerError, Context, ModelCfg, bf16_to_host
+    from paper_2609_36722_amd._lib import HOST_PAGE_FLAG
+
+
+def _say(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def _store_mixed(ctx, rng, lengths, host_set, n_layers):
+    art_k, art_v, ids = {}, {}, {}
+    for a, L in enumerate(lengths):
+        k = rng.integers(0, 2 ** 16, size=(n_layers, 8, L, 128), dtype=np.uint16)
+        v = rng.integers(0, 2 ** 16, size=(n_layers, 8, L, 128), dtype=np.uint16)
+        store = ctx.store_artifact_host if a in host_set else ctx.store_artifact
+        ids[a] = store(dev_bf16(k), dev_bf16(v))
+        art_k[a], art_v[a] = k.transpose(0, 2, 1, 3), v.transpose(0, 2, 1, 3)   # [layers][L][Hkv][d]
+    return art_k, art_v, ids
+
+
+def test_host_pool_assembly_bit_exact():
+    _say("host pool assembly")
+    rng = np.random.default_rng(81)
+    lengths = [17, 40, 1, 33, 300]
+    host = {1, 2, 4}
+    with Context(ModelCfg(n_layers=3, hidden=256), pool_pages=8) as ctx:
+        ctx.host_pool_create(40)
+        art_k, art_v, ids = _store_mixed(ctx, rng, lengths, host, 3)
+        assert ctx.host_pool_info() == (40, 40 - 3 - 1 - 19)
+        for a in host:
+            pages, _ = ctx.artifact_pages(ids[a])
+            assert all(p & HOST_PAGE_FLAG for p in pages)
+        reqs = [([1, 0, 4], 5), ([], 3), ([2, 2, 3, 1], 0)]
+        requests, caps = [[ids[a] for a in r] for r, _ in reqs], [c for _, c in reqs]
+        ne, rows = ctx.assemble_plan(requests, caps)
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        kv = torch.zeros(3 * 2 * 8 * rows * 128, dtype=torch.bfloat16, device="cuda")
+        cu, al = ctx.assemble_kv(requests, caps, bt, kv, rows)
+        torch.cuda.synchronize()
+        entries, cu2 = oracle.block_table(lengths, reqs, 16)
+        phys = {a: ctx.artifact_pages(ids[a])[0] for a in ids}
+        want = np.array([[phys[a][p], nv, dst, r] for a, p, nv, r, dst in entries.tolist()], np.int32).reshape(-1, 4)
+        assert np.array_equal(bt.cpu().numpy().reshape(-1, 4), want)
+        cache, _ = oracle.assemble(art_k, art_v, reqs, 8, 128)
+        got = bf16_to_host(kv).reshape(3, 2, 8, rows, 128)
+        for r in range(len(reqs)):
+            lo, n = cu[r], al[r]
+            assert np.array_equal(got[:, :, :, lo:lo + n], cache[:, :, :, lo:lo + n]), f"request {r}"
+        # layer by layer on a second stream, from the same table
+        kv2 = torch.zeros_like(kv)
+        cu3, al3 = ctx.assemble_table(requests, caps, bt, rows)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        for l in (2, 0, 1):
+            ctx.gather_layers(bt, ne, l, 1, kv2, rows, stream=side)
+        torch.cuda.synchronize()
+        got2 = bf16_to_host(kv2).reshape(3, 2, 8, rows, 128)
+        for r in range(len(reqs)):
+            lo, n = cu[r], al[r]
+            assert np.array_equal(got2[:, :, :, lo:lo + n], cache[:, :, :, lo:lo + n]), f"request {r} per layer"
+        # release a host artifact and reuse its pages for a new one
+        ctx.release_artifact(ids[4])
+        assert ctx.host_pool_info()[1] == 40 - 3 - 1
+        k = rng.integers(0, 2 ** 16, size=(3, 8, 200, 128), dtype=np.uint16)
+        nid = ctx.store_artifact_host(dev_bf16(k), dev_bf16(k))
+        ne, rows = ctx.assemble_plan([[nid]], [0])
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        kv = torch.zeros(3 * 2 * 8 * rows * 128, dtype=torch.bfloat16, device="cuda")
+        ctx.assemble_kv([[nid]], [0], bt, kv, rows)
+        torch.cuda.synchronize()
+        got = bf16_to_host(kv).reshape(3, 2, 8, rows, 128)
+        assert np.array_equal(got[:, 0], k) and np.array_equal(got[:, 1], k)
+
+
+def test_host_pool_segments_and_errors():
+    _say("host pool segments + errors")
+    rng = np.random.default_rng(82)
+    lengths = [50, 20]
+    with Context(ModelCfg(n_layers=2, hidden=256), pool_pages=4) as ctx:
+        with pytest.raises(AttunerError) as e:
+            ctx.store_artifact_host(torch.zeros(2, 8, 4, 128, dtype=torch.bfloat16, device="cuda"),
+                                    torch.zeros(2, 8, 4, 128, dtype=torch.bfloat16, device="cuda"))
+        assert e.value.status == -1                 # no host pool yet
+        ctx.host_pool_create(8)
+        with pytest.raises(AttunerError) as e:
+            ctx.host_pool_create(8)                 # a second one
+        assert e.value.status == -1
+        art_k, art_v, ids = _store_mixed(ctx, rng, lengths, {0}, 2)
+        with pytest.raises(AttunerError) as e:
+            ctx.store_artifact_host(torch.zeros(2, 8, 100, 128, dtype=torch.bfloat16, device="cuda"),
+                                    torch.zeros(2, 8, 100, 128, dtype=torch.bfloat16, device="cuda"))
+        assert e.value.status == -2                 # host pool full (7 pages needed, 4 free)
+        prompts = [[-3, 0, -2, 1, -4]]
+        segs = [[ids[s] if s >= 0 else s for s in p] for p in prompts]
+        ne, rows, ns = ctx.assemble_segments_plan(segs)
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        kv = torch.zeros(2 * 2 * 8 * rows * 128, dtype=torch.bfloat16, device="cuda")
+        cu, spans = ctx.assemble_segments(segs, bt, kv, rows)
+        torch.cuda.synchronize()
+        e2, _, _ = oracle.block_table_segments(lengths, prompts, 16)
+        got = bf16_to_host(kv).reshape(2, 2, 8, rows, 128)
+        for a_idx, p, nv, r, dst in e2.tolist():
+            src = slice(16 * p, 16 * p + nv)
+            assert np.array_equal(got[:, 0, :, dst:dst + nv], art_k[a_idx][:, src].transpose(0, 2, 1, 3))
+            assert np.array_equal(got[:, 1, :, dst:dst + nv], art_v[a_idx][:, src].transpose(0, 2, 1, 3))
+
+
+# ----------------------------------------------------------------------------
+# merged deployment: W_Q + s B A, then the rank-0 projection
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("rank,H", [(16, 2560), (5, 512), (64, 256)])
+def test_merge_lora_then_rank0_projection(rank, H):
+    _say(f"merge lora r={rank} H={H}")
+    import math
+    import synthdata as sd
+    from tests._gpu import host_f64
+    from tests._tol import assert_intermediate_close
+    rng = np.random.default_rng(90 + rank)
+    N, lora_cols, T = 6144, 4096, 37
+    f = lambda *s_, std=1.0: sd.f32_to_bf16_bits(rng.standard_normal(s_).astype(np.float32) * np.float32(std))
+    w, a, b, x = f(N, H, std=0.02), f(rank, H, std=1 / math.sqrt(H)), f(lora_cols, rank, std=0.3), f(T, H)
+    scale = 16.0 / rank
+    d = oracle.decode_bf16
+    with Context(ModelCfg(n_layers=1, hidden=H), pool_pages=0) as ctx:
+        wm = torch.empty(N, H, dtype=torch.bfloat16, device="cuda")
+        ctx.merge_lora(dev_bf16(w), dev_bf16(a), dev_bf16(b), rank, scale, lora_cols, wm)
+        out = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+        ctx.qproj_lora(dev_bf16(x), wm, None, None, 0, 0.0, 0, out)
+        torch.cuda.synchronize()
+        got_w = host_f64(wm)
+        got = host_f64(out)
+    ref_w = oracle.merge_lora(d(w), d(a), d(b), scale, lora_cols)
+    # one bf16 rounding of a value summed in fp32: one unit in the last place
+    # of the exact value, plus the fp32 sum's own error ((rank + 2) roundings
+    # of at most 2^-24 of the magnitudes involved), which a cancellation
+    # (w + update ~ 0) can make the larger of the two
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref_w), 1e-30))) - 7)
+    mag = np.abs(d(w))
+    mag[:lora_cols] += abs(scale) * (np.abs(d(b)) @ np.abs(d(a)))
+    bound = ulp + (rank + 2) * 2.0 ** -24 * mag
+    assert np.all(np.abs(got_w - ref_w) <= bound), "merged weights beyond one bf16 rounding of the fp32 sum"
+    assert np.array_equal(bf16_to_host(wm)[lora_cols:], w[lora_cols:]), "k/v rows must be copied unchanged"
+    ref = oracle.qproj_lora(d(x), d(w), d(a), d(b), scale, lora_cols)
+    assert_intermediate_close(got, ref, "merged projection")

@@ -708,3 +708,19 @@ def test_interleaved_causality_and_leading_token():
     # the first online token sees only its own key: O = its value (GQA repeat)
     G = heads[0] // heads[1]
     assert np.max(np.abs(base["o"][0] - np.repeat(base["v"][0], G, axis=0))) <= 1e-12
+
+
+def test_merge_lora_equals_the_unmerged_projection():
+    # merged deployment (W_Q + s B A) against the adapter applied on the fly,
+    # and the k/v rows untouched
+    rng = np.random.default_rng(91)
+    x, w = rng.standard_normal((5, 24)), rng.standard_normal((40, 24))
+    a, b = rng.standard_normal((3, 24)), rng.standard_normal((32, 3))
+    wm = oracle.merge_lora(w, a, b, 0.37, 32)
+    assert np.array_equal(wm[32:], w[32:])
+    got = oracle.qproj_lora(x, wm)
+    want = oracle.qproj_lora(x, w, a, b, 0.37, 32)
+    assert np.max(np.abs(got - want)) <= 1e-12
+    # element (n, k) of the update by a plain loop
+    n, k = 7, 11
+    assert abs(wm[n, k] - w[n, k] - 0.37 * sum(b[n, j] * a[j, k] for j in range(3))) <= 1e-14
