@@ -215,6 +215,7 @@ struct attuner_ctx {
   DeviceBuf ws_part;    // split-KV partials
   DeviceBuf ws_qkv;     // full prefill: fused projection output
   DeviceBuf ws_logits;  // LM-head logits (fp32)
+  DeviceBuf ws_split;   // key-split partials of a plain product (fp32)
   DeviceBuf ws_rows;    // token ids of an embedding lookup / rows of a row-subset RMSNorm
   DeviceBuf rope;       // (cos, sin) table [rope_pos][64]
   int64_t rope_pos = 0;
@@ -610,6 +611,7 @@ void attuner_destroy(attuner_ctx* c) {
   c->ws_part.release();
   c->ws_qkv.release();
   c->ws_logits.release();
+  c->ws_split.release();
   c->ws_rows.release();
   c->rope.release();
   if (g_tracer == &c->tracer) g_tracer = nullptr;
@@ -1020,6 +1022,21 @@ static attuner_status check_gemm_args(int32_t n_tok, const void* x, int32_t k_di
   return ATTUNER_OK;
 }
 
+// A plain product with epilogue epi: plans tile and key split, grows the
+// split workspace when the plan splits the k range.
+static attuner_status run_gemm(attuner_ctx* c, int32_t n_tok, const void* x, int32_t k_dim, const void* w,
+                               int32_t n_out, GemmEpi epi, void* out, hipStream_t s) {
+  const GemmPlan plan = plan_gemm(n_tok, n_out, k_dim, false);
+  float* ws = nullptr;
+  if (n_tok > kGemvMaxTok && plan.n_split > 1) {
+    HIP_TRY(c->ws_split.ensure((size_t)plan.n_split * n_tok * n_out * sizeof(float)));
+    ws = static_cast<float*>(c->ws_split.ptr);
+  }
+  HIP_TRY(launch_gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), n_tok, n_out, k_dim, epi,
+                      static_cast<uint16_t*>(out), plan, ws, s));
+  return ATTUNER_OK;
+}
+
 attuner_status attuner_linear(attuner_ctx* c, int32_t n_tok, const void* x, int32_t k_dim, const void* w,
                               int32_t n_out, const void* residual, void* out, void* stream) {
   if (!c) return fail(ATTUNER_EINVAL, "null ctx");
@@ -1029,9 +1046,7 @@ attuner_status attuner_linear(attuner_ctx* c, int32_t n_tok, const void* x, int3
   if (n_tok == 0) return ATTUNER_OK;
   DeviceGuard dg(c->device);
   const GemmEpi epi{residual ? kEpiResidual : kEpiBf16, static_cast<const uint16_t*>(residual), nullptr};
-  HIP_TRY(launch_gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), n_tok, n_out, k_dim, epi,
-                      static_cast<uint16_t*>(out), static_cast<hipStream_t>(stream)));
-  return ATTUNER_OK;
+  return run_gemm(c, n_tok, x, k_dim, w, n_out, epi, out, static_cast<hipStream_t>(stream));
 }
 
 attuner_status attuner_gate_up_swiglu(attuner_ctx* c, int32_t n_tok, const void* x, int32_t k_dim, const void* w_gu,
@@ -1042,10 +1057,8 @@ attuner_status attuner_gate_up_swiglu(attuner_ctx* c, int32_t n_tok, const void*
   if (st != ATTUNER_OK) return st;
   if (n_tok == 0) return ATTUNER_OK;
   DeviceGuard dg(c->device);
-  HIP_TRY(launch_gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_gu), n_tok, 2 * n_inter, k_dim,
-                      GemmEpi{kEpiSwiglu, nullptr, nullptr}, static_cast<uint16_t*>(out),
-                      static_cast<hipStream_t>(stream)));
-  return ATTUNER_OK;
+  return run_gemm(c, n_tok, x, k_dim, w_gu, 2 * n_inter, GemmEpi{kEpiSwiglu, nullptr, nullptr}, out,
+                  static_cast<hipStream_t>(stream));
 }
 
 attuner_status attuner_lm_head_argmax(attuner_ctx* c, int32_t n_rows, const void* x, const void* w_lm, int32_t vocab,
@@ -1061,8 +1074,8 @@ attuner_status attuner_lm_head_argmax(attuner_ctx* c, int32_t n_rows, const void
   hipStream_t s = static_cast<hipStream_t>(stream);
   HIP_TRY(c->ws_logits.ensure((size_t)n_rows * vocab * sizeof(float)));
   float* logits = static_cast<float*>(c->ws_logits.ptr);
-  HIP_TRY(launch_gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_lm), n_rows, vocab, H,
-                      GemmEpi{kEpiF32, nullptr, logits}, nullptr, s));
+  st = run_gemm(c, n_rows, x, H, w_lm, vocab, GemmEpi{kEpiF32, nullptr, logits}, nullptr, s);
+  if (st != ATTUNER_OK) return st;
   HIP_TRY(launch_argmax_rows(logits, n_rows, vocab, ids, max_logit, s));
   return ATTUNER_OK;
 }

@@ -23,6 +23,8 @@
 
 #include <type_traits>
 
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -163,7 +165,7 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
                                                                    const bf16_t* __restrict__ b, int rank, int r_pad,
                                                                    int lora_cols, const float* __restrict__ t_part,
                                                                    int n_slice, GemmEpi epi, bf16_t* out, int n_mt,
-                                                                   int n_nt) {
+                                                                   int n_nt, int kt_split) {
   constexpr int NW = WN * WM;
   constexpr int TN = BN / WN, TM = BM / WM;
   constexpr int FN = TN / 32, FM = TM / 32;
@@ -181,9 +183,13 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
   // share operand panels in its L2.  The order walks groups of kGroupM token
   // tiles across all feature tiles, token tile fastest: 32 concurrent
   // workgroups cover about kGroupM x 8 tiles (kGroupM x-panels, 8 W-panels).
+  // Split-K (kt_split > 0): workgroup blockIdx.x / total takes k-tiles
+  // [split * kt_split, (split + 1) * kt_split) of tile blockIdx.x % total and
+  // writes its fp32 partial to slice `split` of epi.out_f32.
   const int total = n_mt * n_nt;
   const int per_xcd = total >> 3;
-  int lin = blockIdx.x;
+  const int split = kt_split > 0 ? (int)blockIdx.x / total : 0;
+  int lin = kt_split > 0 ? (int)blockIdx.x % total : (int)blockIdx.x;
   if (lin < 8 * per_xcd) lin = (lin & 7) * per_xcd + (lin >> 3);
   const int in_group = kGroupM * n_nt;
   const int first_m = (lin / in_group) * kGroupM;
@@ -199,7 +205,8 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
   const int wm = wave % WM;
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int n_kt = K / BK;
+  const int kt0 = split * kt_split;
+  const int n_kt = kt_split > 0 ? min(K / BK - kt0, kt_split) : K / BK;
   const uint32_t lds0 = lds_addr(lds);
 
   f32x16 acc[FN][FM];
@@ -241,7 +248,7 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
         // A rows past rank repeat row rank - 1: finite, and met by zero B columns
         base = a + (int64_t)min(row - BN - BM, rank - 1) * K;
       }
-      src[j] = base + 8 * lg;
+      src[j] = base + 8 * lg + (int64_t)kt0 * BK;
       doff[j] = 1024u * blk;
     }
 #pragma unroll
@@ -318,6 +325,7 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
     kloop(std::integral_constant<bool, false>{});
   }
 
+  if (kt_split > 0) epi.out_f32 += (int64_t)split * M * N;
   lora_epilogue_store<FN, FM>(acc, n0 + wn * TN, m0 + wm * TM, wm * TM, l32, hi, M, N, b, rank, r_pad, lora_cols,
                               t_part, n_slice, t_lds, epi, out);
 }
@@ -388,41 +396,55 @@ hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int
 
 namespace {
 
-hipError_t launch_gemm_any(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden, const uint16_t* a,
-                           float scale, const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
-                           GemmEpi epi, uint16_t* out, hipStream_t stream) {
-  if (n_tok == 0) return hipSuccess;
-  if (n_tok <= kGemvMaxTok) return launch_gemv(x, w, n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, epi, out,
-                                              stream);
-  const int n_slice = lora_down_slices(hidden);
-  // Tile choice.  One workgroup per CU at a time, and a workgroup's k-loop
-  // runs at the CU's operand ingest rate, so a launch takes about
-  // ceil(workgroups / 256) rounds of (BM + BN) * hidden * 2 ingested bytes.
-  // Pick the tile (tokens x features) that minimises rounds * (BM + BN);
-  // ties go to the earlier entry.  Measured on gfx950 with 6144 outputs and
-  // hidden 2560 / 4096 this picks the fastest tile at T = 64 (64x64), 256
-  // (64x96), 512 (128x96), 1024 (256x96) and 8448 (256x256).
-  struct Tile {
-    int bm, bn;
-  };
-  constexpr Tile kTiles[] = {{256, 256}, {128, 256}, {256, 96}, {128, 128}, {128, 96}, {64, 96}, {64, 64}};
-  int best = -1;
-  int64_t best_cost = 0;
-  for (int i = 0; i < (int)(sizeof(kTiles) / sizeof(kTiles[0])); ++i) {
-    if (n_out % kTiles[i].bn != 0) continue;
-    const int64_t wgs = (int64_t)((n_tok + kTiles[i].bm - 1) / kTiles[i].bm) * (n_out / kTiles[i].bn);
-    const int64_t cost = (wgs + 255) / 256 * (kTiles[i].bm + kTiles[i].bn);
-    if (best < 0 || cost < best_cost) {
-      best = i;
-      best_cost = cost;
-    }
+// Sum of the n_split fp32 partials [n_split][M][N] and the epilogue of epi
+// (thread = 4 consecutive outputs of one token).
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int n_split, int M, int N,
+                                                            GemmEpi epi, bf16_t* out) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;  // quad index
+  if (q >= (int64_t)M * N / 4) return;
+  const int64_t m = q / (N / 4);
+  const int n = (int)(q % (N / 4)) * 4;
+  const int64_t plane = (int64_t)M * N;
+  f32x4 c = *reinterpret_cast<const f32x4*>(part + m * N + n);
+  for (int s = 1; s < n_split; ++s) c += *reinterpret_cast<const f32x4*>(part + s * plane + m * N + n);
+  if (epi.mode == kEpiF32) {
+    *reinterpret_cast<f32x4*>(epi.out_f32 + m * N + n) = c;
+    return;
   }
-#define ATTUNER_GEMM(BM_, BN_, WN_, WM_, NST_)                                                               \
-  ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, WM_, NST_>),                           \
-                 dim3(((n_tok + (BM_) - 1) / (BM_)) * (n_out / (BN_))), dim3(64 * (WN_) * (WM_)), stream, x, w, \
-                 n_tok, n_out, hidden, a, scale, b, rank, r_pad, lora_cols, t_part, n_slice, epi, out,             \
-                 (n_tok + (BM_) - 1) / (BM_), n_out / (BN_))
-  switch (best) {
+  if (epi.mode == kEpiSwiglu) {
+    const float s0 = c[0] / (1.0f + __expf(-c[0])) * c[1];
+    const float s1 = c[2] / (1.0f + __expf(-c[2])) * c[3];
+    *reinterpret_cast<uint32_t*>(out + m * (N / 2) + n / 2) = pack_bf16x2(s0, s1);
+    return;
+  }
+  if (epi.mode == kEpiResidual) {
+    const u32x2 r = *reinterpret_cast<const u32x2*>(epi.residual + m * N + n);
+    c[0] += __uint_as_float(r[0] << 16);
+    c[1] += __uint_as_float(r[0] & 0xFFFF0000u);
+    c[2] += __uint_as_float(r[1] << 16);
+    c[3] += __uint_as_float(r[1] & 0xFFFF0000u);
+  }
+  u32x2 pk;
+  pk[0] = pack_bf16x2(c[0], c[1]);
+  pk[1] = pack_bf16x2(c[2], c[3]);
+  *reinterpret_cast<u32x2*>(out + m * N + n) = pk;
+}
+
+struct Tile {
+  int bm, bn;
+};
+constexpr Tile kTiles[] = {{256, 256}, {128, 256}, {256, 96}, {128, 128}, {128, 96}, {64, 96}, {64, 64}};
+constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
+
+hipError_t launch_tile(int tile, int kt_split, int grid, const uint16_t* x, const uint16_t* w, int n_tok, int n_out,
+                       int hidden, const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad,
+                       int lora_cols, const float* t_part, int n_slice, GemmEpi epi, uint16_t* out,
+                       hipStream_t stream) {
+#define ATTUNER_GEMM(BM_, BN_, WN_, WM_, NST_)                                                                 \
+  ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, WM_, NST_>), dim3((unsigned)grid),     \
+                 dim3(64 * (WN_) * (WM_)), stream, x, w, n_tok, n_out, hidden, a, scale, b, rank, r_pad,       \
+                 lora_cols, t_part, n_slice, epi, out, (n_tok + (BM_) - 1) / (BM_), n_out / (BN_), kt_split)
+  switch (tile) {
     case 0: ATTUNER_GEMM(256, 256, 4, 2, 2); break;
     case 1: ATTUNER_GEMM(128, 256, 4, 2, 3); break;
     case 2: ATTUNER_GEMM(256, 96, 3, 4, 3); break;
@@ -438,16 +460,92 @@ hipError_t launch_gemm_any(const uint16_t* x, const uint16_t* w, int n_tok, int 
 
 }  // namespace
 
+// Tile and key split of a product, by a model fitted to gfx950 runs.  One
+// workgroup per CU at a time; a workgroup's time is the larger of its operand
+// ingest ((BM + BN) * k-range * 2 bytes at about 52 GB/s per CU, 42 GB/s for
+// the 256 x 256 tile whose ring holds only two k-tiles) and its MFMA work
+// (2 BM BN k-range at about 6 TFLOP/s per CU); a launch takes ceil(workgroups
+// / 256) such rounds plus a fixed 4 us.  Without a low-rank term, and when a
+// tile's workgroups would leave CUs idle, the k range may be split across
+// workgroups: shorter k-loops, paid for by the fp32 partials (split * M * N *
+// 8 bytes written and read at about 4 TB/s) and a 3 us reduce launch.  The
+// plan minimises the model; ties go to the earlier tile and to no split.  On
+// gfx950 it picks the measured fastest plan for the q/k/v projection (6144
+// outputs, hidden 2560 / 4096) at T = 64 (64x64), 256 (64x96), 512 (128x96),
+// 1024 (256x96) and 8448 (256x256), and for the o/gate-up/down products of
+// the 4B and 8B layers at 256 and 1024 tokens (e.g. down at 256 tokens:
+// 128x128 in 6 splits, 28.9 us against 46.5 us unsplit).
+GemmPlan plan_gemm(int n_tok, int n_out, int k_dim, bool lora) {
+  constexpr double kIngest = 52e9, kIngest256 = 42e9, kMfmaPerCu = 6e12, kFixed = 4e-6;
+  constexpr double kPartBw = 4e12, kReduceLaunch = 3e-6;
+  constexpr int kSplits[] = {1, 2, 3, 4, 6, 8, 12, 16};
+  const int n_kt = k_dim / BK;
+  GemmPlan best{-1, 1, 0};
+  double best_t = 0.0;
+  for (int i = 0; i < kNumTiles; ++i) {
+    if (n_out % kTiles[i].bn != 0) continue;
+    const int64_t tiles = (int64_t)((n_tok + kTiles[i].bm - 1) / kTiles[i].bm) * (n_out / kTiles[i].bn);
+    const double rate = i == 0 ? kIngest256 : kIngest;
+    for (int s : kSplits) {
+      // splits only add workgroups where the tiles alone leave CUs idle
+      if (s > 1 && (lora || n_kt < 4 * s || tiles >= 256)) break;
+      const int kts = (n_kt + s - 1) / s;
+      const int used = (n_kt + kts - 1) / kts;  // splits that hold k-tiles
+      const int64_t wgs = tiles * used;
+      const double k_range = (double)kts * BK;
+      const double per_wg = std::max((kTiles[i].bm + kTiles[i].bn) * k_range * 2 / rate,
+                                     2.0 * kTiles[i].bm * kTiles[i].bn * k_range / kMfmaPerCu);
+      double t = (double)((wgs + 255) / 256) * per_wg + kFixed;
+      if (used > 1) t += (double)used * n_tok * n_out * 8 / kPartBw + kReduceLaunch;
+      if (best.tile < 0 || t < best_t * (1.0 - 1e-9)) {
+        best = GemmPlan{i, used, used > 1 ? kts : 0};
+        best_t = t;
+      }
+    }
+  }
+  return best;
+}
+
+namespace {
+
+hipError_t launch_gemm_any(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden, const uint16_t* a,
+                           float scale, const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
+                           GemmEpi epi, uint16_t* out, const GemmPlan* plan, float* split_ws, hipStream_t stream) {
+  if (n_tok == 0) return hipSuccess;
+  if (n_tok <= kGemvMaxTok) return launch_gemv(x, w, n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, epi, out,
+                                              stream);
+  const int n_slice = lora_down_slices(hidden);
+  const GemmPlan pl = plan ? *plan : plan_gemm(n_tok, n_out, hidden, r_pad > 0);
+  if (pl.tile < 0) return hipErrorInvalidValue;
+  const int tiles = ((n_tok + kTiles[pl.tile].bm - 1) / kTiles[pl.tile].bm) * (n_out / kTiles[pl.tile].bn);
+  if (pl.n_split <= 1)
+    return launch_tile(pl.tile, 0, tiles, x, w, n_tok, n_out, hidden, a, scale, b, rank, r_pad, lora_cols, t_part,
+                       n_slice, epi, out, stream);
+  if (split_ws == nullptr || r_pad > 0) return hipErrorInvalidValue;
+  const GemmEpi part{kEpiF32, nullptr, split_ws};
+  hipError_t e = launch_tile(pl.tile, pl.kt_split, tiles * pl.n_split, x, w, n_tok, n_out, hidden, nullptr, 0.f,
+                             nullptr, 0, 0, 0, nullptr, n_slice, part, nullptr, stream);
+  if (e != hipSuccess) return e;
+  const int64_t quads = (int64_t)n_tok * n_out / 4;
+  ATTUNER_LAUNCH("splitk_reduce_kernel", splitk_reduce_kernel, dim3((unsigned)((quads + 255) / 256)), dim3(256), stream,
+                 split_ws, pl.n_split, n_tok, n_out, epi, out);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
                             const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad, int lora_cols,
                             const float* t_part, uint16_t* out, hipStream_t stream) {
+  const GemmPlan pl = plan_gemm(n_tok, n_out, hidden, true);  // no key split here
   return launch_gemm_any(x, w, n_tok, n_out, hidden, a, scale, b, rank, r_pad, lora_cols, t_part,
-                         GemmEpi{kEpiBf16, nullptr, nullptr}, out, stream);
+                         GemmEpi{kEpiBf16, nullptr, nullptr}, out, &pl, nullptr, stream);
 }
 
 hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, GemmEpi epi,
-                       uint16_t* out, hipStream_t stream) {
-  return launch_gemm_any(x, w, n_tok, n_out, k_dim, nullptr, 0.f, nullptr, 0, 0, 0, nullptr, epi, out, stream);
+                       uint16_t* out, const GemmPlan& plan, float* split_ws, hipStream_t stream) {
+  return launch_gemm_any(x, w, n_tok, n_out, k_dim, nullptr, 0.f, nullptr, 0, 0, 0, nullptr, epi, out, &plan,
+                         split_ws, stream);
 }
 
 }  // namespace attuner

@@ -76,8 +76,18 @@ struct GemmEpi {
   const uint16_t* residual;
   float* out_f32;
 };
+// Tile (index into the launcher's tile list) and key split of a product:
+// n_split > 1 splits the k range into chunks of kt_split 64-wide k-tiles and
+// needs a workspace of n_split * n_tok * n_out floats (never with a low-rank
+// term).  plan_gemm picks both by the ingest cost model.
+struct GemmPlan {
+  int tile;
+  int n_split;
+  int kt_split;
+};
+GemmPlan plan_gemm(int n_tok, int n_out, int k_dim, bool lora);
 hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, GemmEpi epi,
-                       uint16_t* out, hipStream_t stream);
+                       uint16_t* out, const GemmPlan& plan, float* split_ws, hipStream_t stream);
 
 // The same product for at most kGemvMaxTok tokens as a weight-streaming
 // GEMV (any mode; the low-rank term needs t_part from launch_lora_down);
