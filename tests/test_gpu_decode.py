@@ -157,3 +157,10 @@ def test_decode_capacity_error():
                             q[:, HQ * D + HKV * D:], ld, g, g, kv, 8, torch.empty(1, HQ, D, dtype=torch.bfloat16,
                                                                                   device="cuda"))
         assert e.value.status == -1
+
+
+def test_decode_c5_context_one_request():
+    # the c5 request's context: 32 x 1024 artifact keys + 1024 suffix keys, then the new token
+    _say("decode c5 context")
+    got, ref = _run_decode(46, [1024] * 32, [(tuple(range(32)), 1024)])
+    assert_o_close(got, ref)

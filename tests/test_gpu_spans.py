@@ -125,3 +125,63 @@ def test_span_errors():
                           q[:, (HQ + HKV) * D:], ld, g, g, kv, 10, torch.empty(4, HQ, D, dtype=torch.bfloat16,
                                                                                  device="cuda"))
         assert e.value.status == -1
+
+
+def test_interleaved_c2_prompt():
+    # the c2 request with online text around its artifacts (a 32-token system
+    # span, 8 tokens between consecutive artifacts, the 256-token suffix), as
+    # bench.py --spans 8 times it, in its launch plan; every online row's O
+    # against the oracle (a few seconds of fp64)
+    _say("interleaved c2 prompt")
+    rng = np.random.default_rng(77)
+    H, rank, scale, layer = 2560, 16, 1.0, 0
+    lengths = [1024] * 8
+    prompt = [-32]
+    for j in range(8):
+        if j:
+            prompt.append(-8)
+        prompt.append(j)
+    prompt.append(-256)
+    with Context(ModelCfg(n_layers=1, hidden=H), pool_pages=8 * 64) as ctx:
+        art_k, art_v, ids = {}, {}, {}
+        for a, L in enumerate(lengths):
+            k, v = _bits(rng, (1, HKV, L, D)), _bits(rng, (1, HKV, L, D))
+            ids[a] = ctx.store_artifact(dev_bf16(k), dev_bf16(v))
+            art_k[a], art_v[a] = k, v
+        segs = [[ids[s] if s >= 0 else s for s in prompt]]
+        ne, rows, ns = ctx.assemble_segments_plan(segs)
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        kv = torch.zeros(2 * HKV * rows * D, dtype=torch.bfloat16, device="cuda")
+        cu, spans = ctx.assemble_segments(segs, bt, kv, rows)
+        n_on = sum(l for _, _, l in spans)
+        x = _bits(rng, (n_on, H))
+        wq, wk, wv = _bits(rng, (HQ * D, H), 0.02), _bits(rng, (HKV * D, H), 0.02), _bits(rng, (HKV * D, H), 0.02)
+        a, b = _bits(rng, (rank, H), 1 / math.sqrt(H)), _bits(rng, (HQ * D, rank), 0.01)
+        g1 = sd.f32_to_bf16_bits(np.ones(D, np.float32))
+        n_out = (HQ + 2 * HKV) * D
+        qkv = torch.empty(n_on, n_out, dtype=torch.bfloat16, device="cuda")
+        ctx.qproj_lora(dev_bf16(x), dev_bf16(np.concatenate([wq, wk, wv])), dev_bf16(a), dev_bf16(b), rank, scale,
+                       HQ * D, qkv)
+        cu_q = [0]
+        for _, _, l in spans:
+            cu_q.append(cu_q[-1] + l)
+        o = torch.empty(n_on, HQ, D, dtype=torch.bfloat16, device="cuda")
+        ctx.span_attn(layer, cu_q, [cu[r] for r, _, _ in spans], [off for _, off, _ in spans], None,
+                      qkv[:, :HQ * D], n_out, qkv[:, HQ * D:(HQ + HKV) * D], qkv[:, (HQ + HKV) * D:], n_out,
+                      dev_bf16(g1), dev_bf16(g1), kv, rows, o)
+        torch.cuda.synchronize()
+        got_o = host_f64(o)
+        cache = bf16_to_host(kv).reshape(1, 2, HKV, rows, D)
+    d = oracle.decode_bf16
+    ak = {i: d(art_k[i][0]).transpose(1, 0, 2) for i in range(8)}
+    av = {i: d(art_v[i][0]).transpose(1, 0, 2) for i in range(8)}
+    ref = oracle.interleaved_layer(prompt, d(x), d(wq), d(wk), d(wv), d(a), d(b), scale, d(g1), d(g1), ak, av,
+                                   HQ, HKV, 1e6, 1e-6)
+    assert_o_close(got_o, ref["o"], "O")
+    t0 = 0
+    for _, _, l in spans:
+        assert_o_close_per_request(got_o[t0:t0 + l], ref["o"][t0:t0 + l], f"span at row {t0}")
+        t0 += l
+    # cached rows of the first and last artifact stayed put
+    for j, off in ((0, 32), (7, 32 + 7 * (1024 + 8))):
+        assert np.array_equal(cache[0, 0, :, off:off + 1024], art_k[j][0]), f"artifact {j} keys"
