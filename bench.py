@@ -817,11 +817,17 @@ def decode_main(args):
     ctx_len = [art_len[r] + wl.requests[r].suffix_len for r in range(n_req)]
     torch.cuda.synchronize()
 
+    if args.merged:   # the deployment form: W_q + s B A once, then the rank-0 projection
+        for l in range(NL):
+            ctx.merge_lora(wqkv[l], a_l[l], b_l[l], wl.rank, wl.scale, nq, wqkv[l])
+        torch.cuda.synchronize()
+    step_rank = 0 if args.merged else wl.rank
+
     def layer_loop(mark=None):
         for l in range(NL):
             if mark:
                 mark("qkv_proj")
-            ctx.qproj_lora(x_new, wqkv[l], a_l[l], b_l[l], wl.rank, wl.scale, nq, qkv[l])
+            ctx.qproj_lora(x_new, wqkv[l], a_l[l], b_l[l], step_rank, wl.scale, nq, qkv[l])
             if mark:
                 mark("decode_attn")
             q = qkv[l]
@@ -906,6 +912,7 @@ def decode_main(args):
         "data": "synthetic (seeded device-side N(0,1) / N(0,0.02) bf16 draws, distinct weights per layer)",
         "config": {"workload": wl.name + "+decode", "layers": NL, "hidden": H, "requests": n_req,
                    "keys_per_request": n_keys, "lora_rank": wl.rank},
+        "adapter": "merged into W_q (rank-0 projection)" if args.merged else "unmerged (LoRA down-projection + GEMV)",
         "layer_loop": "hip_graph" if graph is not None else "eager",
         "roofline": {"bound": "hbm", "kernel": "decode_attention_kernel", "achieved": round(attn_gbps, 1),
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(attn_gbps / PEAK_HBM_GBPS, 4),

@@ -7,8 +7,9 @@
 // whole 128-byte lines) and of every token's x, accumulate bf16 dot2
 // products in fp32, and the rows' sums meet in a wave reduction.  The
 // low-rank term (rows below lora_cols) enters before the reduction: lane j
-// adds t[token][j] * B[row][j], t = scale * x A^T summed from the slice
-// partials of the down-projection kernel.  Lane t then stores token t.
+// adds t[token][j] * B[row][j], t = scale * x A^T summed once per workgroup
+// (into LDS) from the slice partials of the down-projection kernel.  Lane t
+// then stores token t.
 
 #include "common.h"
 #include "kernels.h"
@@ -20,7 +21,12 @@ namespace {
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kChunkBatch = 4;  // 16-byte chunks per row and lane in flight
+// 16-byte chunks per row and lane in flight: fewer for more tokens, which
+// each add a chunk of x per chunk of W
+template <int T>
+constexpr int chunk_batch() {
+  return T <= 8 ? 4 : 2;
+}
 
 // The operands go through scalar parameters: a bit cast applied to a vector
 // element expression directly reads element 0 whatever the index (seen with
@@ -43,6 +49,20 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int n0 = (blockIdx.x * 4 + wave) * 2;
+  // t = scale * x A^T for the workgroup's rows (all below lora_cols or none:
+  // lora_cols is a multiple of 32, a workgroup owns 8 rows), summed once
+  // from the slice partials into LDS by all threads
+  __shared__ float t_lds[T][64];
+  const bool lora_rows = r_pad > 0 && (int)blockIdx.x * 8 < lora_cols;
+  if (lora_rows) {
+    for (int i = threadIdx.x; i < T * r_pad; i += 256) {
+      const int t = i / r_pad, j = i % r_pad;
+      float tv = 0.f;
+      for (int z = 0; z < n_slice; ++z) tv += t_part[((int64_t)z * T + t) * r_pad + j];
+      t_lds[t][j] = tv;
+    }
+    __syncthreads();
+  }
   if (n0 >= N) return;
   const bf16_t* w0 = w + (int64_t)n0 * K;
   const bf16_t* w1 = w0 + K;
@@ -54,6 +74,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
 
   // whole batches of kChunkBatch chunks per lane (all loads issued, then the
   // products), then the chunks left one at a time
+  constexpr int kChunkBatch = chunk_batch<T>();
   int c = lane;
   for (; c + 64 * (kChunkBatch - 1) < nc; c += 64 * kChunkBatch) {
     u32x4 wa[kChunkBatch], wb[kChunkBatch], xv[kChunkBatch][T];
@@ -84,16 +105,14 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
     }
   }
 
-  // rows below lora_cols (a multiple of 32, so both rows or neither)
-  if (r_pad > 0 && n0 < lora_cols && lane < rank) {
+  // rows below lora_cols: lane j < rank adds t[token][j] * B[row][j]
+  if (lora_rows && lane < rank) {
     const float b0 = bf16_to_f32(b[(int64_t)n0 * rank + lane]);
     const float b1 = bf16_to_f32(b[(int64_t)(n0 + 1) * rank + lane]);
 #pragma unroll
     for (int t = 0; t < T; ++t) {
-      float tv = 0.f;
-      for (int z = 0; z < n_slice; ++z) tv += t_part[((int64_t)z * T + t) * r_pad + lane];
-      acc[0][t] = fmaf(tv, b0, acc[0][t]);
-      acc[1][t] = fmaf(tv, b1, acc[1][t]);
+      acc[0][t] = fmaf(t_lds[t][lane], b0, acc[0][t]);
+      acc[1][t] = fmaf(t_lds[t][lane], b1, acc[1][t]);
     }
   }
 
@@ -150,6 +169,14 @@ hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_ou
     ATTUNER_GEMV(6)
     ATTUNER_GEMV(7)
     ATTUNER_GEMV(8)
+    ATTUNER_GEMV(9)
+    ATTUNER_GEMV(10)
+    ATTUNER_GEMV(11)
+    ATTUNER_GEMV(12)
+    ATTUNER_GEMV(13)
+    ATTUNER_GEMV(14)
+    ATTUNER_GEMV(15)
+    ATTUNER_GEMV(16)
     default: return hipErrorInvalidValue;
   }
 #undef ATTUNER_GEMV

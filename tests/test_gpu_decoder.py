@@ -259,10 +259,10 @@ def test_decoder_stack_two_layers():
 
 
 # ----------------------------------------------------------------------------
-# the few-token path (at most 8 tokens: the weight-streaming GEMV) in every mode
+# the few-token path (at most 16 tokens: the weight-streaming GEMV) in every mode
 # ----------------------------------------------------------------------------
 
-@pytest.mark.parametrize("T,rank", [(1, 16), (2, 8), (3, 48), (5, 0), (8, 32), (7, 5)])
+@pytest.mark.parametrize("T,rank", [(1, 16), (2, 8), (3, 48), (5, 0), (8, 32), (7, 5), (12, 16), (16, 0), (9, 64)])
 def test_few_token_qproj_lora(T, rank):
     _say(f"few-token qproj T={T} r={rank}")
     rng = np.random.default_rng(100 + T + rank)
@@ -283,7 +283,7 @@ def test_few_token_qproj_lora(T, rank):
     assert_intermediate_close(got[:, lora_cols:], ref[:, lora_cols:], "k/v columns")
 
 
-@pytest.mark.parametrize("T", [2, 4, 6, 8])
+@pytest.mark.parametrize("T", [2, 4, 6, 8, 10, 16])
 def test_few_token_modes(T):
     _say(f"few-token modes T={T}")
     rng = np.random.default_rng(200 + T)
