@@ -272,6 +272,12 @@ attuner_status ensure_rope(attuner_ctx* c, int64_t n) {
 // One request of a norm+rope / attention batch, in host form.
 struct ReqDesc {
   int32_t q_start, q_len, kv_start, art_len, pos0;
+  int32_t span0 = 0, n_span = 0;  // packed online spans (attention only; see AttnReq)
+};
+
+// A packed online span for the attention pass: its first q row and offset.
+struct SpanRow {
+  int32_t row, off;
 };
 
 attuner_status run_norm_rope(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int32_t total_q, const void* q_raw,
@@ -384,7 +390,7 @@ std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc
 
 attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int32_t total_q, const void* q,
                              const uint16_t* k_plane, const uint16_t* v_plane, int64_t head_stride, void* o,
-                             float* lse, hipStream_t stream) {
+                             float* lse, hipStream_t stream, const std::vector<SpanRow>* spans = nullptr) {
   AttnParams p;
   memset(&p, 0, sizeof p);
   p.q = static_cast<const uint16_t*>(q);
@@ -413,8 +419,15 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
     p.req[r].n_qblk = nq;
     p.req[r].wg_start = units;
     p.req[r].n_split = ns;
+    p.req[r].span0 = reqs[r].span0;
+    p.req[r].n_span = reqs[r].n_span;
     units += nq * ns;
   }
+  if (spans)
+    for (size_t i = 0; i < spans->size(); ++i) {
+      p.span_row[i] = (*spans)[i].row;
+      p.span_off[i] = (*spans)[i].off;
+    }
   p.n_split = n_split;
   p.n_units = units;
   if (n_split > 1) {
@@ -1230,7 +1243,51 @@ attuner_status attuner_span_attn(attuner_ctx* c, int32_t layer, int32_t n_spans,
   uint16_t* vp = cache_plane(req_kv, c, layer, 1, cache_rows);
   st = run_norm_rope(c, reqs, total_q, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, o, kp, vp, hs, s);
   if (st != ATTUNER_OK) return st;
-  return run_attention(c, reqs, total_q, o, kp, vp, hs, o, lse, s);
+  // Attention: consecutive spans of one request (same kv_start, rows back to
+  // back) share one work-list entry, their rows packed into common 64-row
+  // blocks, each row seeing the keys up to its own position.  A short span
+  // then rides in a block with its neighbours instead of walking its whole
+  // prefix of key tiles alone.
+  std::vector<ReqDesc> packed;
+  std::vector<SpanRow> table;
+  for (size_t i = 0; i < reqs.size();) {
+    if (reqs[i].q_len == 0) {
+      ++i;
+      continue;
+    }
+    // merge while the next span continues the rows and starts at or past the
+    // end of the previous one (positions must grow from row to row)
+    size_t j = i + 1;
+    size_t last = i;  // last span with rows in the group
+    while (j < reqs.size() && reqs[j].kv_start == reqs[i].kv_start &&
+           (reqs[j].q_len == 0 ||
+            (reqs[j].q_start == reqs[last].q_start + reqs[last].q_len &&
+             reqs[j].art_len >= reqs[last].art_len + reqs[last].q_len))) {
+      if (reqs[j].q_len > 0) last = j;
+      ++j;
+    }
+    ReqDesc g = reqs[i];
+    int32_t n_rows = 0, n_sp = 0;
+    const int32_t span0 = (int32_t)table.size();
+    for (size_t k = i; k < j; ++k) {
+      if (reqs[k].q_len == 0) continue;
+      table.push_back(SpanRow{reqs[k].q_start, reqs[k].art_len});
+      n_rows += reqs[k].q_len;
+      g.art_len = reqs[k].art_len + reqs[k].q_len - n_rows;  // art_len + q_len = last row's position + 1
+      ++n_sp;
+    }
+    g.q_len = n_rows;
+    if (n_sp > 1) {
+      g.span0 = span0;
+      g.n_span = n_sp;
+    } else {
+      table.pop_back();
+      g.art_len = reqs[i].art_len;
+    }
+    packed.push_back(g);
+    i = j;
+  }
+  return run_attention(c, packed, total_q, o, kp, vp, hs, o, lse, s, &table);
 }
 
 attuner_status attuner_decode_attn(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_ctx,

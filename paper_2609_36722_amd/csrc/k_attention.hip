@@ -2,7 +2,9 @@
 // (eq. 3 form: softmax(q K^T / sqrt(d) + M) V with the causal mask; appendix
 // A.5: scaled dot-product attention over the assembled context).  Suffix row
 // i of a request sees cache keys 0 .. art_len + i: every artifact key and the
-// suffix causally.
+// suffix causally.  Rows of several online spans of one prompt may share a
+// request entry (packed back to back): each row then sees the keys up to its
+// own position, which only grows from row to row.
 //
 // Work unit = (request, block of 64 suffix tokens, KV head g, key split), one
 // workgroup of eight waves: the four query heads that share KV head g times
@@ -230,7 +232,21 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   const int qb = rq.n_qblk - 1 - unit / rq.n_split;
   const int t0 = qb * BQ;
   const int blk_rows = min(BQ, rq.q_len - t0);
-  const int kv_len = rq.art_len + t0 + blk_rows;  // keys any row of the block sees
+  // last visible key of row tt of the request (rows past the end take the
+  // last row's); grows with tt
+  auto lim = [&](int tt) __attribute__((always_inline)) {
+    tt = min(tt, rq.q_len - 1);
+    if (rq.n_span == 0) return rq.art_len + tt;
+    const int row = rq.q_start + tt;
+    int base_row = p.span_row[rq.span0], base_off = p.span_off[rq.span0];
+    for (int j = rq.span0 + 1; j < rq.span0 + rq.n_span; ++j)
+      if (p.span_row[j] <= row) {
+        base_row = p.span_row[j];
+        base_off = p.span_off[j];
+      }
+    return base_off + row - base_row;
+  };
+  const int kv_len = lim(t0 + blk_rows - 1) + 1;  // keys any row of the block sees
   const int n_tiles = (kv_len + BKV - 1) / BKV;
   const int per = (n_tiles + rq.n_split - 1) / rq.n_split;
   const int tb = min(n_tiles, split * per);
@@ -285,9 +301,9 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   for (int i = 0; i < 4; ++i) acc[i] = f32x16{};
 
   const float sc = p.score_scale;
-  const int vis_lim = rq.art_len + t;  // last visible key of this row
+  const int vis_lim = lim(t);  // last visible key of this row
 
-  const int mask_from = rq.art_len + t0w;  // tiles ending past this key need the mask
+  const int mask_from = lim(t0w);  // tiles ending past this key need the mask
   // tiles before tp end at or before the diagonal of every row of the wave
   const int tp = min(max((mask_from + 1) / BKV, tb), te);
 

@@ -157,6 +157,12 @@ struct AttnReq {
   int32_t n_qblk;    // ceil(q_len / 64)
   int32_t wg_start;  // first work unit of the request (units = qblocks * n_split)
   int32_t n_split;   // key splits of the request's blocks (<= AttnParams::n_split)
+  // n_span == 0: row i sees keys 0 .. art_len + i.  Otherwise the rows are
+  // online spans packed back to back (span_row / span_off entries span0 ..
+  // span0 + n_span - 1): a row of the span starting at q row R with offset
+  // F sees keys 0 .. F + (row - R); positions only grow with the row.
+  int32_t span0;
+  int32_t n_span;
 };
 
 struct AttnParams {
@@ -175,6 +181,8 @@ struct AttnParams {
   float score_scale;       // log2(e) / sqrt(d)
   int32_t n_req;
   AttnReq req[kMaxReq];
+  int32_t span_row[kMaxReq];  // first q row of each packed span
+  int32_t span_off[kMaxReq];  // its offset (first position) in its request's cache rows
 };
 
 // Attention, plus the split-KV merge kernel when n_split > 1 (at most

@@ -185,3 +185,37 @@ def test_interleaved_c2_prompt():
     # cached rows of the first and last artifact stayed put
     for j, off in ((0, 32), (7, 32 + 7 * (1024 + 8))):
         assert np.array_equal(cache[0, 0, :, off:off + 1024], art_k[j][0]), f"artifact {j} keys"
+
+
+def test_spans_given_out_of_prompt_order():
+    # the same prompt's spans listed last-first (rows of the question before
+    # the header's): positions no longer grow along the rows, so the spans
+    # must not share query blocks; O must match the in-order call row for row
+    _say("spans out of prompt order")
+    rng = np.random.default_rng(78)
+    H, L = 512, 100
+    with Context(ModelCfg(n_layers=1, hidden=H), pool_pages=8) as ctx:
+        k, v = _bits(rng, (1, HKV, L, D)), _bits(rng, (1, HKV, L, D))
+        aid = ctx.store_artifact(dev_bf16(k), dev_bf16(v))
+        ne, rows, ns = ctx.assemble_segments_plan([[-5, aid, -7]])
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        kv = torch.zeros(2 * HKV * rows * D, dtype=torch.bfloat16, device="cuda")
+        cu, spans = ctx.assemble_segments([[-5, aid, -7]], bt, kv, rows)
+        n_out = (HQ + 2 * HKV) * D
+        qkv = dev_bf16(_bits(rng, (12, n_out)))
+        g = torch.ones(D, dtype=torch.bfloat16, device="cuda")
+
+        def run(order):
+            q = torch.cat([qkv[0:5], qkv[5:12]] if order == "in" else [qkv[5:12], qkv[0:5]]).contiguous()
+            o = torch.empty(12, HQ, D, dtype=torch.bfloat16, device="cuda")
+            if order == "in":
+                cq, offs = [0, 5, 12], [0, 5 + L]
+            else:
+                cq, offs = [0, 7, 12], [5 + L, 0]
+            ctx.span_attn(0, cq, [0, 0], offs, None, q[:, :HQ * D], n_out, q[:, HQ * D:(HQ + HKV) * D],
+                          q[:, (HQ + HKV) * D:], n_out, g, g, kv, rows, o)
+            torch.cuda.synchronize()
+            return host_f64(o)
+        a = run("in")
+        b = run("out")
+    assert np.array_equal(np.concatenate([b[7:12], b[0:7]]), a)
