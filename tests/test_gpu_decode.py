@@ -164,3 +164,29 @@ def test_decode_c5_context_one_request():
     _say("decode c5 context")
     got, ref = _run_decode(46, [1024] * 32, [(tuple(range(32)), 1024)])
     assert_o_close(got, ref)
+
+
+def test_decode_64_requests_and_the_limit():
+    # the largest batch one call takes (ATTUNER_MAX_REQUESTS), short and long
+    # contexts mixed; one more request is refused before any launch
+    _say("decode 64 requests")
+    rng = np.random.default_rng(47)
+    lengths = [int(v) for v in rng.integers(1, 700, size=20)]
+    reqs = []
+    for i in range(64):
+        k = int(rng.integers(0, 4))
+        reqs.append((tuple(int(a) for a in rng.choice(20, size=k, replace=False)), int(rng.integers(0, 40))))
+    got, ref = _run_decode(48, lengths, reqs)
+    assert_o_close(got, ref, "batch")
+    for r in range(64):
+        assert_o_close_per_request(got[r], ref[r], f"request {r}")
+    with Context(ModelCfg(n_layers=1, hidden=256), pool_pages=1) as ctx:
+        kv = torch.zeros(2 * HKV * 65 * D, dtype=torch.bfloat16, device="cuda")
+        q = torch.zeros(65, HQ * D + 2 * HKV * D, dtype=torch.bfloat16, device="cuda")
+        g = torch.ones(D, dtype=torch.bfloat16, device="cuda")
+        ld = q.shape[1]
+        with pytest.raises(AttunerError) as e:
+            ctx.decode_attn(0, list(range(66)), [0] * 65, None, q[:, :HQ * D], ld, q[:, HQ * D:HQ * D + HKV * D],
+                            q[:, HQ * D + HKV * D:], ld, g, g, kv, 65, torch.empty(65, HQ, D, dtype=torch.bfloat16,
+                                                                                   device="cuda"))
+        assert e.value.status == -5

@@ -15,7 +15,7 @@ import torch
 import oracle
 import synthdata as sd
 from synthdata.workloads import ModelShape, Request, custom_workload
-from tests._tol import assert_intermediate_close, assert_o_close, lse_bar
+from tests._tol import assert_intermediate_close, assert_o_close, assert_o_close_per_request, lse_bar
 
 pytestmark = pytest.mark.gpu
 
@@ -514,3 +514,32 @@ def test_error_codes():
             with pytest.raises(AttunerError) as e:
                 ctx.suffix_attn(0, [0, 4], [0, rows], [1], [1], q_raw, ld, k_raw, v_raw, ld, g, g, kv, rows, q)
             assert e.value.status == -1
+
+
+def test_suffix_attn_64_requests():
+    # 64 requests in one call (the work list's capacity): empty, one-token and
+    # multi-block suffixes over shared and private artifacts
+    _say("suffix attention 64 requests")
+    shape = ModelShape(hidden=256)
+    rng = np.random.default_rng(93)
+    lengths = [int(v) for v in rng.integers(1, 300, size=12)]
+    reqs = []
+    for i in range(64):
+        k = int(rng.integers(0, 3))
+        reqs.append(Request(tuple(int(a) for a in rng.choice(12, size=k, replace=False)),
+                            int(rng.choice([0, 1, 5, 64, 70]))))
+    wl = custom_workload("batch64", 94, shape, lengths, reqs, rank=8, scale=2.0, gamma="uniform")
+    g = GpuWorkload(wl)
+    try:
+        out = g.run_layer(0, with_lse=False)
+        got = host_f64(out["o"])
+        refs = []
+        for r in range(64):
+            if wl.requests[r].suffix_len == 0:
+                continue
+            ref = g.oracle_layer(0, r)["o"]
+            assert_o_close_per_request(got[g.cu_q[r]:g.cu_q[r + 1]], ref, f"O request {r}")
+            refs.append(ref)
+        assert_o_close(got, np.concatenate(refs), "batch O")
+    finally:
+        g.close()
