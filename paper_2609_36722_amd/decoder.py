@@ -14,7 +14,10 @@ Per layer l, on the residual stream h [T][H] of the T suffix tokens:
     h   = h + g W_down^T                             attuner_linear (residual, in place)
 then the last suffix token of each request: RMSNorm * gamma_final, LM head,
 argmax (attuner_rms_norm on a row subset, attuner_lm_head_argmax).  Layer 0's
-h is the embedding rows of the suffix tokens (attuner_embed).
+h is the embedding rows of the suffix tokens (attuner_embed).  Decode steps
+run the same layers for one new token per request, with attuner_decode_attn
+in place of the suffix attention (the generated tokens keep the adapted
+query projection, section 4).
 
 Every step runs in the library's kernels; torch only holds the device
 buffers.  The weights are the caller's device tensors (bf16, row-major); the
@@ -150,3 +153,54 @@ class DecoderStack:
         self.embed(token_ids, stream)
         self.layers(cu_ctx, art_len, pos0, req_kv, cache_rows, stream)
         return self.first_token(stream)
+
+    # ---- decode: one generated token per request ----------------------------------
+    def _decode_buffers(self):
+        if getattr(self, "hd", None) is None:
+            n, cfg, dev = len(self.last_rows), self.ctx.cfg, self.w.embed.device
+            bf = dict(dtype=torch.bfloat16, device=dev)
+            self.hd = torch.empty(n, cfg.hidden, **bf)
+            self.xd = torch.empty(n, cfg.hidden, **bf)
+            self.qkvd = torch.empty(n, self.nq + 2 * self.nkv, **bf)
+            self.od = torch.empty(n, cfg.n_q_heads, cfg.head_dim, **bf)
+            self.gd = torch.empty(n, self.w.intermediate, **bf)
+
+    def decode_embed(self, token_ids: Sequence[int], stream=None) -> None:
+        """hd = the embedding rows of one new token per request."""
+        self._decode_buffers()
+        if len(token_ids) != len(self.last_rows):
+            raise ValueError(f"{len(token_ids)} token ids for {len(self.last_rows)} requests")
+        self.ctx.embed(token_ids, self.w.embed, self.hd, stream=stream)
+
+    def decode_layers(self, cu_ctx, ctx_len, req_kv: torch.Tensor, cache_rows: int, stream=None) -> None:
+        """Every layer for the new tokens (row r = request r, at position
+        ctx_len[r], its key/value written to cache row cu_ctx[r] + ctx_len[r]),
+        attending to the ctx_len[r] keys before it (attuner_decode_attn); the
+        projections of a few tokens run as GEMVs.  No host-to-device copy."""
+        self._decode_buffers()
+        c, w, ld = self.ctx, self.w, self.nq + 2 * self.nkv
+        q = self.qkvd[:, :self.nq]
+        k, v = self.qkvd[:, self.nq:self.nq + self.nkv], self.qkvd[:, self.nq + self.nkv:]
+        for l, lw in enumerate(w.layers):
+            c.rms_norm(self.hd, lw.gamma_in, self.xd, stream=stream)
+            c.qproj_lora(self.xd, lw.wqkv, lw.a, lw.b, w.rank if lw.a is not None else 0, w.scale, self.nq, self.qkvd,
+                         stream=stream)
+            c.decode_attn(l, cu_ctx, ctx_len, None, q, ld, k, v, ld, lw.gamma_q, lw.gamma_k, req_kv, cache_rows,
+                          self.od, stream=stream)
+            c.linear(self.od.view(-1, self.nq), lw.wo, self.hd, residual=self.hd, stream=stream)
+            c.rms_norm(self.hd, lw.gamma_post, self.xd, stream=stream)
+            c.gate_up_swiglu(self.xd, lw.w_gu, self.gd, stream=stream)
+            c.linear(self.gd, lw.w_down, self.hd, residual=self.hd, stream=stream)
+
+    def decode_token(self, stream=None) -> torch.Tensor:
+        """ids[r] = greedy next token of request r from hd (device int32)."""
+        self.ctx.rms_norm(self.hd, self.w.gamma_final, self.x_last, stream=stream)
+        self.ctx.lm_head_argmax(self.x_last, self.w.w_lm, self.ids, self.max_logit, stream=stream)
+        return self.ids
+
+    def decode(self, token_ids: Sequence[int], cu_ctx, ctx_len, req_kv: torch.Tensor, cache_rows: int,
+               stream=None) -> torch.Tensor:
+        """One decode step: the next token of every request (device int32)."""
+        self.decode_embed(token_ids, stream)
+        self.decode_layers(cu_ctx, ctx_len, req_kv, cache_rows, stream)
+        return self.decode_token(stream)

@@ -30,7 +30,7 @@ class GpuWorkload:
     """A workload stored in a fresh context: its artifacts in the pool and the
     request caches assembled, for the given model layers."""
 
-    def __init__(self, wl: sd.Workload, layers: Sequence[int] = (0,), extra_pages: int = 0):
+    def __init__(self, wl: sd.Workload, layers: Sequence[int] = (0,), extra_pages: int = 0, suffix_extra: int = 0):
         self.wl = wl
         self.layers = list(layers)
         s = wl.shape
@@ -51,7 +51,7 @@ class GpuWorkload:
             vd = dev_bf16(np.ascontiguousarray(v.transpose(0, 2, 1, 3)))
             self.ids[a] = self.ctx.store_artifact(kd, vd)
         self.requests = [[self.ids[a] for a in r.artifact_ids] for r in wl.requests]
-        self.suffix_cap = [r.suffix_len for r in wl.requests]
+        self.suffix_cap = [r.suffix_len + suffix_extra for r in wl.requests]
         self.n_entries, self.rows = self.ctx.assemble_plan(self.requests, self.suffix_cap)
         self.block_table = torch.zeros(max(1, self.n_entries) * 4, dtype=torch.int32, device="cuda")
         self.req_kv = torch.zeros(len(self.layers) * 2 * s.n_kv_heads * self.rows * s.head_dim,

@@ -1,17 +1,18 @@
 """GPU parity of the decoder layer around the suffix path (embedding rows,
 RMSNorm, o_proj / down_proj with the residual, the SwiGLU gate/up GEMM, the
-LM head with the greedy pick, and a two-layer stack chained through them)
-against the fp64 oracle, through the C ABI.
+LM head with the greedy pick, and a two-layer stack chained through them,
+prefill and decode) against the fp64 oracle, through the C ABI.  The oracle
+only ever takes the seeded inputs.
 
-Bars: the embedding lookup bit-exact; bf16-stored outputs of one step (and
-one layer run from the GPU's own input) within the intermediate bar
-(max|err| <= 1e-2 max|ref|, mean|err| <= 2^-8 mean|ref|); the stack run end to
-end from the embedding within L * 2^-8 mean|ref| after L layers (the errors
-of each layer's bf16 stores add along the residual stream);
-the greedy token by the rule for an argmax decided in floating point: the
-chosen id's exact logit is within the fp32 accumulation bound of the exact
-maximum, and equals the exact argmax wherever the exact top-two gap exceeds
-twice that bound.
+Bars: the embedding lookup bit-exact; bf16-stored outputs of one step within
+the intermediate bar (max|err| <= 1e-2 max|ref|, mean|err| <= 2^-8
+mean|ref|); the stack run end to end from the embedding within L * 2^-8
+mean|ref| after L layers (the errors of each layer's bf16 stores add along
+the residual stream).  The greedy token, an argmax decided in floating
+point: for the same bf16 input, the chosen id's exact logit is within the
+fp32 accumulation bound of the exact maximum, and equals the exact argmax
+wherever the exact top-two gap exceeds twice that bound; after the stack,
+the same with the bound widened by what the stack bar lets the input move.
 """
 
 import math
@@ -200,11 +201,41 @@ def _oracle_weights(wl, l, I):
     return w
 
 
-def test_decoder_stack_two_layers():
-    _say("decoder stack 2 layers")
+def _pick_bound(x_ref, w):
+    """Bound on |logit_v(x) - logit_v(x_ref)| for an x within the two-layer
+    stack bar of x_ref (max|x - x_ref| <= 1e-2 max|x_ref| per element):
+    sum_k |dx_k| |w_vk| <= 1e-2 max|x_ref| * max_v sum_k |w_vk|, plus the fp32
+    accumulation bound."""
+    return 1e-2 * np.abs(x_ref).max() * np.abs(w).sum(axis=1).max() + _fp32_bound(x_ref, w).max()
+
+
+def _check_pick_near(ids, x_ref, w):
+    """ids from a GPU x close to x_ref: each id's exact logit at x_ref is within
+    twice the bound of the exact maximum (the two logits each move by at most
+    the bound), and equals the exact argmax where the top-two gap exceeds it."""
+    logits = oracle.linear(x_ref, w)
+    for r in range(logits.shape[0]):
+        b = _pick_bound(x_ref[r:r + 1], w)
+        top = int(np.argmax(logits[r]))
+        assert logits[r, int(ids[r])] >= logits[r, top] - 2 * b, f"row {r}: id {ids[r]} far from the maximum"
+        second = np.partition(logits[r], -2)[-2]
+        if logits[r, top] - second > 2 * b:
+            assert int(ids[r]) == top, f"row {r}: id {ids[r]}, exact argmax {top} with a clear gap"
+
+
+def test_decoder_stack_two_layers_then_decode():
+    # the whole stack on the GPU against the whole stack in the oracle, both
+    # from the same seeded token ids: prefill of the suffix to the first
+    # token, then two decode steps with seeded next tokens (the oracle takes
+    # no GPU value as input)
+    _say("decoder stack 2 layers + 2 decode steps")
     wl, I, V = _stack_case()
     s = wl.shape
-    g = GpuWorkload(wl, layers=[0, 1])
+    n_dec = 2
+    g = GpuWorkload(wl, layers=[0, 1], suffix_extra=n_dec)
+    n_req = len(wl.requests)
+    tokens = [sd.suffix_tokens(wl, r, V) for r in range(n_req)]
+    dec_tokens = np.random.default_rng(96).integers(0, V, size=(n_dec, n_req))
     try:
         layers = []
         for l in range(2):
@@ -219,43 +250,63 @@ def test_decoder_stack_two_layers():
         sw = StackWeights(embed=dev_bf16(lm["embed"]), gamma_final=dev_bf16(lm["gamma_final"]),
                           w_lm=dev_bf16(lm["w_lm"]), layers=layers, rank=wl.rank, scale=wl.scale)
         stack = DecoderStack(g.ctx, sw, [r.suffix_len for r in wl.requests])
-        tokens = [sd.suffix_tokens(wl, r, V) for r in range(len(wl.requests))]
         stack.embed(np.concatenate(tokens).tolist())
-        hs = [host_f64(stack.h)]
-        for l in range(2):
-            stack.layers(g.cu_ctx, g.art_len, g.pos0, g.req_kv, g.rows, first=l, count=1)
-            torch.cuda.synchronize()
-            hs.append(host_f64(stack.h))
+        h_emb = host_f64(stack.h)
+        stack.layers(g.cu_ctx, g.art_len, g.pos0, g.req_kv, g.rows)
         ids = stack.first_token().cpu().numpy()
-        mx = stack.max_logit.cpu().numpy().astype(np.float64)
-        x_last = host_f64(stack.x_last)
+        h_pre, x_last = host_f64(stack.h), host_f64(stack.x_last)
+        dec = []
+        for j in range(n_dec):
+            ctx_len = [g.art_len[r] + wl.requests[r].suffix_len + j for r in range(n_req)]
+            ids_j = stack.decode(dec_tokens[j].tolist(), g.cu_ctx, ctx_len, g.req_kv, g.rows).cpu().numpy()
+            dec.append((host_f64(stack.hd), host_f64(stack.x_last), ids_j))
         torch.cuda.synchronize()
     finally:
         g.close()
 
     emb = oracle.decode_bf16(lm["embed"])
     h0 = np.concatenate([emb[t] for t in tokens])
-    assert np.array_equal(hs[0], h0), "embedding rows"
+    assert np.array_equal(h_emb, h0), "embedding rows"
     ws = [_oracle_weights(wl, l, I) for l in range(2)]
-    h_e2e = []
+    gf, w_lm = oracle.decode_bf16(lm["gamma_final"]), oracle.decode_bf16(lm["w_lm"])
+    args = lambda r, l, keys, vals, p0: (keys, vals, p0, s.n_q_heads, s.n_kv_heads, s.rope_theta, s.rms_eps, wl.scale)
+    # prefill in the oracle: every layer's keys/values of the context kept per request
+    ctx_k, ctx_v, h_ref, x_ref = [], [], [], []
     for r, req in enumerate(wl.requests):
         lo, hi = g.cu_q[r], g.cu_q[r + 1]
         h = h0[lo:hi]
+        ks, vs = [], []
         for l in range(2):
             ka = np.concatenate([oracle.decode_bf16(g.art_k[a][l]) for a in req.artifact_ids])
             va = np.concatenate([oracle.decode_bf16(g.art_v[a][l]) for a in req.artifact_ids])
-            args = (ka, va, wl.pos0(req), s.n_q_heads, s.n_kv_heads, s.rope_theta, s.rms_eps, wl.scale)
-            # each layer from the GPU's own input, then the whole stack from the embedding
-            one = oracle.decoder_layer(hs[l][lo:hi], ws[l], *args)
-            assert_intermediate_close(hs[l + 1][lo:hi], one["h"], f"request {r} layer {l} h")
-            h = oracle.decoder_layer(h, ws[l], *args)["h"]
-        h_e2e.append(h)
-    assert_stack_close(hs[2], np.concatenate(h_e2e), 2, "two-layer stack h")
-    # final norm of the last token of each request, then the greedy pick
-    last = [g.cu_q[r + 1] - 1 for r in range(len(wl.requests))]
-    gf = oracle.decode_bf16(lm["gamma_final"])
-    assert_intermediate_close(x_last, oracle.rms_norm_heads(hs[2][last], gf, s.rms_eps), "final norm")
-    _check_pick(ids, mx, x_last, oracle.decode_bf16(lm["w_lm"]))
+            out = oracle.decoder_layer(h, ws[l], *args(r, l, ka, va, wl.pos0(req)))
+            ks.append(np.concatenate([ka, out["k_hat"]]))
+            vs.append(np.concatenate([va, out["v"]]))
+            h = out["h"]
+        ctx_k.append(ks)
+        ctx_v.append(vs)
+        h_ref.append(h)
+        x_ref.append(oracle.rms_norm_heads(h[-1:], gf, s.rms_eps))
+    assert_stack_close(h_pre, np.concatenate(h_ref), 2, "two-layer stack h")
+    x_ref = np.concatenate(x_ref)
+    assert_stack_close(x_last, x_ref, 2, "final norm of the last rows")
+    _check_pick_near(ids, x_ref, w_lm)
+    # two decode steps in the oracle over its own growing context
+    for j in range(n_dec):
+        hd_ref, xd_ref = [], []
+        for r, req in enumerate(wl.requests):
+            h = emb[dec_tokens[j, r]][None, :]
+            p0 = g.art_len[r] + req.suffix_len + j
+            for l in range(2):
+                out = oracle.decoder_layer(h, ws[l], *args(r, l, ctx_k[r][l], ctx_v[r][l], p0))
+                ctx_k[r][l] = np.concatenate([ctx_k[r][l], out["k_hat"]])
+                ctx_v[r][l] = np.concatenate([ctx_v[r][l], out["v"]])
+                h = out["h"]
+            hd_ref.append(h)
+            xd_ref.append(oracle.rms_norm_heads(h, gf, s.rms_eps))
+        hd, xd, ids_j = dec[j]
+        assert_stack_close(hd, np.concatenate(hd_ref), 2, f"decode step {j} h")
+        _check_pick_near(ids_j, np.concatenate(xd_ref), w_lm)
 
 
 # ----------------------------------------------------------------------------

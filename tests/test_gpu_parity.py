@@ -114,7 +114,9 @@ def test_gather_layers_split_from_table_bit_exact():
         torch.cuda.synchronize()
         got1 = bf16_to_host(one).reshape(3, 2, 8, rows, 128)
         assert not got1[0].any() and not got1[2].any()
-        assert np.array_equal(got1[1], got[1])
+        for r in range(len(reqs)):
+            lo, n = cu[r], al[r]
+            assert np.array_equal(got1[1, :, :, lo:lo + n], want[1, :, :, lo:lo + n]), f'layer 1, request {r}'
         with pytest.raises(AttunerError) as e:
             ctx.gather_layers(bt, ne, 2, 2, kv, rows)      # past the last layer
         assert e.value.status == -5
