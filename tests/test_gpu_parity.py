@@ -347,7 +347,7 @@ def test_suffix_layer_c1(gamma, scale):
         # the suffix keys and values now sit after the artifacts in the cache
         c = g.cache_view()
         L = g.art_len[0]
-        keys = oracle.decode_bf16(c[0, 0, :, :L]).transpose(1, 0, 2)
+        keys = np.concatenate([oracle.decode_bf16(g.art_k[a][0]) for a in g.wl.requests[0].artifact_ids])
         bar = lse_bar(ref["q_hat"], np.concatenate([keys, ref["k_hat"]]), 32, 8)
         assert np.abs(out["lse"].cpu().numpy() - ref["lse"]).max() <= bar
         assert_intermediate_close(oracle.decode_bf16(c[0, 0, :, L:L + 64]).transpose(1, 0, 2), ref["k_hat"], "k_hat")
