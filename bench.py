@@ -598,19 +598,20 @@ def model_main(args):
         L = wl.artifact_lengths[a]
         ids[a] = ctx.store_artifact(randn(NL, s.n_kv_heads, L, s.head_dim), randn(NL, s.n_kv_heads, L, s.head_dim))
     requests = [[ids[a] for a in r.artifact_ids] for r in wl.requests]
-    caps = [r.suffix_len for r in wl.requests]
+    caps = [r.suffix_len + (1 if args.decode else 0) for r in wl.requests]   # + the decoded token's row
     n_entries, rows = ctx.assemble_plan(requests, caps)
     bt = torch.zeros(max(1, n_entries) * 4, dtype=torch.int32, device=dev)
     req_kv = torch.zeros(NL * 2 * s.n_kv_heads * rows * s.head_dim, dtype=torch.bfloat16, device=dev)
     tokens = np.concatenate([sd.suffix_tokens(wl, r, V) for r in range(len(wl.requests))]).tolist()
     pos0 = [wl.pos0(r) for r in wl.requests]
-    stack = DecoderStack(ctx, sw, caps)
+    stack = DecoderStack(ctx, sw, [r.suffix_len for r in wl.requests])
     torch.cuda.synchronize()
     log(args, f"weights {weight_bytes / 1e9:.2f} GB and artifacts resident ({time.time() - t0:.1f} s)")
 
     def make_step(stk, reqs, cps, table, kv, n_rows, toks, p0):
         """One step: assembly, embedding, the layer loop (a graph once captured), first token."""
         state = {"graph": None, "cu": None, "al": None}
+        make_step.last_state = state
 
         def assemble():
             state["cu"], state["al"] = ctx.assemble_kv(reqs, cps, table, kv, n_rows)
@@ -686,6 +687,48 @@ def model_main(args):
     log(args, f"timed {args.steps} steps: {ms_step:.3f} ms to the first token; breakdown (eager) " +
         ", ".join(f"{k} {v:.3f}" for k, v in breakdown.items()))
 
+    # ---- one decode step through the whole stack (--decode) ---------------------
+    decode = None
+    if args.decode:
+        cu_d, al_d = make_step.last_state["cu"], make_step.last_state["al"]
+        ctx_len = [al_d[r] + wl.requests[r].suffix_len for r in range(len(wl.requests))]
+        nxt = stack.ids.cpu().tolist()
+        stack.decode(nxt, cu_d, ctx_len, req_kv, rows)          # buffers and workspaces
+        torch.cuda.synchronize()
+        dgraph = None
+        if not args.no_graph:
+            cap = torch.cuda.Stream()
+            cap.wait_stream(stream)
+            dgraph = torch.cuda.CUDAGraph()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(dgraph, stream=cap):
+                stack.decode_layers(cu_d, ctx_len, req_kv, rows)
+            torch.cuda.synchronize()
+
+        def dstep():
+            stack.decode_embed(nxt)
+            if dgraph is not None:
+                dgraph.replay()
+            else:
+                stack.decode_layers(cu_d, ctx_len, req_kv, rows)
+            stack.decode_token()
+
+        for _ in range(3):
+            dstep()
+        torch.cuda.synchronize()
+        d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        d0.record(stream)
+        for _ in range(args.steps):
+            dstep()
+        d1.record(stream)
+        torch.cuda.synchronize()
+        d_ms = d0.elapsed_time(d1) / args.steps
+        decode = {"ms_per_step": round(d_ms, 4), "tokens_per_s": round(len(wl.requests) / (d_ms * 1e-3), 2),
+                  "keys_per_request": [c + 1 for c in ctx_len],
+                  "note": "one generated token per request through every layer (projections as GEMVs), at the "
+                          "first decode position; the layer loop replayed as a graph"}
+        log(args, f"decode step through the stack: {d_ms:.3f} ms ({decode['tokens_per_s']:.1f} tokens/s)")
+
     # ---- GEMM rates over the step (eager call times summed over the layers) -----
     T = wl.total_suffix
     gemm_work = {"qkv_proj": (H, nq + 2 * nkv), "o_proj": (nq, H), "gate_up": (H, 2 * I), "down_proj": (I, H)}
@@ -746,6 +789,7 @@ def model_main(args):
         "first_token_ids": first_ids,
         "full_prefill": full,
         "speedup_vs_full_prefill": full["speedup"] if full else None,
+        "decode": decode,
         "paper_context": PAPER_CONTEXT,
     }
     print(json.dumps(out), flush=True)
