@@ -381,9 +381,10 @@ attuner_status attuner_span_attn(attuner_ctx* ctx, int32_t layer, int32_t n_span
  * ctx_len[r] + 1 keys j = 0 .. ctx_len[r].  Requires ctx_len[r] + 1 <=
  * cu_ctx[r+1] - cu_ctx[r] (the suffix capacity given to the assembly must
  * cover the generated tokens) and n_q_heads = 4 n_kv_heads.  q_raw/k_raw/
- * v_raw/ld_q/ld_kv/gamma as in attuner_qk_norm_rope; o: device [n_req][Hq][d]
- * bf16 (also stages the normalised queries).  Long contexts are split into
- * key chunks merged in fp32 (context workspace).
+ * v_raw/ld_q/ld_kv/gamma as in attuner_qk_norm_rope (the normalisation and
+ * rotation run inside the decode launch); o: device [n_req][Hq][d] bf16, not
+ * overlapping q_raw, k_raw or v_raw.  Long contexts are split into key
+ * chunks merged in fp32 (context workspace).
  * ------------------------------------------------------------------------ */
 attuner_status attuner_decode_attn(attuner_ctx* ctx, int32_t layer, int32_t n_req, const int32_t* cu_ctx,
                                    const int32_t* ctx_len, const int32_t* pos, const void* q_raw,

@@ -443,11 +443,25 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
 
 // One new token per request (reqs[r].q_len == 1, row r): attention over the
 // request's art_len + 1 keys, cut into equal chunks.
-attuner_status run_decode(attuner_ctx* c, const std::vector<ReqDesc>& reqs, const void* q, const uint16_t* k_plane,
-                          const uint16_t* v_plane, int64_t head_stride, void* o, hipStream_t stream) {
+attuner_status run_decode(attuner_ctx* c, const std::vector<ReqDesc>& reqs, const void* q_raw, int64_t ld_q,
+                          const void* k_raw, const void* v_raw, int64_t ld_kv, const void* gamma_q,
+                          const void* gamma_k, uint16_t* k_plane, uint16_t* v_plane, int64_t head_stride, void* o,
+                          hipStream_t stream) {
+  int64_t max_pos = 0;
+  for (const auto& r : reqs) max_pos = std::max<int64_t>(max_pos, (int64_t)r.pos0 + 1);
+  attuner_status st = ensure_rope(c, max_pos);
+  if (st != ATTUNER_OK) return st;
   DecodeParams p;
   memset(&p, 0, sizeof p);
-  p.q = static_cast<const uint16_t*>(q);
+  p.q_raw = static_cast<const uint16_t*>(q_raw);
+  p.k_raw = static_cast<const uint16_t*>(k_raw);
+  p.v_raw = static_cast<const uint16_t*>(v_raw);
+  p.ld_q = ld_q;
+  p.ld_kv = ld_kv;
+  p.gamma_q = static_cast<const uint16_t*>(gamma_q);
+  p.gamma_k = static_cast<const uint16_t*>(gamma_k);
+  p.rope = static_cast<const float2*>(c->rope.ptr);
+  p.eps = c->cfg.rms_eps;
   p.k = k_plane;
   p.v = v_plane;
   p.kv_head_stride = head_stride;
@@ -475,6 +489,7 @@ attuner_status run_decode(attuner_ctx* c, const std::vector<ReqDesc>& reqs, cons
     p.req[r].n_keys = n_keys;
     p.req[r].split0 = splits;
     p.req[r].n_split = (n_keys + p.chunk - 1) / p.chunk;
+    p.req[r].pos = reqs[r].pos0;
     splits += p.req[r].n_split;
   }
   p.total_splits = splits;
@@ -1317,9 +1332,7 @@ attuner_status attuner_decode_attn(attuner_ctx* c, int32_t layer, int32_t n_req,
   const int64_t hs = cache_rows * c->cfg.head_dim;
   uint16_t* kp = cache_plane(req_kv, c, layer, 0, cache_rows);
   uint16_t* vp = cache_plane(req_kv, c, layer, 1, cache_rows);
-  st = run_norm_rope(c, reqs, total_q, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, o, kp, vp, hs, s);
-  if (st != ATTUNER_OK) return st;
-  return run_decode(c, reqs, o, kp, vp, hs, o, s);
+  return run_decode(c, reqs, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, kp, vp, hs, o, s);
 }
 
 attuner_status attuner_full_prefill(attuner_ctx* c, int32_t n_tok, int32_t pos0, const void* x, const void* wqkv,

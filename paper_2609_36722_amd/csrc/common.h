@@ -52,6 +52,72 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// ---- RMSNorm pieces shared by every kernel that normalises a row ------------
+// Sum of squares of 8 bf16 values added to ss in order, and the scaled
+// bf16 values of a row chunk.
+
+__device__ __forceinline__ float accum_squares(float ss, u32x4 v) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float lo = __uint_as_float(v[e] << 16), hi = __uint_as_float(v[e] & 0xFFFF0000u);
+    ss += lo * lo + hi * hi;
+  }
+  return ss;
+}
+
+// bf16(x * inv * gamma) for 8 values
+__device__ __forceinline__ u32x4 norm_chunk(u32x4 v, u32x4 g, float inv) {
+  u32x4 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float lo = __uint_as_float(v[e] << 16) * inv * __uint_as_float(g[e] << 16);
+    const float hi = __uint_as_float(v[e] & 0xFFFF0000u) * inv * __uint_as_float(g[e] & 0xFFFF0000u);
+    o[e] = pack_bf16x2(lo, hi);
+  }
+  return o;
+}
+
+// Per-head RMSNorm over 128 dims + RoPE (rotate-half: dim i pairs with
+// 64 + i) held by an 8-lane group: lane j has dims 8j .. 8j + 7 in xa and
+// 64 + 8j .. 64 + 8j + 7 in xb, gamma likewise in ga / gb, and cs[e] =
+// (cos, sin) of pairs 8j + 2e and 8j + 2e + 1 at the token's position.  The
+// head's sum of squares is the lane's plus three exchanges in the group.
+__device__ __forceinline__ void head_norm_rope(u32x4 xa, u32x4 xb, u32x4 ga, u32x4 gb, const f32x4 cs[4], float eps,
+                                               u32x4& oa, u32x4& ob) {
+  float x0[8], x1[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x0[2 * e] = __uint_as_float(xa[e] << 16);
+    x0[2 * e + 1] = __uint_as_float(xa[e] & 0xFFFF0000u);
+    x1[2 * e] = __uint_as_float(xb[e] << 16);
+    x1[2 * e + 1] = __uint_as_float(xb[e] & 0xFFFF0000u);
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ss += x0[e] * x0[e] + x1[e] * x1[e];
+  ss += __shfl_xor(ss, 1, 8);
+  ss += __shfl_xor(ss, 2, 8);
+  ss += __shfl_xor(ss, 4, 8);
+  const float inv = 1.0f / sqrtf(ss * (1.0f / 128) + eps);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float o0[2], o1[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int k = 2 * e + u;
+      const float g0 = __uint_as_float(u ? (ga[e] & 0xFFFF0000u) : (ga[e] << 16));
+      const float g1 = __uint_as_float(u ? (gb[e] & 0xFFFF0000u) : (gb[e] << 16));
+      const float y0 = x0[k] * inv * g0;
+      const float y1 = x1[k] * inv * g1;
+      const float c = cs[e][2 * u], sn = cs[e][2 * u + 1];
+      o0[u] = y0 * c - y1 * sn;
+      o1[u] = y1 * c + y0 * sn;
+    }
+    oa[e] = pack_bf16x2(o0[0], o0[1]);
+    ob[e] = pack_bf16x2(o1[0], o1[1]);
+  }
+}
+
 // ---- direct global -> LDS copies ------------------------------------------
 
 // s_waitcnt immediate that waits until at most n vector-memory operations of

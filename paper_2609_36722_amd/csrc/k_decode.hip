@@ -70,15 +70,48 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
   const int grp = threadIdx.x >> 3;
   const int sub = threadIdx.x & 7;
 
-  const bf16_t* qrow = p.q + ((int64_t)rq.q_row * p.n_q_heads + g * G) * D;
+  // The new token's 4 query rows of this KV head, normalised and rotated
+  // from the raw projection (every key group derives them: a few hundred
+  // ALU operations against the chunk's stream), in the layout of the key
+  // loads: dims 8 sub .. 8 sub + 7 and their rotary partners 64 + 8 sub ...
+  f32x4 cs[4];
+  {
+    const f32x4* cs4 = reinterpret_cast<const f32x4*>(p.rope + (int64_t)rq.pos * 64 + 8 * sub);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) cs[e] = cs4[e];
+  }
+  const bf16_t* qrow = p.q_raw + (int64_t)rq.q_row * p.ld_q + g * G * D;
+  const u32x4 gqa = *reinterpret_cast<const u32x4*>(p.gamma_q + 8 * sub);
+  const u32x4 gqb = *reinterpret_cast<const u32x4*>(p.gamma_q + 64 + 8 * sub);
   u32x4 qa[G], qb[G];
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    qa[h] = *reinterpret_cast<const u32x4*>(qrow + h * D + 8 * sub);
-    qb[h] = *reinterpret_cast<const u32x4*>(qrow + h * D + 64 + 8 * sub);
+  for (int h = 0; h < G; ++h)
+    head_norm_rope(*reinterpret_cast<const u32x4*>(qrow + h * D + 8 * sub),
+                   *reinterpret_cast<const u32x4*>(qrow + h * D + 64 + 8 * sub), gqa, gqb, cs, p.eps, qa[h], qb[h]);
+  bf16_t* kbase = p.k + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
+  bf16_t* vbase = p.v + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
+  // The workgroup whose chunk holds the last key (the new token's) normalises
+  // and rotates that key and writes it and its value into their cache row
+  // before its key loop reads the row (the workgroup barrier orders the
+  // writes of group 0 before every group's loads); no other workgroup reads
+  // the row.
+  if (sid - rq.split0 == rq.n_split - 1) {
+    if (grp == 0) {
+      const bf16_t* kr = p.k_raw + (int64_t)rq.q_row * p.ld_kv + g * D;
+      const bf16_t* vr = p.v_raw + (int64_t)rq.q_row * p.ld_kv + g * D;
+      u32x4 ka, kb;
+      head_norm_rope(*reinterpret_cast<const u32x4*>(kr + 8 * sub), *reinterpret_cast<const u32x4*>(kr + 64 + 8 * sub),
+                     *reinterpret_cast<const u32x4*>(p.gamma_k + 8 * sub),
+                     *reinterpret_cast<const u32x4*>(p.gamma_k + 64 + 8 * sub), cs, p.eps, ka, kb);
+      const int64_t row = (int64_t)(rq.n_keys - 1) * D;
+      *reinterpret_cast<u32x4*>(kbase + row + 8 * sub) = ka;
+      *reinterpret_cast<u32x4*>(kbase + row + 64 + 8 * sub) = kb;
+      *reinterpret_cast<u32x4*>(vbase + row + 8 * sub) = *reinterpret_cast<const u32x4*>(vr + 8 * sub);
+      *reinterpret_cast<u32x4*>(vbase + row + 64 + 8 * sub) = *reinterpret_cast<const u32x4*>(vr + 64 + 8 * sub);
+      __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));  // the stores have reached the cache
+    }
+    __syncthreads();
   }
-  const bf16_t* kbase = p.k + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
-  const bf16_t* vbase = p.v + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
 
   float m[G], l[G], o[G][16];
 #pragma unroll

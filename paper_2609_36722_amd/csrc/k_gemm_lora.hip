@@ -512,8 +512,8 @@ hipError_t launch_gemm_any(const uint16_t* x, const uint16_t* w, int n_tok, int 
                            float scale, const uint16_t* b, int rank, int r_pad, int lora_cols, const float* t_part,
                            GemmEpi epi, uint16_t* out, const GemmPlan* plan, float* split_ws, hipStream_t stream) {
   if (n_tok == 0) return hipSuccess;
-  if (n_tok <= kGemvMaxTok) return launch_gemv(x, w, n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, epi, out,
-                                              stream);
+  if (n_tok <= kGemvMaxTok)
+    return launch_gemv(x, w, n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, epi, out, stream);
   const int n_slice = lora_down_slices(hidden);
   const GemmPlan pl = plan ? *plan : plan_gemm(n_tok, n_out, hidden, r_pad > 0);
   if (pl.tile < 0) return hipErrorInvalidValue;

@@ -2,14 +2,15 @@
 // x W^T with the same epilogue modes and low-rank update as the GEMM, for
 // n_tok <= kGemvMaxTok.  With a handful of tokens each weight is used once
 // per token, so the launch streams W from HBM and an MFMA tile would be
-// mostly empty: every wave owns two consecutive output rows, its 64 lanes
-// read 16-byte chunks of both rows (consecutive lanes, consecutive chunks:
-// whole 128-byte lines) and of every token's x, accumulate bf16 dot2
-// products in fp32, and the rows' sums meet in a wave reduction.  The
-// low-rank term (rows below lora_cols) enters before the reduction: lane j
-// adds t[token][j] * B[row][j], t = scale * x A^T summed once per workgroup
-// (into LDS) from the slice partials of the down-projection kernel.  Lane t
-// then stores token t.
+// mostly empty: a group of KW waves owns two consecutive output rows, its
+// lanes read 16-byte chunks of both rows (consecutive lanes, consecutive
+// chunks: whole 128-byte lines; the KW waves take every KW-th 1 KB piece of
+// the rows, so a long row is cut into fewer sequential load batches) and of
+// every token's x, accumulate bf16 dot2 products in fp32, and the rows' sums
+// meet in a wave reduction (and, for KW > 1, in LDS).  The low-rank term
+// (rows below lora_cols) enters before the reduction: lane j of the group's
+// first wave adds t[token][j] * B[row][j], t = scale * x A^T summed once per
+// workgroup (into LDS) from the slice partials of the down-projection kernel.
 
 #include "common.h"
 #include "kernels.h"
@@ -41,19 +42,22 @@ __device__ __forceinline__ float dot8(u32x4 a, u32x4 b, float c) {
   return c;
 }
 
-template <int T>
+template <int T, int KW>
 __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w, int N,
                                                    int K, const bf16_t* __restrict__ b, int rank, int r_pad,
                                                    int lora_cols, const float* __restrict__ t_part, int n_slice,
                                                    GemmEpi epi, bf16_t* out) {
+  constexpr int kGroups = 4 / KW;      // row pairs per workgroup
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const int n0 = (blockIdx.x * 4 + wave) * 2;
+  const int kp = wave % KW;            // which pieces of the rows this wave takes
+  const int n0 = (blockIdx.x * kGroups + wave / KW) * 2;
   // t = scale * x A^T for the workgroup's rows (all below lora_cols or none:
-  // lora_cols is a multiple of 32, a workgroup owns 8 rows), summed once
-  // from the slice partials into LDS by all threads
+  // lora_cols is a multiple of 32, a workgroup owns at most 8 rows), summed
+  // once from the slice partials into LDS by all threads
   __shared__ float t_lds[T][64];
-  const bool lora_rows = r_pad > 0 && (int)blockIdx.x * 8 < lora_cols;
+  __shared__ f32x2 part[4][T];
+  const bool lora_rows = r_pad > 0 && (int)blockIdx.x * 2 * kGroups < lora_cols;
   if (lora_rows) {
     for (int i = threadIdx.x; i < T * r_pad; i += 256) {
       const int t = i / r_pad, j = i % r_pad;
@@ -63,10 +67,12 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
     }
     __syncthreads();
   }
-  if (n0 >= N) return;
+  const int nc = K / 8;
+  auto xchunk = [&](int t, int c) __attribute__((always_inline)) {
+    return *reinterpret_cast<const u32x4*>(x + (int64_t)t * K + 8 * c);
+  };
   const bf16_t* w0 = w + (int64_t)n0 * K;
   const bf16_t* w1 = w0 + K;
-  const int nc = K / 8;
 
   float acc[2][T];
 #pragma unroll
@@ -75,16 +81,17 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
   // whole batches of kChunkBatch chunks per lane (all loads issued, then the
   // products), then the chunks left one at a time
   constexpr int kChunkBatch = chunk_batch<T>();
-  int c = lane;
-  for (; c + 64 * (kChunkBatch - 1) < nc; c += 64 * kChunkBatch) {
+  constexpr int kStride = 64 * KW;
+  int c = lane + 64 * kp;
+  for (; c + kStride * (kChunkBatch - 1) < nc; c += kStride * kChunkBatch) {
     u32x4 wa[kChunkBatch], wb[kChunkBatch], xv[kChunkBatch][T];
 #pragma unroll
     for (int j = 0; j < kChunkBatch; ++j) {
-      const int cj = c + 64 * j;
+      const int cj = c + kStride * j;
       wa[j] = *reinterpret_cast<const u32x4*>(w0 + 8 * cj);
       wb[j] = *reinterpret_cast<const u32x4*>(w1 + 8 * cj);
 #pragma unroll
-      for (int t = 0; t < T; ++t) xv[j][t] = *reinterpret_cast<const u32x4*>(x + (int64_t)t * K + 8 * cj);
+      for (int t = 0; t < T; ++t) xv[j][t] = xchunk(t, cj);
     }
 #pragma unroll
     for (int j = 0; j < kChunkBatch; ++j)
@@ -94,19 +101,20 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
         acc[1][t] = dot8(wb[j], xv[j][t], acc[1][t]);
       }
   }
-  for (; c < nc; c += 64) {
+  for (; c < nc; c += kStride) {
     const u32x4 wa = *reinterpret_cast<const u32x4*>(w0 + 8 * c);
     const u32x4 wb = *reinterpret_cast<const u32x4*>(w1 + 8 * c);
 #pragma unroll
     for (int t = 0; t < T; ++t) {
-      const u32x4 xv = *reinterpret_cast<const u32x4*>(x + (int64_t)t * K + 8 * c);
+      const u32x4 xv = xchunk(t, c);
       acc[0][t] = dot8(wa, xv, acc[0][t]);
       acc[1][t] = dot8(wb, xv, acc[1][t]);
     }
   }
 
-  // rows below lora_cols: lane j < rank adds t[token][j] * B[row][j]
-  if (lora_rows && lane < rank) {
+  // rows below lora_cols: lane j < rank of the group's first wave adds
+  // t[token][j] * B[row][j]
+  if (lora_rows && kp == 0 && lane < rank) {
     const float b0 = bf16_to_f32(b[(int64_t)n0 * rank + lane]);
     const float b1 = bf16_to_f32(b[(int64_t)(n0 + 1) * rank + lane]);
 #pragma unroll
@@ -124,6 +132,19 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
     if (lane == t) {
       y0 = s0;
       y1 = s1;
+    }
+  }
+  if (KW > 1) {
+    // the group's waves meet in LDS; its first wave finishes the rows
+    if (lane < T) part[wave][lane] = f32x2{y0, y1};
+    __syncthreads();
+    if (kp != 0) return;
+    if (lane < T) {
+#pragma unroll
+      for (int q = 1; q < KW; ++q) {
+        y0 += part[wave + q][lane][0];
+        y1 += part[wave + q][lane][1];
+      }
     }
   }
   if (lane >= T) return;
@@ -145,6 +166,16 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
   *reinterpret_cast<uint32_t*>(out + (int64_t)t * N + n0) = pack_bf16x2(y0, y1);
 }
 
+// Waves per row pair (measured on the model's projection shapes): one for
+// more than 8 tokens, whose x chunks already fill the loads in flight; else
+// four for long rows (K >= 8192, or K >= 4096 from 4 tokens on), two
+// otherwise.
+int gemv_kw(int n_tok, int k_dim) {
+  if (n_tok > 8) return 1;
+  if (k_dim >= 8192 || (n_tok >= 4 && k_dim >= 4096)) return 4;
+  return 2;
+}
+
 }  // namespace
 
 hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, const uint16_t* b,
@@ -154,32 +185,44 @@ hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_ou
   if (n_tok > kGemvMaxTok || n_out % 8 != 0 || k_dim % 8 != 0 || (r_pad > 0 && t_part == nullptr))
     return hipErrorInvalidValue;
   const int n_slice = lora_down_slices(k_dim);
-  const dim3 grid((unsigned)(n_out / 8));
-#define ATTUNER_GEMV(T_)                                                                                     \
-  case T_:                                                                                                   \
-    ATTUNER_LAUNCH("gemv_kernel", gemv_kernel<T_>, grid, dim3(256), stream, x, w, n_out, k_dim, b, rank, r_pad, \
-                   lora_cols, t_part, n_slice, epi, out);                                                     \
+  const int kw = gemv_kw(n_tok, k_dim);
+  const dim3 grid((unsigned)(n_out * kw / 8));
+#define ATTUNER_GEMV_KW(T_, KW_)                                                                             \
+  ATTUNER_LAUNCH("gemv_kernel", (gemv_kernel<T_, KW_>), grid, dim3(256), stream, x, w, n_out, k_dim, b, rank, \
+                 r_pad, lora_cols, t_part, n_slice, epi, out)
+#define ATTUNER_GEMV_SMALL(T_) \
+  case T_:                     \
+    if (kw == 4)               \
+      ATTUNER_GEMV_KW(T_, 4);  \
+    else                       \
+      ATTUNER_GEMV_KW(T_, 2);  \
+    break;
+#define ATTUNER_GEMV_LARGE(T_) \
+  case T_:                     \
+    ATTUNER_GEMV_KW(T_, 1);    \
     break;
   switch (n_tok) {
-    ATTUNER_GEMV(1)
-    ATTUNER_GEMV(2)
-    ATTUNER_GEMV(3)
-    ATTUNER_GEMV(4)
-    ATTUNER_GEMV(5)
-    ATTUNER_GEMV(6)
-    ATTUNER_GEMV(7)
-    ATTUNER_GEMV(8)
-    ATTUNER_GEMV(9)
-    ATTUNER_GEMV(10)
-    ATTUNER_GEMV(11)
-    ATTUNER_GEMV(12)
-    ATTUNER_GEMV(13)
-    ATTUNER_GEMV(14)
-    ATTUNER_GEMV(15)
-    ATTUNER_GEMV(16)
+    ATTUNER_GEMV_SMALL(1)
+    ATTUNER_GEMV_SMALL(2)
+    ATTUNER_GEMV_SMALL(3)
+    ATTUNER_GEMV_SMALL(4)
+    ATTUNER_GEMV_SMALL(5)
+    ATTUNER_GEMV_SMALL(6)
+    ATTUNER_GEMV_SMALL(7)
+    ATTUNER_GEMV_SMALL(8)
+    ATTUNER_GEMV_LARGE(9)
+    ATTUNER_GEMV_LARGE(10)
+    ATTUNER_GEMV_LARGE(11)
+    ATTUNER_GEMV_LARGE(12)
+    ATTUNER_GEMV_LARGE(13)
+    ATTUNER_GEMV_LARGE(14)
+    ATTUNER_GEMV_LARGE(15)
+    ATTUNER_GEMV_LARGE(16)
     default: return hipErrorInvalidValue;
   }
-#undef ATTUNER_GEMV
+#undef ATTUNER_GEMV_KW
+#undef ATTUNER_GEMV_SMALL
+#undef ATTUNER_GEMV_LARGE
   return hipGetLastError();
 }
 

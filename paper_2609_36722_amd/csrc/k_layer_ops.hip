@@ -47,17 +47,16 @@ __global__ __launch_bounds__(256) void rms_norm_rows_kernel(const bf16_t* __rest
   const int n_chunk = dim / 8;
   u32x4 v[kMaxPass];
   float ss = 0.f;
+  // every load first (chunks past the row read as zeros, which add nothing),
+  // then the squares
 #pragma unroll
   for (int k = 0; k < kMaxPass; ++k) {
     const int c = lane + 64 * k;
     v[k] = u32x4{0u, 0u, 0u, 0u};
     if (c < n_chunk) v[k] = *reinterpret_cast<const u32x4*>(xr + 8 * c);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float lo = __uint_as_float(v[k][e] << 16), hi = __uint_as_float(v[k][e] & 0xFFFF0000u);
-      ss += lo * lo + hi * hi;
-    }
   }
+#pragma unroll
+  for (int k = 0; k < kMaxPass; ++k) ss = accum_squares(ss, v[k]);
   ss = wave_sum(ss);
   const float inv = 1.0f / sqrtf(ss / (float)dim + eps);
   bf16_t* orow = out + (int64_t)r * dim;
@@ -66,14 +65,7 @@ __global__ __launch_bounds__(256) void rms_norm_rows_kernel(const bf16_t* __rest
     const int c = lane + 64 * k;
     if (c >= n_chunk) continue;
     const u32x4 g = *reinterpret_cast<const u32x4*>(gamma + 8 * c);
-    u32x4 o;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float lo = __uint_as_float(v[k][e] << 16) * inv * __uint_as_float(g[e] << 16);
-      const float hi = __uint_as_float(v[k][e] & 0xFFFF0000u) * inv * __uint_as_float(g[e] & 0xFFFF0000u);
-      o[e] = pack_bf16x2(lo, hi);
-    }
-    *reinterpret_cast<u32x4*>(orow + 8 * c) = o;
+    *reinterpret_cast<u32x4*>(orow + 8 * c) = norm_chunk(v[k], g, inv);
   }
 }
 

@@ -8,7 +8,9 @@
 // 16-byte loads), so the rotation needs no data exchange and the RMS is an
 // in-lane sum plus three exchanges within the group.  Angles come from a
 // host-built table of (cos, sin) of pos * theta^(-2j/128), evaluated in fp64
-// and stored fp32.  Rows, gamma and outputs are 16-byte aligned.
+// and stored fp32.  Rows, gamma and outputs are 16-byte aligned.  The
+// arithmetic (head_norm_rope) is shared with the decode kernel, which applies
+// it to the new token inside its own launch.
 
 #include "common.h"
 #include "kernels.h"
@@ -63,39 +65,8 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(NormRopeParams p) {
     va = *reinterpret_cast<const u32x4*>(vs + j0);
     vb = *reinterpret_cast<const u32x4*>(vs + 64 + j0);
   }
-  float x0[8], x1[8];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    x0[2 * e] = __uint_as_float(xa[e] << 16);
-    x0[2 * e + 1] = __uint_as_float(xa[e] & 0xFFFF0000u);
-    x1[2 * e] = __uint_as_float(xb[e] << 16);
-    x1[2 * e + 1] = __uint_as_float(xb[e] & 0xFFFF0000u);
-  }
-  float ss = 0.f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) ss += x0[e] * x0[e] + x1[e] * x1[e];
-  ss += __shfl_xor(ss, 1, 8);
-  ss += __shfl_xor(ss, 2, 8);
-  ss += __shfl_xor(ss, 4, 8);
-  const float inv = 1.0f / sqrtf(ss * (1.0f / kHeadDim) + p.eps);
   u32x4 oa, ob;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    float o0[2], o1[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int k = 2 * e + u;
-      const float g0 = __uint_as_float(u ? (ga[e] & 0xFFFF0000u) : (ga[e] << 16));
-      const float g1 = __uint_as_float(u ? (gb[e] & 0xFFFF0000u) : (gb[e] << 16));
-      const float y0 = x0[k] * inv * g0;
-      const float y1 = x1[k] * inv * g1;
-      const float c = cs[e][2 * u], sn = cs[e][2 * u + 1];
-      o0[u] = y0 * c - y1 * sn;
-      o1[u] = y1 * c + y0 * sn;
-    }
-    oa[e] = pack_bf16x2(o0[0], o0[1]);
-    ob[e] = pack_bf16x2(o1[0], o1[1]);
-  }
+  head_norm_rope(xa, xb, ga, gb, cs, p.eps, oa, ob);
   *reinterpret_cast<u32x4*>(dst + j0) = oa;
   *reinterpret_cast<u32x4*>(dst + 64 + j0) = ob;
 

@@ -193,17 +193,28 @@ hipError_t launch_attention(const AttnParams& p, hipStream_t stream);
 // ---- decode: one new token per request over its whole cache ----------------
 
 struct DecodeReq {
-  int32_t q_row;     // row of the request's token in q / o
+  int32_t q_row;     // row of the request's token in q_raw / k_raw / v_raw / o
   int32_t kv_start;  // cache row of key 0 of the request
-  int32_t n_keys;    // keys it attends to (its own, already in the cache, is the last)
+  int32_t n_keys;    // keys it attends to (its own, written by the launch, is the last)
   int32_t split0;    // first key chunk of the request in the launch
   int32_t n_split;   // chunks of the request (ceil(n_keys / chunk))
+  int32_t pos;       // RoPE position of the new token
 };
 
+// The new token's q/k/v rows come raw from the projection: the kernel applies
+// the per-head RMSNorm (gamma_q, gamma_k) and RoPE (table rope[pos][64] of
+// (cos, sin)) and writes k and v into cache row kv_start + n_keys - 1.
 struct DecodeParams {
-  const uint16_t* q;       // [rows][Hq][128]
-  const uint16_t* k;       // K head 0; head stride kv_head_stride
-  const uint16_t* v;
+  const uint16_t* q_raw;   // row r at q_raw + r * ld_q: [Hq][128]
+  const uint16_t* k_raw;   // row r at k_raw + r * ld_kv: [Hkv][128]
+  const uint16_t* v_raw;
+  int64_t ld_q, ld_kv;
+  const uint16_t* gamma_q;
+  const uint16_t* gamma_k;
+  const float2* rope;
+  float eps;
+  uint16_t* k;             // K head 0 of the cache; head stride kv_head_stride
+  uint16_t* v;
   int64_t kv_head_stride;
   uint16_t* o;             // [rows][Hq][128]
   float* part_o;           // [total_splits][Hq][128] fp32, unnormalised

@@ -190,3 +190,32 @@ def test_decode_64_requests_and_the_limit():
                             q[:, HQ * D + HKV * D:], ld, g, g, kv, 65, torch.empty(65, HQ, D, dtype=torch.bfloat16,
                                                                                    device="cuda"))
         assert e.value.status == -5
+
+
+def test_decode_new_key_row_equals_norm_rope_kernel():
+    # the decode launch normalises and rotates the new key itself (in the
+    # workgroup whose chunk ends with it): the cache rows it writes equal, bit
+    # for bit, those of the standalone norm + RoPE kernel on the same rows
+    _say("decode new key row vs norm + RoPE kernel")
+    rng = np.random.default_rng(49)
+    ctx_len = [0, 127, 1000, 4095]
+    n = len(ctx_len)
+    cu = [0]
+    for c in ctx_len:
+        cu.append(cu[-1] + c + 3)
+    rows = cu[-1]
+    with Context(ModelCfg(n_layers=2, hidden=256), pool_pages=1) as ctx:
+        bf = dict(dtype=torch.bfloat16, device="cuda")
+        kv_a = dev_bf16(_bits(rng, (2, 2, HKV, rows, D)))
+        kv_b = kv_a.clone()
+        qkv = dev_bf16(_bits(rng, (n, HQ * D + 2 * HKV * D), 2.0))
+        gq = dev_bf16(sd.f32_to_bf16_bits(rng.uniform(0.5, 1.5, D).astype(np.float32)))
+        gk = dev_bf16(sd.f32_to_bf16_bits(rng.uniform(0.5, 1.5, D).astype(np.float32)))
+        ld = qkv.shape[1]
+        q, k, v = qkv[:, :HQ * D], qkv[:, HQ * D:HQ * D + HKV * D], qkv[:, HQ * D + HKV * D:]
+        o = torch.empty(n, HQ, D, **bf)
+        ctx.decode_attn(1, cu, ctx_len, None, q, ld, k, v, ld, gq, gk, kv_a, rows, o)
+        q_hat = torch.empty(n, HQ, D, **bf)
+        ctx.qk_norm_rope(1, list(range(n + 1)), cu, ctx_len, None, q, ld, k, v, ld, gq, gk, q_hat, kv_b, rows)
+        torch.cuda.synchronize()
+        assert torch.equal(kv_a.view(torch.int16), kv_b.view(torch.int16))
