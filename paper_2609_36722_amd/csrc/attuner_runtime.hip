@@ -1100,11 +1100,13 @@ attuner_status attuner_lm_head_argmax(attuner_ctx* c, int32_t n_rows, const void
   if (!ids) return fail(ATTUNER_EINVAL, "null ids");
   DeviceGuard dg(c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  HIP_TRY(c->ws_logits.ensure((size_t)n_rows * vocab * sizeof(float)));
+  const size_t logit_bytes = (size_t)n_rows * vocab * sizeof(float);
+  HIP_TRY(c->ws_logits.ensure(logit_bytes + argmax_scratch_bytes(n_rows)));
   float* logits = static_cast<float*>(c->ws_logits.ptr);
   st = run_gemm(c, n_rows, x, H, w_lm, vocab, GemmEpi{kEpiF32, nullptr, logits}, nullptr, s);
   if (st != ATTUNER_OK) return st;
-  HIP_TRY(launch_argmax_rows(logits, n_rows, vocab, ids, max_logit, s));
+  HIP_TRY(launch_argmax_rows(logits, n_rows, vocab, ids, max_logit, static_cast<char*>(c->ws_logits.ptr) + logit_bytes,
+                             s));
   return ATTUNER_OK;
 }
 

@@ -11,9 +11,9 @@
 // is an in-lane sum plus a wave reduction, and the output is written from
 // the same registers.  dim is a multiple of 8 and at most 64 * 8 * kMaxPass.
 //
-// argmax_rows_kernel: one 1024-thread workgroup per row; thread t scans the
-// 16-byte groups t, t + 1024, ... keeping (largest value, smallest index),
-// then a wave reduction and one through LDS.
+// argmax: 64 workgroups per row each scan a slice of the row's 16-byte groups
+// keeping (largest value, smallest index), reduced in the wave and through
+// LDS; a second one-wave launch per row reduces the 64 slice results.
 
 #include "common.h"
 #include "kernels.h"
@@ -74,28 +74,9 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
 
-__global__ __launch_bounds__(1024) void argmax_rows_kernel(const float* __restrict__ logits, int n,
-                                                           int32_t* __restrict__ ids, float* __restrict__ max_out) {
-  __shared__ float sv[16];
-  __shared__ int si[16];
-  const float* row = logits + (int64_t)blockIdx.x * n;
-  float bv = -INFINITY;
-  int bi = n;  // no element seen
-  const int n4 = n / 4;
-  for (int g = threadIdx.x; g < n4; g += 1024) {
-    const f32x4 v = *reinterpret_cast<const f32x4*>(row + 4 * g);
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (better(v[e], 4 * g + e, bv, bi)) {
-        bv = v[e];
-        bi = 4 * g + e;
-      }
-  }
-  for (int i = 4 * n4 + threadIdx.x; i < n; i += 1024)
-    if (better(row[i], i, bv, bi)) {
-      bv = row[i];
-      bi = i;
-    }
+constexpr int kArgmaxSlices = 64;  // workgroups per row in the first pass
+
+__device__ __forceinline__ void wave_best(float& bv, int& bi) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     const float ov = __shfl_xor(bv, off, 64);
@@ -105,6 +86,38 @@ __global__ __launch_bounds__(1024) void argmax_rows_kernel(const float* __restri
       bi = oi;
     }
   }
+}
+
+// First pass: workgroup (slice, row) finds the best (value, index) of its
+// slice of the row's 16-byte groups (the last slice also takes the values
+// past the last whole group).
+__global__ __launch_bounds__(256) void argmax_slices_kernel(const float* __restrict__ logits, int n,
+                                                            float* __restrict__ part_v, int32_t* __restrict__ part_i) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int sl = blockIdx.x;
+  const float* row = logits + (int64_t)blockIdx.y * n;
+  const int n4 = n / 4;
+  const int per = (n4 + kArgmaxSlices - 1) / kArgmaxSlices;
+  const int g0 = sl * per, g1 = min(n4, g0 + per);
+  float bv = -INFINITY;
+  int bi = n;  // no element seen
+  for (int g = g0 + (int)threadIdx.x; g < g1; g += 256) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(row + 4 * g);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (better(v[e], 4 * g + e, bv, bi)) {
+        bv = v[e];
+        bi = 4 * g + e;
+      }
+  }
+  if (sl == kArgmaxSlices - 1)
+    for (int i = 4 * n4 + threadIdx.x; i < n; i += 256)
+      if (better(row[i], i, bv, bi)) {
+        bv = row[i];
+        bi = i;
+      }
+  wave_best(bv, bi);
   const int wave = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
     sv[wave] = bv;
@@ -112,11 +125,26 @@ __global__ __launch_bounds__(1024) void argmax_rows_kernel(const float* __restri
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int w = 1; w < 16; ++w)
+    for (int w = 1; w < 4; ++w)
       if (better(sv[w], si[w], bv, bi)) {
         bv = sv[w];
         bi = si[w];
       }
+    part_v[(int64_t)blockIdx.y * kArgmaxSlices + sl] = bv;
+    part_i[(int64_t)blockIdx.y * kArgmaxSlices + sl] = bi;
+  }
+}
+
+// Second pass: one wave per row over its slices' results.  The slices are
+// disjoint index ranges, so the (value, smallest index) order gives the
+// row's argmax whatever the order of the reduction.
+__global__ __launch_bounds__(64) void argmax_merge_kernel(const float* __restrict__ part_v,
+                                                          const int32_t* __restrict__ part_i, int n,
+                                                          int32_t* __restrict__ ids, float* __restrict__ max_out) {
+  float bv = part_v[(int64_t)blockIdx.x * kArgmaxSlices + threadIdx.x];
+  int bi = part_i[(int64_t)blockIdx.x * kArgmaxSlices + threadIdx.x];
+  wave_best(bv, bi);
+  if (threadIdx.x == 0) {
     ids[blockIdx.x] = bi < n ? bi : 0;  // a row of NaNs only: index 0
     if (max_out != nullptr) max_out[blockIdx.x] = bv;
   }
@@ -142,11 +170,17 @@ hipError_t launch_rms_norm_rows(const uint16_t* x, int64_t ld_x, const int32_t* 
   return hipGetLastError();
 }
 
-hipError_t launch_argmax_rows(const float* logits, int n_rows, int n, int32_t* ids, float* max_out,
+size_t argmax_scratch_bytes(int n_rows) { return (size_t)n_rows * kArgmaxSlices * (sizeof(float) + sizeof(int32_t)); }
+
+hipError_t launch_argmax_rows(const float* logits, int n_rows, int n, int32_t* ids, float* max_out, void* scratch,
                               hipStream_t stream) {
   if (n_rows == 0) return hipSuccess;
-  ATTUNER_LAUNCH("argmax_rows_kernel", argmax_rows_kernel, dim3((unsigned)n_rows), dim3(1024), stream, logits, n,
-                 ids, max_out);
+  float* part_v = static_cast<float*>(scratch);
+  int32_t* part_i = reinterpret_cast<int32_t*>(part_v + (size_t)n_rows * kArgmaxSlices);
+  ATTUNER_LAUNCH("argmax_slices_kernel", argmax_slices_kernel, dim3(kArgmaxSlices, (unsigned)n_rows), dim3(256),
+                 stream, logits, n, part_v, part_i);
+  ATTUNER_LAUNCH("argmax_merge_kernel", argmax_merge_kernel, dim3((unsigned)n_rows), dim3(kArgmaxSlices), stream,
+                 part_v, part_i, n, ids, max_out);
   return hipGetLastError();
 }
 

@@ -113,8 +113,10 @@ hipError_t launch_rms_norm_rows(const uint16_t* x, int64_t ld_x, const int32_t* 
                                 const uint16_t* gamma, float eps, uint16_t* out, hipStream_t stream);
 
 // ids[r] = the smallest index of the largest value of logits[r][0 .. n-1]
-// (fp32), max_out[r] = that value (max_out may be null).
-hipError_t launch_argmax_rows(const float* logits, int n_rows, int n, int32_t* ids, float* max_out,
+// (fp32), max_out[r] = that value (max_out may be null).  scratch: device
+// memory of argmax_scratch_bytes(n_rows) for the per-slice results.
+size_t argmax_scratch_bytes(int n_rows);
+hipError_t launch_argmax_rows(const float* logits, int n_rows, int n, int32_t* ids, float* max_out, void* scratch,
                               hipStream_t stream);
 
 // ---- a4: QK-RMSNorm + RoPE ------------------------------------------------
