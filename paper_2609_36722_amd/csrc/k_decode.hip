@@ -70,6 +70,33 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
   const int grp = threadIdx.x >> 3;
   const int sub = threadIdx.x & 7;
 
+  bf16_t* kbase = p.k + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
+  bf16_t* vbase = p.v + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
+  // Steps of U keys per group, double-buffered: the loads of step i + 1 are
+  // issued before the arithmetic of step i.
+  struct Buf {
+    u32x4 ka[U], kc[U], va[U], vc[U];
+  };
+  auto load = [&](int key0, Buf& b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int key = min(key0 + u * GROUPS, k1 - 1);  // past the chunk: a valid row, masked below
+      const bf16_t* kr = kbase + (int64_t)key * D;
+      const bf16_t* vr = vbase + (int64_t)key * D;
+      b.ka[u] = *reinterpret_cast<const u32x4*>(kr + 8 * sub);
+      b.kc[u] = *reinterpret_cast<const u32x4*>(kr + 64 + 8 * sub);
+      b.va[u] = *reinterpret_cast<const u32x4*>(vr + 8 * sub);
+      b.vc[u] = *reinterpret_cast<const u32x4*>(vr + 64 + 8 * sub);
+    }
+  };
+  // The first step's keys and values are requested before the query
+  // prologue, which they do not depend on; the workgroup whose chunk holds
+  // the new key requests them after writing that key's row (below).
+  const bool last = sid - rq.split0 == rq.n_split - 1;
+  const int key_first = k0 + grp;
+  Buf b0, b1;
+  if (!last) load(key_first, b0);
+
   // The new token's 4 query rows of this KV head, normalised and rotated
   // from the raw projection (every key group derives them: a few hundred
   // ALU operations against the chunk's stream), in the layout of the key
@@ -88,14 +115,12 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
   for (int h = 0; h < G; ++h)
     head_norm_rope(*reinterpret_cast<const u32x4*>(qrow + h * D + 8 * sub),
                    *reinterpret_cast<const u32x4*>(qrow + h * D + 64 + 8 * sub), gqa, gqb, cs, p.eps, qa[h], qb[h]);
-  bf16_t* kbase = p.k + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
-  bf16_t* vbase = p.v + g * p.kv_head_stride + (int64_t)rq.kv_start * D;
   // The workgroup whose chunk holds the last key (the new token's) normalises
   // and rotates that key and writes it and its value into their cache row
   // before its key loop reads the row (the workgroup barrier orders the
   // writes of group 0 before every group's loads); no other workgroup reads
   // the row.
-  if (sid - rq.split0 == rq.n_split - 1) {
+  if (last) {
     if (grp == 0) {
       const bf16_t* kr = p.k_raw + (int64_t)rq.q_row * p.ld_kv + g * D;
       const bf16_t* vr = p.v_raw + (int64_t)rq.q_row * p.ld_kv + g * D;
@@ -111,6 +136,7 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
       __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));  // the stores have reached the cache
     }
     __syncthreads();
+    load(key_first, b0);
   }
 
   float m[G], l[G], o[G][16];
@@ -122,23 +148,6 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
     for (int i = 0; i < 16; ++i) o[h][i] = 0.f;
   }
 
-  // Steps of U keys per group, double-buffered: the loads of step i + 1 are
-  // issued before the arithmetic of step i.
-  struct Buf {
-    u32x4 ka[U], kc[U], va[U], vc[U];
-  };
-  auto load = [&](int key0, Buf& b) __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int key = min(key0 + u * GROUPS, k1 - 1);  // past the chunk: a valid row, masked below
-      const bf16_t* kr = kbase + (int64_t)key * D;
-      const bf16_t* vr = vbase + (int64_t)key * D;
-      b.ka[u] = *reinterpret_cast<const u32x4*>(kr + 8 * sub);
-      b.kc[u] = *reinterpret_cast<const u32x4*>(kr + 64 + 8 * sub);
-      b.va[u] = *reinterpret_cast<const u32x4*>(vr + 8 * sub);
-      b.vc[u] = *reinterpret_cast<const u32x4*>(vr + 64 + 8 * sub);
-    }
-  };
   auto step = [&](int key0, const Buf& b) __attribute__((always_inline)) {
     float sc[U][G];
 #pragma unroll
@@ -189,10 +198,8 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
   };
 
   constexpr int STEP = GROUPS * U;
-  int key0 = k0 + grp;
+  int key0 = key_first;
   if (key0 < k1) {
-    Buf b0, b1;
-    load(key0, b0);
     while (true) {
       if (key0 + STEP < k1) load(key0 + STEP, b1);
       step(key0, b0);
