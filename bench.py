@@ -935,7 +935,7 @@ def decode_main(args):
     attn_gbps = (kv_bytes + io_bytes) / (attn_ms * 1e-3) / 1e9
     # the projection of a few tokens: the weight-streaming GEMV (+ the LoRA
     # down-projection kernel); more tokens take the MFMA GEMM
-    proj = [k for k in ("gemv_kernel", "lora_down_kernel", "gemm_lora_kernel") if k in per_kernel]
+    proj = [k for k in ("gemv_kernel", "gemv_mfma_kernel", "lora_down_kernel", "gemm_lora_kernel") if k in per_kernel]
     gemm_ms = sum(per_kernel[k]["avg_ms"] for k in proj)
     gemm_w_gbps = n_out * H * 2 / (gemm_ms * 1e-3) / 1e9
     log(args, f"decode step {ms_step:.3f} ms ({n_req / (ms_step * 1e-3):.1f} tokens/s); decode attention "

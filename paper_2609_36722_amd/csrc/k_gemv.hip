@@ -22,6 +22,23 @@ namespace {
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
+// t[i] = sum over the n_slice slice partials p[z * stride + i], added in slice
+// order; the loads go out eight at a time (one round trip per eight slices,
+// not one per slice)
+__device__ __forceinline__ float slice_sum(const float* __restrict__ p, int n_slice, int64_t stride, int64_t i) {
+  float tv = 0.f;
+  int z = 0;
+  for (; z + 8 <= n_slice; z += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = p[(z + u) * stride + i];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) tv += v[u];
+  }
+  for (; z < n_slice; ++z) tv += p[z * stride + i];
+  return tv;
+}
+
 // 16-byte chunks per row and lane in flight: fewer for more tokens, which
 // each add a chunk of x per chunk of W
 template <int T>
@@ -61,9 +78,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
   if (lora_rows) {
     for (int i = threadIdx.x; i < T * r_pad; i += 256) {
       const int t = i / r_pad, j = i % r_pad;
-      float tv = 0.f;
-      for (int z = 0; z < n_slice; ++z) tv += t_part[((int64_t)z * T + t) * r_pad + j];
-      t_lds[t][j] = tv;
+      t_lds[t][j] = slice_sum(t_part, n_slice, (int64_t)T * r_pad, (int64_t)t * r_pad + j);
     }
     __syncthreads();
   }
@@ -166,6 +181,124 @@ __global__ __launch_bounds__(256) void gemv_kernel(const bf16_t* __restrict__ x,
   *reinterpret_cast<uint32_t*>(out + (int64_t)t * N + n0) = pack_bf16x2(y0, y1);
 }
 
+// The same product on the matrix cores, for more tokens: with 16 tokens the
+// dot-product form reads every x chunk again for each row pair (x traffic
+// 8 times W's), while a 16 x 16 x 32 MFMA takes 16 tokens against 16 rows at
+// once.  Workgroup = 16 output rows; lane l of a wave loads 64 contiguous
+// bytes of row l % 16 and of token l % 16's x at k offset 32 (l / 16) of a
+// 128-wide batch, and the four 16-byte pieces feed four MFMAs (the product
+// sums over k, so any k order shared by both operands is exact).  The eight
+// waves take every eighth batch and meet in LDS; tokens past n_tok are zero.
+template <int CB, int NW>
+__global__ __launch_bounds__(64 * NW) void gemv_mfma_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w,
+                                                        int T, int N, int K, const bf16_t* __restrict__ b, int rank,
+                                                        int r_pad, int lora_cols, const float* __restrict__ t_part,
+                                                        int n_slice, GemmEpi epi, bf16_t* out) {
+  __shared__ float t_lds[16][64];
+  __shared__ f32x4 part[NW][64];
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int n0 = blockIdx.x * 16;
+  const bool lora_rows = r_pad > 0 && n0 < lora_cols;  // lora_cols % 32 == 0: all 16 rows or none
+  if (lora_rows) {
+    for (int i = threadIdx.x; i < T * r_pad; i += 64 * NW) {
+      const int t = i / r_pad, j = i % r_pad;
+      t_lds[t][j] = slice_sum(t_part, n_slice, (int64_t)T * r_pad, (int64_t)t * r_pad + j);
+    }
+  }
+  const int col = lane & 15, grp = lane >> 4;
+  const bool tok_ok = col < T;
+  const bf16_t* wr = w + (int64_t)(n0 + col) * K + 32 * grp;
+  const bf16_t* xr = x + (int64_t)min(col, T - 1) * K + 32 * grp;
+  const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+  // wave 0 adds the low-rank term at the end: its B row (rank <= 16) is
+  // requested now, with the weights
+  constexpr int kPreRank = 16;
+  float bpre[kPreRank];
+  const bool pre = lora_rows && wave == 0 && rank <= kPreRank;
+  if (pre) {
+#pragma unroll
+    for (int j = 0; j < kPreRank; ++j) bpre[j] = j < rank ? bf16_to_f32(b[(int64_t)(n0 + col) * rank + j]) : 0.f;
+  }
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nb = K / 128;
+  int bi = wave;
+  for (; bi + NW * (CB - 1) < nb; bi += NW * CB) {
+    u32x4 wv[CB][4], xv[CB][4];
+#pragma unroll
+    for (int j = 0; j < CB; ++j) {
+      const int kb = (bi + NW * j) * 128;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        wv[j][e] = *reinterpret_cast<const u32x4*>(wr + kb + 8 * e);
+        xv[j][e] = *reinterpret_cast<const u32x4*>(xr + kb + 8 * e);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < CB; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(tok_ok ? xv[j][e] : zero), as_bf16x8(wv[j][e]), acc,
+                                                      0, 0, 0);
+  }
+  for (; bi < nb; bi += NW) {
+    const int kb = bi * 128;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const u32x4 wv = *reinterpret_cast<const u32x4*>(wr + kb + 8 * e);
+      const u32x4 xv = *reinterpret_cast<const u32x4*>(xr + kb + 8 * e);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(tok_ok ? xv : zero), as_bf16x8(wv), acc, 0, 0, 0);
+    }
+  }
+  part[wave][lane] = acc;
+  __syncthreads();
+  if (wave != 0) return;
+  // acc[v] = C[token 4 grp + v][row n0 + col]
+  const int n = n0 + col;
+  float y[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    y[v] = part[0][lane][v];
+#pragma unroll
+    for (int q = 1; q < NW; ++q) y[v] += part[q][lane][v];
+  }
+  if (pre) {
+#pragma unroll
+    for (int j = 0; j < kPreRank; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (j < rank && 4 * grp + v < T) y[v] = fmaf(t_lds[4 * grp + v][j], bpre[j], y[v]);
+  } else if (lora_rows) {
+    for (int j = 0; j < rank; ++j) {
+      const float bj = bf16_to_f32(b[(int64_t)n * rank + j]);
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (4 * grp + v < T) y[v] = fmaf(t_lds[4 * grp + v][j], bj, y[v]);
+    }
+  }
+  float yp[4];  // the partner row's value (row n ^ 1, lane l ^ 1): SwiGLU pairs
+#pragma unroll
+  for (int v = 0; v < 4; ++v) yp[v] = __shfl_xor(y[v], 1, 64);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int t = 4 * grp + v;
+    if (t >= T) continue;
+    if (epi.mode == kEpiF32) {
+      epi.out_f32[(int64_t)t * N + n] = y[v];
+    } else if (epi.mode == kEpiSwiglu) {
+      if ((col & 1) == 0) out[(int64_t)t * (N / 2) + n / 2] = f32_to_bf16(y[v] / (1.0f + __expf(-y[v])) * yp[v]);
+    } else if (epi.mode == kEpiResidual) {
+      out[(int64_t)t * N + n] = f32_to_bf16(y[v] + bf16_to_f32(epi.residual[(int64_t)t * N + n]));
+    } else {
+      out[(int64_t)t * N + n] = f32_to_bf16(y[v]);
+    }
+  }
+}
+
+// From this many tokens the matrix-core form (k_dim % 128 == 0, n_out % 16
+// == 0) replaces the dot-product one.
+constexpr int kGemvMfmaMinTok = 9;
+
 // Waves per row pair (measured on the model's projection shapes): one for
 // more than 8 tokens, whose x chunks already fill the loads in flight; else
 // four for long rows (K >= 8192, or K >= 4096 from 4 tokens on), two
@@ -185,6 +318,11 @@ hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_ou
   if (n_tok > kGemvMaxTok || n_out % 8 != 0 || k_dim % 8 != 0 || (r_pad > 0 && t_part == nullptr))
     return hipErrorInvalidValue;
   const int n_slice = lora_down_slices(k_dim);
+  if (n_tok >= kGemvMfmaMinTok && k_dim % 128 == 0 && n_out % 16 == 0) {
+    ATTUNER_LAUNCH("gemv_mfma_kernel", (gemv_mfma_kernel<2, 8>), dim3((unsigned)(n_out / 16)), dim3(512), stream, x, w,
+                   n_tok, n_out, k_dim, b, rank, r_pad, lora_cols, t_part, n_slice, epi, out);
+    return hipGetLastError();
+  }
   const int kw = gemv_kw(n_tok, k_dim);
   const dim3 grid((unsigned)(n_out * kw / 8));
 #define ATTUNER_GEMV_KW(T_, KW_)                                                                             \

@@ -92,7 +92,8 @@ hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, int n_tok, int n_ou
 // The same product for at most kGemvMaxTok tokens as a weight-streaming
 // GEMV (any mode; the low-rank term needs t_part from launch_lora_down);
 // n_out and k_dim multiples of 8.  launch_gemm_lora and launch_gemm route
-// such token counts here.
+// such token counts here; from 9 tokens (k_dim % 128 == 0, n_out % 16 ==
+// 0) the GEMV runs on the matrix cores.
 constexpr int kGemvMaxTok = 16;
 hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, const uint16_t* b,
                        int rank, int r_pad, int lora_cols, const float* t_part, GemmEpi epi, uint16_t* out,
