@@ -357,3 +357,18 @@ def test_few_token_modes(T):
         assert_intermediate_close(host_f64(hd), oracle.linear(d(g), d(wd), d(h)), "down + residual")
         assert_intermediate_close(host_f64(sw), oracle.swiglu(d(x), d(wg), d(wu)), "swiglu")
         _check_pick(ids.cpu().numpy(), mx.cpu().numpy().astype(np.float64), d(x), d(wl))
+
+
+@pytest.mark.parametrize("T", [3, 12])
+def test_few_token_k_not_a_multiple_of_128(T):
+    # k = 320 (a multiple of 64, not of 128): 12 tokens stay on the dot-product
+    # GEMV instead of the matrix-core one; the residual added in place
+    _say(f"few-token K=320 T={T}")
+    rng = np.random.default_rng(400 + T)
+    d = oracle.decode_bf16
+    with Context(ModelCfg(n_layers=1, hidden=320), pool_pages=0) as ctx:
+        x, w, h = _bits(rng, (T, 320)), _bits(rng, (512, 320), 1 / math.sqrt(320)), _bits(rng, (T, 512))
+        hd = dev_bf16(h)
+        ctx.linear(dev_bf16(x), dev_bf16(w), hd, residual=hd)
+        torch.cuda.synchronize()
+        assert_intermediate_close(host_f64(hd), oracle.linear(d(x), d(w), d(h)), "linear + residual")
