@@ -45,15 +45,19 @@ __global__ __launch_bounds__(256) void rms_norm_rows_kernel(const bf16_t* __rest
   const int64_t src_row = rows != nullptr ? rows[r] : r;
   const bf16_t* xr = x + src_row * ld_x;
   const int n_chunk = dim / 8;
-  u32x4 v[kMaxPass];
+  u32x4 v[kMaxPass], g[kMaxPass];
   float ss = 0.f;
-  // every load first (chunks past the row read as zeros, which add nothing),
-  // then the squares
+  // every load first, gamma's with the row's (one round trip; chunks past
+  // the row read as zeros, which add nothing), then the squares
 #pragma unroll
   for (int k = 0; k < kMaxPass; ++k) {
     const int c = lane + 64 * k;
     v[k] = u32x4{0u, 0u, 0u, 0u};
-    if (c < n_chunk) v[k] = *reinterpret_cast<const u32x4*>(xr + 8 * c);
+    g[k] = v[k];
+    if (c < n_chunk) {
+      v[k] = *reinterpret_cast<const u32x4*>(xr + 8 * c);
+      g[k] = *reinterpret_cast<const u32x4*>(gamma + 8 * c);
+    }
   }
 #pragma unroll
   for (int k = 0; k < kMaxPass; ++k) ss = accum_squares(ss, v[k]);
@@ -64,8 +68,7 @@ __global__ __launch_bounds__(256) void rms_norm_rows_kernel(const bf16_t* __rest
   for (int k = 0; k < kMaxPass; ++k) {
     const int c = lane + 64 * k;
     if (c >= n_chunk) continue;
-    const u32x4 g = *reinterpret_cast<const u32x4*>(gamma + 8 * c);
-    *reinterpret_cast<u32x4*>(orow + 8 * c) = norm_chunk(v[k], g, inv);
+    *reinterpret_cast<u32x4*>(orow + 8 * c) = norm_chunk(v[k], g[k], inv);
   }
 }
 
