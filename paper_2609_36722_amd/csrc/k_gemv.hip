@@ -23,19 +23,17 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // t[i] = sum over the n_slice slice partials p[z * stride + i], added in slice
-// order; the loads go out eight at a time (one round trip per eight slices,
-// not one per slice)
+// order; the loads go out sixteen at a time (one round trip for up to 16
+// slices, i.e. a hidden size up to 4096; missing slices add zero)
 __device__ __forceinline__ float slice_sum(const float* __restrict__ p, int n_slice, int64_t stride, int64_t i) {
   float tv = 0.f;
-  int z = 0;
-  for (; z + 8 <= n_slice; z += 8) {
-    float v[8];
+  for (int z = 0; z < n_slice; z += 16) {
+    float v[16];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = p[(z + u) * stride + i];
+    for (int u = 0; u < 16; ++u) v[u] = z + u < n_slice ? p[(z + u) * stride + i] : 0.f;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) tv += v[u];
+    for (int u = 0; u < 16; ++u) tv += v[u];
   }
-  for (; z < n_slice; ++z) tv += p[z * stride + i];
   return tv;
 }
 
