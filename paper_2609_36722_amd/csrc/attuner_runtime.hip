@@ -484,14 +484,18 @@ attuner_status run_decode(attuner_ctx* c, const std::vector<ReqDesc>& reqs, cons
     for (const auto& r : reqs) wgs += ((int64_t)r.art_len + 1 + ch - 1) / ch;
     return wgs * c->cfg.n_kv_heads;
   };
+  // (a chunk past the longest request's keys cannot lower the count further)
+  int64_t max_keys = 1;
+  for (const auto& r : reqs) max_keys = std::max<int64_t>(max_keys, (int64_t)r.art_len + 1);
+  const int32_t whole = (int32_t)std::max<int64_t>(128, (max_keys + 63) / 64 * 64);
   auto smallest_fitting = [&](int64_t limit, int32_t max_chunk) {
     int32_t ch = 128;
     while (wgs_for(ch) > limit && ch < max_chunk) ch += 64;
     return ch;
   };
-  int32_t chunk = smallest_fitting(256, 2048);
-  if (wgs_for(chunk) > 256) chunk = smallest_fitting(512, 2048);
-  if (wgs_for(chunk) > 512) chunk = smallest_fitting(1024, INT32_MAX - 64);
+  int32_t chunk = smallest_fitting(256, std::min(2048, whole));
+  if (wgs_for(chunk) > 256) chunk = smallest_fitting(512, std::min(2048, whole));
+  if (wgs_for(chunk) > 512) chunk = smallest_fitting(1024, whole);
   p.chunk = chunk;
   int32_t splits = 0;
   for (size_t r = 0; r < reqs.size(); ++r) {
