@@ -219,3 +219,14 @@ def test_decode_new_key_row_equals_norm_rope_kernel():
         ctx.qk_norm_rope(1, list(range(n + 1)), cu, ctx_len, None, q, ld, k, v, ld, gq, gk, q_hat, kv_b, rows)
         torch.cuda.synchronize()
         assert torch.equal(kv_a.view(torch.int16), kv_b.view(torch.int16))
+
+
+def test_decode_long_batch_two_rounds_of_chunks():
+    # sixteen requests of ~10k keys: too many keys for one round of workgroups
+    # within 2048-key chunks, so the chunks are sized for two full rounds
+    # (about 1280 keys, eight chunks per request merged)
+    _say("decode 16 x 10k keys")
+    got, ref = _run_decode(50, [10000] * 16, [((i,), 5 + i) for i in range(16)])
+    assert_o_close(got, ref, "batch")
+    for r in range(16):
+        assert_o_close_per_request(got[r], ref[r], f"request {r}")
