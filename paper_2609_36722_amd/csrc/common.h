@@ -129,15 +129,17 @@ __host__ __device__ constexpr int vmcnt_wait(int n) { return (n & 15) | (7 << 4)
 // 16 bytes land at LDS byte lds_base + 16 i (lds_base wave-uniform, in M0).
 // Issued as inline assembly so the compiler does not track these LDS writes
 // (its tracking would add a full vmcnt(0) wait before every LDS read); the
-// caller orders them with an explicit vmcnt wait and a barrier.
+// caller orders them with an explicit vmcnt wait and a barrier.  The LDS
+// base is an input operand bound to M0 ("{m0}"), so the compiler writes M0
+// itself and knows the register is live there; the asm only adds one wait
+// state between that write and the load.
 __device__ __forceinline__ void lds_dma16(const void* gaddr, uint32_t lds_base) {
   asm volatile(
-      "s_mov_b32 m0, %1\n\t"
       "s_nop 0\n\t"
       "global_load_lds_dwordx4 %0, off"
       :
-      : "v"(gaddr), "s"(__builtin_amdgcn_readfirstlane(lds_base))
-      : "memory", "m0");
+      : "v"(gaddr), "{m0}"(__builtin_amdgcn_readfirstlane(lds_base))
+      : "memory");
 }
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {

@@ -67,14 +67,14 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // One 16-byte-per-lane global -> LDS copy with a wave-uniform 64-bit base in
 // SGPRs and a per-lane 32-bit byte offset (the saddr form): the offsets stay
-// fixed from tile to tile, only the scalar base moves.
+// fixed from tile to tile, only the scalar base moves.  The LDS base goes in
+// through an M0-bound input operand, as in lds_dma16.
 __device__ __forceinline__ void lds_dma16_s(const void* sbase, uint32_t voff, uint32_t lds_base) {
   asm volatile(
-      "s_mov_b32 m0, %2\n\t"
       "s_nop 0\n\t"
       "global_load_lds_dwordx4 %0, %1"
       :
-      : "v"(voff), "s"(sbase), "s"(lds_base)
+      : "v"(voff), "s"(sbase), "{m0}"(lds_base)
       : "memory");
 }
 
