@@ -272,8 +272,8 @@ attuner_status attuner_merge_lora(attuner_ctx* ctx, const void* w, int32_t n_out
                                   int32_t lora_cols, void* w_out, void* stream);
 
 /* --------------------------------------------------------------------------
- * a4: per-head QK-RMSNorm + RoPE of the suffix (section 4: the adapted query
- * passes through the model's own query normalisation and RoPE).
+ * a4: per-head QK-RMSNorm + RoPE of the suffix (section 4: the base model's
+ * q-norm and rotary embedding apply to the adapted query unchanged).
  *
  * Per request r (host arrays of n_req entries, cu_q of n_req + 1): suffix
  * tokens are rows cu_q[r] .. cu_q[r+1]-1 of q_raw/k_raw/v_raw; token i of the

@@ -10,6 +10,10 @@ Parity status: every function here is pinned by the CPU test suite against a
 closed form, an invariant, a brute-force loop or a library routine (the
 oracle-pin tests).  The paper prints no kernel-level worked example; the small
 worked examples under ``tests/golden`` are derived by hand from the definitions.
+The decoder layer and stack (``decoder_layer``, ``first_token``), whose
+structure the paper does not give, are pinned against the transformers
+library's Qwen3 implementation run in float64 (the paper's base models) and
+against a brute-force loop in plain Python sums.
 """
 
 from __future__ import annotations
@@ -136,9 +140,9 @@ def qproj_lora(x: np.ndarray, w: np.ndarray, a: Optional[np.ndarray] = None,
 
 
 # ----------------------------------------------------------------------------
-# O4/O5  per-head QK-RMSNorm and rotary embedding (section 4: the adapted
-#        query "then passes through the model's original query normalization
-#        and RoPE")
+# O4/O5  per-head QK-RMSNorm and rotary embedding (section 4: after the
+#        adapted projection, the query goes through the base model's own
+#        per-head q-norm and rotary embedding, unchanged)
 # ----------------------------------------------------------------------------
 
 def rms_norm_heads(u: np.ndarray, gamma: np.ndarray, eps: float) -> np.ndarray:

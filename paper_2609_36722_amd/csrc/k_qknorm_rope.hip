@@ -1,5 +1,6 @@
-// K3: per-head QK-RMSNorm + RoPE of the suffix tokens (section 4: the adapted
-// query passes through the model's own query normalisation and RoPE), and the
+// K3: per-head QK-RMSNorm + RoPE of the suffix tokens (section 4: the base
+// model's q-norm and rotary embedding apply to the adapted query as they
+// would to the plain one), and the
 // write of the suffix keys and values into their request-cache rows.
 //
 // Eight lanes per (token, head slot); slots 0..Hq-1 are query heads,

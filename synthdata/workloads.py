@@ -274,11 +274,14 @@ def decoder_weights(wl: Workload, layer: int, intermediate: int) -> Dict[str, np
 
 
 def lm_weights(wl: Workload, vocab: int) -> Dict[str, np.ndarray]:
-    """bf16 bits of the embedding table [vocab][hidden] ~ N(0, 1) (hidden states
-    of unit scale, as suffix_hidden draws them), the LM head [vocab][hidden] ~
-    N(0, 1/sqrt(hidden)) and the final norm's gamma [hidden]."""
+    """bf16 bits of the embedding table [vocab][hidden] ~ N(0, 0.25), the LM
+    head [vocab][hidden] ~ N(0, 1/sqrt(hidden)) and the final norm's gamma
+    [hidden].  The embedding rows are deliberately not of unit RMS: a decoder
+    layer's input RMSNorm then rescales them by about 4, so a stack that
+    skipped that norm would be visibly wrong (with unit-RMS rows the norm is
+    nearly the identity)."""
     H = wl.shape.hidden
-    return {"embed": _normal_bf16(_rng(wl.index, _LMHEAD, 0), (vocab, H), 1.0),
+    return {"embed": _normal_bf16(_rng(wl.index, _LMHEAD, 0), (vocab, H), 0.25),
             "w_lm": _normal_bf16(_rng(wl.index, _LMHEAD, 1), (vocab, H), 1.0 / float(np.sqrt(H))),
             "gamma_final": _gamma(wl, H, 2000)}
 

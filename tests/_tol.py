@@ -56,21 +56,34 @@ def lse_bar(q_hat, keys, n_q_heads, n_kv_heads) -> float:
     return 2.0 ** -8 * zmax + 1e-3
 
 
+def stack_bar(n_layers: int) -> float:
+    """Relative bar of a decoder stack run end to end against the fp64 stack.
+
+    A layer stores eight intermediates in bf16 on the way from its input to
+    its output (the normalised input, q/k/v, q_hat/k_hat, O, h1, the
+    normalised h1, the SwiGLU activation, h2); each rounding moves a value by
+    at most 2^-8 relative, about 2^-9.5 on average.  The oracle's model of
+    that storage (every intermediate rounded to bf16, tests of the decoder
+    pins) gives a mean error of 0.2 - 0.4 % of mean|ref| per layer across
+    embedding scales, and the GPU stack measured the same; the bar is twice
+    that, n_layers * 2^-7, for the mean and (at least 1e-2) for the max.  The
+    planted-mistake test shows every composition mistake tried lands at
+    several times the bar."""
+    return n_layers * 2.0 ** -7
+
+
 def assert_stack_close(got, ref, n_layers: int, what="stack output"):
-    """Bar on the residual stream after n_layers decoder layers run end to end
-    against an fp64 stack started from the same input.  Each layer stores h
-    to bf16 twice (after the attention residual and after the MLP residual),
-    and every stored rounding moves a value by at most 2^-9 relative; the
-    errors of earlier layers pass through later ones along the residual
-    connection, so they add: mean|err| <= 2 n_layers * 2^-9 * mean|ref|
-    (one layer: the single-step bar 2^-8).  max|err| stays within
-    1e-2 * max|ref|, as for one step."""
+    """mean|err| <= stack_bar(L) * mean|ref| and max|err| <= max(1e-2,
+    stack_bar(L)) * max|ref| after L decoder layers run end to end from the
+    same input as the fp64 stack."""
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     err = np.abs(got - ref)
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
-    assert err.max() <= 1e-2 * np.abs(ref).max(), f"{what}: max|err| {err.max():.3e} vs max|ref| {np.abs(ref).max():.3e}"
-    bar = 2 * n_layers * 2.0 ** -9 * np.abs(ref).mean()
+    rel = stack_bar(n_layers)
+    mx_bar = max(1e-2, rel) * np.abs(ref).max()
+    assert err.max() <= mx_bar, f"{what}: max|err| {err.max():.3e} > {mx_bar:.3e} ({n_layers} layers)"
+    bar = rel * np.abs(ref).mean()
     assert err.mean() <= bar, f"{what}: mean|err| {err.mean():.3e} > {bar:.3e} ({n_layers} layers)"
 
 
