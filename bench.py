@@ -27,10 +27,11 @@ RMSNorm -> gate/up SwiGLU -> down_proj + residual, then the final RMSNorm of
 each request's last token, the LM head and the argmax; the full prefill runs
 all of the request's tokens through the same stack.
 
-Default workload: the Qwen3-4B-shaped 36-layer stack (8 artifacts x 1024
-tokens, 256-token suffix, LoRA rank 16).  One layer's seeded inputs are drawn
-and copied into a distinct device buffer per layer, so every layer reads its
-own memory.
+Default workload: the largest single-GPU configuration, the long-context
+Qwen3-8B-shaped 36-layer stack (32 artifacts x 1024 tokens = 32,768 cached
+tokens per layer, 1024-token suffix, LoRA rank 32).  One layer's seeded inputs
+are drawn and copied into a distinct device buffer per layer, so every layer
+reads its own memory.
 
 Prints one JSON line.  The CPU baseline times the fp64 oracle on a bounded
 sample of the same workload on the host.
@@ -63,7 +64,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c2", choices=["c2", "c3", "c5", "c1", "c4"])
+    ap.add_argument("--workload", default="c5", choices=["c5", "c2", "c3", "c1", "c4"])
     ap.add_argument("--full-steps", type=int, default=3, help="timed full-prefill passes (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline (0: skip)")
     ap.add_argument("--overlap-gather", action="store_true", help="gather layer by layer on a second stream "
@@ -124,36 +125,77 @@ def gather_bytes(shape, art_tokens, n_layers):
 # CPU baseline: the oracle on a bounded sample
 # ----------------------------------------------------------------------------
 
-def cpu_baseline(wl, budget_s, args):
+def _oracle_suffix_layer(wl, l, w, r, n_tok=None, row_block=256):
+    """The oracle's suffix layer for request r of layer l (all its suffix
+    rows, or its first n_tok suffix tokens: an exact sub-problem, since
+    suffix token i depends on no token after it): the oracle's projections,
+    norms and RoPE of every row, then its attention over blocks of rows (each
+    row's softmax is its own; the blocks bound host memory, the arithmetic
+    of every row is the same)."""
     import numpy as np
     import oracle
     import synthdata as sd
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
-    except Exception:
-        threads = os.cpu_count() or 1
     s = wl.shape
+    req = wl.requests[r]
+    kv = [sd.artifact_kv(wl, a, l) for a in req.artifact_ids]
+    ka = np.concatenate([oracle.decode_bf16(k) for k, _ in kv])
+    va = np.concatenate([oracle.decode_bf16(v) for _, v in kv])
+    x = oracle.decode_bf16(sd.suffix_hidden(wl, r, l))
+    if n_tok is not None:
+        x = x[:n_tok]
+    t0 = time.perf_counter()
+    base = oracle.suffix_layer(x, w["wq"], w["wk"], w["wv"], w["a"], w["b"], wl.scale, w["gamma_q"], w["gamma_k"],
+                               ka, va, wl.pos0(req), s.n_q_heads, s.n_kv_heads, s.rope_theta, s.rms_eps,
+                               rows=np.arange(0))
+    keys = np.concatenate([ka, base["k_hat"]])
+    vals = np.concatenate([va, base["v"]])
+    S = x.shape[0]
+    for r0 in range(0, S, row_block):
+        oracle.attention(base["q_hat"], keys, vals, ka.shape[0], rows=np.arange(r0, min(S, r0 + row_block)),
+                         return_lse=True)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(wl, budget_s, args):
+    """The fp64 oracle on the host: whole layers (every request, every suffix
+    row) with numpy's BLAS threads until the budget is spent (at least one
+    layer), and a single-thread figure on the first 64 suffix tokens of
+    request 0 of layer 0."""
+    import oracle
+    import synthdata as sd
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threadpool_limits, blas = None, 1
+    host_cores = os.cpu_count() or 1
+    affinity = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else host_cores
     layers_done, t_total = 0, 0.0
     while layers_done < wl.n_layers and (layers_done == 0 or t_total < budget_s):
         l = layers_done
         w = {k: oracle.decode_bf16(v) for k, v in sd.layer_weights(wl, l).items()}
-        t0 = time.perf_counter()
-        for r, req in enumerate(wl.requests):
-            kv = [sd.artifact_kv(wl, a, l) for a in req.artifact_ids]
-            ka = np.concatenate([oracle.decode_bf16(k) for k, _ in kv])
-            va = np.concatenate([oracle.decode_bf16(v) for _, v in kv])
-            x = oracle.decode_bf16(sd.suffix_hidden(wl, r, l))
-            oracle.suffix_layer(x, w["wq"], w["wk"], w["wv"], w["a"], w["b"], wl.scale, w["gamma_q"], w["gamma_k"],
-                                ka, va, wl.pos0(req), s.n_q_heads, s.n_kv_heads, s.rope_theta, s.rms_eps)
-        t_total += time.perf_counter() - t0
+        for r in range(len(wl.requests)):
+            t_total += _oracle_suffix_layer(wl, l, w, r)
         layers_done += 1
-        log(args, f"cpu oracle: layer {l} done ({t_total:.1f} s so far)")
+        log(args, f"cpu oracle ({blas} BLAS threads): layer {l} done ({t_total:.1f} s so far)")
     per_layer = t_total / layers_done
     value = wl.total_suffix / (per_layer * wl.n_layers)
-    return {"value": value, "unit": "suffix tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{layers_done} of {wl.n_layers} layers of {wl.name} (all suffix rows), fp64 numpy; "
-                      f"{per_layer:.2f} s per layer, stack time extrapolated x{wl.n_layers}/{layers_done}"}
+    single = None
+    if threadpool_limits is not None:
+        n1 = min(64, wl.requests[0].suffix_len)
+        w0 = {k: oracle.decode_bf16(v) for k, v in sd.layer_weights(wl, 0).items()}
+        with threadpool_limits(limits=1):
+            t1 = _oracle_suffix_layer(wl, 0, w0, 0, n1)
+        single = {"value": n1 / (t1 * wl.n_layers), "unit": "suffix tokens/s", "cores": 1,
+                  "sample": f"first {n1} suffix tokens of request 0, layer 0 of {wl.name}, 1 BLAS thread: "
+                            f"{t1:.2f} s, per-token rate over {wl.n_layers} layers"}
+        log(args, f"cpu oracle (1 thread): {n1} tokens of one layer in {t1:.1f} s")
+    return {"value": value, "unit": "suffix tokens/s", "cores": int(blas), "kind": "oracle",
+            "sample": f"{layers_done} of {wl.n_layers} layers of {wl.name} (every suffix row), fp64 numpy with "
+                      f"{blas} BLAS threads (elementwise work on one); {per_layer:.2f} s per layer, stack time "
+                      f"extrapolated x{wl.n_layers}/{layers_done}",
+            "host_cores": host_cores, "affinity_cores": affinity, "blas_threads": int(blas),
+            "single_thread": single}
 
 
 # ----------------------------------------------------------------------------

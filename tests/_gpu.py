@@ -111,3 +111,31 @@ class GpuWorkload:
         return oracle.suffix_layer(x, wf["wq"], wf["wk"], wf["wv"], wf["a"], wf["b"], self.wl.scale, wf["gamma_q"],
                                    wf["gamma_k"], ka, va, self.wl.pos0(r), s.n_q_heads, s.n_kv_heads,
                                    s.rope_theta, s.rms_eps, rows=rows)
+
+    def oracle_layer_blocks(self, li: int, req: int, block: int = 256, say=None):
+        """Every suffix row of one request through the oracle: projections,
+        norms and RoPE of all rows once (suffix_layer with no attention rows),
+        then the oracle's attention over blocks of rows.  Each row's softmax
+        is its own, so the blocks only bound host memory.  Also returns the
+        assembled keys (for the LSE bar)."""
+        s = self.wl.shape
+        base = self.oracle_layer(li, req, rows=np.arange(0))
+        r = self.wl.requests[req]
+        if r.artifact_ids:
+            ka = np.concatenate([oracle.decode_bf16(self.art_k[a][li]) for a in r.artifact_ids])
+            va = np.concatenate([oracle.decode_bf16(self.art_v[a][li]) for a in r.artifact_ids])
+        else:
+            ka = va = np.zeros((0, s.n_kv_heads, s.head_dim))
+        keys = np.concatenate([ka, base["k_hat"]])
+        vals = np.concatenate([va, base["v"]])
+        q_hat = base["q_hat"]
+        S = q_hat.shape[0]
+        o = np.empty_like(q_hat)
+        lse = np.empty(q_hat.shape[:2])
+        for r0 in range(0, S, block):
+            rows = np.arange(r0, min(S, r0 + block))
+            o[rows], lse[rows] = oracle.attention(q_hat, keys, vals, ka.shape[0], rows=rows, return_lse=True)
+            if say is not None:
+                say(f"oracle rows {r0}..{rows[-1]} of {S}")
+        return dict(base, o=o, lse=lse, keys=keys)
+

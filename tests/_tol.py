@@ -50,8 +50,9 @@ def lse_bar(q_hat, keys, n_q_heads, n_kv_heads) -> float:
     k = np.asarray(keys, np.float64)
     G = n_q_heads // n_kv_heads
     zmax = 0.0
-    for g in range(n_kv_heads):
-        z = np.einsum("shd,nd->shn", q[:, g * G:(g + 1) * G, :], k[:, g, :]) / np.sqrt(q.shape[-1])
+    for h in range(n_q_heads):
+        kg = np.ascontiguousarray(k[:, h // G, :])
+        z = (q[:, h, :] @ kg.T) / np.sqrt(q.shape[-1])
         zmax = max(zmax, float(np.abs(z).max()))
     return 2.0 ** -8 * zmax + 1e-3
 
