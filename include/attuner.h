@@ -29,6 +29,18 @@
  *   - `stream` is a hipStream_t (NULL = the null stream).  Every call only
  *     enqueues work on `stream` and returns without waiting for it, except
  *     where noted; results are valid once the stream has reached that point.
+ *   - Workspaces: the context owns scratch buffers (split partials, LoRA
+ *     slice partials, the full-prefill projection, logits, the RoPE table).
+ *     A call that needs more than they hold grows them with hipMalloc and
+ *     never waits for the device (a replaced buffer stays allocated until
+ *     attuner_reserve or attuner_destroy, since queued work may read it).
+ *     attuner_reserve sizes them all up front.
+ *   - Graph capture: while `stream` is capturing a HIP graph, a call that
+ *     would have to grow a workspace or extend the RoPE table fails with
+ *     ERANGE, and a call that copies host arrays to the device
+ *     (attuner_store_artifact(_host), attuner_assemble_*, attuner_embed,
+ *     attuner_rms_norm with a row list) fails with EINVAL; nothing is
+ *     enqueued then.  Every other call, within reserved limits, captures.
  *   - Every call returns a status; on failure nothing is enqueued, and
  *     attuner_last_error() describes the cause.  Arguments are validated on
  *     the host before any launch.
@@ -88,6 +100,25 @@ attuner_status attuner_create(const attuner_model_cfg* cfg, int64_t pool_pages, 
 
 /* Release the context, its pool and workspaces.  Waits for the device. */
 void attuner_destroy(attuner_ctx* ctx);
+
+/* Limits for attuner_reserve.  A zero field reserves nothing of its kind. */
+typedef struct {
+  int32_t max_tokens;   /* token rows of one projection, norm/attention, full-prefill, linear, gate/up,
+                           embedding or row-norm call                                               */
+  int32_t max_position; /* one past the largest token position of any call (RoPE table)             */
+  int32_t max_rank;     /* largest LoRA rank of attuner_qproj_lora / attuner_full_prefill            */
+  int32_t max_out;      /* largest n_out of attuner_linear, 2 * n_inter of attuner_gate_up_swiglu    */
+  int32_t max_lm_rows;  /* rows of one attuner_lm_head_argmax call                                  */
+  int32_t max_vocab;    /* vocab of attuner_lm_head_argmax                                          */
+} attuner_limits;
+
+/* Size every workspace and the RoPE table of the context for calls within
+ * `limits`, so that such calls allocate nothing (what a caller needs before
+ * capturing them into a HIP graph, see the conventions above).  Also frees
+ * buffers that earlier growth replaced.  Synchronous: waits for the device.
+ * Errors: EINVAL (negative limit), ERANGE (max_rank > ATTUNER_MAX_RANK),
+ * ENOMEM, EDEVICE. */
+attuner_status attuner_reserve(attuner_ctx* ctx, const attuner_limits* limits);
 
 /* Pool geometry and occupancy (host outputs; any may be NULL). */
 attuner_status attuner_pool_info(const attuner_ctx* ctx, int64_t* pool_pages, int64_t* free_pages,

@@ -24,6 +24,11 @@ class ModelCfgC(C.Structure):
                 ("rope_theta", C.c_float), ("rms_eps", C.c_float)]
 
 
+class LimitsC(C.Structure):
+    _fields_ = [("max_tokens", C.c_int32), ("max_position", C.c_int32), ("max_rank", C.c_int32),
+                ("max_out", C.c_int32), ("max_lm_rows", C.c_int32), ("max_vocab", C.c_int32)]
+
+
 class KernelTimeC(C.Structure):
     _fields_ = [("kernel", C.c_char * 48), ("launches", C.c_int64), ("total_ms", C.c_double), ("max_ms", C.c_double)]
 
@@ -39,6 +44,7 @@ SIGNATURES = {
     "attuner_last_error": (C.c_char_p, []),
     "attuner_create": (C.c_int, [C.POINTER(ModelCfgC), _i64, _i32, C.POINTER(_vp)]),
     "attuner_destroy": (None, [_vp]),
+    "attuner_reserve": (C.c_int, [_vp, C.POINTER(LimitsC)]),
     "attuner_pool_info": (C.c_int, [_vp, _i64p, _i64p, _i64p]),
     "attuner_store_artifact": (C.c_int, [_vp, _i32, _vp, _vp, _vp, _i32p]),
     "attuner_release_artifact": (C.c_int, [_vp, _i32]),

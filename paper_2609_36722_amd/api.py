@@ -17,7 +17,7 @@ from typing import List, Optional, Sequence, Tuple
 import numpy as np
 import torch
 
-from ._lib import MAX_RANK, MAX_REQUESTS, STATUS, KernelTimeC, ModelCfgC, lib
+from ._lib import MAX_RANK, MAX_REQUESTS, STATUS, KernelTimeC, LimitsC, ModelCfgC, lib
 
 
 class AttunerError(RuntimeError):
@@ -116,6 +116,14 @@ class Context:
 
     def __exit__(self, *exc):
         self.close()
+
+    def reserve(self, max_tokens: int = 0, max_position: int = 0, max_rank: int = 0, max_out: int = 0,
+                max_lm_rows: int = 0, max_vocab: int = 0) -> None:
+        """attuner_reserve: size the workspaces for calls within these limits
+        (then they allocate nothing and can be captured into a graph)."""
+        lim = LimitsC(int(max_tokens), int(max_position), int(max_rank), int(max_out), int(max_lm_rows),
+                      int(max_vocab))
+        _check(lib().attuner_reserve(self._h, C.byref(lim)), "attuner_reserve")
 
     # ---- pool -----------------------------------------------------------------
     def pool_info(self) -> Tuple[int, int, int]:

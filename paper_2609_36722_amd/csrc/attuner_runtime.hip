@@ -42,27 +42,38 @@ attuner_status fail(attuner_status st, const char* fmt, ...) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Growable device buffer.  Growth waits for the device, so buffers are never
-// freed under queued work.
+// Positions of the RoPE table built at create time (attuner_reserve or a
+// later call may extend it).
+constexpr int64_t kRopeInitPositions = 4096;
+// Largest (splits x query rows) of an attention launch with key splits: the
+// partials then take at most this many rows of Hq x (2 d + 8) bytes.
+constexpr int64_t kAttnSplitRowsMax = 16384;
+
+// true when `stream` is capturing work into a HIP graph.  A failed query
+// counts as capturing (the caller then refuses to allocate).
+bool capturing(hipStream_t stream) {
+  hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &st) != hipSuccess) {
+    (void)hipGetLastError();
+    return true;
+  }
+  return st != hipStreamCaptureStatusNone;
+}
+
+// Growable device buffer.  Growth never waits for the device: the old
+// buffer, which work already enqueued may still read, goes to a retired list
+// that is freed when the context is destroyed or attuner_reserve runs.
 struct DeviceBuf {
   void* ptr = nullptr;
   size_t cap = 0;
-  hipError_t ensure(size_t bytes) {
+  hipError_t grow(size_t bytes, std::vector<void*>& retired) {
     if (bytes <= cap) return hipSuccess;
-    if (ptr) {
-      hipError_t e = hipDeviceSynchronize();
-      if (e != hipSuccess) return e;
-      e = hipFree(ptr);
-      ptr = nullptr;
-      cap = 0;
-      if (e != hipSuccess) return e;
-    }
-    size_t want = std::max(bytes, cap * 2);
-    hipError_t e = hipMalloc(&ptr, want);
-    if (e != hipSuccess) {
-      ptr = nullptr;
-      return e;
-    }
+    const size_t want = std::max(bytes, cap * 2);
+    void* p = nullptr;
+    hipError_t e = hipMalloc(&p, want);
+    if (e != hipSuccess) return e;
+    if (ptr) retired.push_back(ptr);
+    ptr = p;
     cap = want;
     return hipSuccess;
   }
@@ -83,6 +94,8 @@ struct Staging {
   bool pending[2] = {false, false};
   int next = 0;
 
+  // (callers check first that `stream` is not capturing: a captured copy
+  // would re-read this slot at every replay, long after it was refilled)
   hipError_t upload(const void* src, size_t bytes, void* dst_dev, hipStream_t stream) {
     if (bytes == 0) return hipSuccess;
     const int s = next;
@@ -210,6 +223,8 @@ struct attuner_ctx {
   std::map<int32_t, Artifact> artifacts;
   int32_t next_id = 0;
 
+  std::vector<void*> retired;       // device buffers replaced by growth (freed at destroy / reserve)
+  std::vector<void*> retired_host;  // pinned RoPE uploads (freed likewise)
   DeviceBuf ws_pages;   // page list of the artifact being stored
   DeviceBuf ws_lora;    // LoRA-down slice partials
   DeviceBuf ws_part;    // split-KV partials
@@ -248,12 +263,61 @@ struct DeviceGuard {
 int q_dim(const attuner_ctx* c) { return c->cfg.n_q_heads * c->cfg.head_dim; }
 int kv_dim(const attuner_ctx* c) { return c->cfg.n_kv_heads * c->cfg.head_dim; }
 
-// (cos, sin) of pos * theta^(-2j/128) for pos < n, evaluated in double.
-attuner_status ensure_rope(attuner_ctx* c, int64_t n) {
+// Grow a workspace to `bytes` for a call on `stream` (no device wait; see
+// DeviceBuf).  Refused while the stream is capturing a graph: the allocation
+// would not be part of the graph, so the caller reserves first.
+attuner_status grow(attuner_ctx* c, DeviceBuf& buf, size_t bytes, hipStream_t stream, const char* what) {
+  if (bytes <= buf.cap) return ATTUNER_OK;
+  if (capturing(stream))
+    return fail(ATTUNER_ERANGE, "the %s workspace must grow to %zu bytes (has %zu) while the stream is capturing a "
+                                "graph: size it first with attuner_reserve", what, bytes, buf.cap);
+  hipError_t e = buf.grow(bytes, c->retired);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(ATTUNER_ENOMEM, "%s workspace of %zu bytes: %s", what, bytes, hipGetErrorString(e));
+  }
+  return ATTUNER_OK;
+}
+
+// Host -> device upload of a small host array through the pinned staging
+// slots; refused while the stream is capturing.
+attuner_status upload_host(attuner_ctx* c, const void* src, size_t bytes, void* dst, hipStream_t stream,
+                           const char* what) {
+  if (bytes == 0) return ATTUNER_OK;
+  if (capturing(stream))
+    return fail(ATTUNER_EINVAL, "%s copies a host array to the device and cannot be captured into a graph", what);
+  HIP_TRY(c->staging.upload(src, bytes, dst, stream));
+  return ATTUNER_OK;
+}
+
+// Refuse a call that uploads a host array while `stream` is capturing,
+// before anything else of the call happens.
+attuner_status upload_check(attuner_ctx* c, hipStream_t stream, const char* what) {
+  (void)c;
+  if (capturing(stream))
+    return fail(ATTUNER_EINVAL, "%s copies a host array to the device and cannot be captured into a graph", what);
+  return ATTUNER_OK;
+}
+
+// (cos, sin) of pos * theta^(-2j/128) for pos < n, evaluated in double and
+// stored fp32.  Growth builds the new table in pinned host memory and copies
+// it on `stream` (no device wait); the old table stays alive for work
+// already enqueued.  Refused while the stream is capturing.
+attuner_status ensure_rope(attuner_ctx* c, int64_t n, hipStream_t stream) {
   if (n <= c->rope_pos) return ATTUNER_OK;
-  int64_t want = 4096;
+  if (capturing(stream))
+    return fail(ATTUNER_ERANGE, "position %lld is past the RoPE table (%lld positions) while the stream is capturing a "
+                                "graph: size it first with attuner_reserve", (long long)n - 1, (long long)c->rope_pos);
+  int64_t want = std::max<int64_t>(kRopeInitPositions, c->rope_pos);
   while (want < n) want *= 2;
-  std::vector<float> tab((size_t)want * 64 * 2);
+  const size_t bytes = (size_t)want * 64 * 2 * sizeof(float);
+  float* tab = nullptr;
+  hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&tab), bytes, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(ATTUNER_ENOMEM, "pinned RoPE table of %zu bytes: %s", bytes, hipGetErrorString(e));
+  }
+  c->retired_host.push_back(tab);
   const double theta = c->cfg.rope_theta;
   for (int j = 0; j < 64; ++j) {
     const double inv_freq = std::pow(theta, -2.0 * j / 128.0);
@@ -263,9 +327,27 @@ attuner_status ensure_rope(attuner_ctx* c, int64_t n) {
       tab[((size_t)p * 64 + j) * 2 + 1] = (float)std::sin(ang);
     }
   }
-  HIP_TRY(c->rope.ensure(tab.size() * sizeof(float)));
-  HIP_TRY(hipMemcpy(c->rope.ptr, tab.data(), tab.size() * sizeof(float), hipMemcpyHostToDevice));
+  DeviceBuf fresh;
+  e = fresh.grow(bytes, c->retired);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(ATTUNER_ENOMEM, "RoPE table of %zu bytes: %s", bytes, hipGetErrorString(e));
+  }
+  HIP_TRY(hipMemcpyAsync(fresh.ptr, tab, bytes, hipMemcpyHostToDevice, stream));
+  if (c->rope.ptr) c->retired.push_back(c->rope.ptr);
+  c->rope = fresh;
   c->rope_pos = want;
+  return ATTUNER_OK;
+}
+
+// Wait for the device, then free what growth retired.
+attuner_status free_retired(attuner_ctx* c) {
+  if (c->retired.empty() && c->retired_host.empty()) return ATTUNER_OK;
+  HIP_TRY(hipDeviceSynchronize());
+  for (void* p : c->retired) (void)hipFree(p);
+  for (void* p : c->retired_host) (void)hipHostFree(p);
+  c->retired.clear();
+  c->retired_host.clear();
   return ATTUNER_OK;
 }
 
@@ -286,7 +368,7 @@ attuner_status run_norm_rope(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
                              int64_t head_stride, hipStream_t stream) {
   int64_t max_pos = 0;
   for (const auto& r : reqs) max_pos = std::max<int64_t>(max_pos, (int64_t)r.pos0 + r.q_len);
-  attuner_status st = ensure_rope(c, max_pos);
+  attuner_status st = ensure_rope(c, max_pos, stream);
   if (st != ATTUNER_OK) return st;
   NormRopeParams p;
   memset(&p, 0, sizeof p);
@@ -344,6 +426,8 @@ std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc
     tiles[r] = ((int64_t)reqs[r].art_len + reqs[r].q_len + 63) / 64;
     longest = std::max(longest, tiles[r]);
   }
+  int64_t total_q = 0;
+  for (const auto& r : reqs) total_q += std::max(0, r.q_len);
   std::vector<int> best(reqs.size(), 1), cand(reqs.size(), 1);
   double best_t = -1.0;
   int64_t prev_tau = -1;
@@ -352,10 +436,14 @@ std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc
     if (tau == prev_tau) continue;
     prev_tau = tau;
     bool any_split = false;
+    int max_ns = 1;
     for (size_t r = 0; r < reqs.size(); ++r) {
       cand[r] = (int)std::min<int64_t>(kMaxAttnSplit, std::max<int64_t>(1, (tiles[r] + tau - 1) / tau));
       any_split |= cand[r] > 1;
+      max_ns = std::max(max_ns, cand[r]);
     }
+    // the partials hold max_ns x total_q rows; plans past the cap are skipped
+    if (any_split && (int64_t)max_ns * total_q > kAttnSplitRowsMax) continue;
     std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
     for (int i = 0; i < kCUs; ++i) free_at.push(0.0);
     double finish = 0.0;
@@ -433,7 +521,8 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   if (n_split > 1) {
     const size_t rows = (size_t)n_split * total_q * c->cfg.n_q_heads;
     const size_t po = rows * c->cfg.head_dim * sizeof(uint16_t);
-    HIP_TRY(c->ws_part.ensure(po + rows * 2 * sizeof(float)));
+    attuner_status st = grow(c, c->ws_part, po + rows * 2 * sizeof(float), stream, "key-split partials");
+    if (st != ATTUNER_OK) return st;
     p.part_o = static_cast<uint16_t*>(c->ws_part.ptr);
     p.part_ml = reinterpret_cast<float*>(static_cast<char*>(c->ws_part.ptr) + po);
   }
@@ -449,7 +538,7 @@ attuner_status run_decode(attuner_ctx* c, const std::vector<ReqDesc>& reqs, cons
                           hipStream_t stream) {
   int64_t max_pos = 0;
   for (const auto& r : reqs) max_pos = std::max<int64_t>(max_pos, (int64_t)r.pos0 + 1);
-  attuner_status st = ensure_rope(c, max_pos);
+  attuner_status st = ensure_rope(c, max_pos, stream);
   if (st != ATTUNER_OK) return st;
   DecodeParams p;
   memset(&p, 0, sizeof p);
@@ -512,7 +601,8 @@ attuner_status run_decode(attuner_ctx* c, const std::vector<ReqDesc>& reqs, cons
   if (splits > (int32_t)reqs.size()) {
     const size_t rows = (size_t)splits * c->cfg.n_q_heads;
     const size_t po = rows * c->cfg.head_dim * sizeof(float);
-    HIP_TRY(c->ws_part.ensure(po + rows * 2 * sizeof(float)));
+    st = grow(c, c->ws_part, po + rows * 2 * sizeof(float), stream, "decode chunk partials");
+    if (st != ATTUNER_OK) return st;
     p.part_o = static_cast<float*>(c->ws_part.ptr);
     p.part_ml = reinterpret_cast<float*>(static_cast<char*>(c->ws_part.ptr) + po);
   }
@@ -587,7 +677,8 @@ attuner_status qproj_impl(attuner_ctx* c, int32_t n_tok, const void* x, const vo
   float* t_part = nullptr;
   if (r_pad > kGemmFusedLoraMaxRank || (r_pad > 0 && n_tok <= kGemvMaxTok)) {
     const size_t part_bytes = (size_t)lora_down_slices(hidden) * n_tok * r_pad * sizeof(float);
-    HIP_TRY(c->ws_lora.ensure(part_bytes));
+    attuner_status st = grow(c, c->ws_lora, part_bytes, stream, "LoRA down-projection");
+    if (st != ATTUNER_OK) return st;
     t_part = static_cast<float*>(c->ws_lora.ptr);
     HIP_TRY(launch_lora_down(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(a), n_tok, hidden, rank,
                              r_pad, scale, t_part, stream));
@@ -641,8 +732,55 @@ attuner_status attuner_create(const attuner_model_cfg* cfg, int64_t pool_pages, 
     }
   }
   for (int32_t p = 0; p < (int32_t)pool_pages; ++p) c->free_pages.insert(c->free_pages.end(), p);
+  attuner_status st = ensure_rope(c, kRopeInitPositions, nullptr);
+  if (st == ATTUNER_OK) st = free_retired(c);  // waits for the table's copy
+  if (st != ATTUNER_OK) {
+    attuner_destroy(c);
+    return st;
+  }
   *out = c;
   return ATTUNER_OK;
+}
+
+attuner_status attuner_reserve(attuner_ctx* c, const attuner_limits* lim) {
+  if (!c || !lim) return fail(ATTUNER_EINVAL, "null ctx or limits");
+  if (lim->max_tokens < 0 || lim->max_position < 0 || lim->max_rank < 0 || lim->max_out < 0 || lim->max_lm_rows < 0 ||
+      lim->max_vocab < 0)
+    return fail(ATTUNER_EINVAL, "negative limit");
+  if (lim->max_rank > ATTUNER_MAX_RANK) return fail(ATTUNER_ERANGE, "max_rank %d > %d", lim->max_rank, ATTUNER_MAX_RANK);
+  DeviceGuard dg(c->device);
+  hipStream_t s = nullptr;
+  attuner_status st = ensure_rope(c, lim->max_position, s);
+  const int64_t T = lim->max_tokens, Hq = c->cfg.n_q_heads, d = c->cfg.head_dim;
+  const int64_t nq = q_dim(c), nkv = kv_dim(c);
+  // LoRA down-projection slice partials (ranks above the fused limit, or few tokens)
+  if (st == ATTUNER_OK && lim->max_rank > 0 && T > 0) {
+    const int64_t r_pad = (lim->max_rank + 15) / 16 * 16;
+    st = grow(c, c->ws_lora, (size_t)lora_down_slices(c->cfg.hidden) * T * r_pad * sizeof(float), s,
+              "LoRA down-projection");
+  }
+  // key-split partials of attention (normalised bf16 O + fp32 max, sum) and
+  // of decode (fp32 O + max, sum; at most 1024 workgroups of n_kv heads)
+  if (st == ATTUNER_OK && T > 0) {
+    const int64_t rows = std::min<int64_t>((int64_t)kMaxAttnSplit * T, kAttnSplitRowsMax) * Hq;
+    const int64_t dec_rows = (1024 / c->cfg.n_kv_heads + ATTUNER_MAX_REQUESTS) * Hq;
+    const size_t bytes = std::max((size_t)rows * (d * 2 + 2 * sizeof(float)), (size_t)dec_rows * (d + 2) * sizeof(float));
+    st = grow(c, c->ws_part, bytes, s, "key-split partials");
+  }
+  if (st == ATTUNER_OK && T > 0)
+    st = grow(c, c->ws_qkv, (size_t)T * (nq + 2 * nkv) * sizeof(uint16_t), s, "full-prefill projection");
+  if (st == ATTUNER_OK && T > 0) st = grow(c, c->ws_rows, (size_t)T * sizeof(int32_t), s, "row list");
+  const int64_t widest = std::max(lim->max_out, lim->max_vocab);
+  if (st == ATTUNER_OK && T > 0 && widest > 0)
+    st = grow(c, c->ws_split,
+              (size_t)std::min<int64_t>(kGemmSplitWsMaxBytes, (int64_t)kMaxGemmSplit * T * widest * 4), s,
+              "key-split product");
+  if (st == ATTUNER_OK && lim->max_lm_rows > 0 && lim->max_vocab > 0)
+    st = grow(c, c->ws_logits,
+              (size_t)lim->max_lm_rows * lim->max_vocab * sizeof(float) + argmax_scratch_bytes(lim->max_lm_rows), s,
+              "logits");
+  if (st == ATTUNER_OK) st = free_retired(c);
+  return st;
 }
 
 void attuner_destroy(attuner_ctx* c) {
@@ -658,6 +796,10 @@ void attuner_destroy(attuner_ctx* c) {
   c->ws_split.release();
   c->ws_rows.release();
   c->rope.release();
+  for (void* p : c->retired) (void)hipFree(p);
+  for (void* p : c->retired_host) (void)hipHostFree(p);
+  c->retired.clear();
+  c->retired_host.clear();
   if (g_tracer == &c->tracer) g_tracer = nullptr;
   c->tracer.release();
   if (c->pool) (void)hipFree(c->pool);
@@ -687,14 +829,17 @@ static attuner_status store_impl(attuner_ctx* c, bool host, int32_t n_tokens, co
                 (long long)need, free_set.size());
   DeviceGuard dg(c->device);
   try {
-    HIP_TRY(c->ws_pages.ensure((size_t)need * sizeof(int32_t)));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    attuner_status st = grow(c, c->ws_pages, (size_t)need * sizeof(int32_t), s, "page list");
+    if (st != ATTUNER_OK) return st;
     Artifact art;
     art.n_tokens = n_tokens;
     art.host = host;
     auto it = free_set.begin();
     for (int64_t i = 0; i < need; ++i) art.pages.push_back(*it++);
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    HIP_TRY(c->staging.upload(art.pages.data(), art.pages.size() * sizeof(int32_t), c->ws_pages.ptr, s));
+    st = upload_host(c, art.pages.data(), art.pages.size() * sizeof(int32_t), c->ws_pages.ptr, s,
+                     "attuner_store_artifact");
+    if (st != ATTUNER_OK) return st;
     HIP_TRY(launch_store_pages(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), n_tokens,
                                static_cast<const int32_t*>(c->ws_pages.ptr), (int)need,
                                host ? c->host_pool_dev : c->pool, host ? c->host_pages : c->pool_pages,
@@ -853,8 +998,9 @@ attuner_status attuner_assemble_table(attuner_ctx* c, int32_t n_req, const int32
   if (art_len && n_req > 0) memcpy(art_len, al.data(), (size_t)n_req * sizeof(int32_t));
   if (entries > 0) {
     DeviceGuard dg(c->device);
-    HIP_TRY(c->staging.upload(table.data(), table.size() * sizeof(int32_t), block_table,
-                              static_cast<hipStream_t>(stream)));
+    attuner_status st = upload_host(c, table.data(), table.size() * sizeof(int32_t), block_table,
+                                    static_cast<hipStream_t>(stream), "attuner_assemble_table");
+    if (st != ATTUNER_OK) return st;
   }
   c->last_table = block_table;
   c->last_entries = entries;
@@ -996,7 +1142,9 @@ attuner_status attuner_assemble_segments(attuner_ctx* c, int32_t n_req, const in
   if (entries > 0) {
     DeviceGuard dg(c->device);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    HIP_TRY(c->staging.upload(table.data(), table.size() * sizeof(int32_t), block_table, s));
+    attuner_status st = upload_host(c, table.data(), table.size() * sizeof(int32_t), block_table, s,
+                                    "attuner_assemble_segments");
+    if (st != ATTUNER_OK) return st;
     HIP_TRY(launch_gather(block_table, entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages, 0,
                           c->cfg.n_layers, c->cfg.n_kv_heads,
                           static_cast<uint16_t*>(req_kv), cache_rows, s));
@@ -1026,8 +1174,12 @@ attuner_status attuner_rms_norm(attuner_ctx* c, const void* x, int64_t n_x_rows,
     for (int32_t i = 0; i < n_rows; ++i)
       if (rows[i] < 0 || rows[i] >= n_x_rows)
         return fail(ATTUNER_ERANGE, "rows[%d] = %d outside [0, %lld)", i, rows[i], (long long)n_x_rows);
-    HIP_TRY(c->ws_rows.ensure((size_t)n_rows * sizeof(int32_t)));
-    HIP_TRY(c->staging.upload(rows, (size_t)n_rows * sizeof(int32_t), c->ws_rows.ptr, s));
+    attuner_status st = upload_check(c, s, "attuner_rms_norm with a row list");
+    if (st != ATTUNER_OK) return st;
+    st = grow(c, c->ws_rows, (size_t)n_rows * sizeof(int32_t), s, "row list");
+    if (st != ATTUNER_OK) return st;
+    st = upload_host(c, rows, (size_t)n_rows * sizeof(int32_t), c->ws_rows.ptr, s, "attuner_rms_norm with a row list");
+    if (st != ATTUNER_OK) return st;
     rows_dev = static_cast<const int32_t*>(c->ws_rows.ptr);
   }
   HIP_TRY(launch_rms_norm_rows(static_cast<const uint16_t*>(x), ld_x, rows_dev, n_rows, dim,
@@ -1049,8 +1201,12 @@ attuner_status attuner_embed(attuner_ctx* c, int32_t n_tok, const int32_t* token
       return fail(ATTUNER_ERANGE, "token_ids[%d] = %d outside [0, %d)", i, token_ids[i], vocab);
   DeviceGuard dg(c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  HIP_TRY(c->ws_rows.ensure((size_t)n_tok * sizeof(int32_t)));
-  HIP_TRY(c->staging.upload(token_ids, (size_t)n_tok * sizeof(int32_t), c->ws_rows.ptr, s));
+  attuner_status st = upload_check(c, s, "attuner_embed");
+  if (st != ATTUNER_OK) return st;
+  st = grow(c, c->ws_rows, (size_t)n_tok * sizeof(int32_t), s, "token id");
+  if (st != ATTUNER_OK) return st;
+  st = upload_host(c, token_ids, (size_t)n_tok * sizeof(int32_t), c->ws_rows.ptr, s, "attuner_embed");
+  if (st != ATTUNER_OK) return st;
   HIP_TRY(launch_embed_rows(static_cast<const uint16_t*>(table), static_cast<const int32_t*>(c->ws_rows.ptr), n_tok,
                             dim, static_cast<uint16_t*>(out), s));
   return ATTUNER_OK;
@@ -1073,7 +1229,8 @@ static attuner_status run_gemm(attuner_ctx* c, int32_t n_tok, const void* x, int
   const GemmPlan plan = plan_gemm(n_tok, n_out, k_dim, false);
   float* ws = nullptr;
   if (n_tok > kGemvMaxTok && plan.n_split > 1) {
-    HIP_TRY(c->ws_split.ensure((size_t)plan.n_split * n_tok * n_out * sizeof(float)));
+    attuner_status st = grow(c, c->ws_split, (size_t)plan.n_split * n_tok * n_out * sizeof(float), s, "key-split product");
+    if (st != ATTUNER_OK) return st;
     ws = static_cast<float*>(c->ws_split.ptr);
   }
   HIP_TRY(launch_gemm(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), n_tok, n_out, k_dim, epi,
@@ -1117,7 +1274,8 @@ attuner_status attuner_lm_head_argmax(attuner_ctx* c, int32_t n_rows, const void
   DeviceGuard dg(c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const size_t logit_bytes = (size_t)n_rows * vocab * sizeof(float);
-  HIP_TRY(c->ws_logits.ensure(logit_bytes + argmax_scratch_bytes(n_rows)));
+  st = grow(c, c->ws_logits, logit_bytes + argmax_scratch_bytes(n_rows), s, "logits");
+  if (st != ATTUNER_OK) return st;
   float* logits = static_cast<float*>(c->ws_logits.ptr);
   st = run_gemm(c, n_rows, x, H, w_lm, vocab, GemmEpi{kEpiF32, nullptr, logits}, nullptr, s);
   if (st != ATTUNER_OK) return st;
@@ -1366,9 +1524,10 @@ attuner_status attuner_full_prefill(attuner_ctx* c, int32_t n_tok, int32_t pos0,
   DeviceGuard dg(c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nq = q_dim(c), nkv = kv_dim(c), n_out = nq + 2 * nkv;
-  HIP_TRY(c->ws_qkv.ensure((size_t)n_tok * n_out * sizeof(uint16_t)));
+  attuner_status st = grow(c, c->ws_qkv, (size_t)n_tok * n_out * sizeof(uint16_t), s, "full-prefill projection");
+  if (st != ATTUNER_OK) return st;
   uint16_t* qkv = static_cast<uint16_t*>(c->ws_qkv.ptr);
-  attuner_status st = qproj_impl(c, n_tok, x, wqkv, n_out, a, b, rank, scale, nq, qkv, s);
+  st = qproj_impl(c, n_tok, x, wqkv, n_out, a, b, rank, scale, nq, qkv, s);
   if (st != ATTUNER_OK) return st;
   std::vector<ReqDesc> reqs(1);
   reqs[0].q_start = 0;

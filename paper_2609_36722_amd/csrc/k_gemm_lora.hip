@@ -491,6 +491,8 @@ GemmPlan plan_gemm(int n_tok, int n_out, int k_dim, bool lora) {
       if (s > 1 && (lora || n_kt < 4 * s || tiles >= 256)) break;
       const int kts = (n_kt + s - 1) / s;
       const int used = (n_kt + kts - 1) / kts;  // splits that hold k-tiles
+      // fp32 partials of every split: bounded, so that a reserved workspace holds any plan
+      if (used > 1 && (int64_t)used * n_tok * n_out * 4 > kGemmSplitWsMaxBytes) break;
       const int64_t wgs = tiles * used;
       const double k_range = (double)kts * BK;
       const double per_wg = std::max((kTiles[i].bm + kTiles[i].bn) * k_range * 2 / rate,

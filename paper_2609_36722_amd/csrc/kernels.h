@@ -95,6 +95,11 @@ hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, int n_tok, int n_ou
 // such token counts here; from 9 tokens (k_dim % 128 == 0, n_out % 16 ==
 // 0) the GEMV runs on the matrix cores.
 constexpr int kGemvMaxTok = 16;
+
+// Key splits of a plain product: at most kMaxGemmSplit, and their fp32
+// partials (splits x n_tok x n_out x 4 bytes) at most kGemmSplitWsMaxBytes.
+constexpr int kMaxGemmSplit = 16;
+constexpr int64_t kGemmSplitWsMaxBytes = (int64_t)64 << 20;
 hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int k_dim, const uint16_t* b,
                        int rank, int r_pad, int lora_cols, const float* t_part, GemmEpi epi, uint16_t* out,
                        hipStream_t stream);
