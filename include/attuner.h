@@ -353,6 +353,37 @@ attuner_status attuner_suffix_attn(attuner_ctx* ctx, int32_t layer, int32_t n_re
                                    int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
                                    int64_t cache_rows, void* o, float* lse, void* stream);
 
+/* Size of the fixed device buffer of attuner_suffix_attn_noalloc (per device). */
+#define ATTUNER_NOALLOC_SCRATCH_BYTES (24 << 20)
+
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ *
+ * attuner_suffix_attn with its key-split partials in a fixed device buffer
+ * of ATTUNER_NOALLOC_SCRATCH_BYTES (24 MiB) instead of a context workspace;
+ * arguments, outputs and errors as attuner_suffix_attn.  The call allocates
+ * nothing and never waits for the device.  The buffer is part of the
+ * library's code object: one copy per device, located when the first
+ * context is created on that device and held until the process ends.
+ *   - The split plan is limited to plans whose partials fit the buffer:
+ *     n_split x (query rows) x Hq x (2 head_dim + 8) bytes <= 24 MiB.  A batch
+ *     whose usual plan does not fit runs with fewer key splits (same result
+ *     within the parity bar); every batch the other call takes is accepted.
+ *   - Token positions must lie in the context's RoPE table (4096 positions
+ *     from create; attuner_reserve extends it); this call does not extend
+ *     it: ERANGE otherwise.
+ *   - Every call on a device shares that device's buffer, which keeps the
+ *     last call's contents: calls that overlap on one device (other streams,
+ *     contexts or threads) race and must be ordered by the caller.  Nothing
+ *     in it has to start at zero: a call reads only partials it wrote.
+ * Errors: as attuner_suffix_attn; ERANGE (position past the RoPE table);
+ * EDEVICE (the buffer's device address could not be looked up). */
+attuner_status attuner_suffix_attn_noalloc(attuner_ctx* ctx, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                           const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                           const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                           int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                           int64_t cache_rows, void* o, float* lse, void* stream);
+
 /* --------------------------------------------------------------------------
  * a6: full-context prefill of one layer with the same kernels (section 2,
  * Full; appendix C.1, Full).

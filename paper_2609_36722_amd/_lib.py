@@ -16,6 +16,7 @@ STATUS = {0: "ATTUNER_OK", -1: "ATTUNER_EINVAL", -2: "ATTUNER_ENOMEM", -3: "ATTU
 MAX_REQUESTS = 64
 MAX_RANK = 64
 HOST_PAGE_FLAG = 1 << 30
+NOALLOC_SCRATCH_BYTES = 24 << 20
 
 
 class ModelCfgC(C.Structure):
@@ -59,6 +60,8 @@ SIGNATURES = {
     "attuner_attention": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _vp, _vp, _i64, _vp, _vp, _vp]),
     "attuner_suffix_attn": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64,
                                       _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "attuner_suffix_attn_noalloc": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp,
+                                              _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
     "attuner_merge_lora": (C.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _i32, C.c_float, _i32, _vp, _vp]),
     "attuner_host_pool_create": (C.c_int, [_vp, _i64]),
     "attuner_store_artifact_host": (C.c_int, [_vp, _i32, _vp, _vp, _vp, _i32p]),

@@ -374,15 +374,18 @@ class Context:
 
     def suffix_attn(self, layer: int, cu_q, cu_ctx, art_len, pos0, q_raw, ld_q: int, k_raw, v_raw, ld_kv: int,
                     gamma_q, gamma_k, req_kv, cache_rows: int, o, lse: Optional[torch.Tensor] = None,
-                    stream=None) -> None:
+                    stream=None, noalloc: bool = False) -> None:
+        """attuner_suffix_attn, or with noalloc=True attuner_suffix_attn_noalloc (the key-split
+        partials in the library's fixed device buffer; allocates nothing)."""
         n = len(art_len)
         self._check_cache(cu_q, cu_ctx, o, req_kv, cache_rows, q_raw, ld_q, k_raw, v_raw, ld_kv)
         _need(lse, int(cu_q[-1]) * self.cfg.n_q_heads, "lse")
-        _check(lib().attuner_suffix_attn(self._h, int(layer), n, _i32(cu_q), _i32(cu_ctx), _i32(art_len),
-                                         _i32(pos0) if pos0 is not None else None, _view_ptr(q_raw), int(ld_q),
-                                         _view_ptr(k_raw), _view_ptr(v_raw), int(ld_kv), _ptr(gamma_q), _ptr(gamma_k),
-                                         _ptr(req_kv), int(cache_rows), _ptr(o), _ptr(lse, 4), _stream(stream)),
-               "attuner_suffix_attn")
+        name = "attuner_suffix_attn_noalloc" if noalloc else "attuner_suffix_attn"
+        _check(getattr(lib(), name)(self._h, int(layer), n, _i32(cu_q), _i32(cu_ctx), _i32(art_len),
+                                    _i32(pos0) if pos0 is not None else None, _view_ptr(q_raw), int(ld_q),
+                                    _view_ptr(k_raw), _view_ptr(v_raw), int(ld_kv), _ptr(gamma_q), _ptr(gamma_k),
+                                    _ptr(req_kv), int(cache_rows), _ptr(o), _ptr(lse, 4), _stream(stream)),
+               name)
 
     def span_attn(self, layer: int, cu_q, kv_start, offset, pos0, q_raw, ld_q: int, k_raw, v_raw, ld_kv: int,
                   gamma_q, gamma_k, req_kv, cache_rows: int, o, lse: Optional[torch.Tensor] = None,

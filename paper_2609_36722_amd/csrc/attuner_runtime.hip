@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <new>
 #include <queue>
 #include <set>
@@ -207,6 +208,53 @@ void trace_launch_end(const char* kernel, hipStream_t stream) {
 }
 
 }  // namespace attuner
+
+// ---- fixed device scratch of attuner_suffix_attn_noalloc --------------------
+// One copy per device, allocated with the code object and held until the
+// process ends.  Host code never uses the name `scratch` as an address (on
+// the host it is only a stand-in for the symbol): its device address is
+// looked up once per device and kept in g_scratch.
+static __device__ __align__(256) char scratch[ATTUNER_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+struct ScratchSlot {
+  bool looked_up = false;
+  hipError_t err = hipSuccess;
+  void* ptr = nullptr;
+};
+
+std::mutex g_scratch_mu;
+ScratchSlot g_scratch[kMaxDevices];
+
+// Look up the device address of `scratch` on `device`, which must be the
+// current device; once per device (later calls return the first result).
+hipError_t locate_scratch(int device) {
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  ScratchSlot& sl = g_scratch[device];
+  if (!sl.looked_up) {
+    void* ptr = nullptr;
+    sl.err = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (sl.err != hipSuccess) {
+      (void)hipGetLastError();
+      ptr = nullptr;
+    }
+    sl.ptr = ptr;
+    sl.looked_up = true;
+  }
+  return sl.err;
+}
+
+void* scratch_ptr(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  return g_scratch[device].looked_up && g_scratch[device].err == hipSuccess ? g_scratch[device].ptr : nullptr;
+}
+
+}  // namespace
 
 struct attuner_ctx {
   attuner_model_cfg cfg;
@@ -409,9 +457,10 @@ attuner_status run_norm_rope(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
 // splits (split size tau = its tiles / k) and every request into
 // ceil(its tiles / tau); a candidate with more splits must be modelled 2%
 // faster to win.
-std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc>& reqs) {
+std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int64_t split_rows_max) {
   std::vector<int32_t> shape;
-  shape.reserve(2 * reqs.size());
+  shape.reserve(2 * reqs.size() + 1);
+  shape.push_back((int32_t)split_rows_max);
   for (const auto& r : reqs) {
     shape.push_back(r.q_len);
     shape.push_back(r.art_len);
@@ -443,7 +492,7 @@ std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc
       max_ns = std::max(max_ns, cand[r]);
     }
     // the partials hold max_ns x total_q rows; plans past the cap are skipped
-    if (any_split && (int64_t)max_ns * total_q > kAttnSplitRowsMax) continue;
+    if (any_split && (int64_t)max_ns * total_q > split_rows_max) continue;
     std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
     for (int i = 0; i < kCUs; ++i) free_at.push(0.0);
     double finish = 0.0;
@@ -476,9 +525,19 @@ std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc
   return best;
 }
 
+// Key-split partials of one attention launch: n_split x total_q x Hq rows
+// of a normalised bf16 O row and an fp32 (max, sum) pair.
+size_t split_row_bytes(const attuner_ctx* c) {
+  return (size_t)c->cfg.n_q_heads * (c->cfg.head_dim * sizeof(uint16_t) + 2 * sizeof(float));
+}
+
+// part_buf / part_bytes: a caller-provided buffer for the key-split
+// partials (the plan is then limited to what fits); null: the context's
+// workspace, grown as needed.
 attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int32_t total_q, const void* q,
                              const uint16_t* k_plane, const uint16_t* v_plane, int64_t head_stride, void* o,
-                             float* lse, hipStream_t stream, const std::vector<SpanRow>* spans = nullptr) {
+                             float* lse, hipStream_t stream, const std::vector<SpanRow>* spans = nullptr,
+                             void* part_buf = nullptr, size_t part_bytes = 0) {
   AttnParams p;
   memset(&p, 0, sizeof p);
   p.q = static_cast<const uint16_t*>(q);
@@ -493,7 +552,9 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c->cfg.head_dim));
   p.n_req = (int32_t)reqs.size();
 
-  const std::vector<int> ns_plan = plan_attention_splits(c, reqs);
+  const int64_t rows_max =
+      part_buf ? std::min<int64_t>(kAttnSplitRowsMax, (int64_t)(part_bytes / split_row_bytes(c))) : kAttnSplitRowsMax;
+  const std::vector<int> ns_plan = plan_attention_splits(c, reqs, rows_max);
   int n_split = 1;
   int32_t units = 0;
   for (size_t r = 0; r < reqs.size(); ++r) {
@@ -521,10 +582,18 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   if (n_split > 1) {
     const size_t rows = (size_t)n_split * total_q * c->cfg.n_q_heads;
     const size_t po = rows * c->cfg.head_dim * sizeof(uint16_t);
-    attuner_status st = grow(c, c->ws_part, po + rows * 2 * sizeof(float), stream, "key-split partials");
-    if (st != ATTUNER_OK) return st;
-    p.part_o = static_cast<uint16_t*>(c->ws_part.ptr);
-    p.part_ml = reinterpret_cast<float*>(static_cast<char*>(c->ws_part.ptr) + po);
+    void* buf = part_buf;
+    if (buf != nullptr) {
+      if (po + rows * 2 * sizeof(float) > part_bytes)
+        return fail(ATTUNER_ERANGE, "key-split partials of %zu bytes exceed the %zu-byte buffer",
+                    po + rows * 2 * sizeof(float), part_bytes);
+    } else {
+      attuner_status st = grow(c, c->ws_part, po + rows * 2 * sizeof(float), stream, "key-split partials");
+      if (st != ATTUNER_OK) return st;
+      buf = c->ws_part.ptr;
+    }
+    p.part_o = static_cast<uint16_t*>(buf);
+    p.part_ml = reinterpret_cast<float*>(static_cast<char*>(buf) + po);
   }
   HIP_TRY(launch_attention(p, stream));
   return ATTUNER_OK;
@@ -732,6 +801,9 @@ attuner_status attuner_create(const attuner_model_cfg* cfg, int64_t pool_pages, 
     }
   }
   for (int32_t p = 0; p < (int32_t)pool_pages; ++p) c->free_pages.insert(c->free_pages.end(), p);
+  // the device address of the fixed scratch (attuner_suffix_attn_noalloc);
+  // a failure is reported by that call only
+  (void)locate_scratch(device);
   attuner_status st = ensure_rope(c, kRopeInitPositions, nullptr);
   if (st == ATTUNER_OK) st = free_retired(c);  // waits for the table's copy
   if (st != ATTUNER_OK) {
@@ -1366,11 +1438,11 @@ attuner_status attuner_attention(attuner_ctx* c, int32_t layer, int32_t n_req, c
                        static_cast<hipStream_t>(stream));
 }
 
-attuner_status attuner_suffix_attn(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_q,
-                                   const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
-                                   const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
-                                   int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
-                                   int64_t cache_rows, void* o, float* lse, void* stream) {
+static attuner_status suffix_attn_impl(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                       const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                       const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                       int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                       int64_t cache_rows, void* o, float* lse, void* stream, bool noalloc) {
   if (!c) return fail(ATTUNER_EINVAL, "null ctx");
   attuner_status st = check_layer(c, layer);
   if (st != ATTUNER_OK) return st;
@@ -1383,6 +1455,17 @@ attuner_status attuner_suffix_attn(attuner_ctx* c, int32_t layer, int32_t n_req,
   if (st != ATTUNER_OK) return st;
   if (!req_kv || !o || !aligned16(req_kv) || !aligned16(o))
     return fail(ATTUNER_EINVAL, "req_kv and o must be non-null and 16-byte aligned");
+  void* part = nullptr;
+  if (noalloc) {
+    part = scratch_ptr(c->device);
+    if (part == nullptr)
+      return fail(ATTUNER_EDEVICE, "the fixed scratch of device %d could not be located", c->device);
+    int64_t max_pos = 0;
+    for (const auto& r : reqs) max_pos = std::max<int64_t>(max_pos, (int64_t)r.pos0 + r.q_len);
+    if (max_pos > c->rope_pos)
+      return fail(ATTUNER_ERANGE, "position %lld is past the RoPE table (%lld positions); this call does not "
+                                  "extend it (attuner_reserve does)", (long long)max_pos - 1, (long long)c->rope_pos);
+  }
   DeviceGuard dg(c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t hs = cache_rows * c->cfg.head_dim;
@@ -1390,7 +1473,26 @@ attuner_status attuner_suffix_attn(attuner_ctx* c, int32_t layer, int32_t n_req,
   uint16_t* vp = cache_plane(req_kv, c, layer, 1, cache_rows);
   st = run_norm_rope(c, reqs, total_q, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, o, kp, vp, hs, s);
   if (st != ATTUNER_OK) return st;
-  return run_attention(c, reqs, total_q, o, kp, vp, hs, o, lse, s);
+  return run_attention(c, reqs, total_q, o, kp, vp, hs, o, lse, s, nullptr, part,
+                       noalloc ? (size_t)ATTUNER_NOALLOC_SCRATCH_BYTES : 0);
+}
+
+attuner_status attuner_suffix_attn(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                   const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                   const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                   int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                   int64_t cache_rows, void* o, float* lse, void* stream) {
+  return suffix_attn_impl(c, layer, n_req, cu_q, cu_ctx, art_len, pos0, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q,
+                          gamma_k, req_kv, cache_rows, o, lse, stream, false);
+}
+
+attuner_status attuner_suffix_attn_noalloc(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                           const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                           const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                           int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                           int64_t cache_rows, void* o, float* lse, void* stream) {
+  return suffix_attn_impl(c, layer, n_req, cu_q, cu_ctx, art_len, pos0, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q,
+                          gamma_k, req_kv, cache_rows, o, lse, stream, true);
 }
 
 attuner_status attuner_span_attn(attuner_ctx* c, int32_t layer, int32_t n_spans, const int32_t* cu_q,
