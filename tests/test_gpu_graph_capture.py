@@ -174,3 +174,70 @@ def test_capture_past_the_rope_table_fails_and_eager_growth_matches():
             g.close()
     assert np.array_equal(results[True][0], results[False][0])
     assert results[True][1] == results[False][1]
+
+
+def test_reserve_then_capture_prefill_without_warmup():
+    # a reservation alone (no eager call first) must size every workspace the
+    # suffix path needs: capture three layers of the Qwen3-4B-shaped step and
+    # a full prefill of 600 tokens with a rank-48 adapter (the separate
+    # down-projection), replay twice, compare with the eager calls bit for bit
+    import synthdata as sd
+    wl = sd.make_workload("c2", gamma="uniform")
+    s = wl.shape
+    g = GpuWorkload(wl, layers=[0, 17, 35])
+    try:
+        T = wl.requests[0].suffix_len
+        nq, nkv = s.q_dim, s.kv_dim
+        n_out = nq + 2 * nkv
+        ins = []
+        for li in range(3):
+            w, x = g.layer_inputs(li)
+            ins.append((dev_bf16(x), dev_bf16(np.concatenate([w["wq"], w["wk"], w["wv"]])), dev_bf16(w["a"]),
+                        dev_bf16(w["b"]), dev_bf16(w["gamma_q"]), dev_bf16(w["gamma_k"])))
+        rng = np.random.default_rng(5)
+        N, r = 600, 48
+        xf = dev_bf16(sd.f32_to_bf16_bits(rng.standard_normal((N, s.hidden)).astype(np.float32)))
+        af = dev_bf16(sd.f32_to_bf16_bits((rng.standard_normal((r, s.hidden)) / np.sqrt(s.hidden)).astype(np.float32)))
+        bfm = dev_bf16(sd.f32_to_bf16_bits((rng.standard_normal((nq, r)) * 0.01).astype(np.float32)))
+        g.ctx.reserve(max_tokens=N, max_position=max(g.rows, N), max_rank=r)
+
+        def run(outs):
+            for li, (x, w, a, b, gq, gk) in enumerate(ins):
+                qkv, o, lse = outs[li]
+                g.ctx.qproj_lora(x, w, a, b, wl.rank, wl.scale, nq, qkv)
+                g.ctx.suffix_attn(li, g.cu_q, g.cu_ctx, g.art_len, g.pos0, qkv[:, :nq], n_out, qkv[:, nq:nq + nkv],
+                                  qkv[:, nq + nkv:], n_out, gq, gk, g.req_kv, g.rows, o, lse)
+            of, kf, vf = outs[3]
+            g.ctx.full_prefill(0, xf, ins[0][1], af, bfm, r, 0.5, ins[0][4], ins[0][5], of, kf, vf)
+
+        def buffers():
+            bufs = [(torch.empty(T, n_out, dtype=torch.bfloat16, device="cuda"),
+                     torch.empty(T, s.n_q_heads, s.head_dim, dtype=torch.bfloat16, device="cuda"),
+                     torch.empty(T, s.n_q_heads, dtype=torch.float32, device="cuda")) for _ in range(3)]
+            bufs.append((torch.empty(N, s.n_q_heads, s.head_dim, dtype=torch.bfloat16, device="cuda"),
+                         torch.empty(s.n_kv_heads, N, s.head_dim, dtype=torch.bfloat16, device="cuda"),
+                         torch.empty(s.n_kv_heads, N, s.head_dim, dtype=torch.bfloat16, device="cuda")))
+            return bufs
+
+        _say("capture after a reservation, no eager call first")
+        cap = buffers()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            run(cap)
+        torch.cuda.synchronize()
+        _say("eager reference")
+        ref = buffers()
+        run(ref)
+        torch.cuda.synchronize()
+        for rep in range(2):
+            for t in cap:
+                for u in t:
+                    u.zero_()
+            torch.cuda.synchronize()
+            gr.replay()
+            torch.cuda.synchronize()
+            for i, (a_, b_) in enumerate(zip(cap, ref)):
+                for u, v in zip(a_, b_):
+                    assert torch.equal(u, v), f"replay {rep}: buffer set {i} differs from the eager calls"
+    finally:
+        g.close()
