@@ -89,7 +89,12 @@ def parse():
                          "(attuner_assemble_segments + per layer attuner_qproj_lora and attuner_span_attn)")
     ap.add_argument("--host-cache", action="store_true",
                     help="keep the artifact caches in pinned host memory (attuner_store_artifact_host): every step "
-                         "then gathers them over the host link into HBM, as the paper's timed TTFT does")
+                         "then moves them over the host link into HBM, as the paper's timed TTFT does")
+    ap.add_argument("--host-route", choices=["staged", "mapped"], default="staged",
+                    help="with --host-cache: 'staged' copies each layer's host pages into an HBM staging pool with "
+                         "bulk hipMemcpyAsync copies (attuner_assemble_table_staged + attuner_stage_layers) beside the layer "
+                         "loop, and gathers each layer from there before its attention; 'mapped' gathers straight "
+                         "from the mapped host pool with the gather kernel")
     ap.add_argument("--merged", action="store_true",
                     help="deployment form: merge each layer's adapter into W_q once before timing "
                          "(attuner_merge_lora) and run the rank-0 projection in the step")
@@ -282,8 +287,11 @@ def main():
     cfg = ModelCfg(n_layers=NL, hidden=s.hidden, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
                    head_dim=s.head_dim, rope_theta=s.rope_theta, rms_eps=s.rms_eps)
     ctx = Context(cfg, pool_pages=0 if args.host_cache else pages)
+    staged = args.host_cache and args.host_route == "staged"
     if args.host_cache:
         ctx.host_pool_create(pages)
+    if staged:
+        ctx.stage_pool_create(pages)
     store = ctx.store_artifact_host if args.host_cache else ctx.store_artifact
     ids = {}
     for a in used:
@@ -320,6 +328,8 @@ def main():
     # the same assembly split: the table (host plan + upload) on the launch
     # stream, then one gather per layer on a second stream
     table_args = (h, len(requests), c_ptr, c_ids, c_cap, block_table.data_ptr(), cu_ctx_arr, art_arr, rows, sp)
+    n_staged = C.c_int64()
+    staged_args = table_args[:-1] + (C.byref(n_staged), sp)
     cu_ctx, art_len = list(cu_ctx_arr), list(art_arr)[:len(requests)]
     cu_q = [0]
     for r in wl.requests:
@@ -404,8 +414,12 @@ def main():
     # does not read the cache).  The layer loop (with
     # the per-layer gathers when overlapped) is replayed as one captured HIP
     # graph unless --no-graph.
+    # With the staged host route bulk copies move layer l's host pages
+    # into the staging pool on the second stream (one event per layer), and
+    # the launch stream gathers layer l from there after its projection.
     layer_gather_bytes = gather_bytes(s, sum(wl.art_len(r) for r in wl.requests), 1)
     overlap = args.overlap_gather if args.overlap_gather is not None else layer_gather_bytes >= 100e6
+    overlap = overlap and not staged
     side = torch.cuda.Stream()
     ev_fork, ev_layer = torch.cuda.Event(), [torch.cuda.Event() for _ in range(NL)]
 
@@ -419,28 +433,41 @@ def main():
         second stream before the layer loop issues the waits on them."""
         msp = C.c_void_p(main.cuda_stream)
         ssp = C.c_void_p(side.cuda_stream)
-        if overlap:
+        if overlap or staged:
             ev_fork.record(main)
             side.wait_event(ev_fork)
             for l in range(NL):
-                check(lib.attuner_gather_layers(h, block_table.data_ptr(), n_entries, l, 1, req_kv.data_ptr(), rows,
-                                                ssp), "attuner_gather_layers")
+                if staged:
+                    check(lib.attuner_stage_layers(h, l, 1, ssp), "attuner_stage_layers")
+                else:
+                    check(lib.attuner_gather_layers(h, block_table.data_ptr(), n_entries, l, 1, req_kv.data_ptr(),
+                                                    rows, ssp), "attuner_gather_layers")
                 ev_layer[l].record(side)
         for l in range(NL):
             check(lib.attuner_qproj_lora(*(qa[l][:-1] + (msp,))), "attuner_qproj_lora")
-            if overlap:
+            if overlap or staged:
                 main.wait_event(ev_layer[l])
+            if staged:
+                check(lib.attuner_gather_layers(h, block_table.data_ptr(), n_entries, l, 1, req_kv.data_ptr(), rows,
+                                                msp), "attuner_gather_layers")
             check(lib.attuner_suffix_attn(*(aa[l][:-1] + (msp,))), "attuner_suffix_attn")
-        if overlap:
+        if overlap or staged:
             main.wait_stream(side)
 
+    # The staged route runs eagerly: the runtime performs a host-to-device
+    # hipMemcpyAsync from the pinned pool as a copy kernel, and in a replayed
+    # graph those copy nodes did not overlap the layer loop's kernels
+    # (measured at 36 layers, 8B shapes, 32 x 1024 artifact tokens: 104.3 ms
+    # per step replayed against 89.6 ms eager).
     graph = None
-    if not args.no_graph:
+    if not args.no_graph and not staged:
         cap = torch.cuda.Stream()
         graph = torch.cuda.CUDAGraph()
         cap.wait_stream(stream)
         side.wait_stream(stream)
-        if overlap:  # the captured gathers read the table the last assemble_table call wrote
+        if staged:  # the captured copies are those of the plan current at capture
+            check(lib.attuner_assemble_table_staged(*staged_args), "attuner_assemble_table_staged")
+        elif overlap:  # the captured gathers read the table the last assemble_table call wrote
             check(lib.attuner_assemble_table(*table_args), "attuner_assemble_table")
         torch.cuda.synchronize()
         with torch.cuda.graph(graph, stream=cap):
@@ -448,13 +475,15 @@ def main():
         torch.cuda.synchronize()
 
     def timed_step():
-        if overlap:
+        if staged:
+            check(lib.attuner_assemble_table_staged(*staged_args), "attuner_assemble_table_staged")
+        elif overlap:
             check(lib.attuner_assemble_table(*table_args), "attuner_assemble_table")
         else:
             check(lib.attuner_assemble_kv(*assemble_args), "attuner_assemble_kv")
         if graph is not None:
             graph.replay()
-        elif overlap:
+        elif overlap or staged:
             layer_loop(stream, qproj_args, attn_args)
         else:
             run_step(None, 0, gather=False)
@@ -474,6 +503,25 @@ def main():
     log(args, f"timed {args.steps} steps ({'graph' if graph is not None else 'eager'} layer loop): "
               f"{ms_step:.3f} ms/step (host wall {1e3 * wall / args.steps:.3f} ms/step); per launch ms "
               f"(eager, events): " + ", ".join(f"{c} {kern_ms[c]:.4f}" for c in cats))
+    host_transfer = None
+    if staged:  # the bulk copies alone: every layer's staging copies, timed on the second stream
+        check(lib.attuner_assemble_table_staged(*staged_args), "attuner_assemble_table_staged")
+        runs = ctx.stage_pool_info()[1]
+        side.wait_stream(stream)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record(side)
+        check(lib.attuner_stage_layers(h, 0, NL, C.c_void_p(side.cuda_stream)), "attuner_stage_layers")
+        c1.record(side)
+        torch.cuda.synchronize()
+        copy_ms = c0.elapsed_time(c1)
+        copy_bytes = n_staged.value * NL * 2 * s.n_kv_heads * 16 * s.head_dim * 2
+        host_transfer = {"route": "bulk copies into an HBM staging pool, then the HBM gather per layer",
+                         "staged_pages": n_staged.value, "copies_per_layer": runs, "bytes_per_step": copy_bytes,
+                         "copy_ms": round(copy_ms, 4), "copy_gbps": round(copy_bytes / (copy_ms * 1e-3) / 1e9, 2)}
+        log(args, f"staging copies alone: {copy_bytes / 1e9:.3f} GB in {copy_ms:.2f} ms "
+                  f"({copy_bytes / (copy_ms * 1e-3) / 1e9:.1f} GB/s, {runs} copies per layer)")
+    elif args.host_cache:
+        host_transfer = {"route": "gather kernel reading the mapped host pool"}
 
     # ---- algorithmic rates -----------------------------------------------------
     reqs_shape = [(wl.art_len(r), r.suffix_len) for r in wl.requests]
@@ -555,8 +603,11 @@ def main():
                    "artifact_tokens": [L for L, _ in reqs_shape], "suffix_tokens": [S for _, S in reqs_shape],
                    "lora_rank": wl.rank, "page_tokens": 16},
         "layer_loop": "hip_graph" if graph is not None else "eager",
-        "gather_schedule": "per layer on a second stream beside the layer loop" if overlap else "all layers first",
-        "artifact_cache": "pinned host memory, gathered over the host link every step" if args.host_cache else "HBM",
+        "gather_schedule": ("per layer: bulk copies on a second stream, HBM gather before the layer's attention"
+                            if staged else "per layer on a second stream beside the layer loop" if overlap
+                            else "all layers first"),
+        "artifact_cache": "pinned host memory, moved over the host link every step" if args.host_cache else "HBM",
+        "host_transfer": host_transfer,
         "adapter": "merged into W_q (rank-0 projection)" if args.merged else "unmerged, fused into the projection",
         "roofline": {"bound": "mfma", "kernel": "attention_kernel", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),

@@ -94,7 +94,8 @@ const char* attuner_last_error(void);
  * n_layers * 2 * n_kv_heads * page_tokens * head_dim * 2 bytes (see
  * attuner_pool_info).  The pool is the only memory allocated here; it is
  * released by attuner_destroy.  Synchronous.
- * Errors: EINVAL (geometry), ENOMEM (allocation), EDEVICE. */
+ * Errors: EINVAL (geometry), ERANGE (pool_pages outside [0, 2^29)), ENOMEM
+ * (allocation), EDEVICE. */
 attuner_status attuner_create(const attuner_model_cfg* cfg, int64_t pool_pages, int32_t device,
                               attuner_ctx** out);
 
@@ -167,7 +168,7 @@ attuner_status attuner_artifact_pages(const attuner_ctx* ctx, int32_t artifact_i
  * pages as (page | ATTUNER_HOST_PAGE_FLAG).  attuner_release_artifact returns
  * pages to the pool they came from.
  * Errors: EINVAL (no host pool / a second one), ERANGE (host_pages outside
- * [1, 2^30)), ENOMEM (pinned allocation, host pool full), EDEVICE.
+ * [1, 2^29)), ENOMEM (pinned allocation, host pool full), EDEVICE.
  * ------------------------------------------------------------------------ */
 #define ATTUNER_HOST_PAGE_FLAG (1 << 30)
 
@@ -239,6 +240,62 @@ attuner_status attuner_assemble_table(attuner_ctx* ctx, int32_t n_req, const int
 attuner_status attuner_gather_layers(attuner_ctx* ctx, const int32_t* block_table, int64_t n_entries,
                                      int32_t layer_begin, int32_t n_layers, void* req_kv,
                                      int64_t cache_rows, void* stream);
+
+/* --------------------------------------------------------------------------
+ * Host-pool artifacts moved by bulk copies into HBM (the transfer of
+ * appendix A.2, done per layer so that it overlaps the compute of earlier
+ * layers; a bulk copy holds far fewer wave slots than the gather kernel
+ * reading host memory page by page, and a page that several requests use
+ * crosses the host link once).
+ *
+ * attuner_stage_pool_create gives the context a staging pool of stage_pages
+ * pages in HBM (same page size and layout as the other pools; released by
+ * attuner_destroy); once per context.
+ *
+ * attuner_assemble_table_staged is attuner_assemble_table, except that every
+ * distinct host page the batch uses gets a staging page (the i-th smallest
+ * host page id gets staging page i; a page used by several requests is
+ * staged once) and the block table names the staging page, as
+ * (page | ATTUNER_STAGE_PAGE_FLAG); HBM-pool pages are unchanged.
+ * *staged_pages (may be null) receives the number of distinct host pages.
+ * It also records the copies that attuner_stage_layers makes: one per
+ * maximal range of consecutive host page ids.
+ *
+ * attuner_stage_layers copies layers layer_begin .. layer_begin + n_layers - 1
+ * of those host pages into the staging pool with hipMemcpyAsync on `stream`
+ * (from the pinned host pool: one copy per run and layer; the HIP runtime
+ * chooses the engine, and for these copies it runs its own copy kernel).  attuner_gather_layers over the staged table then moves the staged
+ * pages of a layer into the request cache like any HBM page; the caller
+ * orders each layer's gather after that layer's staging copy (same stream,
+ * or an event).  The call is the last staged assembly's: once another
+ * assembly call is made on the context it is refused with EINVAL.  Under
+ * graph capture the copies of the current plan are recorded; a replay makes
+ * those same copies, so a captured graph belongs to one batch plan (the same
+ * artifacts in the same order give the same plan).  The staging pool is
+ * shared by every call on the context: a staged assembly must not start
+ * while copies or gathers of the previous one may still be running unless
+ * both use the same plan.
+ * Errors: EINVAL (no staging pool / a second one; the last assembly not
+ * staged), ERANGE (stage_pages outside [1, 2^29); more distinct host pages
+ * than stage_pages; layers outside [0, n_layers)), ENOMEM, EDEVICE; otherwise
+ * as attuner_assemble_table.
+ *
+ * attuner_stage_pool_info: the staging pool's size and the number of copy
+ * runs per layer of the current plan (0 when the last assembly was not
+ * staged).
+ * ------------------------------------------------------------------------ */
+#define ATTUNER_STAGE_PAGE_FLAG (1 << 29)
+
+attuner_status attuner_stage_pool_create(attuner_ctx* ctx, int64_t stage_pages);
+
+attuner_status attuner_assemble_table_staged(attuner_ctx* ctx, int32_t n_req, const int32_t* req_ptr,
+                                             const int32_t* artifact_ids, const int32_t* suffix_cap,
+                                             int32_t* block_table, int32_t* cu_ctx, int32_t* art_len,
+                                             int64_t cache_rows, int64_t* staged_pages, void* stream);
+
+attuner_status attuner_stage_layers(attuner_ctx* ctx, int32_t layer_begin, int32_t n_layers, void* stream);
+
+attuner_status attuner_stage_pool_info(const attuner_ctx* ctx, int64_t* stage_pages, int64_t* runs);
 
 /* --------------------------------------------------------------------------
  * Prompts that interleave cached artifacts with online spans (appendix A.3:

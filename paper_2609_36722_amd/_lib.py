@@ -16,6 +16,7 @@ STATUS = {0: "ATTUNER_OK", -1: "ATTUNER_EINVAL", -2: "ATTUNER_ENOMEM", -3: "ATTU
 MAX_REQUESTS = 64
 MAX_RANK = 64
 HOST_PAGE_FLAG = 1 << 30
+STAGE_PAGE_FLAG = 1 << 29
 NOALLOC_SCRATCH_BYTES = 24 << 20
 
 
@@ -66,6 +67,11 @@ SIGNATURES = {
     "attuner_host_pool_create": (C.c_int, [_vp, _i64]),
     "attuner_store_artifact_host": (C.c_int, [_vp, _i32, _vp, _vp, _vp, _i32p]),
     "attuner_host_pool_info": (C.c_int, [_vp, _i64p, _i64p]),
+    "attuner_stage_pool_create": (C.c_int, [_vp, _i64]),
+    "attuner_assemble_table_staged": (C.c_int, [_vp, _i32, _i32p, _i32p, _i32p, _vp, _i32p, _i32p, _i64, _i64p,
+                                                _vp]),
+    "attuner_stage_layers": (C.c_int, [_vp, _i32, _i32, _vp]),
+    "attuner_stage_pool_info": (C.c_int, [_vp, _i64p, _i64p]),
     "attuner_assemble_segments_plan": (C.c_int, [_vp, _i32, _i32p, _i32p, _i64p, _i64p, _i32p]),
     "attuner_assemble_segments": (C.c_int, [_vp, _i32, _i32p, _i32p, _vp, _i32p, _i32p, _vp, _i64, _vp]),
     "attuner_span_attn": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp, _i64, _vp, _vp,

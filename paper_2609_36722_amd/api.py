@@ -163,6 +163,38 @@ class Context:
         _check(lib().attuner_host_pool_info(self._h, C.byref(pages), C.byref(free)), "attuner_host_pool_info")
         return pages.value, free.value
 
+    # ---- host-pool pages moved by bulk copies into an HBM staging pool ---------------
+    def stage_pool_create(self, stage_pages: int) -> None:
+        _check(lib().attuner_stage_pool_create(self._h, int(stage_pages)), "attuner_stage_pool_create")
+
+    def stage_pool_info(self) -> Tuple[int, int]:
+        """(staging pages, copy runs per layer of the current staged plan)."""
+        pages, runs = C.c_int64(), C.c_int64()
+        _check(lib().attuner_stage_pool_info(self._h, C.byref(pages), C.byref(runs)), "attuner_stage_pool_info")
+        return pages.value, runs.value
+
+    def assemble_table_staged(self, requests: Sequence[Sequence[int]], suffix_cap: Sequence[int],
+                              block_table: torch.Tensor, cache_rows: int,
+                              stream=None) -> Tuple[List[int], List[int], int]:
+        """Like assemble_table, with host pages remapped to staging pages;
+        returns (cu_ctx, art_len, distinct host pages staged)."""
+        ne, _ = self.assemble_plan(requests, suffix_cap)
+        _need(block_table, 4 * ne, "block_table")
+        ptr, ids = self._csr(requests)
+        n = len(requests)
+        cu = (C.c_int32 * (n + 1))()
+        al = (C.c_int32 * max(1, n))()
+        staged = C.c_int64()
+        _check(lib().attuner_assemble_table_staged(self._h, n, _i32(ptr), _i32(ids), _i32(suffix_cap),
+                                                   _ptr(block_table, 4) if block_table is not None else None, cu,
+                                                   al, int(cache_rows), C.byref(staged), _stream(stream)),
+               "attuner_assemble_table_staged")
+        return list(cu), list(al)[:n], staged.value
+
+    def stage_layers(self, layer_begin: int, n_layers: int, stream=None) -> None:
+        _check(lib().attuner_stage_layers(self._h, int(layer_begin), int(n_layers), _stream(stream)),
+               "attuner_stage_layers")
+
     def release_artifact(self, artifact_id: int) -> None:
         _check(lib().attuner_release_artifact(self._h, int(artifact_id)), "attuner_release_artifact")
 

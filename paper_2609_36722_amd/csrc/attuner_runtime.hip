@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -268,6 +269,13 @@ struct attuner_ctx {
   uint16_t* host_pool = nullptr;
   uint16_t* host_pool_dev = nullptr;
   std::set<int32_t> host_free;
+  // staging pool in HBM (same layout) for host pages moved by the copy
+  // engines, and the copies the last staged assembly planned: runs of
+  // {first host page, first staging page, pages}
+  int64_t stage_pages = 0;
+  uint16_t* stage_pool = nullptr;
+  std::vector<std::array<int32_t, 3>> stage_runs;
+  bool last_staged = false;
   std::map<int32_t, Artifact> artifacts;
   int32_t next_id = 0;
 
@@ -780,7 +788,8 @@ attuner_status attuner_create(const attuner_model_cfg* cfg, int64_t pool_pages, 
   if (cfg->hidden <= 0 || cfg->hidden % 64 != 0) return fail(ATTUNER_EINVAL, "hidden %d must be a multiple of 64", cfg->hidden);
   if (cfg->n_layers <= 0 || cfg->n_layers > 65535) return fail(ATTUNER_EINVAL, "n_layers %d outside [1, 65535]", cfg->n_layers);
   if (!(cfg->rope_theta > 1.0f) || !(cfg->rms_eps >= 0.0f)) return fail(ATTUNER_EINVAL, "bad rope_theta or rms_eps");
-  if (pool_pages < 0 || pool_pages > INT32_MAX) return fail(ATTUNER_ERANGE, "pool_pages %lld", (long long)pool_pages);
+  if (pool_pages < 0 || pool_pages >= kStagePageFlag)
+    return fail(ATTUNER_ERANGE, "pool_pages %lld outside [0, 2^29)", (long long)pool_pages);
   int n_dev = 0;
   HIP_TRY(hipGetDeviceCount(&n_dev));
   if (device < 0 || device >= n_dev) return fail(ATTUNER_EINVAL, "device %d of %d", device, n_dev);
@@ -876,6 +885,7 @@ void attuner_destroy(attuner_ctx* c) {
   c->tracer.release();
   if (c->pool) (void)hipFree(c->pool);
   if (c->host_pool) (void)hipHostFree(c->host_pool);
+  if (c->stage_pool) (void)hipFree(c->stage_pool);
   delete c;
 }
 
@@ -934,8 +944,8 @@ attuner_status attuner_store_artifact(attuner_ctx* c, int32_t n_tokens, const vo
 attuner_status attuner_host_pool_create(attuner_ctx* c, int64_t host_pages) {
   if (!c) return fail(ATTUNER_EINVAL, "null ctx");
   if (c->host_pool) return fail(ATTUNER_EINVAL, "the context already has a host pool");
-  if (host_pages <= 0 || host_pages >= kHostPageFlag)
-    return fail(ATTUNER_ERANGE, "host_pages %lld outside [1, 2^30)", (long long)host_pages);
+  if (host_pages <= 0 || host_pages >= kStagePageFlag)
+    return fail(ATTUNER_ERANGE, "host_pages %lld outside [1, 2^29)", (long long)host_pages);
   DeviceGuard dg(c->device);
   void* h = nullptr;
   hipError_t e = hipHostMalloc(&h, (size_t)(host_pages * c->page_bytes), hipHostMallocMapped | hipHostMallocPortable);
@@ -1046,12 +1056,58 @@ attuner_status attuner_assemble_plan(const attuner_ctx* c, int32_t n_req, const 
   return plan_impl(c, n_req, req_ptr, artifact_ids, suffix_cap, n_entries, cache_rows, nullptr, nullptr, nullptr);
 }
 
+static attuner_status assemble_table_impl(attuner_ctx* c, bool staged, int32_t n_req, const int32_t* req_ptr,
+                                          const int32_t* artifact_ids, const int32_t* suffix_cap,
+                                          int32_t* block_table, int32_t* cu_ctx, int32_t* art_len,
+                                          int64_t cache_rows, int64_t* n_staged, void* stream);
+
 attuner_status attuner_assemble_table(attuner_ctx* c, int32_t n_req, const int32_t* req_ptr,
                                       const int32_t* artifact_ids, const int32_t* suffix_cap, int32_t* block_table,
                                       int32_t* cu_ctx, int32_t* art_len, int64_t cache_rows, void* stream) {
+  return assemble_table_impl(c, false, n_req, req_ptr, artifact_ids, suffix_cap, block_table, cu_ctx, art_len,
+                             cache_rows, nullptr, stream);
+}
+
+// The staged form remaps every host page of the batch to a staging page:
+// the distinct host pages, in ascending order, get staging pages 0, 1, ...,
+// so that every maximal range of consecutive host pages is one copy run
+// (artifacts stored one after another in the host pool then move in one copy
+// per layer, whatever order the requests use them in).
+static attuner_status stage_remap(attuner_ctx* c, std::vector<int32_t>& table, int64_t* n_staged) {
+  c->stage_runs.clear();
+  std::vector<int32_t> host;
+  for (size_t e = 0; e < table.size(); e += 4)
+    if (table[e] & kHostPageFlag) host.push_back(table[e] & kPageIdMask);
+  std::sort(host.begin(), host.end());
+  host.erase(std::unique(host.begin(), host.end()), host.end());
+  if ((int64_t)host.size() > c->stage_pages)
+    return fail(ATTUNER_ERANGE, "the batch uses %zu distinct host pages, the staging pool holds %lld", host.size(),
+                (long long)c->stage_pages);
+  for (size_t i = 0; i < host.size(); ++i) {
+    if (i > 0 && host[i] == host[i - 1] + 1)
+      ++c->stage_runs.back()[2];
+    else
+      c->stage_runs.push_back({host[i], (int32_t)i, 1});
+  }
+  for (size_t e = 0; e < table.size(); e += 4) {
+    if (!(table[e] & kHostPageFlag)) continue;
+    const auto it = std::lower_bound(host.begin(), host.end(), table[e] & kPageIdMask);
+    table[e] = (int32_t)(it - host.begin()) | kStagePageFlag;
+  }
+  if (n_staged) *n_staged = (int64_t)host.size();
+  return ATTUNER_OK;
+}
+
+static attuner_status assemble_table_impl(attuner_ctx* c, bool staged, int32_t n_req, const int32_t* req_ptr,
+                                          const int32_t* artifact_ids, const int32_t* suffix_cap,
+                                          int32_t* block_table, int32_t* cu_ctx, int32_t* art_len,
+                                          int64_t cache_rows, int64_t* n_staged, void* stream) {
   if (!c) return fail(ATTUNER_EINVAL, "null ctx");
   c->last_table = nullptr;
   c->last_entries = c->last_rows = -1;
+  c->last_staged = false;
+  c->stage_runs.clear();
+  if (staged && !c->stage_pool) return fail(ATTUNER_EINVAL, "no staging pool (attuner_stage_pool_create)");
   std::vector<int32_t> table;
   std::vector<int32_t> cu(n_req > 0 ? n_req + 1 : 1), al(n_req > 0 ? n_req : 1);
   int64_t entries = 0, rows = 0;
@@ -1059,7 +1115,15 @@ attuner_status attuner_assemble_table(attuner_ctx* c, int32_t n_req, const int32
     attuner_status st = plan_impl(c, n_req, req_ptr, artifact_ids, suffix_cap, &entries, &rows, &table, cu.data(),
                                   al.data());
     if (st != ATTUNER_OK) return st;
+    if (staged) {
+      st = stage_remap(c, table, n_staged);
+      if (st != ATTUNER_OK) {
+        c->stage_runs.clear();
+        return st;
+      }
+    }
   } catch (const std::bad_alloc&) {
+    c->stage_runs.clear();
     return fail(ATTUNER_ENOMEM, "host allocation");
   }
   if (rows != cache_rows)
@@ -1071,12 +1135,70 @@ attuner_status attuner_assemble_table(attuner_ctx* c, int32_t n_req, const int32
   if (entries > 0) {
     DeviceGuard dg(c->device);
     attuner_status st = upload_host(c, table.data(), table.size() * sizeof(int32_t), block_table,
-                                    static_cast<hipStream_t>(stream), "attuner_assemble_table");
-    if (st != ATTUNER_OK) return st;
+                                    static_cast<hipStream_t>(stream),
+                                    staged ? "attuner_assemble_table_staged" : "attuner_assemble_table");
+    if (st != ATTUNER_OK) {
+      c->stage_runs.clear();
+      return st;
+    }
   }
   c->last_table = block_table;
   c->last_entries = entries;
   c->last_rows = rows;
+  c->last_staged = staged;
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_assemble_table_staged(attuner_ctx* c, int32_t n_req, const int32_t* req_ptr,
+                                             const int32_t* artifact_ids, const int32_t* suffix_cap,
+                                             int32_t* block_table, int32_t* cu_ctx, int32_t* art_len,
+                                             int64_t cache_rows, int64_t* staged_pages, void* stream) {
+  return assemble_table_impl(c, true, n_req, req_ptr, artifact_ids, suffix_cap, block_table, cu_ctx, art_len,
+                             cache_rows, staged_pages, stream);
+}
+
+attuner_status attuner_stage_pool_create(attuner_ctx* c, int64_t stage_pages) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (c->stage_pool) return fail(ATTUNER_EINVAL, "the context already has a staging pool");
+  if (stage_pages <= 0 || stage_pages >= kStagePageFlag)
+    return fail(ATTUNER_ERANGE, "stage_pages %lld outside [1, 2^29)", (long long)stage_pages);
+  DeviceGuard dg(c->device);
+  void* d = nullptr;
+  hipError_t e = hipMalloc(&d, (size_t)(stage_pages * c->page_bytes));
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(ATTUNER_ENOMEM, "staging pool of %lld pages (%lld bytes): %s", (long long)stage_pages,
+                (long long)(stage_pages * c->page_bytes), hipGetErrorString(e));
+  }
+  c->stage_pool = static_cast<uint16_t*>(d);
+  c->stage_pages = stage_pages;
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_stage_layers(attuner_ctx* c, int32_t layer_begin, int32_t n_layers, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (!c->last_staged) return fail(ATTUNER_EINVAL, "the last assembly was not attuner_assemble_table_staged");
+  if (layer_begin < 0 || n_layers < 0 || layer_begin > c->cfg.n_layers || n_layers > c->cfg.n_layers - layer_begin)
+    return fail(ATTUNER_ERANGE, "layers [%d, %d) outside [0, %d)", layer_begin, layer_begin + n_layers,
+                c->cfg.n_layers);
+  DeviceGuard dg(c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // one page of one layer: [2][n_kv][16][head_dim] bf16, contiguous in both pools
+  const size_t layer_page = (size_t)(c->page_bytes / c->cfg.n_layers);
+  const char* host = reinterpret_cast<const char*>(c->host_pool);
+  char* stage = reinterpret_cast<char*>(c->stage_pool);
+  for (int32_t l = layer_begin; l < layer_begin + n_layers; ++l)
+    for (const auto& run : c->stage_runs)
+      HIP_TRY(hipMemcpyAsync(stage + ((size_t)l * c->stage_pages + run[1]) * layer_page,
+                             host + ((size_t)l * c->host_pages + run[0]) * layer_page, (size_t)run[2] * layer_page,
+                             hipMemcpyHostToDevice, s));
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_stage_pool_info(const attuner_ctx* c, int64_t* stage_pages, int64_t* runs) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (stage_pages) *stage_pages = c->stage_pages;
+  if (runs) *runs = c->last_staged ? (int64_t)c->stage_runs.size() : 0;
   return ATTUNER_OK;
 }
 
@@ -1094,8 +1216,8 @@ attuner_status attuner_gather_layers(attuner_ctx* c, const int32_t* block_table,
   if (n_entries == 0 || n_layers == 0) return ATTUNER_OK;
   if (!req_kv || !aligned16(req_kv)) return fail(ATTUNER_EINVAL, "req_kv must be non-null and 16-byte aligned");
   DeviceGuard dg(c->device);
-  HIP_TRY(launch_gather(block_table, n_entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages, layer_begin,
-                          n_layers, c->cfg.n_kv_heads,
+  HIP_TRY(launch_gather(block_table, n_entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages,
+                        c->stage_pool, c->stage_pages, layer_begin, n_layers, c->cfg.n_kv_heads,
                         static_cast<uint16_t*>(req_kv), cache_rows, static_cast<hipStream_t>(stream)));
   return ATTUNER_OK;
 }
@@ -1193,6 +1315,8 @@ attuner_status attuner_assemble_segments(attuner_ctx* c, int32_t n_req, const in
   if (!c) return fail(ATTUNER_EINVAL, "null ctx");
   c->last_table = nullptr;
   c->last_entries = c->last_rows = -1;
+  c->last_staged = false;
+  c->stage_runs.clear();
   std::vector<int32_t> table, sp;
   std::vector<int32_t> cu(n_req > 0 ? n_req + 1 : 1);
   int64_t entries = 0, rows = 0;
@@ -1217,8 +1341,8 @@ attuner_status attuner_assemble_segments(attuner_ctx* c, int32_t n_req, const in
     attuner_status st = upload_host(c, table.data(), table.size() * sizeof(int32_t), block_table, s,
                                     "attuner_assemble_segments");
     if (st != ATTUNER_OK) return st;
-    HIP_TRY(launch_gather(block_table, entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages, 0,
-                          c->cfg.n_layers, c->cfg.n_kv_heads,
+    HIP_TRY(launch_gather(block_table, entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages, nullptr, 0,
+                          0, c->cfg.n_layers, c->cfg.n_kv_heads,
                           static_cast<uint16_t*>(req_kv), cache_rows, s));
   }
   c->last_table = block_table;

@@ -1,9 +1,11 @@
 // K1: paged artifact pool -- store and block-table gather (bit-exact copies).
 //
-// Two pools with one layout: the HBM pool and, optionally, a host pool in
-// pinned host memory (the paper keeps artifact caches in CPU RAM and copies
-// them to the GPU per request, inside the timed region, appendix A.2); the
-// gather kernel reads host pages over the host link directly.
+// Pools with one layout: the HBM pool and, optionally, a host pool in pinned
+// host memory (the paper keeps artifact caches in CPU RAM and copies them to
+// the GPU per request, inside the timed region, appendix A.2) and a staging
+// pool in HBM.  The gather kernel reads host pages over the host link
+// directly, or, after bulk copies moved them into the staging pool,
+// from there (a block-table entry's flag bits say which pool).
 // Pool layout: [n_layers][pool_pages][2 (K, V)][n_kv][16 tokens][128] bf16, so
 // one page of one layer is a contiguous 2 * n_kv * 4 KiB block and each
 // (K|V, head) slab of it is 4 KiB.  Request cache layout:
@@ -70,8 +72,10 @@ constexpr int kGatherRun = 4;  // block-table entries per gather workgroup
 
 __global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ table, int64_t n_entries,
                                                      const u32x4* __restrict__ dev_pool, int64_t dev_pages,
-                                                     const u32x4* __restrict__ host_pool, int64_t host_pages, int n_kv,
-                                                     u32x4* __restrict__ req_kv, int64_t cache_rows, int layer_begin) {
+                                                     const u32x4* __restrict__ host_pool, int64_t host_pages,
+                                                     const u32x4* __restrict__ stage_pool, int64_t stage_pages,
+                                                     int n_kv, u32x4* __restrict__ req_kv, int64_t cache_rows,
+                                                     int layer_begin) {
   const int n_slab = 2 * n_kv;
   const int64_t e0 = (int64_t)blockIdx.x * kGatherRun;
   const int s = (int)(blockIdx.y % n_slab);  // slab s = c * n_kv + g
@@ -87,9 +91,10 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ ta
     ent[i] = e0 + i < n_entries ? table[e0 + i] : int4{0, 0, 0, 0};
     if (rr < ent[i].y) {
       const bool host = (ent[i].x & kHostPageFlag) != 0;
-      const u32x4* __restrict__ pool = host ? host_pool : dev_pool;
-      const int64_t pool_pages = host ? host_pages : dev_pages;
-      const int64_t src = ((int64_t)layer * pool_pages + (ent[i].x & ~kHostPageFlag)) * n_slab + s;
+      const bool staged = (ent[i].x & kStagePageFlag) != 0;
+      const u32x4* __restrict__ pool = staged ? stage_pool : host ? host_pool : dev_pool;
+      const int64_t pool_pages = staged ? stage_pages : host ? host_pages : dev_pages;
+      const int64_t src = ((int64_t)layer * pool_pages + (ent[i].x & kPageIdMask)) * n_slab + s;
       buf[i] = __builtin_nontemporal_load(pool + (src * kPageTokens + rr) * 16 + chunk);
     }
   }
@@ -113,8 +118,9 @@ hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens
 }
 
 hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint16_t* pool, int64_t pool_pages,
-                         const uint16_t* host_pool, int64_t host_pages, int layer_begin, int n_layers, int n_kv,
-                         uint16_t* req_kv, int64_t cache_rows, hipStream_t stream) {
+                         const uint16_t* host_pool, int64_t host_pages, const uint16_t* stage_pool,
+                         int64_t stage_pages, int layer_begin, int n_layers, int n_kv, uint16_t* req_kv,
+                         int64_t cache_rows, hipStream_t stream) {
   if (n_entries == 0 || n_layers == 0) return hipSuccess;
   const int64_t runs = (n_entries + kGatherRun - 1) / kGatherRun;
   if (runs > INT32_MAX) return hipErrorInvalidValue;
@@ -125,7 +131,8 @@ hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint
     dim3 grid(static_cast<unsigned>(runs), static_cast<unsigned>(nl * 2 * n_kv));
     ATTUNER_LAUNCH("gather_kernel", gather_kernel, grid, dim3(256), stream, reinterpret_cast<const int4*>(table_dev),
                    n_entries, reinterpret_cast<const u32x4*>(pool), pool_pages,
-                   reinterpret_cast<const u32x4*>(host_pool), host_pages, n_kv, reinterpret_cast<u32x4*>(req_kv),
+                   reinterpret_cast<const u32x4*>(host_pool), host_pages,
+                   reinterpret_cast<const u32x4*>(stage_pool), stage_pages, n_kv, reinterpret_cast<u32x4*>(req_kv),
                    cache_rows, layer_begin + l0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -39,9 +39,15 @@ hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens
 // is page (page & ~kHostPageFlag) of the host pool (pinned host memory, same
 // layout, read by the kernel over the host link); others are HBM pool pages.
 constexpr int32_t kHostPageFlag = 1 << 30;
+// A page with kStagePageFlag set is page (page & kPageIdMask) of the staging
+// pool: device memory that host pages were copied into for the current
+// assembly (same layout as the other pools).
+constexpr int32_t kStagePageFlag = 1 << 29;
+constexpr int32_t kPageIdMask = kStagePageFlag - 1;
 hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint16_t* pool, int64_t pool_pages,
-                         const uint16_t* host_pool, int64_t host_pages, int layer_begin, int n_layers, int n_kv,
-                         uint16_t* req_kv, int64_t cache_rows, hipStream_t stream);
+                         const uint16_t* host_pool, int64_t host_pages, const uint16_t* stage_pool,
+                         int64_t stage_pages, int layer_begin, int n_layers, int n_kv, uint16_t* req_kv,
+                         int64_t cache_rows, hipStream_t stream);
 
 // ---- a3: LoRA-down and the projection GEMM --------------------------------
 

@@ -2,7 +2,8 @@
 host pages over the host link into the request cache, bit-exact against the
 oracle's assembly, mixed with HBM-pool artifacts, all layers at once and
 layer by layer, and in an interleaved prompt; pages are reused after a
-release."""
+release.  The copy-engine route (host pages copied into an HBM staging pool,
+then gathered) gives the same cache, eagerly and from a replayed graph."""
 
 import numpy as np
 import pytest
@@ -15,7 +16,7 @@ pytestmark = pytest.mark.gpu
 if torch.cuda.is_available():
     from tests._gpu import dev_bf16
     from paper_2609_36722_amd.api import AttunerError, Context, ModelCfg, bf16_to_host
-    from paper_2609_36722_amd._lib import HOST_PAGE_FLAG
+    from paper_2609_36722_amd._lib import HOST_PAGE_FLAG, STAGE_PAGE_FLAG
 
 
 def _say(msg):
@@ -118,6 +119,173 @@ def test_host_pool_segments_and_errors():
             src = slice(16 * p, 16 * p + nv)
             assert np.array_equal(got[:, 0, :, dst:dst + nv], art_k[a_idx][:, src].transpose(0, 2, 1, 3))
             assert np.array_equal(got[:, 1, :, dst:dst + nv], art_v[a_idx][:, src].transpose(0, 2, 1, 3))
+
+
+# ----------------------------------------------------------------------------
+# copy-engine route: host pages -> HBM staging pool -> request cache
+# ----------------------------------------------------------------------------
+
+def _staged_table_want(ctx, ids, lengths, reqs):
+    """The block table the staged assembly must write: the oracle's entries
+    through the physical pages, the i-th smallest distinct host page renamed
+    to staging page i; and the distinct count."""
+    entries, _ = oracle.block_table(lengths, reqs, 16)
+    phys = {a: ctx.artifact_pages(ids[a])[0] for a in ids}
+    host = sorted({phys[a][p] for a, p, _, _, _ in entries.tolist() if phys[a][p] & HOST_PAGE_FLAG})
+    slot = {pg: i for i, pg in enumerate(host)}
+    rows = []
+    for a, p, nv, r, dst in entries.tolist():
+        pg = phys[a][p]
+        if pg & HOST_PAGE_FLAG:
+            pg = slot[pg] | STAGE_PAGE_FLAG
+        rows.append([pg, nv, dst, r])
+    return np.array(rows, np.int32).reshape(-1, 4), len(slot)
+
+
+def _check_cache(kv, cache, cu, al, n_layers, rows, what):
+    got = bf16_to_host(kv).reshape(n_layers, 2, 8, rows, 128)
+    for r in range(len(cu) - 1):
+        lo, n = cu[r], al[r]
+        assert np.array_equal(got[:, :, :, lo:lo + n], cache[:, :, :, lo:lo + n]), f"{what}: request {r}"
+
+
+def test_staged_assembly_bit_exact():
+    _say("staged host pool assembly")
+    rng = np.random.default_rng(83)
+    lengths = [17, 40, 1, 33, 300]
+    host = {1, 2, 4}
+    with Context(ModelCfg(n_layers=3, hidden=256), pool_pages=8) as ctx:
+        ctx.host_pool_create(40)
+        art_k, art_v, ids = _store_mixed(ctx, rng, lengths, host, 3)
+        reqs = [([1, 0, 4], 5), ([], 3), ([2, 2, 3, 1], 0)]
+        requests, caps = [[ids[a] for a in r] for r, _ in reqs], [c for _, c in reqs]
+        ne, rows = ctx.assemble_plan(requests, caps)
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        with pytest.raises(AttunerError) as e:
+            ctx.assemble_table_staged(requests, caps, bt, rows)
+        assert e.value.status == -1                 # no staging pool yet
+        ctx.stage_pool_create(23)                   # the batch's distinct host pages: 3 + 1 + 19
+        with pytest.raises(AttunerError) as e:
+            ctx.stage_pool_create(23)
+        assert e.value.status == -1
+        cu, al, staged = ctx.assemble_table_staged(requests, caps, bt, rows)
+        torch.cuda.synchronize()
+        want, n_distinct = _staged_table_want(ctx, ids, lengths, reqs)
+        assert staged == n_distinct == 23
+        assert np.array_equal(bt.cpu().numpy().reshape(-1, 4), want)
+        pages, runs = ctx.stage_pool_info()
+        assert pages == 23 and runs == 1             # host pages 0..22: one copy per layer
+        cache, cu_o = oracle.assemble(art_k, art_v, reqs, 8, 128)
+        assert list(cu) == list(cu_o)
+        # layer by layer: copies on one stream, each layer's gather on a
+        # second one after that layer's copies (event)
+        kv = torch.zeros(3 * 2 * 8 * rows * 128, dtype=torch.bfloat16, device="cuda")
+        copy, side = torch.cuda.Stream(), torch.cuda.Stream()
+        copy.wait_stream(torch.cuda.current_stream())
+        side.wait_stream(torch.cuda.current_stream())
+        for l in (2, 0, 1):
+            ctx.stage_layers(l, 1, stream=copy)
+            ev = torch.cuda.Event()
+            ev.record(copy)
+            side.wait_event(ev)
+            ctx.gather_layers(bt, ne, l, 1, kv, rows, stream=side)
+        torch.cuda.synchronize()
+        _check_cache(kv, cache, cu, al, 3, rows, "per layer")
+        # all layers at once, one stream
+        kv.zero_()
+        ctx.stage_layers(0, 3)
+        ctx.gather_layers(bt, ne, 0, 3, kv, rows)
+        torch.cuda.synchronize()
+        _check_cache(kv, cache, cu, al, 3, rows, "all layers")
+        # host pages with a gap (artifact 2's page left out): two copy runs
+        reqs3 = [([4, 0, 1], 2)]
+        req3 = [[ids[a] for a in r] for r, _ in reqs3]
+        ne3, rows3 = ctx.assemble_plan(req3, [2])
+        bt3 = torch.zeros(ne3 * 4, dtype=torch.int32, device="cuda")
+        cu3, al3, n3 = ctx.assemble_table_staged(req3, [2], bt3, rows3)
+        want3, _ = _staged_table_want(ctx, ids, lengths, reqs3)
+        assert n3 == 22 and ctx.stage_pool_info()[1] == 2
+        kv3 = torch.zeros(3 * 2 * 8 * rows3 * 128, dtype=torch.bfloat16, device="cuda")
+        ctx.stage_layers(0, 3)
+        ctx.gather_layers(bt3, ne3, 0, 3, kv3, rows3)
+        torch.cuda.synchronize()
+        assert np.array_equal(bt3.cpu().numpy().reshape(-1, 4), want3)
+        _check_cache(kv3, oracle.assemble(art_k, art_v, reqs3, 8, 128)[0], cu3, al3, 3, rows3, "two runs")
+        # a repeated host artifact is staged once
+        req2 = requests + [[ids[4], ids[1]]]
+        ne2, rows2 = ctx.assemble_plan(req2, caps + [0])
+        bt2 = torch.zeros(ne2 * 4, dtype=torch.int32, device="cuda")
+        assert ctx.assemble_table_staged(req2, caps + [0], bt2, rows2)[2] == 23
+        # errors: layers out of range, staging after a plain assembly
+        cu, al, _ = ctx.assemble_table_staged(requests, caps, bt, rows)
+        with pytest.raises(AttunerError) as e:
+            ctx.stage_layers(2, 2)
+        assert e.value.status == -5
+        ctx.assemble_table(requests, caps, bt, rows)
+        with pytest.raises(AttunerError) as e:
+            ctx.stage_layers(0, 1)
+        assert e.value.status == -1
+        assert ctx.stage_pool_info()[1] == 0
+
+
+def test_staged_assembly_capacity():
+    _say("staged assembly: staging pool too small")
+    rng = np.random.default_rng(84)
+    with Context(ModelCfg(n_layers=2, hidden=256), pool_pages=0) as ctx:
+        ctx.host_pool_create(8)
+        ctx.stage_pool_create(3)
+        _, _, ids = _store_mixed(ctx, rng, [40, 20], {0, 1}, 2)   # 3 + 2 host pages
+        ne, rows = ctx.assemble_plan([[ids[0]]], [0])
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        assert ctx.assemble_table_staged([[ids[0]]], [0], bt, rows)[2] == 3
+        ne, rows = ctx.assemble_plan([[ids[0], ids[1]]], [0])
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        with pytest.raises(AttunerError) as e:
+            ctx.assemble_table_staged([[ids[0], ids[1]]], [0], bt, rows)
+        assert e.value.status == -5
+        with pytest.raises(AttunerError) as e:      # the failed plan left nothing to stage
+            ctx.stage_layers(0, 1)
+        assert e.value.status == -1
+
+
+def test_staged_assembly_graph_replays():
+    """Copies and gathers captured in one HIP graph, replayed three times with
+    eager work and synchronisations between replays: every replay rebuilds
+    the cache the oracle assembles."""
+    _say("staged assembly in a captured graph")
+    rng = np.random.default_rng(85)
+    lengths = [64, 48, 100, 16]
+    with Context(ModelCfg(n_layers=2, hidden=256), pool_pages=8) as ctx:
+        ctx.host_pool_create(16)
+        ctx.stage_pool_create(16)
+        art_k, art_v, ids = _store_mixed(ctx, rng, lengths, {0, 2, 3}, 2)
+        reqs = [([0, 1, 2], 7), ([3, 0], 4)]
+        requests, caps = [[ids[a] for a in r] for r, _ in reqs], [c for _, c in reqs]
+        ne, rows = ctx.assemble_plan(requests, caps)
+        bt = torch.zeros(ne * 4, dtype=torch.int32, device="cuda")
+        kv = torch.zeros(2 * 2 * 8 * rows * 128, dtype=torch.bfloat16, device="cuda")
+        cu, al, _ = ctx.assemble_table_staged(requests, caps, bt, rows)
+        cache, _ = oracle.assemble(art_k, art_v, reqs, 8, 128)
+        torch.cuda.synchronize()
+        cap, copy = torch.cuda.Stream(), torch.cuda.Stream()
+        graph = torch.cuda.CUDAGraph()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.graph(graph, stream=cap):
+            copy.wait_stream(cap)
+            for l in range(2):
+                ctx.stage_layers(l, 1, stream=copy)
+                ev = torch.cuda.Event()
+                ev.record(copy)
+                cap.wait_event(ev)
+                ctx.gather_layers(bt, ne, l, 1, kv, rows, stream=cap)
+        torch.cuda.synchronize()
+        for rep in range(3):
+            kv.zero_()
+            ctx.assemble_table_staged(requests, caps, bt, rows)   # same plan each time
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            _check_cache(kv, cache, cu, al, 2, rows, f"replay {rep}")
 
 
 # ----------------------------------------------------------------------------
