@@ -534,7 +534,9 @@ def main():
 
     attn_tflops = attn_f / (attn_kernel_ms * 1e-3) / 1e12          # attention_kernel alone
     attn_call_tflops = attn_f / (kern_ms["attn"] * 1e-3) / 1e12   # attuner_suffix_attn call (+ norm, merge)
-    gemm_kernel_ms = kavg("gemm_lora_kernel")
+    # the projection runs one GEMM kernel per layer (which one: the tile plan)
+    gemm_name = next(k for k in ("gemm_kg2_kernel", "gemm_lora_kernel") if k in ktimes)
+    gemm_kernel_ms = kavg(gemm_name)
     gemm_tflops = gemm_f / (gemm_kernel_ms * 1e-3) / 1e12
     gather_kernel_ms = kavg("gather_kernel")
     gather_gbps = g_bytes / (gather_kernel_ms * 1e-3) / 1e9
@@ -618,7 +620,7 @@ def main():
                           "call_tflops": round(attn_call_tflops, 2)},
             "qproj_lora_gemm": {"tflops": round(gemm_tflops, 2), "mfma_frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
                                 "kernel_ms": round(gemm_kernel_ms, 5), "call_ms": round(kern_ms["qproj"], 5),
-                                "flops_per_layer": gemm_f},
+                                "flops_per_layer": gemm_f, "kernel": gemm_name},
             "kv_gather": {"gbps": round(gather_gbps, 1), "hbm_frac": round(gather_gbps / PEAK_HBM_GBPS, 4),
                           "kernel_ms": round(gather_kernel_ms, 5), "call_ms": round(kern_ms["gather"], 5),
                           "bytes_per_step": g_bytes},
@@ -1032,7 +1034,8 @@ def decode_main(args):
     attn_gbps = (kv_bytes + io_bytes) / (attn_ms * 1e-3) / 1e9
     # the projection of a few tokens: the weight-streaming GEMV (+ the LoRA
     # down-projection kernel); more tokens take the MFMA GEMM
-    proj = [k for k in ("gemv_kernel", "gemv_mfma_kernel", "lora_down_kernel", "gemm_lora_kernel") if k in per_kernel]
+    proj = [k for k in ("gemv_kernel", "gemv_mfma_kernel", "lora_down_kernel", "gemm_lora_kernel", "gemm_kg2_kernel")
+            if k in per_kernel]
     gemm_ms = sum(per_kernel[k]["avg_ms"] for k in proj)
     gemm_w_gbps = n_out * H * 2 / (gemm_ms * 1e-3) / 1e9
     log(args, f"decode step {ms_step:.3f} ms ({n_req / (ms_step * 1e-3):.1f} tokens/s); decode attention "

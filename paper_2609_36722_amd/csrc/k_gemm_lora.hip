@@ -158,7 +158,7 @@ __device__ __forceinline__ void lora_epilogue_store(f32x16 (&acc)[FN][FM], int n
 // one barrier per k-tile.  A k-tile stage is (BN + BM) rows of 128 bytes,
 // moved as 1 KiB blocks of 8 rows (lane i -> row 8 blk + i / 8, physical
 // chunk i % 8, holding the logical chunk the swizzle maps there).
-template <int BM, int BN, int WN, int WM, int NST>
+template <int BM, int BN, int WN, int WM, int NST, bool ILV>
 __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t* __restrict__ x,
                                                                    const bf16_t* __restrict__ w, int M, int N, int K,
                                                                    const bf16_t* __restrict__ a, float scale,
@@ -266,10 +266,16 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
       __builtin_amdgcn_s_waitcnt(vmcnt_wait((NST - 2) * PW));
       barrier_no_fence();
       const int nk = min(kt + NST - 1, n_kt - 1);
-#pragma unroll
-      for (int j = 0; j < PW; ++j) lds_dma16(src[j] + nk * BK, lds0 + (uint32_t)(nslot * STAGE * 16) + doff[j]);
-
       const u32x4* cur = lds + slot * STAGE;
+      // ILV: the stage's copies are spread over the k-steps (one after
+      // every second MFMA, the rest after the last k-step), so that a wave
+      // whose copies wait for room in the memory pipeline has MFMAs in
+      // flight; otherwise all are issued here
+      int d = ILV ? 0 : PW;
+      if (!ILV) {
+#pragma unroll
+        for (int j = 0; j < PW; ++j) lds_dma16(src[j] + nk * BK, lds0 + (uint32_t)(nslot * STAGE * 16) + doff[j]);
+      }
 #pragma unroll
       for (int ks = 0; ks < BK / 16; ++ks) {
         const int ch = 2 * ks + hi;
@@ -284,10 +290,20 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
           const int row = BN + wm * TM + j * 32 + l32;
           bfr[j] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
         }
+        int q = 0;
 #pragma unroll
         for (int i = 0; i < FN; ++i)
 #pragma unroll
-          for (int j = 0; j < FM; ++j) acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
+          for (int j = 0; j < FM; ++j) {
+            acc[i][j] = mfma32(af[i], bfr[j], acc[i][j]);
+            if (ILV && (q & 1) == 1 && d < PW) {
+              __builtin_amdgcn_sched_barrier(0);
+              lds_dma16(src[d] + nk * BK, lds0 + (uint32_t)(nslot * STAGE * 16) + doff[d]);
+              __builtin_amdgcn_sched_barrier(0);
+              ++d;
+            }
+            ++q;
+          }
         if (LA && wn < FM) {
           const int row = BN + BM + l32;
           const bf16x8 ar = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
@@ -296,6 +312,9 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
             if (j % WN == wn) tacc[j] = mfma32(ar, bfr[j], tacc[j]);
         }
       }
+#pragma unroll
+      for (int e = 0; e < PW; ++e)
+        if (e >= d) lds_dma16(src[e] + nk * BK, lds0 + (uint32_t)(nslot * STAGE * 16) + doff[e]);
       slot = slot + 1 == NST ? 0 : slot + 1;
       nslot = nslot + 1 == NST ? 0 : nslot + 1;
     }
@@ -328,6 +347,218 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void gemm_lora_kernel(const bf16_t
   if (kt_split > 0) epi.out_f32 += (int64_t)split * M * N;
   lora_epilogue_store<FN, FM>(acc, n0 + wn * TN, m0 + wm * TM, wm * TM, l32, hi, M, N, b, rank, r_pad, lora_cols,
                               t_part, n_slice, t_lds, epi, out);
+}
+
+// The same product with two k-groups of waves.  Each wave holds a 96 x 64
+// (features x tokens) tile of C^T, which reads 5 LDS fragments per 6 MFMAs
+// (3 per 2 for the 32 x 64 tile above), and the waves of group g take
+// k-steps g and g + 2 of every 64-deep k-tile, so that two waves share each
+// SIMD and cover each other's LDS latency.  After the k-loop the groups
+// exchange halves through LDS: group g gives its partner its partial sums of
+// token block 1 - g and adds the partner's partial sums of token block g,
+// then applies the epilogue to block g.  The fused LoRA down-projection is
+// split the same way (each group's t^T over its k-steps, summed in LDS).
+template <int BM, int BN, int WN, int WM, int NST>
+__global__ __launch_bounds__(128 * WN * WM, 1) void gemm_kg2_kernel(const bf16_t* __restrict__ x,
+                                                                   const bf16_t* __restrict__ w, int M, int N, int K,
+                                                                   const bf16_t* __restrict__ a, float scale,
+                                                                   const bf16_t* __restrict__ b, int rank, int r_pad,
+                                                                   int lora_cols, const float* __restrict__ t_part,
+                                                                   int n_slice, GemmEpi epi, bf16_t* out, int n_mt,
+                                                                   int n_nt, int kt_split) {
+  constexpr int NWG = WN * WM;  // waves per k-group
+  constexpr int NW = 2 * NWG;
+  constexpr int TN = BN / WN, TM = BM / WM;
+  constexpr int FN = TN / 32, FM = TM / 32;
+  static_assert(FM == 2 && FN >= 1 && TN % 32 == 0, "each group finishes one of a wave's two token blocks");
+  constexpr int ROWS = BN + BM + kLoraRows;
+  static_assert((BN + BM) % 8 == 0, "stage must be whole 1 KiB blocks");
+  constexpr int STAGE = ROWS * kChunksPerRow;
+  __shared__ u32x4 lds[NST * STAGE];
+  // after the k-loop: t staging [BM][kLoraRows + 1] floats, then the exchange
+  // [2 groups][NWG waves][FN][16][64 lanes] floats
+  constexpr int kTsFloats = (BM * (kLoraRows + 1) + 63) / 64 * 64;
+  static_assert((kTsFloats + 2 * NWG * FN * 16 * 64) * 4 <= NST * STAGE * 16, "exchange must fit the ring");
+
+  const int total = n_mt * n_nt;
+  const int per_xcd = total >> 3;
+  const int split = kt_split > 0 ? (int)blockIdx.x / total : 0;
+  int lin = kt_split > 0 ? (int)blockIdx.x % total : (int)blockIdx.x;
+  if (lin < 8 * per_xcd) lin = (lin & 7) * per_xcd + (lin >> 3);
+  const int in_group = kGroupM * n_nt;
+  const int first_m = (lin / in_group) * kGroupM;
+  const int gm = min(n_mt - first_m, kGroupM);
+  const int mt = first_m + (lin % in_group) % gm;
+  const int nt = (lin % in_group) / gm;
+  const int n0 = nt * BN;
+  const int m0 = mt * BM;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int kg = wave / NWG;
+  const int wv = wave % NWG;
+  const int wn = wv / WM;
+  const int wm = wv % WM;
+  const int l32 = lane & 31;
+  const int hi = lane >> 5;
+  const int kt0 = split * kt_split;
+  const int n_kt = kt_split > 0 ? min(K / BK - kt0, kt_split) : K / BK;
+  const uint32_t lds0 = lds_addr(lds);
+
+  f32x16 acc[FN][FM];
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j) acc[i][j] = f32x16{};
+  const bool fused = t_part == nullptr && r_pad > 0 && n0 < lora_cols;
+  f32x16 tacc[FM];
+#pragma unroll
+  for (int j = 0; j < FM; ++j) tacc[j] = f32x16{};
+
+  auto kloop = [&](auto la_tag) __attribute__((always_inline)) {
+    constexpr bool LA = decltype(la_tag)::value;
+    constexpr int NBLK = (BN + BM + (LA ? kLoraRows : 0)) / 8;
+    constexpr int PW = (NBLK + NW - 1) / NW;
+    static_assert((NST - 2) * PW <= 63, "vmcnt range");
+    const bf16_t* src[PW];
+    uint32_t doff[PW];
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      const int blk = min(wave + NW * j, NBLK - 1);
+      const int row = 8 * blk + (lane >> 3);
+      const int lg = swz(row, lane & 7);
+      const bf16_t* base;
+      if (row < BN) {
+        base = w + (int64_t)(n0 + row) * K;
+      } else if (row < BN + BM) {
+        const int m = min(m0 + row - BN, M - 1);
+        base = x + (int64_t)m * K;
+      } else {
+        base = a + (int64_t)min(row - BN - BM, rank - 1) * K;
+      }
+      src[j] = base + 8 * lg + (int64_t)kt0 * BK;
+      doff[j] = 1024u * blk;
+    }
+#pragma unroll
+    for (int st = 0; st < NST - 1; ++st) {
+      const int kt = min(st, n_kt - 1);
+#pragma unroll
+      for (int j = 0; j < PW; ++j) lds_dma16(src[j] + kt * BK, lds0 + (uint32_t)(st * STAGE * 16) + doff[j]);
+    }
+    int slot = 0, nslot = NST - 1;
+    for (int kt = 0; kt < n_kt; ++kt) {
+      __builtin_amdgcn_s_waitcnt(vmcnt_wait((NST - 2) * PW));
+      barrier_no_fence();
+      const int nk = min(kt + NST - 1, n_kt - 1);
+      const u32x4* cur = lds + slot * STAGE;
+      // fragments of both k-steps (the second read while the first multiplies)
+      bf16x8 af[2][FN], bfr[2][FM], ar[2];
+      auto load = [&](int s2) __attribute__((always_inline)) {
+        const int ch = 2 * (kg + 2 * s2) + hi;
+#pragma unroll
+        for (int i = 0; i < FN; ++i) {
+          const int row = wn * TN + i * 32 + l32;
+          af[s2][i] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+        }
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+          const int row = BN + wm * TM + j * 32 + l32;
+          bfr[s2][j] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+        }
+        if (LA && wn < FM) {
+          const int row = BN + BM + l32;
+          ar[s2] = as_bf16x8(cur[row * kChunksPerRow + swz(row, ch)]);
+        }
+      };
+      constexpr int HALF = (PW + 1) / 2;
+      load(0);
+      load(1);
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        int q = 0;
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+          for (int j = 0; j < FM; ++j) {
+            acc[i][j] = mfma32(af[s2][i], bfr[s2][j], acc[i][j]);
+            if (q % 2 == 1) {
+              const int d = s2 * HALF + q / 2;
+              if (d < PW && q / 2 < HALF) {
+                __builtin_amdgcn_sched_barrier(0);
+                lds_dma16(src[d] + nk * BK, lds0 + (uint32_t)(nslot * STAGE * 16) + doff[d]);
+                __builtin_amdgcn_sched_barrier(0);
+              }
+            }
+            ++q;
+          }
+        if (LA && wn < FM) {
+#pragma unroll
+          for (int j = 0; j < FM; ++j)
+            if (j % WN == wn) tacc[j] = mfma32(ar[s2], bfr[s2][j], tacc[j]);
+        }
+        // DMAs of this half not yet issued (more than FN * FM / 2 of them)
+#pragma unroll
+        for (int e = (FN * FM) / 2; e < HALF; ++e) {
+          const int d = s2 * HALF + e;
+          if (d < PW) lds_dma16(src[d] + nk * BK, lds0 + (uint32_t)(nslot * STAGE * 16) + doff[d]);
+        }
+      }
+      slot = slot + 1 == NST ? 0 : slot + 1;
+      nslot = nslot + 1 == NST ? 0 : nslot + 1;
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+  };
+
+  if (fused) kloop(std::integral_constant<bool, true>{});
+  else kloop(std::integral_constant<bool, false>{});
+  __syncthreads();  // every wave is done with the ring
+
+  float* ts = reinterpret_cast<float*>(lds);
+  float* xch = ts + kTsFloats;
+  const float* t_lds = nullptr;
+  if (fused) {
+    // t^T accumulator: lane holds ranks 8 (v / 4) + 4 hi + v % 4 of token
+    // l32 of each 32-token block; staged as t[token][rank] (row stride
+    // kLoraRows + 1), group 0's sums first, group 1's added
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      if (kg == g) {
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+          if (j % WN != wn || wn >= FM) continue;
+          const int ml = wm * TM + j * 32 + l32;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            float* d = ts + ml * (kLoraRows + 1) + 8 * (v >> 2) + 4 * hi + (v & 3);
+            *d = g == 0 ? scale * tacc[j][v] : *d + scale * tacc[j][v];
+          }
+        }
+      }
+      __syncthreads();
+    }
+    t_lds = ts;
+  }
+
+  if (kt_split > 0) epi.out_f32 += (int64_t)split * M * N;
+  auto finish = [&](auto j_tag) __attribute__((always_inline)) {
+    constexpr int J = decltype(j_tag)::value;  // the token block this group finishes
+    float* give = xch + ((kg * NWG + wv) * FN) * 1024;
+    float* take = xch + (((1 - kg) * NWG + wv) * FN) * 1024;
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) give[(i * 16 + v) * 64 + lane] = acc[i][1 - J][v];
+    __syncthreads();
+    f32x16 mine[FN][1];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mine[i][0][v] = acc[i][J][v] + take[(i * 16 + v) * 64 + lane];
+    lora_epilogue_store<FN, 1>(mine, n0 + wn * TN, m0 + wm * TM + 32 * J, wm * TM + 32 * J, l32, hi, M, N, b, rank,
+                               r_pad, lora_cols, t_part, n_slice, t_lds, epi, out);
+  };
+  if (kg == 0) finish(std::integral_constant<int, 0>{});
+  else finish(std::integral_constant<int, 1>{});
 }
 
 // t = scale * x A^T with MFMAs, as fp32 partial sums per 256-wide slice of the
@@ -433,28 +664,36 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 struct Tile {
   int bm, bn;
 };
-constexpr Tile kTiles[] = {{256, 256}, {128, 256}, {256, 96}, {128, 128}, {128, 96}, {64, 96}, {64, 64}};
+constexpr Tile kTiles[] = {{256, 256}, {128, 256}, {256, 96}, {128, 128}, {128, 96}, {64, 96}, {64, 64},
+                           {128, 192}};
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
+
 
 hipError_t launch_tile(int tile, int kt_split, int grid, const uint16_t* x, const uint16_t* w, int n_tok, int n_out,
                        int hidden, const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad,
                        int lora_cols, const float* t_part, int n_slice, GemmEpi epi, uint16_t* out,
                        hipStream_t stream) {
-#define ATTUNER_GEMM(BM_, BN_, WN_, WM_, NST_)                                                                 \
-  ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, WM_, NST_>), dim3((unsigned)grid),     \
+#define ATTUNER_GEMM(BM_, BN_, WN_, WM_, NST_, ILV_)                                                           \
+  ATTUNER_LAUNCH("gemm_lora_kernel", (gemm_lora_kernel<BM_, BN_, WN_, WM_, NST_, ILV_>), dim3((unsigned)grid), \
                  dim3(64 * (WN_) * (WM_)), stream, x, w, n_tok, n_out, hidden, a, scale, b, rank, r_pad,       \
                  lora_cols, t_part, n_slice, epi, out, (n_tok + (BM_) - 1) / (BM_), n_out / (BN_), kt_split)
+#define ATTUNER_GEMM_KG2(BM_, BN_, WN_, WM_, NST_)                                                             \
+  ATTUNER_LAUNCH("gemm_kg2_kernel", (gemm_kg2_kernel<BM_, BN_, WN_, WM_, NST_>), dim3((unsigned)grid),       \
+                 dim3(128 * (WN_) * (WM_)), stream, x, w, n_tok, n_out, hidden, a, scale, b, rank, r_pad,      \
+                 lora_cols, t_part, n_slice, epi, out, (n_tok + (BM_) - 1) / (BM_), n_out / (BN_), kt_split)
   switch (tile) {
-    case 0: ATTUNER_GEMM(256, 256, 4, 2, 2); break;
-    case 1: ATTUNER_GEMM(128, 256, 4, 2, 3); break;
-    case 2: ATTUNER_GEMM(256, 96, 3, 4, 3); break;
-    case 3: ATTUNER_GEMM(128, 128, 2, 2, 4); break;
-    case 4: ATTUNER_GEMM(128, 96, 3, 2, 4); break;
-    case 5: ATTUNER_GEMM(64, 96, 3, 2, 5); break;
-    case 6: ATTUNER_GEMM(64, 64, 2, 2, 6); break;
+    case 0: ATTUNER_GEMM(256, 256, 4, 2, 2, true); break;
+    case 1: ATTUNER_GEMM(128, 256, 4, 2, 3, false); break;
+    case 2: ATTUNER_GEMM(256, 96, 3, 4, 3, false); break;
+    case 3: ATTUNER_GEMM(128, 128, 2, 2, 4, false); break;
+    case 4: ATTUNER_GEMM(128, 96, 3, 2, 4, false); break;
+    case 5: ATTUNER_GEMM(64, 96, 3, 2, 5, false); break;
+    case 6: ATTUNER_GEMM(64, 64, 2, 2, 6, false); break;
+    case 7: ATTUNER_GEMM_KG2(128, 192, 2, 2, 3); break;
     default: return hipErrorInvalidValue;  // callers keep n_out a multiple of 64: 64x64 always fits
   }
 #undef ATTUNER_GEMM
+#undef ATTUNER_GEMM_KG2
   return hipGetLastError();
 }
 
