@@ -661,11 +661,14 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   *reinterpret_cast<u32x2*>(out + m * N + n) = pk;
 }
 
+// rate: the operand ingest per CU the tile model assumes (measured on
+// gfx950; the two-k-group kernel overlaps its MFMAs with the copies best)
 struct Tile {
   int bm, bn;
+  double rate;
 };
-constexpr Tile kTiles[] = {{256, 256}, {128, 256}, {256, 96}, {128, 128}, {128, 96}, {64, 96}, {64, 64},
-                           {128, 192}};
+constexpr Tile kTiles[] = {{256, 256, 42e9}, {128, 256, 52e9}, {256, 96, 52e9}, {128, 128, 52e9}, {128, 96, 52e9},
+                           {64, 96, 52e9},   {64, 64, 52e9},   {128, 192, 60e9}, {128, 96, 60e9}};
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
 
@@ -690,6 +693,7 @@ hipError_t launch_tile(int tile, int kt_split, int grid, const uint16_t* x, cons
     case 5: ATTUNER_GEMM(64, 96, 3, 2, 5, false); break;
     case 6: ATTUNER_GEMM(64, 64, 2, 2, 6, false); break;
     case 7: ATTUNER_GEMM_KG2(128, 192, 2, 2, 3); break;
+    case 8: ATTUNER_GEMM_KG2(128, 96, 1, 2, 4); break;
     default: return hipErrorInvalidValue;  // callers keep n_out a multiple of 64: 64x64 always fits
   }
 #undef ATTUNER_GEMM
@@ -701,8 +705,9 @@ hipError_t launch_tile(int tile, int kt_split, int grid, const uint16_t* x, cons
 
 // Tile and key split of a product, by a model fitted to gfx950 runs.  One
 // workgroup per CU at a time; a workgroup's time is the larger of its operand
-// ingest ((BM + BN) * k-range * 2 bytes at about 52 GB/s per CU, 42 GB/s for
-// the 256 x 256 tile whose ring holds only two k-tiles) and its MFMA work
+// ingest ((BM + BN) * k-range * 2 bytes at the tile's rate: about 52 GB/s per
+// CU, 42 GB/s for the 256 x 256 tile whose ring holds only two k-tiles, 60
+// GB/s for the two-k-group tiles) and its MFMA work
 // (2 BM BN k-range at about 6 TFLOP/s per CU); a launch takes ceil(workgroups
 // / 256) such rounds plus a fixed 4 us.  Without a low-rank term, and when a
 // tile's workgroups would leave CUs idle, the k range may be split across
@@ -710,12 +715,13 @@ hipError_t launch_tile(int tile, int kt_split, int grid, const uint16_t* x, cons
 // 8 bytes written and read at about 4 TB/s) and a 3 us reduce launch.  The
 // plan minimises the model; ties go to the earlier tile and to no split.  On
 // gfx950 it picks the measured fastest plan for the q/k/v projection (6144
-// outputs, hidden 2560 / 4096) at T = 64 (64x64), 256 (64x96), 512 (128x96),
-// 1024 (256x96) and 8448 (256x256), and for the o/gate-up/down products of
-// the 4B and 8B layers at 256 and 1024 tokens (e.g. down at 256 tokens:
-// 128x128 in 6 splits, 28.9 us against 46.5 us unsplit).
+// outputs, hidden 2560 / 4096) at T = 64 (64x64), 256 (64x96), 512 (the
+// two-k-group 128x96), 1024 (the two-k-group 128x192) and 33792 (256x256),
+// and for the o/gate-up/down products of the 4B and 8B layers at 256 and
+// 1024 tokens (e.g. down at 256 tokens: 128x128 in 6 splits, 28.9 us against
+// 46.5 us unsplit).
 GemmPlan plan_gemm(int n_tok, int n_out, int k_dim, bool lora) {
-  constexpr double kIngest = 52e9, kIngest256 = 42e9, kMfmaPerCu = 6e12, kFixed = 4e-6;
+  constexpr double kMfmaPerCu = 6e12, kFixed = 4e-6;
   constexpr double kPartBw = 4e12, kReduceLaunch = 3e-6;
   constexpr int kSplits[] = {1, 2, 3, 4, 6, 8, 12, 16};
   const int n_kt = k_dim / BK;
@@ -724,7 +730,7 @@ GemmPlan plan_gemm(int n_tok, int n_out, int k_dim, bool lora) {
   for (int i = 0; i < kNumTiles; ++i) {
     if (n_out % kTiles[i].bn != 0) continue;
     const int64_t tiles = (int64_t)((n_tok + kTiles[i].bm - 1) / kTiles[i].bm) * (n_out / kTiles[i].bn);
-    const double rate = i == 0 ? kIngest256 : kIngest;
+    const double rate = kTiles[i].rate;
     for (int s : kSplits) {
       // splits only add workgroups where the tiles alone leave CUs idle
       if (s > 1 && (lora || n_kt < 4 * s || tiles >= 256)) break;
