@@ -749,11 +749,11 @@ attuner_status qproj_impl(attuner_ctx* c, int32_t n_tok, const void* x, const vo
   const int hidden = c->cfg.hidden;
   const int r_pad = rank > 0 && lora_cols > 0 ? (rank + 15) / 16 * 16 : 0;
   // ranks up to kGemmFusedLoraMaxRank: the GEMM computes t = scale * x A^T
-  // itself; larger ranks, and the GEMV of a few tokens, take a separate
-  // down-projection kernel first
+  // itself where its tile hides the work; larger ranks, the GEMV of a few
+  // tokens and the largest tile take a separate down-projection kernel first
   float* t_part = nullptr;
-  if (r_pad > kGemmFusedLoraMaxRank || (r_pad > 0 && n_tok <= kGemvMaxTok)) {
-    const size_t part_bytes = (size_t)lora_down_slices(hidden) * n_tok * r_pad * sizeof(float);
+  if (r_pad > 0 && (r_pad > kGemmFusedLoraMaxRank || n_tok <= kGemvMaxTok || !gemm_fuses_lora(n_tok, n_out, hidden))) {
+    const size_t part_bytes = (size_t)lora_down_slices(hidden, n_tok) * n_tok * r_pad * sizeof(float);
     attuner_status st = grow(c, c->ws_lora, part_bytes, stream, "LoRA down-projection");
     if (st != ATTUNER_OK) return st;
     t_part = static_cast<float*>(c->ws_lora.ptr);
@@ -837,7 +837,7 @@ attuner_status attuner_reserve(attuner_ctx* c, const attuner_limits* lim) {
   // LoRA down-projection slice partials (ranks above the fused limit, or few tokens)
   if (st == ATTUNER_OK && lim->max_rank > 0 && T > 0) {
     const int64_t r_pad = (lim->max_rank + 15) / 16 * 16;
-    st = grow(c, c->ws_lora, (size_t)lora_down_slices(c->cfg.hidden) * T * r_pad * sizeof(float), s,
+    st = grow(c, c->ws_lora, (size_t)lora_down_slices(c->cfg.hidden, 1) * T * r_pad * sizeof(float), s,
               "LoRA down-projection");
   }
   // key-split partials of attention (normalised bf16 O + fp32 max, sum) and

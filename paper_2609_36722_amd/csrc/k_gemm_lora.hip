@@ -34,7 +34,8 @@ namespace {
 
 constexpr int BK = 64;
 constexpr int kChunksPerRow = BK / 8;  // 16-byte chunks per LDS row
-constexpr int kLoraSlice = 256;        // hidden elements per lora_down workgroup
+constexpr int kLoraSlice = 256;        // hidden elements per lora_down chunk (four waves x 64)
+constexpr int kLoraSliceWide = 1024;   // hidden elements per lora_down workgroup above kGemvMaxTok tokens
 constexpr int kLoraRows = 32;          // A rows staged per k-tile when the down-projection is fused
 constexpr int kGroupM = 4;             // token tiles per group of the tile order
 
@@ -561,13 +562,16 @@ __global__ __launch_bounds__(128 * WN * WM, 1) void gemm_kg2_kernel(const bf16_t
   else finish(std::integral_constant<int, 1>{});
 }
 
-// t = scale * x A^T with MFMAs, as fp32 partial sums per 256-wide slice of the
-// hidden dimension: workgroup (32-token block, slice), each wave multiplies a
-// 64-wide part of the slice and the four waves are summed through LDS.
-// t_part[slice][token][r_pad]; ranks rank .. r_pad-1 come out zero.
+// t = scale * x A^T with MFMAs, as fp32 partial sums per slice of the hidden
+// dimension (slice_w wide: 256 for the few-token GEMV, which has few token
+// blocks to spread, kLoraSliceWide otherwise, so that a GEMM epilogue sums
+// fewer partials): workgroup (32-token block, slice), each wave multiplies a
+// 64-wide part of every 256-wide chunk of the slice and the four waves are
+// summed through LDS.  t_part[slice][token][r_pad]; ranks rank .. r_pad-1
+// come out zero.
 __global__ __launch_bounds__(256) void lora_down_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ a,
                                                         int n_tok, int hidden, int rank, int r_pad, float scale,
-                                                        float* __restrict__ t_part) {
+                                                        int slice_w, float* __restrict__ t_part) {
   __shared__ float red[4][2][16][64];
   const int mb = blockIdx.x, kz = blockIdx.y;
   const int m0 = mb * 32;
@@ -577,25 +581,27 @@ __global__ __launch_bounds__(256) void lora_down_kernel(const bf16_t* __restrict
   const int m = min(m0 + l32, n_tok - 1);
   const bf16_t* xr = x + (int64_t)m * hidden;
 
-  u32x4 xa[4], ab[4][2];
-#pragma unroll
-  for (int st = 0; st < 4; ++st) {
-    const int k = kz * kLoraSlice + wave * 64 + st * 16 + 8 * hf;
-    const bool kin = k < hidden;
-    xa[st] = kin ? *reinterpret_cast<const u32x4*>(xr + k) : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int n = 32 * nb + l32;
-      ab[st][nb] = (kin && nb < nblk && n < rank) ? *reinterpret_cast<const u32x4*>(a + (int64_t)n * hidden + k)
-                                                 : u32x4{0u, 0u, 0u, 0u};
-    }
-  }
   f32x16 acc[2] = {f32x16{}, f32x16{}};
+  for (int c0 = kz * slice_w; c0 < min(hidden, (kz + 1) * slice_w); c0 += kLoraSlice) {
+    u32x4 xa[4], ab[4][2];
 #pragma unroll
-  for (int st = 0; st < 4; ++st)
+    for (int st = 0; st < 4; ++st) {
+      const int k = c0 + wave * 64 + st * 16 + 8 * hf;
+      const bool kin = k < hidden;
+      xa[st] = kin ? *reinterpret_cast<const u32x4*>(xr + k) : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-      if (nb < nblk) acc[nb] = mfma32(as_bf16x8(xa[st]), as_bf16x8(ab[st][nb]), acc[nb]);
+      for (int nb = 0; nb < 2; ++nb) {
+        const int n = 32 * nb + l32;
+        ab[st][nb] = (kin && nb < nblk && n < rank) ? *reinterpret_cast<const u32x4*>(a + (int64_t)n * hidden + k)
+                                                   : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        if (nb < nblk) acc[nb] = mfma32(as_bf16x8(xa[st]), as_bf16x8(ab[st][nb]), acc[nb]);
+  }
   // acc[nb][v] = C[token 8(v/4) + 4hf + v%4][rank 32nb + l32]
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb)
@@ -615,13 +621,19 @@ __global__ __launch_bounds__(256) void lora_down_kernel(const bf16_t* __restrict
 
 }  // namespace
 
-int lora_down_slices(int hidden) { return (hidden + kLoraSlice - 1) / kLoraSlice; }
+static int lora_slice_width(int n_tok) { return n_tok <= kGemvMaxTok ? kLoraSlice : kLoraSliceWide; }
+
+int lora_down_slices(int hidden, int n_tok) {
+  const int w = lora_slice_width(n_tok);
+  return (hidden + w - 1) / w;
+}
 
 hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int hidden, int rank, int r_pad,
                             float scale, float* t_part, hipStream_t stream) {
   if (n_tok == 0 || r_pad == 0) return hipSuccess;
-  ATTUNER_LAUNCH("lora_down_kernel", lora_down_kernel, dim3((n_tok + 31) / 32, lora_down_slices(hidden)), dim3(256),
-                 stream, x, a, n_tok, hidden, rank, r_pad, scale, t_part);
+  ATTUNER_LAUNCH("lora_down_kernel", lora_down_kernel,
+                 dim3((n_tok + 31) / 32, lora_down_slices(hidden, n_tok)), dim3(256), stream, x, a, n_tok, hidden,
+                 rank, r_pad, scale, lora_slice_width(n_tok), t_part);
   return hipGetLastError();
 }
 
@@ -761,7 +773,7 @@ hipError_t launch_gemm_any(const uint16_t* x, const uint16_t* w, int n_tok, int 
   if (n_tok == 0) return hipSuccess;
   if (n_tok <= kGemvMaxTok)
     return launch_gemv(x, w, n_tok, n_out, hidden, b, rank, r_pad, lora_cols, t_part, epi, out, stream);
-  const int n_slice = lora_down_slices(hidden);
+  const int n_slice = lora_down_slices(hidden, n_tok);
   const GemmPlan pl = plan ? *plan : plan_gemm(n_tok, n_out, hidden, r_pad > 0);
   if (pl.tile < 0) return hipErrorInvalidValue;
   const int tiles = ((n_tok + kTiles[pl.tile].bm - 1) / kTiles[pl.tile].bm) * (n_out / kTiles[pl.tile].bn);
@@ -780,6 +792,15 @@ hipError_t launch_gemm_any(const uint16_t* x, const uint16_t* w, int n_tok, int 
 }
 
 }  // namespace
+
+// The 256 x 256 tile's eight waves keep its MFMAs busy, so the redundant
+// down-projection (every feature tile of the adapted columns computes t for
+// its tokens) shows in full there: at 5368 tokens x 4096 -> 6144 (rank 16)
+// 268 us fused against 244 us for lora_down_kernel + the GEMM reading t.  The
+// other tiles hide it (1024 tokens, rank 32: 63.6 us fused, 67.4 separate).
+bool gemm_fuses_lora(int n_tok, int n_out, int hidden) {
+  return plan_gemm(n_tok, n_out, hidden, true).tile != 0;
+}
 
 hipError_t launch_gemm_lora(const uint16_t* x, const uint16_t* w, int n_tok, int n_out, int hidden,
                             const uint16_t* a, float scale, const uint16_t* b, int rank, int r_pad, int lora_cols,

@@ -315,7 +315,7 @@ hipError_t launch_gemv(const uint16_t* x, const uint16_t* w, int n_tok, int n_ou
   if (n_tok == 0) return hipSuccess;
   if (n_tok > kGemvMaxTok || n_out % 8 != 0 || k_dim % 8 != 0 || (r_pad > 0 && t_part == nullptr))
     return hipErrorInvalidValue;
-  const int n_slice = lora_down_slices(k_dim);
+  const int n_slice = lora_down_slices(k_dim, n_tok);
   if (n_tok >= kGemvMfmaMinTok && k_dim % 128 == 0 && n_out % 16 == 0) {
     ATTUNER_LAUNCH("gemv_mfma_kernel", (gemv_mfma_kernel<2, 8>), dim3((unsigned)(n_out / 16)), dim3(512), stream, x, w,
                    n_tok, n_out, k_dim, b, rank, r_pad, lora_cols, t_part, n_slice, epi, out);

@@ -51,10 +51,13 @@ hipError_t launch_gather(const int32_t* table_dev, int64_t n_entries, const uint
 
 // ---- a3: LoRA-down and the projection GEMM --------------------------------
 
-// t = scale * x a^T as fp32 partial sums over 256-wide slices of the hidden
-// dimension: t_part[lora_down_slices(hidden)][n_tok][r_pad]; ranks rank ..
-// r_pad-1 are zero.
-int lora_down_slices(int hidden);
+// t = scale * x a^T as fp32 partial sums over slices of the hidden
+// dimension: t_part[lora_down_slices(hidden, n_tok)][n_tok][r_pad]; ranks
+// rank .. r_pad-1 are zero.  The slice count never exceeds that of one token.
+int lora_down_slices(int hidden, int n_tok);
+// Whether the projection GEMM of this shape computes t itself (rank <=
+// kGemmFusedLoraMaxRank); otherwise launch_lora_down runs first.
+bool gemm_fuses_lora(int n_tok, int n_out, int hidden);
 hipError_t launch_lora_down(const uint16_t* x, const uint16_t* a, int n_tok, int hidden, int rank, int r_pad,
                             float scale, float* t_part, hipStream_t stream);
 
