@@ -99,6 +99,10 @@ def test_rms_norm_rows(H, n, rows):
     (300, 4096, 2560, "separate"),   # o_proj of the 4B stack (K = Hq d), ragged tokens
     (256, 9728, 2560, "inplace"),    # down_proj of the 4B stack, residual read and written in place
     (513, 12288, 4096, "inplace"),   # down_proj of the 8B stack
+    # products the tile plan gives to the two-k-group kernel (6144 outputs):
+    (450, 4096, 6144, "none"),       # 128 x 96 tile, ragged last token tile
+    (256, 4096, 6144, "separate"),   # 128 x 96 tile in 2 key splits (fp32 partials + reduce)
+    (96, 4096, 6144, "inplace"),     # 128 x 96 tile in 4 key splits, fewer tokens than a tile
 ])
 def test_linear_parity(T, K, N, res):
     _say(f"linear T={T} K={K} N={N} residual={res}")
@@ -119,7 +123,8 @@ def test_linear_parity(T, K, N, res):
     assert_intermediate_close(got, ref, "linear")
 
 
-@pytest.mark.parametrize("T,K,I", [(1, 2560, 9728), (100, 2560, 9728), (513, 4096, 12288), (64, 256, 32)])
+@pytest.mark.parametrize("T,K,I", [(1, 2560, 9728), (100, 2560, 9728), (513, 4096, 12288), (64, 256, 32),
+                                   (1000, 4096, 12288)])   # the last: two-k-group 128 x 192 tile, ragged
 def test_gate_up_swiglu_parity(T, K, I):
     _say(f"gate_up_swiglu T={T} K={K} I={I}")
     rng = np.random.default_rng(T + K + I)
