@@ -15,13 +15,17 @@
 // layer for a run of kGatherRun consecutive block-table entries: thread t
 // owns row t / 16 and 16-byte chunk t % 16 of the slab in each entry, so a
 // workgroup reads kGatherRun 4 KiB spans and writes them to one cache plane,
-// where consecutive entries' rows follow each other (one contiguous run of up
-// to 16 KiB).  Measured on gfx950 against one workgroup per page (all 16
-// slabs, i.e. 16 writes 9 MB apart at the 33k-row cache): 1.89 -> 1.57 ms for
-// the 9.66 GB of the 36-layer 32k-token cache (6.2 TB/s), 0.42 -> 0.38 ms for
-// 2.4 GB; runs of 8 entries (8 loads in flight per thread) are slower.
-// Loads and stores are streaming (non-temporal: every byte is touched once).
-// The store kernel keeps one workgroup per page.
+// where consecutive entries' rows follow each other.  Measured on gfx950 for
+// the 9.66 GB of the 36-layer 32k-token cache: one workgroup per page (all 16
+// slabs, 16 writes 9 MB apart) 1.89 ms, runs of 4 entries 1.52-1.55 ms (66
+// VGPRs), single entries 1.50 ms (8 VGPRs); runs of 8 are slower.  With 8
+// VGPRs the gather's waves also fit beside the attention kernel's (two waves
+// of 240 VGPRs per SIMD leave 32), so per-layer gathers on a second stream
+// hide better: 36-layer steps 22.22 -> 22.06 ms (32k cached tokens), 8.02 ->
+// 7.82 ms (17.7k), 3.32 -> 3.26 ms (8k) against runs of 4.  Loads and stores
+// are streaming (non-temporal: every byte is touched once).  The block-table
+// entries are wave-uniform and live in scalar registers.  The store kernel
+// keeps one workgroup per page.
 
 #include <algorithm>
 
@@ -68,7 +72,7 @@ __global__ __launch_bounds__(256) void store_pages_kernel(const u32x4* __restric
   }
 }
 
-constexpr int kGatherRun = 4;  // block-table entries per gather workgroup
+constexpr int kGatherRun = 1;  // block-table entries per gather workgroup
 
 __global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ table, int64_t n_entries,
                                                      const u32x4* __restrict__ dev_pool, int64_t dev_pages,
