@@ -178,10 +178,11 @@ def _gemm_case(M, H, N, rank, lora_cols, seed, b_std=0.01):
     (1024, 512, 512, 64, 512),     # 128-token tiles, maximum rank
     (130, 256, 256, 0, 0),         # no adapter (merged deployment form)
     # token counts at which the launcher picks each larger tile (tokens x features)
-    (1000, 512, 6144, 32, 4096),   # 256 x 96, ragged last token tile
-    (500, 512, 6144, 16, 4096),    # 128 x 96
+    (1000, 512, 6144, 32, 4096),   # two-k-group 128 x 192, ragged last token tile, LoRA-down fused
+    (500, 512, 6144, 16, 4096),    # two-k-group 128 x 96 (four waves)
+    (1024, 2560, 6144, 48, 4096),  # two-k-group 128 x 192 reading t (rank > 32: 3 hidden slices, the last partial)
     (2048, 256, 2560, 8, 2048),    # 128 x 256
-    (2100, 256, 6144, 16, 4096),   # 256 x 256, ragged
+    (2100, 256, 6144, 16, 4096),   # 256 x 256, ragged; t from the separate down-projection
     (1024, 256, 1280, 12, 1024),   # 128 x 128; rank 12 reads B element by element
 ])
 def test_qproj_lora_parity(M, H, N, rank, lora_cols):
