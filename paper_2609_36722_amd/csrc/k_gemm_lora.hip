@@ -1,25 +1,31 @@
 // K2: bf16 MFMA projection GEMM with the rank-r LoRA update fused into its
 // epilogue (query-side adaptation, section 4 eq. 4):
 //   out[i][n] = x[i] . w[n]  +  (n < lora_cols ? t[i] . b[n] : 0),
-//   t = scale * x A^T  (lora_down_kernel, run first).
+//   t = scale * x A^T  (computed by the GEMM's own k-loop for r <= 32, else
+//   by lora_down_kernel first).
 //
 // The GEMM is computed as C^T = W x^T so that the MFMA accumulator of a lane
 // holds four consecutive output features of one token (8-byte stores).  Both
 // operands are K-contiguous in memory ([rows][hidden]), so tiles go to LDS
 // without a transpose.  Workgroup tile BN (features) x BM (tokens) x 64 (k),
-// WN x WM waves, 32x32x16 MFMAs, fp32 accumulation.  At suffix sizes the
-// kernel is bound by how fast CUs ingest operand tiles (measured on gfx950:
-// ~35-60 GB/s per CU, ~9 TB/s over the chip, with or without the MFMAs), so
-// the tile shape is chosen to minimise ingested bytes, M N K 2 (1/BM + 1/BN),
-// while keeping every CU busy.  LDS rows are 128 bytes (eight 16-byte
+// 32x32x16 MFMAs, fp32 accumulation, the operand tiles copied global -> LDS
+// by the DMA form of the load.  Two kernels: gemm_lora_kernel (one wave per
+// wave tile) and gemm_kg2_kernel (96 x 64 wave tiles, two groups of waves on
+// alternate k-steps).  At suffix sizes the operand ingest per CU is the
+// ceiling (measured on gfx950: about 58 GB/s per CU, 15 TB/s out of the L2s,
+// the same rate hipBLASLt's kernels reach on these shapes), so the tile shape
+// is chosen to minimise ingested bytes, M N K 2 (1/BM + 1/BN), while keeping
+// every CU busy, and the copies are spread between the MFMAs so that the
+// compute hides under the ingest.  LDS rows are 128 bytes (eight 16-byte
 // chunks); chunk c of row r is stored at c ^ ((r >> 1) & 7), so the 16 rows
 // one operand read touches in a cycle land on 16 distinct bank groups.
 //
 // The LoRA term enters as extra MFMA k-steps after the main loop: A operand
 // = rows of B (rank padded to 16 with zeros), B operand = t rounded to a
 // bf16 hi/lo pair, so t keeps ~16 significant bits and the update is summed
-// in fp32.  lora_down_kernel leaves t as fp32 partial sums over 256-wide
-// slices of the hidden dimension; the epilogue adds the slices in order.
+// in fp32.  lora_down_kernel leaves t as fp32 partial sums over slices of
+// the hidden dimension (256 or 1024 wide); the epilogue adds the slices in
+// order.
 
 #include <type_traits>
 
