@@ -298,6 +298,7 @@ struct attuner_ctx {
   // request), reused while the shape repeats (every layer of a stack)
   std::vector<int32_t> split_shape;
   std::vector<int> split_plan;
+  std::vector<int> split_order;  // launch order of the requests' workgroups
   Staging staging;
   Tracer tracer;
 };
@@ -455,17 +456,21 @@ attuner_status run_norm_rope(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   return ATTUNER_OK;
 }
 
-// Key splits per request for one attention launch.  A workgroup serves one
-// 64-token query block of one KV head (one per CU at a time) over a range of
-// key tiles; workgroups start in launch order on whichever CU frees first.
-// The modelled finish time of a plan is that greedy schedule over 256 CUs,
-// with a workgroup costing its tiles plus kWgOverhead tiles (loading Q and
-// the first tile, the epilogue) and a plan with splits paying kMergeCost for
-// the merge launch.  Candidates cut the longest request into k = 1 .. 16
-// splits (split size tau = its tiles / k) and every request into
-// ceil(its tiles / tau); a candidate with more splits must be modelled 2%
-// faster to win.
-std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int64_t split_rows_max) {
+// Key splits per request for one attention launch, and the order in which
+// the requests' workgroups are launched.  A workgroup serves one 64-token
+// query block of one KV head (one per CU at a time) over a range of key
+// tiles; workgroups start in launch order on whichever CU frees first.  The
+// modelled finish time of a plan is that greedy schedule over 256 CUs, with
+// a workgroup costing its tiles plus kWgOverhead tiles (loading Q and the
+// first tile, the epilogue) and a plan with splits paying kMergeCost for the
+// merge launch.  Candidates cut the longest request into k = 1 .. 16 splits
+// (split size tau = its tiles / k) and every request into ceil(its tiles /
+// tau); each is modelled with the requests in their own order and in order
+// of decreasing workgroup length (longest first, which shortens the tail of
+// a batch of unequal contexts); a candidate with more splits must be
+// modelled 2% faster to win.  *order receives the launch order.
+std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int64_t split_rows_max,
+                                       std::vector<int>* order) {
   std::vector<int32_t> shape;
   shape.reserve(2 * reqs.size() + 1);
   shape.push_back((int32_t)split_rows_max);
@@ -473,7 +478,10 @@ std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc
     shape.push_back(r.q_len);
     shape.push_back(r.art_len);
   }
-  if (shape == c->split_shape) return c->split_plan;
+  if (shape == c->split_shape) {
+    if (order) *order = c->split_order;
+    return c->split_plan;
+  }
   constexpr double kWgOverhead = 4.0, kMergeCost = 3.0;
   constexpr int kCUs = 256;
   std::vector<int64_t> tiles(reqs.size(), 0);
@@ -486,6 +494,8 @@ std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc
   int64_t total_q = 0;
   for (const auto& r : reqs) total_q += std::max(0, r.q_len);
   std::vector<int> best(reqs.size(), 1), cand(reqs.size(), 1);
+  std::vector<int> best_order(reqs.size()), in_order(reqs.size()), longest_first(reqs.size());
+  for (size_t r = 0; r < reqs.size(); ++r) best_order[r] = in_order[r] = (int)r;
   double best_t = -1.0;
   int64_t prev_tau = -1;
   for (int k = 1; k <= kMaxAttnSplit && longest > 0; ++k) {
@@ -501,35 +511,45 @@ std::vector<int> plan_attention_splits(attuner_ctx* c, const std::vector<ReqDesc
     }
     // the partials hold max_ns x total_q rows; plans past the cap are skipped
     if (any_split && (int64_t)max_ns * total_q > split_rows_max) continue;
-    std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
-    for (int i = 0; i < kCUs; ++i) free_at.push(0.0);
-    double finish = 0.0;
-    for (size_t r = 0; r < reqs.size(); ++r) {
-      const int nq = (reqs[r].q_len + 63) / 64;
-      const int ns = cand[r];
-      for (int u = 0; u < nq * ns; ++u) {
-        const int split = u % ns, qb = nq - 1 - u / ns;
-        const int64_t t0 = 64LL * qb;
-        const int64_t n_t = ((int64_t)reqs[r].art_len + t0 + std::min<int64_t>(64, reqs[r].q_len - t0) + 63) / 64;
-        const int64_t per = (n_t + ns - 1) / ns;
-        const int64_t tb = std::min<int64_t>(n_t, split * per), te = std::min<int64_t>(n_t, tb + per);
-        const double dur = (double)(te - tb) + kWgOverhead;
-        for (int g = 0; g < c->cfg.n_kv_heads; ++g) {
-          const double t = free_at.top() + dur;
-          free_at.pop();
-          free_at.push(t);
-          finish = std::max(finish, t);
+    // longest workgroups first (ties: request order)
+    longest_first = in_order;
+    std::stable_sort(longest_first.begin(), longest_first.end(), [&](int a, int b) {
+      return tiles[a] * cand[b] > tiles[b] * cand[a];  // tiles / splits, compared without division
+    });
+    for (const std::vector<int>* ord : {&in_order, &longest_first}) {
+      std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+      for (int i = 0; i < kCUs; ++i) free_at.push(0.0);
+      double finish = 0.0;
+      for (int r : *ord) {
+        const int nq = (reqs[r].q_len + 63) / 64;
+        const int ns = cand[r];
+        for (int u = 0; u < nq * ns; ++u) {
+          const int split = u % ns, qb = nq - 1 - u / ns;
+          const int64_t t0 = 64LL * qb;
+          const int64_t n_t = ((int64_t)reqs[r].art_len + t0 + std::min<int64_t>(64, reqs[r].q_len - t0) + 63) / 64;
+          const int64_t per = (n_t + ns - 1) / ns;
+          const int64_t tb = std::min<int64_t>(n_t, split * per), te = std::min<int64_t>(n_t, tb + per);
+          const double dur = (double)(te - tb) + kWgOverhead;
+          for (int g = 0; g < c->cfg.n_kv_heads; ++g) {
+            const double t = free_at.top() + dur;
+            free_at.pop();
+            free_at.push(t);
+            finish = std::max(finish, t);
+          }
         }
       }
-    }
-    if (any_split) finish += kMergeCost;
-    if (best_t < 0.0 || finish < 0.98 * best_t) {
-      best_t = finish;
-      best = cand;
+      if (any_split) finish += kMergeCost;
+      if (best_t < 0.0 || finish < 0.98 * best_t) {
+        best_t = finish;
+        best = cand;
+        best_order = *ord;
+      }
     }
   }
   c->split_shape = shape;
   c->split_plan = best;
+  c->split_order = best_order;
+  if (order) *order = best_order;
   return best;
 }
 
@@ -562,22 +582,26 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
 
   const int64_t rows_max =
       part_buf ? std::min<int64_t>(kAttnSplitRowsMax, (int64_t)(part_bytes / split_row_bytes(c))) : kAttnSplitRowsMax;
-  const std::vector<int> ns_plan = plan_attention_splits(c, reqs, rows_max);
+  std::vector<int> order;
+  const std::vector<int> ns_plan = plan_attention_splits(c, reqs, rows_max, &order);
   int n_split = 1;
   int32_t units = 0;
-  for (size_t r = 0; r < reqs.size(); ++r) {
+  // table entry i is request order[i]: the kernel needs only each entry's
+  // workgroups to be contiguous, and every entry carries its own rows
+  for (size_t i = 0; i < order.size(); ++i) {
+    const int r = order[i];
     const int nq = (reqs[r].q_len + 63) / 64;
     const int ns = ns_plan[r];
     n_split = std::max(n_split, ns);
-    p.req[r].q_start = reqs[r].q_start;
-    p.req[r].q_len = reqs[r].q_len;
-    p.req[r].kv_start = reqs[r].kv_start;
-    p.req[r].art_len = reqs[r].art_len;
-    p.req[r].n_qblk = nq;
-    p.req[r].wg_start = units;
-    p.req[r].n_split = ns;
-    p.req[r].span0 = reqs[r].span0;
-    p.req[r].n_span = reqs[r].n_span;
+    p.req[i].q_start = reqs[r].q_start;
+    p.req[i].q_len = reqs[r].q_len;
+    p.req[i].kv_start = reqs[r].kv_start;
+    p.req[i].art_len = reqs[r].art_len;
+    p.req[i].n_qblk = nq;
+    p.req[i].wg_start = units;
+    p.req[i].n_split = ns;
+    p.req[i].span0 = reqs[r].span0;
+    p.req[i].n_span = reqs[r].n_span;
     units += nq * ns;
   }
   if (spans)
