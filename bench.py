@@ -481,7 +481,7 @@ def main():
             main.wait_stream(side)
 
     # The staged route runs eagerly: the runtime performs a host-to-device
-    # hipMemcpyAsync from the pinned pool as a copy kernel, and in a replayed
+    # hipMemcpyAsync from the pinned pool on a DMA engine, and in a replayed
     # graph those copy nodes did not overlap the layer loop's kernels
     # (measured at 36 layers, 8B shapes, 32 x 1024 artifact tokens: 104.3 ms
     # per step replayed against 89.6 ms eager).

@@ -264,7 +264,8 @@ attuner_status attuner_gather_layers(attuner_ctx* ctx, const int32_t* block_tabl
  * attuner_stage_layers copies layers layer_begin .. layer_begin + n_layers - 1
  * of those host pages into the staging pool with hipMemcpyAsync on `stream`
  * (from the pinned host pool: one copy per run and layer; the HIP runtime
- * chooses the engine, and for these copies it runs its own copy kernel).  attuner_gather_layers over the staged table then moves the staged
+ * chooses the engine; for these copies it uses the DMA engines, so they
+ * occupy no compute units).  attuner_gather_layers over the staged table then moves the staged
  * pages of a layer into the request cache like any HBM page; the caller
  * orders each layer's gather after that layer's staging copy (same stream,
  * or an event).  The call is the last staged assembly's: once another
