@@ -17,8 +17,14 @@
 //                accumulator of a lane holds 32 keys of ONE token and the row
 //                max / row sum are in-lane plus one exchange with lane ^ 32;
 //   online softmax in the log2 domain: p = 2^(s * log2(e)/sqrt(d) - m) as one
-//                FMA and one v_exp_f32; the reference max m only moves when a
-//                tile exceeds it by 2^8, so the O rescale is rare;
+//                FMA and one v_exp_f32.  Only a range's first tile and the
+//                masked diagonal tiles take a row max; the other tiles use
+//                the current reference m and are redone with the exact max
+//                only when their p sum grows past a bound, so neither the
+//                max nor the O rescale costs anything in the common case.
+//                Each lane sums p over its own 32 keys of a tile into its
+//                partial l; the two lanes of a token combine their partials
+//                once at the end;
 //   O^T += V^T P^T  (MFMA A = V^T, B = P^T straight from the S^T accumulator
 //                converted to bf16 in registers).
 // The loop is software-pipelined inside each wave: QK of tile i is issued
@@ -57,6 +63,8 @@ constexpr int NSTAGE = 4;    // K/V tiles in LDS: i - 1 (its PV), i (its QK), i 
 constexpr int D = kHeadDim;
 constexpr int CH = D / 8;    // 16-byte chunks per K/V row
 constexpr int NTHREADS = 512;
+constexpr float kLazyMax = 8.0f;   // masked tiles: m moves only past this margin (log2 units)
+constexpr float kSumLim = 4096.f;  // unmasked tiles: a lane's tile sum above this redoes the tile
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -144,10 +152,12 @@ __device__ __forceinline__ void mask_tile(f32x16 (&s)[2], int kv0, int vis_lim, 
 }
 
 // Row max, lazy reference update (the reference m only moves when the tile
-// max exceeds it by more than 8 in log2 units: l and O accumulate against the
-// same reference, so the result is unchanged and p <= 2^8), l *= alpha, and
-// the scores turned into exponents s * log2(e)/sqrt(d) - m.  Returns alpha.
-__device__ __forceinline__ float max_tile(f32x16 (&s)[2], float sc, float& m_i, float& l_i) {
+// max exceeds it by more than `lazy` in log2 units: l and O accumulate against
+// the same reference, so the result is unchanged), l *= alpha, and the scores
+// turned into exponents s * log2(e)/sqrt(d) - m.  Returns alpha.  l is the
+// lane's own partial sum; lanes l32 and l32 + 32 hold the same token and get
+// the same m (the max is exchanged), so one alpha serves both partials.
+__device__ __forceinline__ float max_tile(f32x16 (&s)[2], float sc, float& m_i, float& l_i, float lazy) {
   float mx = -INFINITY;
 #pragma unroll
   for (int kh = 0; kh < 2; ++kh)
@@ -155,7 +165,7 @@ __device__ __forceinline__ float max_tile(f32x16 (&s)[2], float sc, float& m_i, 
     for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kh][v]);
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
   const float m_tile = mx * sc;
-  const float m_new = m_tile > m_i + 8.0f ? m_tile : m_i;
+  const float m_new = m_tile > m_i + lazy ? m_tile : m_i;
   const float m_use = m_new == -INFINITY ? 0.f : m_new;
   const float alpha = __builtin_amdgcn_exp2f(m_i - m_use);
   l_i *= alpha;
@@ -167,8 +177,17 @@ __device__ __forceinline__ float max_tile(f32x16 (&s)[2], float sc, float& m_i, 
   return alpha;
 }
 
-// p = 2^(exponent), l += row sum, and the bf16 P^T operand (16-key groups j).
-__device__ __forceinline__ void exp_tile(f32x16 (&s)[2], float& l_i, bf16x8 (&pk)[4]) {
+// Exponents of a tile against the current reference m (finite), no max.
+__device__ __forceinline__ void shift_tile(f32x16 (&s)[2], float sc, float m_i) {
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s[kh][v] = fmaf(s[kh][v], sc, -m_i);
+}
+
+// p = 2^(exponent) and the bf16 P^T operand (16-key groups j).  Returns the
+// lane's sum of p over its 32 keys.
+__device__ __forceinline__ float exp_tile(f32x16 (&s)[2], bf16x8 (&pk)[4]) {
   float rs = 0.f;
 #pragma unroll
   for (int kh = 0; kh < 2; ++kh)
@@ -177,7 +196,6 @@ __device__ __forceinline__ void exp_tile(f32x16 (&s)[2], float& l_i, bf16x8 (&pk
       s[kh][v] = __builtin_amdgcn_exp2f(s[kh][v]);
       rs += s[kh][v];
     }
-  l_i += rs + __shfl_xor(rs, 32, 64);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     u32x4 w;
@@ -186,6 +204,7 @@ __device__ __forceinline__ void exp_tile(f32x16 (&s)[2], float& l_i, bf16x8 (&pk
       w[e] = pack_bf16x2(s[j >> 1][(j & 1) * 8 + 2 * e], s[j >> 1][(j & 1) * 8 + 2 * e + 1]);
     pk[j] = as_bf16x8(w);
   }
+  return rs;
 }
 
 // O^T += V^T P^T.  The S^T accumulator hands a lane the keys of each 16-key
@@ -328,47 +347,69 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
 
   // Unmasked tiles, software-pipelined inside the wave: QK of `tile` is
   // issued alongside the exponentials of tile - 1, and PV of tile - 1
-  // alongside the row max of `tile`.  S^T alternates between sa and sb.
-  if (tb < tp) {
-    f32x16 sa[2], sb[2];
-    bf16x8 pk[4];
-    tile_sync(tb);
-    qk_tile(kst(tb), qf, l32, hf, sa);
-    max_tile(sa, sc, m_i, l_i);
-    auto step = [&](f32x16 (&sn)[2], f32x16 (&so)[2], int tile) __attribute__((always_inline)) {
-      tile_sync(tile);
-      qk_tile(kst(tile), qf, l32, hf, sn);
-      exp_tile(so, l_i, pk);
-      pv_tile(vst(tile - 1), pk, hf, vrow, vcol, acc);
-      const float alpha = max_tile(sn, sc, m_i, l_i);
-      rescale(acc, alpha);  // after PV(tile - 1), before PV(tile)
-    };
-    int tile = tb + 1;
-    for (; tile + 1 < tp; tile += 2) {
-      step(sb, sa, tile);
-      step(sa, sb, tile + 1);
+  // alongside the exponents of `tile`.  S^T alternates between sa and sb.
+  // Only the first tile takes a row max: later tiles' exponents are taken
+  // against the current reference m.  A lane whose sum over a tile exceeds
+  // kSumLim (some p large, or an overflow) marks itself; if any lane of the
+  // workgroup did, the whole range is run again with a row max per tile (the
+  // second pass below), so every p kept is at most kSumLim.
+  bool bad = false;
+  for (bool redo = false;; redo = true) {
+    if (!redo && tb < tp) {
+      f32x16 sa[2], sb[2];
+      bf16x8 pk[4];
+      tile_sync(tb);
+      qk_tile(kst(tb), qf, l32, hf, sa);
+      max_tile(sa, sc, m_i, l_i, kLazyMax);
+      auto finish = [&](f32x16 (&so)[2]) __attribute__((always_inline)) {
+        const float rs = exp_tile(so, pk);
+        bad = bad || !(rs <= kSumLim);
+        l_i += rs;
+      };
+      auto step = [&](f32x16 (&sn)[2], f32x16 (&so)[2], int tile) __attribute__((always_inline)) {
+        tile_sync(tile);
+        qk_tile(kst(tile), qf, l32, hf, sn);
+        finish(so);
+        pv_tile(vst(tile - 1), pk, hf, vrow, vcol, acc);
+        shift_tile(sn, sc, m_i);
+      };
+      int tile = tb + 1;
+      for (; tile + 1 < tp; tile += 2) {
+        step(sb, sa, tile);
+        step(sa, sb, tile + 1);
+      }
+      if (tile < tp) {
+        step(sb, sa, tile);
+        finish(sb);
+      } else {
+        finish(sa);
+      }
+      pv_tile(vst(tp - 1), pk, hf, vrow, vcol, acc);
     }
-    if (tile < tp) {
-      step(sb, sa, tile);
-      exp_tile(sb, l_i, pk);
-    } else {
-      exp_tile(sa, l_i, pk);
-    }
-    pv_tile(vst(tp - 1), pk, hf, vrow, vcol, acc);
-  }
 
-  // tiles reaching the diagonal: plain masked steps
-  for (int tile = tp; tile < te; ++tile) {
-    f32x16 s[2];
-    bf16x8 pk[4];
-    tile_sync(tile);
-    const int kv0 = tile * BKV;
-    qk_tile(kst(tile), qf, l32, hf, s);
-    if (kv0 + BKV - 1 > mask_from) mask_tile(s, kv0, vis_lim, hf);
-    rescale(acc, max_tile(s, sc, m_i, l_i));
-    exp_tile(s, l_i, pk);
-    pv_tile(vst(tile), pk, hf, vrow, vcol, acc);
+    // tiles reaching the diagonal (all tiles in the second pass): one row max
+    // per tile, plain steps
+    for (int tile = redo ? tb : tp; tile < te; ++tile) {
+      f32x16 s[2];
+      bf16x8 pk[4];
+      tile_sync(tile);
+      const int kv0 = tile * BKV;
+      qk_tile(kst(tile), qf, l32, hf, s);
+      if (kv0 + BKV - 1 > mask_from) mask_tile(s, kv0, vis_lim, hf);
+      rescale(acc, max_tile(s, sc, m_i, l_i, kLazyMax));
+      l_i += exp_tile(s, pk);
+      pv_tile(vst(tile), pk, hf, vrow, vcol, acc);
+    }
+    // every wave has left the ring when this returns
+    if (redo || !__syncthreads_or(bad)) break;
+    m_i = -INFINITY;
+    l_i = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = f32x16{};
+    if (tb < te) dma_tile(kb, vb, tb * BKV, kv_len, k_base, v_base, dl, wave);
+    if (tb + 1 < te) dma_tile(kb, vb, (tb + 1) * BKV, kv_len, k_base + kStage, v_base + kStage, dl, wave);
   }
+  l_i += __shfl_xor(l_i, 32, 64);  // the two lanes of a token hold its two partial sums
 
   // ---- epilogue: O / l (the output, or with n_split > 1 this split's
   // normalised partial) goes through LDS, so that each store below is 16

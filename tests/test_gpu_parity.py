@@ -306,6 +306,51 @@ def test_attention_parity(reqs):
         assert np.abs(got_lse[cu_q[r]:cu_q[r + 1]] - ref_lse).max() <= 1e-3 * max(1.0, np.abs(ref_lse).max())
 
 
+@pytest.mark.parametrize("kind", ["rising", "spike"])
+def test_attention_scores_outrun_first_tile(kind):
+    # Scores that grow along the keys ("rising": by about 40 log2 units over
+    # the artifact) or one key far above the rest ("spike": about 260 log2
+    # units, past the fp32 range of 2^(s - m) for the first tile's m): the
+    # exponentials of later tiles against the first tile's reference would
+    # exceed any fixed bound, so the result rests on the kernel's redo with a
+    # row max per tile.
+    _say(f"attention scores outrunning the first tile: {kind}")
+    rng = np.random.default_rng(23 if kind == "rising" else 29)
+    n_q, n_kv, d = 32, 8, 128
+    reqs = [(2048, 64), (4096, 100), (300, 20)]
+    cu_q, cu_ctx, art_len = [0], [0], []
+    for L, S in reqs:
+        cu_q.append(cu_q[-1] + S)
+        cu_ctx.append(cu_ctx[-1] + L + S)
+        art_len.append(L)
+    T, rows = cu_q[-1], cu_ctx[-1]
+    q = rng.standard_normal((T, n_q, d)).astype(np.float32) * 0.5 + 1.0
+    kc = rng.standard_normal((n_kv, rows, d)).astype(np.float32)
+    for r, (L, S) in enumerate(reqs):
+        pos = np.arange(L + S)
+        if kind == "rising":   # mean score grows by ~ 40 log2 units over the artifact
+            kc[:, cu_ctx[r]:cu_ctx[r] + L + S, :] += (3.0 * pos / max(L, 1))[None, :, None]
+        else:                  # one artifact key far above all others
+            kc[:, cu_ctx[r] + (2 * L) // 3, :] = 16.0
+    vc = rng.standard_normal((n_kv, rows, d)).astype(np.float32)
+    q = sd.f32_to_bf16_bits(q)
+    cache = sd.f32_to_bf16_bits(np.stack([kc, vc])[None])
+    with Context(ModelCfg(n_layers=1, hidden=256), pool_pages=0) as ctx:
+        o = torch.empty(T, n_q, d, dtype=torch.bfloat16, device="cuda")
+        lse = torch.empty(T, n_q, dtype=torch.float32, device="cuda")
+        ctx.attention(0, cu_q, cu_ctx, art_len, dev_bf16(q), dev_bf16(cache), rows, o, lse)
+        torch.cuda.synchronize()
+        got, got_lse = host_f64(o), lse.cpu().numpy()
+    assert np.isfinite(got).all() and np.isfinite(got_lse).all()
+    qf, cf = oracle.decode_bf16(q), oracle.decode_bf16(cache)
+    for r, (L, S) in enumerate(reqs):
+        kk = cf[0, 0, :, cu_ctx[r]:cu_ctx[r] + L + S].transpose(1, 0, 2)
+        vv = cf[0, 1, :, cu_ctx[r]:cu_ctx[r] + L + S].transpose(1, 0, 2)
+        ref, ref_lse = oracle.attention(qf[cu_q[r]:cu_q[r + 1]], kk, vv, L, return_lse=True)
+        assert_o_close(got[cu_q[r]:cu_q[r + 1]], ref, f"O request {r}")
+        assert np.abs(got_lse[cu_q[r]:cu_q[r + 1]] - ref_lse).max() <= 1e-3 * max(1.0, np.abs(ref_lse).max())
+
+
 def test_attention_never_reads_future_suffix_rows():
     # a huge value planted at suffix row j must not move any row i < j
     _say("attention future-row probe")
