@@ -63,8 +63,8 @@ constexpr int NSTAGE = 4;    // K/V tiles in LDS: i - 1 (its PV), i (its QK), i 
 constexpr int D = kHeadDim;
 constexpr int CH = D / 8;    // 16-byte chunks per K/V row
 constexpr int NTHREADS = 512;
-constexpr float kLazyMax = 8.0f;   // masked tiles: m moves only past this margin (log2 units)
-constexpr float kSumLim = 4096.f;  // unmasked tiles: a lane's tile sum above this redoes the tile
+constexpr float kLazyMax = 8.0f;   // tiles that take a row max: m moves only past this margin (log2 units)
+constexpr float kSumLim = 4096.f;  // unmasked tiles: a lane's tile sum above this sends the workgroup through a second pass
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
