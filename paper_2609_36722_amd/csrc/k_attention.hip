@@ -19,9 +19,10 @@
 //   online softmax in the log2 domain: p = 2^(s * log2(e)/sqrt(d) - m) as one
 //                FMA and one v_exp_f32.  Only a range's first tile and the
 //                masked diagonal tiles take a row max; the other tiles use
-//                the current reference m and are redone with the exact max
-//                only when their p sum grows past a bound, so neither the
-//                max nor the O rescale costs anything in the common case.
+//                the current reference m, and only if some tile's p sum
+//                passes a bound does the workgroup run its key range again
+//                with a row max per tile, so neither the max nor the O
+//                rescale costs anything in the common case.
 //                Each lane sums p over its own 32 keys of a tile into its
 //                partial l; the two lanes of a token combine their partials
 //                once at the end;
