@@ -114,6 +114,22 @@ def test_decode_ragged_batch():
         assert_o_close_per_request(got[r], ref[r], f"request {r}")
 
 
+@pytest.mark.parametrize("seed", [201, 202, 203])
+def test_decode_random_batches(seed):
+    # Seeded random batches (1-32 requests over a pool of 12 artifacts of
+    # 1-2500 tokens, 0-6 artifacts each with repeats, 0-400 prior rows): the
+    # chunk size, the chunk count per request and the merge launch vary.
+    rng = np.random.default_rng(seed)
+    arts = [int(rng.integers(1, 2501)) for _ in range(12)]
+    n = int(rng.integers(1, 33))
+    reqs = [(tuple(int(a) for a in rng.integers(0, 12, int(rng.integers(0, 7)))), int(rng.integers(0, 401)))
+            for _ in range(n)]
+    _say(f"decode random batch seed {seed}: {n} requests")
+    got, ref = _run_decode(seed, arts, reqs)
+    for r in range(got.shape[0]):
+        assert_o_close_per_request(got[r], ref[r], f"request {r}")
+
+
 def test_decode_single_key_is_value():
     _say("decode single key")
     got, ref = _run_decode(42, [16], [((), 0)], gamma="ones")

@@ -306,6 +306,45 @@ def test_attention_parity(reqs):
         assert np.abs(got_lse[cu_q[r]:cu_q[r + 1]] - ref_lse).max() <= 1e-3 * max(1.0, np.abs(ref_lse).max())
 
 
+@pytest.mark.parametrize("seed", [101, 102, 103, 104])
+def test_attention_random_batches(seed):
+    # Seeded random batches (1-24 requests, 0-3000 cached keys, 0-300 suffix
+    # rows): the key-split plan and the launch order (request order or
+    # longest first, whichever the host's model prefers) vary from batch to
+    # batch; every request's rows against the oracle.
+    rng = np.random.default_rng(seed)
+    n_req = int(rng.integers(1, 25))
+    reqs = [(int(rng.integers(0, 3001)), int(rng.integers(0, 301))) for _ in range(n_req)]
+    if all(S == 0 for _, S in reqs):
+        reqs[0] = (reqs[0][0], 17)
+    _say(f"attention random batch seed {seed}: {reqs}")
+    n_q, n_kv, d = 32, 8, 128
+    cu_q, cu_ctx, art_len = [0], [0], []
+    for L, S in reqs:
+        cu_q.append(cu_q[-1] + S)
+        cu_ctx.append(cu_ctx[-1] + L + S + int(rng.integers(0, 5)))   # a few spare rows, varying
+        art_len.append(L)
+    T, rows = cu_q[-1], cu_ctx[-1]
+    f = lambda *s: sd.f32_to_bf16_bits(rng.standard_normal(s).astype(np.float32))
+    q = f(T, n_q, d)
+    cache = f(1, 2, n_kv, rows, d)
+    with Context(ModelCfg(n_layers=1, hidden=256), pool_pages=0) as ctx:
+        o = torch.empty(T, n_q, d, dtype=torch.bfloat16, device="cuda")
+        lse = torch.empty(T, n_q, dtype=torch.float32, device="cuda")
+        ctx.attention(0, cu_q, cu_ctx, art_len, dev_bf16(q), dev_bf16(cache), rows, o, lse)
+        torch.cuda.synchronize()
+        got, got_lse = host_f64(o), lse.cpu().numpy()
+    qf, cf = oracle.decode_bf16(q), oracle.decode_bf16(cache)
+    for r, (L, S) in enumerate(reqs):
+        if S == 0:
+            continue
+        kk = cf[0, 0, :, cu_ctx[r]:cu_ctx[r] + L + S].transpose(1, 0, 2)
+        vv = cf[0, 1, :, cu_ctx[r]:cu_ctx[r] + L + S].transpose(1, 0, 2)
+        ref, ref_lse = oracle.attention(qf[cu_q[r]:cu_q[r + 1]], kk, vv, L, return_lse=True)
+        assert_o_close(got[cu_q[r]:cu_q[r + 1]], ref, f"O request {r}")
+        assert np.abs(got_lse[cu_q[r]:cu_q[r + 1]] - ref_lse).max() <= 1e-3 * max(1.0, np.abs(ref_lse).max())
+
+
 @pytest.mark.parametrize("kind", ["rising", "spike"])
 def test_attention_scores_outrun_first_tile(kind):
     # Scores that grow along the keys ("rising": by about 40 log2 units over
