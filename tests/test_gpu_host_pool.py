@@ -228,6 +228,80 @@ def test_staged_assembly_bit_exact():
         assert ctx.stage_pool_info()[1] == 0
 
 
+@pytest.mark.parametrize("seed", [91, 92])
+def test_random_store_release_assemble_bit_exact(seed):
+    # A seeded sequence of stores (1-200 tokens, into HBM or pinned host
+    # pages) and releases fragments both pools; every few operations a random
+    # batch (repeats allowed) is assembled three ways: all layers at once
+    # (host pages read over the link), layer by layer from the same table,
+    # and staged through HBM by bulk copies.  Block tables and caches must
+    # equal the oracle's, bit for bit.
+    rng = np.random.default_rng(seed)
+    n_layers = 2
+    _say(f"random store/release/assemble, seed {seed}")
+    with Context(ModelCfg(n_layers=n_layers, hidden=256), pool_pages=48) as ctx:
+        ctx.host_pool_create(48)
+        ctx.stage_pool_create(48)
+        live = {}   # artifact id -> (length, k, v) in the oracle's [layers][L][Hkv][d] layout
+        checks = 0
+        for op in range(40):
+            if live and (rng.random() < 0.3 or op % 9 == 8):
+                victim = int(rng.choice(sorted(live)))
+                ctx.release_artifact(victim)
+                del live[victim]
+            else:
+                L = int(rng.integers(1, 201))
+                k = rng.integers(0, 2 ** 16, size=(n_layers, 8, L, 128), dtype=np.uint16)
+                v = rng.integers(0, 2 ** 16, size=(n_layers, 8, L, 128), dtype=np.uint16)
+                store = ctx.store_artifact_host if rng.random() < 0.5 else ctx.store_artifact
+                try:
+                    aid = store(dev_bf16(k), dev_bf16(v))
+                except AttunerError as e:
+                    assert e.status == -2   # that pool is full: ENOMEM, nothing stored
+                    continue
+                live[aid] = (L, k.transpose(0, 2, 1, 3), v.transpose(0, 2, 1, 3))
+            if op % 5 != 4 or not live:
+                continue
+            order = sorted(live)
+            reqs = [([int(a) for a in rng.choice(order, int(rng.integers(0, 5)))], int(rng.integers(0, 21)))
+                    for _ in range(int(rng.integers(1, 6)))]
+            requests, caps = [r for r, _ in reqs], [c for _, c in reqs]
+            lengths = {a: live[a][0] for a in order}
+            # the oracle indexes artifacts 0..n-1: map ids to positions
+            pos = {a: i for i, a in enumerate(order)}
+            oreqs = [([pos[a] for a in r], c) for r, c in reqs]
+            olen = [lengths[a] for a in order]
+            art_k = {pos[a]: live[a][1] for a in order}
+            art_v = {pos[a]: live[a][2] for a in order}
+            entries, cu_o = oracle.block_table(olen, oreqs, 16)
+            cache, _ = oracle.assemble(art_k, art_v, oreqs, 8, 128)
+            phys = {pos[a]: ctx.artifact_pages(a)[0] for a in order}
+            want = np.array([[phys[a][p], nv, dst, r] for a, p, nv, r, dst in entries.tolist()],
+                            np.int32).reshape(-1, 4)
+            ne, rows = ctx.assemble_plan(requests, caps)
+            bt = torch.zeros(max(1, ne) * 4, dtype=torch.int32, device="cuda")
+            kv = torch.zeros(n_layers * 2 * 8 * rows * 128, dtype=torch.bfloat16, device="cuda")
+            cu, al = ctx.assemble_kv(requests, caps, bt, kv, rows)
+            torch.cuda.synchronize()
+            assert list(cu) == list(cu_o)
+            assert np.array_equal(bt.cpu().numpy().reshape(-1, 4)[:ne], want), f"op {op}: block table"
+            _check_cache(kv, cache, cu, al, n_layers, rows, f"op {op}, all layers")
+            kv.zero_()
+            ctx.assemble_table(requests, caps, bt, rows)
+            for l in rng.permutation(n_layers):
+                ctx.gather_layers(bt, ne, int(l), 1, kv, rows)
+            torch.cuda.synchronize()
+            _check_cache(kv, cache, cu, al, n_layers, rows, f"op {op}, per layer")
+            kv.zero_()
+            ctx.assemble_table_staged(requests, caps, bt, rows)
+            ctx.stage_layers(0, n_layers)
+            ctx.gather_layers(bt, ne, 0, n_layers, kv, rows)
+            torch.cuda.synchronize()
+            _check_cache(kv, cache, cu, al, n_layers, rows, f"op {op}, staged")
+            checks += 1
+        assert checks >= 5
+
+
 def test_staged_assembly_capacity():
     _say("staged assembly: staging pool too small")
     rng = np.random.default_rng(84)
