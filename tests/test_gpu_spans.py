@@ -36,11 +36,32 @@ def _bits(rng, shape, std=1.0):
 @pytest.mark.parametrize("H,rank,layer", [(512, 16, 1), (2560, 8, 0)])
 def test_interleaved_spans(H, rank, layer):
     _say(f"interleaved spans H={H} r={rank} layer={layer}")
-    rng = np.random.default_rng(70 + H + rank)
-    n_layers = 2
-    lengths = [40, 17, 64, 1, 300]
     # prompts in order: artifacts by index, online spans as -n
-    prompts = [[-7, 0, -3, 1, -20], [2, -5], [-9], [3, 3, -1, 0], [4, -64, 2, -70]]
+    _run_interleaved(H, rank, layer, [40, 17, 64, 1, 300],
+                     [[-7, 0, -3, 1, -20], [2, -5], [-9], [3, 3, -1, 0], [4, -64, 2, -70]], 70 + H + rank)
+
+
+@pytest.mark.parametrize("seed", [301, 302, 303])
+def test_interleaved_random_prompts(seed):
+    # Seeded random prompts: 1-6 prompts of 1-7 segments each, artifacts of
+    # 1-400 tokens (repeats allowed) between online spans of 1-80 tokens,
+    # every prompt with at least one online span.
+    rng = np.random.default_rng(seed)
+    lengths = [int(rng.integers(1, 401)) for _ in range(int(rng.integers(1, 7)))]
+    prompts = []
+    for _ in range(int(rng.integers(1, 7))):
+        segs = [int(rng.integers(0, len(lengths))) if rng.random() < 0.5 else -int(rng.integers(1, 81))
+                for _ in range(int(rng.integers(1, 8)))]
+        if all(x >= 0 for x in segs):
+            segs.insert(int(rng.integers(0, len(segs) + 1)), -int(rng.integers(1, 81)))
+        prompts.append(segs)
+    _say(f"interleaved random prompts seed {seed}: lengths {lengths}, prompts {prompts}")
+    _run_interleaved(512, 16, int(rng.integers(0, 2)), lengths, prompts, seed)
+
+
+def _run_interleaved(H, rank, layer, lengths, prompts, seed):
+    rng = np.random.default_rng(seed)
+    n_layers = 2
     scale = 16.0 / rank
     with Context(ModelCfg(n_layers=n_layers, hidden=H), pool_pages=sum(math.ceil(L / 16) for L in lengths)) as ctx:
         art_k, art_v, ids = {}, {}, {}
