@@ -200,6 +200,34 @@ def test_qproj_lora_parity(M, H, N, rank, lora_cols):
     assert_intermediate_close(got, ref, "q/k/v projection")
 
 
+@pytest.mark.parametrize("seed", [401, 402, 403, 404, 405, 406])
+def test_qproj_lora_random_shapes(seed):
+    # Seeded random shapes (tokens 1-16 or 17-1600, hidden a multiple of 64,
+    # outputs a multiple of 128,
+    # rank 0-64, adapted columns a multiple of 32): the launcher's tile,
+    # the fused or separate down-projection and the few-token GEMV paths
+    # vary with the shape.  B ~ N(0, 1) so that the low-rank term is not lost
+    # in the base term's rounding.
+    rng = np.random.default_rng(seed)
+    M = int(rng.integers(1, 17)) if seed % 3 == 0 else int(rng.integers(17, 1601))   # every third: the GEMV
+    H = 64 * int(rng.integers(2, 33))
+    N = 128 * int(rng.integers(1, 33))
+    rank = int(rng.integers(0, 65))
+    lora_cols = 32 * int(rng.integers(1, N // 32 + 1)) if rank else 0
+    _say(f"qproj random shape seed {seed}: M={M} H={H} N={N} r={rank} lora_cols={lora_cols}")
+    scale = 16.0 / max(rank, 1)
+    x, w, a, b = _gemm_case(M, H, N, rank, lora_cols, seed=seed, b_std=1.0)
+    with Context(ModelCfg(n_layers=1, hidden=H), pool_pages=0) as ctx:
+        out = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+        ctx.qproj_lora(dev_bf16(x), dev_bf16(w), dev_bf16(a) if rank else None, dev_bf16(b) if rank else None,
+                       rank, scale, lora_cols, out)
+        torch.cuda.synchronize()
+        got = host_f64(out)
+    ref = oracle.qproj_lora(oracle.decode_bf16(x), oracle.decode_bf16(w), oracle.decode_bf16(a) if rank else None,
+                            oracle.decode_bf16(b) if rank else None, scale, lora_cols)
+    assert_intermediate_close(got, ref, "q/k/v projection")
+
+
 @pytest.mark.parametrize("rank", [8, 16, 32])
 def test_lora_delta(rank):
     # B ~ N(0, 1) makes the low-rank term dominate, so a dropped, mis-scaled or
