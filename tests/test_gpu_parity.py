@@ -203,11 +203,10 @@ def test_qproj_lora_parity(M, H, N, rank, lora_cols):
 @pytest.mark.parametrize("seed", [401, 402, 403, 404, 405, 406])
 def test_qproj_lora_random_shapes(seed):
     # Seeded random shapes (tokens 1-16 or 17-1600, hidden a multiple of 64,
-    # outputs a multiple of 128,
-    # rank 0-64, adapted columns a multiple of 32): the launcher's tile,
-    # the fused or separate down-projection and the few-token GEMV paths
-    # vary with the shape.  B ~ N(0, 1) so that the low-rank term is not lost
-    # in the base term's rounding.
+    # outputs a multiple of 128, rank 0-64, adapted columns a multiple of
+    # 32): the launcher's tile, the fused or separate down-projection and the
+    # few-token GEMV paths vary with the shape.  B ~ N(0, 1) so that the
+    # low-rank term is not lost in the base term's rounding.
     rng = np.random.default_rng(seed)
     M = int(rng.integers(1, 17)) if seed % 3 == 0 else int(rng.integers(17, 1601))   # every third: the GEMV
     H = 64 * int(rng.integers(2, 33))
