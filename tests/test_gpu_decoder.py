@@ -123,6 +123,33 @@ def test_linear_parity(T, K, N, res):
     assert_intermediate_close(got, ref, "linear")
 
 
+@pytest.mark.parametrize("seed", [501, 502, 503, 504, 505, 506])
+def test_linear_random_shapes(seed):
+    # Seeded random shapes (tokens 1-16 or 17-1200, k and outputs multiples
+    # of 64) and residual forms: the plan's tile, its key split (a plain
+    # product may split the k range when its tiles leave CUs idle) and the
+    # few-token paths vary with the shape.
+    rng = np.random.default_rng(seed)
+    T = int(rng.integers(1, 17)) if seed % 3 == 0 else int(rng.integers(17, 1201))
+    K, N = 64 * int(rng.integers(1, 81)), 64 * int(rng.integers(1, 81))
+    res = ["none", "separate", "inplace"][int(rng.integers(0, 3))]
+    _say(f"linear random shape seed {seed}: T={T} K={K} N={N} residual={res}")
+    x, w = _bits(rng, (T, K)), _bits(rng, (N, K), 1 / math.sqrt(K))
+    r = _bits(rng, (T, N)) if res != "none" else None
+    with Context(ModelCfg(n_layers=1, hidden=256), pool_pages=0) as ctx:
+        if res == "inplace":
+            out = dev_bf16(r)
+            ctx.linear(dev_bf16(x), dev_bf16(w), out, residual=out)
+        else:
+            out = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+            ctx.linear(dev_bf16(x), dev_bf16(w), out, residual=dev_bf16(r) if r is not None else None)
+        torch.cuda.synchronize()
+        got = host_f64(out)
+    ref = oracle.linear(oracle.decode_bf16(x), oracle.decode_bf16(w),
+                        oracle.decode_bf16(r) if r is not None else None)
+    assert_intermediate_close(got, ref, "linear")
+
+
 @pytest.mark.parametrize("T,K,I", [(1, 2560, 9728), (100, 2560, 9728), (513, 4096, 12288), (64, 256, 32),
                                    (1000, 4096, 12288)])   # the last: two-k-group 128 x 192 tile, ragged
 def test_gate_up_swiglu_parity(T, K, I):
