@@ -68,11 +68,14 @@ def parse():
     ap.add_argument("--full-steps", type=int, default=3, help="timed full-prefill passes (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline (0: skip)")
     ov = ap.add_mutually_exclusive_group()
-    ov.add_argument("--overlap-gather", dest="overlap_gather", action="store_true", default=None,
-                    help="gather layer by layer on a second stream beside the layer loop (default when a layer "
-                         "gathers >= 100 MB: measured on MI355X -2.4%% per step at c5, -2.8%% at c3, +2.6%% at c2)")
-    ov.add_argument("--gather-first", dest="overlap_gather", action="store_false",
-                    help="gather every layer before the layer loop (default below 100 MB per layer)")
+    ov.add_argument("--fold-gather", dest="gather_mode", action="store_const", const="fold", default=None,
+                    help="gather layer 0 first, then let layer l's attention launch copy layer l + 1's pages "
+                         "(attuner_suffix_attn_gather; the default: measured on MI355X against the better of "
+                         "the two below, -0.6%% per step at c5, -3.8%% at c3, -7.0%% at c2)")
+    ov.add_argument("--overlap-gather", dest="gather_mode", action="store_const", const="overlap",
+                    help="gather layer by layer on a second stream beside the layer loop")
+    ov.add_argument("--gather-first", dest="gather_mode", action="store_const", const="first",
+                    help="gather every layer before the layer loop")
     ap.add_argument("--no-graph", action="store_true", help="launch the per-layer loop eagerly instead of "
                     "replaying it as a captured HIP graph")
     ap.add_argument("--copy-probe-mb", type=int, default=0, help="run one device copy of this many MiB first "
@@ -232,16 +235,16 @@ def cpu_baseline(wl, budget_s, args):
 # roofline traffic from committed counter summaries
 # ----------------------------------------------------------------------------
 
-def kernel_traffic(kernel_file, workload):
-    """HBM bytes per launch from profiles/<kernel>_<workload>_traffic.json, only
-    if the kernel source is unchanged since the counters were taken."""
+def kernel_traffic(kernel_file, workload, kernel):
+    """HBM bytes per launch of `kernel` from profiles/attention_<workload>_traffic.json,
+    only if the counters are that kernel's and its source is unchanged since."""
     path = os.path.join(ROOT, "profiles", f"attention_{workload}_traffic.json")
     src = os.path.join(ROOT, "paper_2609_36722_amd", "csrc", kernel_file)
     try:
         with open(path) as f:
             rec = json.load(f)
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-        if rec.get("source_sha256") != sha:
+        if rec.get("source_sha256") != sha or rec.get("kernel") != kernel:
             return None
         return float(rec["hbm_bytes_per_launch"])
     except Exception:
@@ -383,7 +386,9 @@ def main():
         pool = iter(timing_events(2 * sum(per_step[c] for c in cats) * n_steps))
         return {c: [(next(pool), next(pool)) for _ in range(per_step[c] * n_steps)] for c in cats}
 
-    def run_step(evs, idx, gather=True):
+    def run_step(evs, idx, gather=True, fold=False):
+        """One eager step, events around every call.  fold: the table, layer
+        0's gather, then layer l's attention launch copies layer l + 1's pages."""
         def call(cat, j, fn, a):
             if evs is not None:
                 evs[cat][j][0].record(stream)
@@ -392,11 +397,21 @@ def main():
                 raise RuntimeError(f"{fn.__name__}: {lib.attuner_last_error().decode()}")
             if evs is not None:
                 evs[cat][j][1].record(stream)
-        if gather:
+        if fold:
+            rc_ = lib.attuner_assemble_table(*table_args)
+            if rc_ != 0:
+                raise RuntimeError(f"attuner_assemble_table: {lib.attuner_last_error().decode()}")
+            call("gather", idx, lib.attuner_gather_layers,
+                 (h, block_table.data_ptr(), n_entries, 0, 1, req_kv.data_ptr(), rows, sp))
+        elif gather:
             call("gather", idx, lib.attuner_assemble_kv, assemble_args)
         for l in range(NL):
             call("qproj", idx * NL + l, lib.attuner_qproj_lora, qproj_args[l])
-            call("attn", idx * NL + l, lib.attuner_suffix_attn, attn_args[l])
+            if fold and l + 1 < NL:
+                call("attn", idx * NL + l, lib.attuner_suffix_attn_gather,
+                     attn_args[l][:-1] + (block_table.data_ptr(), n_entries, l + 1, sp))
+            else:
+                call("attn", idx * NL + l, lib.attuner_suffix_attn, attn_args[l])
 
     if args.copy_probe_mb > 0:
         nbytes = args.copy_probe_mb << 20
@@ -408,9 +423,13 @@ def main():
         log(args, f"copy probe: {args.copy_probe_mb} MiB read + written by one elementwise kernel")
         del a_src, a_dst
 
+    mode = args.gather_mode or "fold"
+    overlap = mode == "overlap" and not staged
+    fold = mode == "fold" and not staged and NL > 1
+
     log(args, f"warmup {args.warmup} steps")
     for i in range(args.warmup):
-        run_step(None, 0)
+        run_step(None, 0, fold=fold)
     torch.cuda.synchronize()
 
     # per-kernel times: eager steps with events around every call, and the
@@ -420,29 +439,29 @@ def main():
     for _ in range(2):   # the first pass is discarded (see TRACE_PASSES)
         ctx.trace_begin()
         for i in range(n_ev):
-            run_step(evs, i)
+            run_step(evs, i, fold=fold)
         torch.cuda.synchronize()
         ktimes = ctx.trace_end()
     kern_ms = {c: sum(a.elapsed_time(b) for a, b in evs[c]) / len(evs[c]) for c in cats}
     per_kernel = {k: {"launches": n, "avg_ms": round(t / n, 5), "max_ms": round(mx, 5)}
                   for k, (n, t, mx) in ktimes.items()}
-    attn_kernel_ms = ktimes["attention_kernel"][1] / ktimes["attention_kernel"][0]
+    # the dominant kernel: with the fold, the launches that also copy the next layer's pages
+    attn_kname = "attention_gather_kernel" if fold else "attention_kernel"
+    attn_kernel_ms = ktimes[attn_kname][1] / ktimes[attn_kname][0]
     log(args, "kernel avg ms: " + ", ".join(f"{k} {v['avg_ms']:.4f} (x{v['launches']})" for k, v in per_kernel.items()))
 
-    # The timed step.  By default all layers are gathered first
+    # The timed step.  By default (fold) the block table (host plan + upload)
+    # goes first, then layer 0's pages are gathered, and layer l's
+    # attuner_suffix_attn_gather copies layer l + 1's pages inside its
+    # attention launch.  With --gather-first every layer is gathered first
     # (attuner_assemble_kv), then the layer loop runs.  With --overlap-gather
-    # the block table (host plan + upload) goes first on the launch stream;
-    # the 36 per-layer gathers are then issued on a second stream, and layer
-    # l's attuner_suffix_attn waits for its own layer's gather (its projection
-    # does not read the cache).  The layer loop (with
-    # the per-layer gathers when overlapped) is replayed as one captured HIP
-    # graph unless --no-graph.
-    # With the staged host route bulk copies move layer l's host pages
-    # into the staging pool on the second stream (one event per layer), and
-    # the launch stream gathers layer l from there after its projection.
-    layer_gather_bytes = gather_bytes(s, sum(wl.art_len(r) for r in wl.requests), 1)
-    overlap = args.overlap_gather if args.overlap_gather is not None else layer_gather_bytes >= 100e6
-    overlap = overlap and not staged
+    # the per-layer gathers are issued on a second stream, and layer l's
+    # attuner_suffix_attn waits for its own layer's gather (its projection
+    # does not read the cache).  The layer loop (with the per-layer gathers
+    # when overlapped) is replayed as one captured HIP graph unless
+    # --no-graph.  With the staged host route bulk copies move layer l's host
+    # pages into the staging pool on the second stream (one event per layer),
+    # and the launch stream gathers layer l from there after its projection.
     side = torch.cuda.Stream()
     ev_fork, ev_layer = torch.cuda.Event(), [torch.cuda.Event() for _ in range(NL)]
     for e in [ev_fork] + ev_layer:   # created now, at their first record
@@ -459,6 +478,9 @@ def main():
         second stream before the layer loop issues the waits on them."""
         msp = C.c_void_p(main.cuda_stream)
         ssp = C.c_void_p(side.cuda_stream)
+        if fold:
+            check(lib.attuner_gather_layers(h, block_table.data_ptr(), n_entries, 0, 1, req_kv.data_ptr(), rows,
+                                            msp), "attuner_gather_layers")
         if overlap or staged:
             ev_fork.record(main)
             side.wait_event(ev_fork)
@@ -476,7 +498,11 @@ def main():
             if staged:
                 check(lib.attuner_gather_layers(h, block_table.data_ptr(), n_entries, l, 1, req_kv.data_ptr(), rows,
                                                 msp), "attuner_gather_layers")
-            check(lib.attuner_suffix_attn(*(aa[l][:-1] + (msp,))), "attuner_suffix_attn")
+            if fold and l + 1 < NL:
+                check(lib.attuner_suffix_attn_gather(*(aa[l][:-1] + (block_table.data_ptr(), n_entries, l + 1, msp))),
+                      "attuner_suffix_attn_gather")
+            else:
+                check(lib.attuner_suffix_attn(*(aa[l][:-1] + (msp,))), "attuner_suffix_attn")
         if overlap or staged:
             main.wait_stream(side)
 
@@ -493,7 +519,7 @@ def main():
         side.wait_stream(stream)
         if staged:  # the captured copies are those of the plan current at capture
             check(lib.attuner_assemble_table_staged(*staged_args), "attuner_assemble_table_staged")
-        elif overlap:  # the captured gathers read the table the last assemble_table call wrote
+        elif overlap or fold:  # the captured gathers read the table the last assemble_table call wrote
             check(lib.attuner_assemble_table(*table_args), "attuner_assemble_table")
         torch.cuda.synchronize()
         with torch.cuda.graph(graph, stream=cap):
@@ -503,13 +529,13 @@ def main():
     def timed_step():
         if staged:
             check(lib.attuner_assemble_table_staged(*staged_args), "attuner_assemble_table_staged")
-        elif overlap:
+        elif overlap or fold:
             check(lib.attuner_assemble_table(*table_args), "attuner_assemble_table")
         else:
             check(lib.attuner_assemble_kv(*assemble_args), "attuner_assemble_kv")
         if graph is not None:
             graph.replay()
-        elif overlap or staged:
+        elif overlap or staged or fold:
             layer_loop(stream, qproj_args, attn_args)
         else:
             run_step(None, 0, gather=False)
@@ -554,18 +580,20 @@ def main():
     attn_f = attention_flops(s, reqs_shape)
     gemm_f = gemm_flops(s, T, 0 if args.merged else wl.rank)
     g_bytes = gather_bytes(s, sum(L for L, _ in reqs_shape), NL)
+    g_layer_bytes = gather_bytes(s, sum(L for L, _ in reqs_shape), 1)
+    g_launch_bytes = g_layer_bytes if fold else g_bytes   # the gather_kernel launch of the instrumented step
     def kavg(name):  # kernel-only average duration (ms) from the library's launch tracer
         n, tot, _ = ktimes[name]
         return tot / n
 
-    attn_tflops = attn_f / (attn_kernel_ms * 1e-3) / 1e12          # attention_kernel alone
+    attn_tflops = attn_f / (attn_kernel_ms * 1e-3) / 1e12          # the attention kernel alone
     attn_call_tflops = attn_f / (kern_ms["attn"] * 1e-3) / 1e12   # attuner_suffix_attn call (+ norm, merge)
     # the projection runs one GEMM kernel per layer (which one: the tile plan)
     gemm_name = next(k for k in ("gemm_kg2_kernel", "gemm_lora_kernel") if k in ktimes)
     gemm_kernel_ms = kavg(gemm_name)
     gemm_tflops = gemm_f / (gemm_kernel_ms * 1e-3) / 1e12
     gather_kernel_ms = kavg("gather_kernel")
-    gather_gbps = g_bytes / (gather_kernel_ms * 1e-3) / 1e9
+    gather_gbps = g_launch_bytes / (gather_kernel_ms * 1e-3) / 1e9
     norm_bytes = T * (nq + 2 * nkv) * 2 * 2
     norm_kernel_ms = kavg("qk_norm_rope_kernel")
     norm_gbps = norm_bytes / (norm_kernel_ms * 1e-3) / 1e9
@@ -611,7 +639,8 @@ def main():
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(wl, args.cpu_seconds, args)
 
-    traffic = kernel_traffic("k_attention.hip", args.workload)
+    attn_rname = "attention_kernel<true>" if fold else "attention_kernel<false>"   # as rocprofv3 names it
+    traffic = kernel_traffic("k_attention.hip", args.workload, attn_rname)
     achieved = attn_tflops
     out = {
         "metric": METRIC,
@@ -633,17 +662,20 @@ def main():
         "layer_loop": "hip_graph" if graph is not None else "eager",
         "gather_schedule": ("per layer: bulk copies on a second stream, HBM gather before the layer's attention"
                             if staged else "per layer on a second stream beside the layer loop" if overlap
+                            else "layer 0 first, layer l + 1 inside layer l's attention launch" if fold
                             else "all layers first"),
         "artifact_cache": "pinned host memory, moved over the host link every step" if args.host_cache else "HBM",
         "host_transfer": host_transfer,
         "adapter": "merged into W_q (rank-0 projection)" if args.merged else "unmerged, fused into the projection",
-        "roofline": {"bound": "mfma", "kernel": "attention_kernel", "achieved": round(achieved, 2),
+        "roofline": {"bound": "mfma", "kernel": attn_rname, "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic, "flops_per_launch": attn_f, "launch_ms": round(attn_kernel_ms, 5)},
+                     "traffic": traffic, "flops_per_launch": attn_f, "launch_ms": round(attn_kernel_ms, 5),
+                     "copy_bytes_per_launch": g_layer_bytes if fold else 0},
         "kernels": {
             "attention": {"tflops": round(attn_tflops, 2), "mfma_frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
                           "kernel_ms": round(attn_kernel_ms, 5), "suffix_attn_call_ms": round(kern_ms["attn"], 5),
-                          "call_tflops": round(attn_call_tflops, 2)},
+                          "call_tflops": round(attn_call_tflops, 2), "kernel": attn_kname,
+                          "attention_kernel_alone_ms": round(kavg("attention_kernel"), 5)},
             "qproj_lora_gemm": {"tflops": round(gemm_tflops, 2), "mfma_frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
                                 "kernel_ms": round(gemm_kernel_ms, 5), "call_ms": round(kern_ms["qproj"], 5),
                                 "flops_per_layer": gemm_f, "kernel": gemm_name},

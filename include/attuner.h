@@ -411,6 +411,31 @@ attuner_status attuner_suffix_attn(attuner_ctx* ctx, int32_t layer, int32_t n_re
                                    int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
                                    int64_t cache_rows, void* o, float* lse, void* stream);
 
+/* attuner_suffix_attn for `layer` that also performs
+ * attuner_gather_layers(ctx, block_table, n_entries, gather_layer, 1, req_kv,
+ * cache_rows, stream): the layer-by-layer prefill of section 2 (equation 3)
+ * copies each layer's cached artifact pages (appendix A.2) before that
+ * layer's attention, and this call lets the copy of the next layer ride in
+ * the attention launch of this one, where it overlaps the attention's
+ * matrix work.  Results are bit-identical to the two calls made apart.
+ *   block_table, n_entries, cache_rows: those of the last
+ *   attuner_assemble_table call (else ATTUNER_EINVAL), as for
+ *   attuner_gather_layers.  gather_layer in [0, n_layers) (else
+ *   ATTUNER_ERANGE) and != layer (else ATTUNER_EINVAL): the attention
+ *   reads `layer`'s rows while the copy writes gather_layer's.
+ * The copy rides in the attention launch when every page of that table is
+ * in the HBM pool, 8 n_kv_heads is a power of two and one layer's pool and
+ * cache planes are below 4 GiB; otherwise (host or staged pages, other
+ * shapes, no suffix tokens) the call runs attuner_gather_layers first and
+ * then attuner_suffix_attn, on `stream`.  Other arguments, outputs and
+ * errors as attuner_suffix_attn. */
+attuner_status attuner_suffix_attn_gather(attuner_ctx* ctx, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                          const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                          const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                          int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                          int64_t cache_rows, void* o, float* lse, const int32_t* block_table,
+                                          int64_t n_entries, int32_t gather_layer, void* stream);
+
 /* Size of the fixed device buffer of attuner_suffix_attn_noalloc (per device). */
 #define ATTUNER_NOALLOC_SCRATCH_BYTES (24 << 20)
 

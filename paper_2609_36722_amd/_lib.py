@@ -63,6 +63,8 @@ SIGNATURES = {
                                       _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
     "attuner_suffix_attn_noalloc": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp,
                                               _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "attuner_suffix_attn_gather": (C.c_int, [_vp, _i32, _i32, _i32p, _i32p, _i32p, _i32p, _vp, _i64, _vp, _vp,
+                                             _i64, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _i64, _i32, _vp]),
     "attuner_merge_lora": (C.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _i32, C.c_float, _i32, _vp, _vp]),
     "attuner_host_pool_create": (C.c_int, [_vp, _i64]),
     "attuner_store_artifact_host": (C.c_int, [_vp, _i32, _vp, _vp, _vp, _i32p]),

@@ -419,6 +419,25 @@ class Context:
                                     _ptr(req_kv), int(cache_rows), _ptr(o), _ptr(lse, 4), _stream(stream)),
                name)
 
+    def suffix_attn_gather(self, layer: int, cu_q, cu_ctx, art_len, pos0, q_raw, ld_q: int, k_raw, v_raw,
+                           ld_kv: int, gamma_q, gamma_k, req_kv, cache_rows: int, o, block_table: torch.Tensor,
+                           n_entries: int, gather_layer: int, lse: Optional[torch.Tensor] = None,
+                           stream=None) -> None:
+        """attuner_suffix_attn_gather: suffix_attn for `layer` that also copies gather_layer's artifact
+        pages (gather_layers(block_table, n_entries, gather_layer, 1, ...)) inside the attention launch."""
+        n = len(art_len)
+        self._check_cache(cu_q, cu_ctx, o, req_kv, cache_rows, q_raw, ld_q, k_raw, v_raw, ld_kv)
+        _need(lse, int(cu_q[-1]) * self.cfg.n_q_heads, "lse")
+        _need(block_table, 4 * int(n_entries), "block_table")
+        _check(lib().attuner_suffix_attn_gather(self._h, int(layer), n, _i32(cu_q), _i32(cu_ctx), _i32(art_len),
+                                                _i32(pos0) if pos0 is not None else None, _view_ptr(q_raw),
+                                                int(ld_q), _view_ptr(k_raw), _view_ptr(v_raw), int(ld_kv),
+                                                _ptr(gamma_q), _ptr(gamma_k), _ptr(req_kv), int(cache_rows),
+                                                _ptr(o), _ptr(lse, 4),
+                                                _ptr(block_table, 4) if block_table is not None else None,
+                                                int(n_entries), int(gather_layer), _stream(stream)),
+               "attuner_suffix_attn_gather")
+
     def span_attn(self, layer: int, cu_q, kv_start, offset, pos0, q_raw, ld_q: int, k_raw, v_raw, ld_kv: int,
                   gamma_q, gamma_k, req_kv, cache_rows: int, o, lse: Optional[torch.Tensor] = None,
                   stream=None) -> None:

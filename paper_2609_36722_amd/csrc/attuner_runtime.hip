@@ -294,6 +294,7 @@ struct attuner_ctx {
   // attuner_gather_layers accepts)
   const int32_t* last_table = nullptr;
   int64_t last_entries = -1, last_rows = -1;
+  bool last_hbm_only = false;  // every page of that table is an HBM-pool page
   // key splits chosen for the last attention batch shape (q_len, art_len per
   // request), reused while the shape repeats (every layer of a stack)
   std::vector<int32_t> split_shape;
@@ -562,10 +563,19 @@ size_t split_row_bytes(const attuner_ctx* c) {
 // part_buf / part_bytes: a caller-provided buffer for the key-split
 // partials (the plan is then limited to what fits); null: the context's
 // workspace, grown as needed.
+// A copy of one layer's pages that the attention launch carries (AttnParams g_*).
+struct GatherArgs {
+  const int32_t* table;
+  int64_t entries;
+  int32_t layer;
+  uint16_t* req_kv;
+  int64_t cache_rows;
+};
+
 attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int32_t total_q, const void* q,
                              const uint16_t* k_plane, const uint16_t* v_plane, int64_t head_stride, void* o,
                              float* lse, hipStream_t stream, const std::vector<SpanRow>* spans = nullptr,
-                             void* part_buf = nullptr, size_t part_bytes = 0) {
+                             void* part_buf = nullptr, size_t part_bytes = 0, const GatherArgs* gather = nullptr) {
   AttnParams p;
   memset(&p, 0, sizeof p);
   p.q = static_cast<const uint16_t*>(q);
@@ -611,6 +621,22 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
     }
   p.n_split = n_split;
   p.n_units = units;
+  if (gather != nullptr) {
+    const int n_slab = 2 * c->cfg.n_kv_heads;
+    const int64_t chunks = gather->entries * n_slab * 4;
+    const int64_t wgs = (int64_t)units * c->cfg.n_kv_heads;
+    p.g_table = gather->table;
+    p.g_pool = c->pool;
+    p.g_pool_pages = c->pool_pages;
+    p.g_req_kv = gather->req_kv;
+    p.g_cache_rows = gather->cache_rows;
+    p.g_chunks = (int32_t)chunks;
+    p.g_per_wg = (int32_t)((chunks + wgs - 1) / wgs);
+    p.g_layer = gather->layer;
+    int shift = 0;
+    while ((1 << shift) < n_slab * 4) ++shift;
+    p.g_shift = shift;
+  }
   if (n_split > 1) {
     const size_t rows = (size_t)n_split * total_q * c->cfg.n_q_heads;
     const size_t po = rows * c->cfg.head_dim * sizeof(uint16_t);
@@ -1170,6 +1196,9 @@ static attuner_status assemble_table_impl(attuner_ctx* c, bool staged, int32_t n
   c->last_entries = entries;
   c->last_rows = rows;
   c->last_staged = staged;
+  c->last_hbm_only = true;
+  for (size_t e = 0; e < table.size(); e += 4)
+    if (table[e] & (kHostPageFlag | kStagePageFlag)) c->last_hbm_only = false;
   return ATTUNER_OK;
 }
 
@@ -1590,7 +1619,8 @@ static attuner_status suffix_attn_impl(attuner_ctx* c, int32_t layer, int32_t n_
                                        const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
                                        const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
                                        int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
-                                       int64_t cache_rows, void* o, float* lse, void* stream, bool noalloc) {
+                                       int64_t cache_rows, void* o, float* lse, void* stream, bool noalloc,
+                                       const GatherArgs* gather = nullptr) {
   if (!c) return fail(ATTUNER_EINVAL, "null ctx");
   attuner_status st = check_layer(c, layer);
   if (st != ATTUNER_OK) return st;
@@ -1622,7 +1652,7 @@ static attuner_status suffix_attn_impl(attuner_ctx* c, int32_t layer, int32_t n_
   st = run_norm_rope(c, reqs, total_q, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, o, kp, vp, hs, s);
   if (st != ATTUNER_OK) return st;
   return run_attention(c, reqs, total_q, o, kp, vp, hs, o, lse, s, nullptr, part,
-                       noalloc ? (size_t)ATTUNER_NOALLOC_SCRATCH_BYTES : 0);
+                       noalloc ? (size_t)ATTUNER_NOALLOC_SCRATCH_BYTES : 0, gather);
 }
 
 attuner_status attuner_suffix_attn(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_q,
@@ -1641,6 +1671,45 @@ attuner_status attuner_suffix_attn_noalloc(attuner_ctx* c, int32_t layer, int32_
                                            int64_t cache_rows, void* o, float* lse, void* stream) {
   return suffix_attn_impl(c, layer, n_req, cu_q, cu_ctx, art_len, pos0, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q,
                           gamma_k, req_kv, cache_rows, o, lse, stream, true);
+}
+
+attuner_status attuner_suffix_attn_gather(attuner_ctx* c, int32_t layer, int32_t n_req, const int32_t* cu_q,
+                                          const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
+                                          const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,
+                                          int64_t ld_kv, const void* gamma_q, const void* gamma_k, void* req_kv,
+                                          int64_t cache_rows, void* o, float* lse, const int32_t* block_table,
+                                          int64_t n_entries, int32_t gather_layer, void* stream) {
+  if (!c) return fail(ATTUNER_EINVAL, "null ctx");
+  if (c->last_entries < 0 || block_table != c->last_table || n_entries != c->last_entries ||
+      cache_rows != c->last_rows)
+    return fail(ATTUNER_EINVAL, "block_table, n_entries and cache_rows must be those of the last "
+                                "attuner_assemble_table call");
+  if (gather_layer < 0 || gather_layer >= c->cfg.n_layers)
+    return fail(ATTUNER_ERANGE, "gather_layer %d outside [0, %d)", gather_layer, c->cfg.n_layers);
+  if (gather_layer == layer)
+    return fail(ATTUNER_EINVAL, "gather_layer must differ from layer (the attention reads that layer's rows)");
+  if (!req_kv || !aligned16(req_kv)) return fail(ATTUNER_EINVAL, "req_kv must be non-null and 16-byte aligned");
+  // the attention launch carries the copy when the table names HBM pages only
+  // and one layer's offsets fit 32 bits; otherwise the gather runs first
+  const int64_t n_slab = 2 * c->cfg.n_kv_heads;
+  const bool pow2 = ((n_slab * 4) & (n_slab * 4 - 1)) == 0;
+  const bool fits = n_entries * n_slab * 4 < INT32_MAX && c->pool_pages * n_slab * kPageTokens * 16 < (1LL << 32) &&
+                    n_slab * cache_rows * 16 < (1LL << 32);
+  int32_t total_q = 0;
+  for (int32_t r = 0; cu_q && r < n_req; ++r) total_q += cu_q[r + 1] - cu_q[r];
+  if (n_entries == 0 || !c->last_hbm_only || !pow2 || !fits || total_q == 0 || !c->pool) {
+    if (n_entries > 0) {
+      DeviceGuard dg(c->device);
+      HIP_TRY(launch_gather(block_table, n_entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages,
+                            c->stage_pool, c->stage_pages, gather_layer, 1, c->cfg.n_kv_heads,
+                            static_cast<uint16_t*>(req_kv), cache_rows, static_cast<hipStream_t>(stream)));
+    }
+    return suffix_attn_impl(c, layer, n_req, cu_q, cu_ctx, art_len, pos0, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q,
+                            gamma_k, req_kv, cache_rows, o, lse, stream, false);
+  }
+  const GatherArgs g{block_table, n_entries, gather_layer, static_cast<uint16_t*>(req_kv), cache_rows};
+  return suffix_attn_impl(c, layer, n_req, cu_q, cu_ctx, art_len, pos0, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q,
+                          gamma_k, req_kv, cache_rows, o, lse, stream, false, &g);
 }
 
 attuner_status attuner_span_attn(attuner_ctx* c, int32_t layer, int32_t n_spans, const int32_t* cu_q,

@@ -237,9 +237,18 @@ __device__ __forceinline__ void rescale(f32x16 (&acc)[4], float alpha) {
   }
 }
 
+// GATHER: the launch also copies another layer's pages into the request cache
+// (AttnParams g_*): each wave takes every eighth chunk of its workgroup's
+// range, one per tile.  A chunk is fetched into one of the wave's three LDS
+// slots by the DMA form of the load right after the tile's K/V copies, and
+// stored from there two tiles later, when the tile's wait has covered it:
+// loads complete in the order issued, and a store can only lengthen a wait.
+template <bool GATHER>
 __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   __shared__ u32x4 k_lds[NSTAGE][BKV * CH];
   __shared__ u32x4 v_lds[NSTAGE][BKV * CH];
+  constexpr int kGSlots = 3;
+  __shared__ u32x4 g_lds[GATHER ? NTHREADS / 64 * kGSlots * 64 : 1];
 
   const int hkv = p.n_kv_heads;
   const int g = blockIdx.x % hkv;
@@ -289,6 +298,56 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   constexpr uint32_t kStage = BKV * CH * 16;  // bytes per stage of K (and of V)
   const DmaLane dl = dma_lane(wave, lane);
 
+  // Gather state (wave-uniform): the wave's chunks are g_first + 8 n for
+  // n < g_count; chunk n is fetched at the wave's sync n into slot n % 3 and
+  // stored at sync n + 3 (or after the loops).  g_prev: the previous sync
+  // fetched a chunk after its tile's K/V copies.
+  int g_first = 0, g_count = 0, g_syncs = 0;
+  bool g_prev = false;
+  if constexpr (GATHER) {
+    const int cb = blockIdx.x * p.g_per_wg;
+    const int ce = min(p.g_chunks, cb + p.g_per_wg);
+    g_first = cb + wave;
+    g_count = ce > g_first ? (ce - g_first + NTHREADS / 64 - 1) / (NTHREADS / 64) : 0;
+  }
+  // the copied layer's pool pages and cache planes, and chunk c's 16-byte
+  // piece for this lane in each (offsets in 16-byte units); returns whether
+  // this lane's row holds a token (rows past n_valid do not)
+  const int g_nslab = 2 * hkv;
+  const u32x4* g_src = reinterpret_cast<const u32x4*>(p.g_pool) +
+                       (int64_t)p.g_layer * p.g_pool_pages * g_nslab * (kPageTokens * CH);
+  u32x4* g_dst = reinterpret_cast<u32x4*>(p.g_req_kv) + (int64_t)p.g_layer * g_nslab * p.g_cache_rows * CH;
+  auto g_addr = [&](int c, uint32_t& so, uint32_t& dof) __attribute__((always_inline)) {
+    const int e = c >> p.g_shift;
+    const int rem = c & ((1 << p.g_shift) - 1);
+    const int sl = rem >> 2, qt = rem & 3;
+    // through the constant address space: a scalar load, waited for with
+    // the LDS counter, so the vector-memory wait of the K/V ring is left alone
+    const __attribute__((address_space(4))) int32_t* ent =
+        (const __attribute__((address_space(4))) int32_t*)p.g_table + 4 * e;  // {page, n_valid, dst_row, req}
+    const int row = 4 * qt + (lane >> 4);
+    const bool valid = row < ent[1];
+    const uint32_t rr = valid ? (uint32_t)row : 0u;
+    so = ((uint32_t)((ent[0] & kPageIdMask) * g_nslab + sl) * kPageTokens + rr) * CH + (uint32_t)(lane & 15);
+    dof = ((uint32_t)sl * (uint32_t)p.g_cache_rows + (uint32_t)ent[2] + rr) * CH + (uint32_t)(lane & 15);
+    return valid;
+  };
+  const uint32_t g_base = lds_addr(g_lds) + (uint32_t)wave * kGSlots * 1024u;
+  // store the wave's chunk n from its slot (its fetch is complete)
+  auto g_store = [&](int n) __attribute__((always_inline)) {
+    uint32_t so, dof;
+    const bool valid = g_addr(g_first + n * (NTHREADS / 64), so, dof);
+    // the lane's 16-byte piece of the slot, at 16 (lane >> 4) + (lane & 15):
+    // formed here from the two values the addresses above use, in an opaque
+    // step, so that the compiler keeps no register for it across the tile
+    // loop (it spilled one, and a reload's wait drains the K/V ring)
+    uint32_t piece;
+    asm volatile("v_lshl_or_b32 %0, %1, 4, %2" : "=v"(piece) : "v"(lane >> 4), "v"(lane & 15));
+    const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)(uintptr_t)(
+        g_base + (uint32_t)(n % kGSlots) * 1024u + piece * 16u);
+    if (valid) __builtin_nontemporal_store(v, g_dst + dof);
+  };
+
   // Prologue: the Q rows and the DMA of tile tb fly together and one wait
   // covers both (Q is then in registers, so the compiler needs no
   // vector-memory wait inside the tile loop); tile tb + 1 follows.
@@ -333,12 +392,32 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
   // if any, may still fly), then everyone's; the stage of tile - 2 is free
   // and receives tile + 2.
   auto tile_sync = [&](int tile) __attribute__((always_inline)) {
-    if (tile + 1 < te) __builtin_amdgcn_s_waitcnt(vmcnt_wait(4));
-    else __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+    // The loads after this tile's copies: tile + 1's four and, with the
+    // gather, the chunk the previous sync fetched after them; waiting for
+    // all but those leaves only tile + 1 in flight.  The chunk fetched two
+    // syncs ago is complete as well (tile + 1's copies came after it).
+    if (tile + 1 < te) {
+      if (GATHER && g_prev) __builtin_amdgcn_s_waitcnt(vmcnt_wait(5));
+      else __builtin_amdgcn_s_waitcnt(vmcnt_wait(4));
+    } else {
+      __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+    }
     barrier_no_fence();
     if (tile + 2 < te) {
       const uint32_t nb = (uint32_t)((tile - tb + 2) & (NSTAGE - 1)) * kStage;
       dma_tile(kb, vb, (tile + 2) * BKV, kv_len, k_base + nb, v_base + nb, dl, wave);
+    }
+    if constexpr (GATHER) {
+      const int n = g_syncs;
+      if (n >= kGSlots && n - kGSlots < g_count) g_store(n - kGSlots);  // frees slot n % 3
+      g_prev = false;
+      if (n < g_count) {
+        uint32_t so, dof;
+        (void)g_addr(g_first + n * (NTHREADS / 64), so, dof);
+        lds_dma16(g_src + so, g_base + (uint32_t)(n % kGSlots) * 1024u);
+        g_prev = tile + 2 < te;  // the next sync counts it only if it follows tile + 2's copies
+      }
+      g_syncs = n + 1;
     }
   };
   auto kst = [&](int tile) __attribute__((always_inline)) { return k_lds[(tile - tb) & (NSTAGE - 1)]; };
@@ -407,8 +486,19 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
     l_i = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[i] = f32x16{};
+    g_prev = false;  // the last fetch came before the new copies
     if (tb < te) dma_tile(kb, vb, tb * BKV, kv_len, k_base, v_base, dl, wave);
     if (tb + 1 < te) dma_tile(kb, vb, (tb + 1) * BKV, kv_len, k_base + kStage, v_base + kStage, dl, wave);
+  }
+  if constexpr (GATHER) {
+    // the chunks still in LDS, then the rest of the wave's chunks directly
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+    for (int n = max(0, g_syncs - kGSlots); n < min(g_syncs, g_count); ++n) g_store(n);
+    for (int n = g_syncs; n < g_count; ++n) {
+      uint32_t so, dof;
+      if (g_addr(g_first + n * (NTHREADS / 64), so, dof))
+        __builtin_nontemporal_store(__builtin_nontemporal_load(g_src + so), g_dst + dof);
+    }
   }
   l_i += __shfl_xor(l_i, 32, 64);  // the two lanes of a token hold its two partial sums
 
@@ -524,8 +614,12 @@ __global__ __launch_bounds__(256, 2) void attn_combine_kernel(AttnParams p) {
 
 hipError_t launch_attention(const AttnParams& p, hipStream_t stream) {
   if (p.n_units == 0) return hipSuccess;
-  ATTUNER_LAUNCH("attention_kernel", attention_kernel, dim3((unsigned)(p.n_units * p.n_kv_heads)), dim3(NTHREADS),
-                 stream, p);
+  if (p.g_table != nullptr)
+    ATTUNER_LAUNCH("attention_gather_kernel", attention_kernel<true>, dim3((unsigned)(p.n_units * p.n_kv_heads)),
+                   dim3(NTHREADS), stream, p);
+  else
+    ATTUNER_LAUNCH("attention_kernel", attention_kernel<false>, dim3((unsigned)(p.n_units * p.n_kv_heads)),
+                   dim3(NTHREADS), stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_split == 1) return e;
   if (p.n_split > kMaxSplit || p.n_q_heads != 4 * p.n_kv_heads) return hipErrorInvalidValue;

@@ -200,6 +200,20 @@ struct AttnParams {
   AttnReq req[kMaxReq];
   int32_t span_row[kMaxReq];  // first q row of each packed span
   int32_t span_off[kMaxReq];  // its offset (first position) in its request's cache rows
+  // Optional: copy one layer's pages (HBM pool) into the request cache beside
+  // the attention, in 1 KiB chunks (4 rows of one (K|V, head) slab of one
+  // block-table entry): g_chunks = entries * 2 * n_kv * 4, g_per_wg of them
+  // per workgroup.  g_table null: none.  The host keeps one layer's pool and
+  // cache offsets below 2^32 16-byte units.
+  const int32_t* g_table;  // block table {page, n_valid, dst_row, request} per entry
+  const uint16_t* g_pool;
+  int64_t g_pool_pages;
+  uint16_t* g_req_kv;
+  int64_t g_cache_rows;
+  int32_t g_chunks;        // < 2^31
+  int32_t g_per_wg;
+  int32_t g_layer;
+  int32_t g_shift;         // log2(chunks per entry), 4 * 2 * n_kv a power of two
 };
 
 // Attention, plus the split-KV merge kernel when n_split > 1 (at most

@@ -30,7 +30,8 @@ class GpuWorkload:
     """A workload stored in a fresh context: its artifacts in the pool and the
     request caches assembled, for the given model layers."""
 
-    def __init__(self, wl: sd.Workload, layers: Sequence[int] = (0,), extra_pages: int = 0, suffix_extra: int = 0):
+    def __init__(self, wl: sd.Workload, layers: Sequence[int] = (0,), extra_pages: int = 0, suffix_extra: int = 0,
+                 host_artifacts: Sequence[int] = ()):
         self.wl = wl
         self.layers = list(layers)
         s = wl.shape
@@ -39,6 +40,8 @@ class GpuWorkload:
         used = sorted({a for r in wl.requests for a in r.artifact_ids})
         pages = sum(math.ceil(wl.artifact_lengths[a] / 16) for a in used) + extra_pages
         self.ctx = Context(self.cfg, pool_pages=max(1, pages))
+        if host_artifacts:  # these artifacts go to the pinned host pool
+            self.ctx.host_pool_create(sum(math.ceil(wl.artifact_lengths[a] / 16) for a in set(host_artifacts)))
         self.ids: Dict[int, int] = {}
         self.art_k: Dict[int, np.ndarray] = {}  # bits [n_layers][L][n_kv][d]
         self.art_v: Dict[int, np.ndarray] = {}
@@ -49,7 +52,8 @@ class GpuWorkload:
             self.art_k[a], self.art_v[a] = k, v
             kd = dev_bf16(np.ascontiguousarray(k.transpose(0, 2, 1, 3)))
             vd = dev_bf16(np.ascontiguousarray(v.transpose(0, 2, 1, 3)))
-            self.ids[a] = self.ctx.store_artifact(kd, vd)
+            store = self.ctx.store_artifact_host if a in host_artifacts else self.ctx.store_artifact
+            self.ids[a] = store(kd, vd)
         self.requests = [[self.ids[a] for a in r.artifact_ids] for r in wl.requests]
         self.suffix_cap = [r.suffix_len + suffix_extra for r in wl.requests]
         self.n_entries, self.rows = self.ctx.assemble_plan(self.requests, self.suffix_cap)
