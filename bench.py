@@ -765,16 +765,26 @@ def model_main(args):
     torch.cuda.synchronize()
     log(args, f"weights {weight_bytes / 1e9:.2f} GB and artifacts resident ({time.time() - t0:.1f} s)")
 
+    fold = (args.gather_mode or "fold") == "fold" and NL > 1
+
     def make_step(stk, reqs, cps, table, kv, n_rows, toks, p0):
-        """One step: assembly, embedding, the layer loop (a graph once captured), first token."""
+        """One step: assembly, embedding, the layer loop (a graph once captured), first token.
+        With the fold the assembly gathers layer 0 only and each layer's attention launch
+        copies the next layer's pages."""
         state = {"graph": None, "cu": None, "al": None}
         make_step.last_state = state
+        n_ent = ctx.assemble_plan(reqs, cps)[0]
 
         def assemble():
-            state["cu"], state["al"] = ctx.assemble_kv(reqs, cps, table, kv, n_rows)
+            if fold:
+                state["cu"], state["al"] = ctx.assemble_table(reqs, cps, table, n_rows)
+                ctx.gather_layers(table, n_ent, 0, 1, kv, n_rows)
+            else:
+                state["cu"], state["al"] = ctx.assemble_kv(reqs, cps, table, kv, n_rows)
 
         def layer_loop(mark=None):
-            stk.layers(state["cu"], state["al"], p0, kv, n_rows, mark=mark)
+            stk.layers(state["cu"], state["al"], p0, kv, n_rows, mark=mark,
+                       gather=(table, n_ent) if fold else None)
 
         def step():
             assemble()
@@ -942,6 +952,8 @@ def model_main(args):
                    "requests": len(wl.requests), "artifact_tokens": [wl.art_len(r) for r in wl.requests],
                    "suffix_tokens": [r.suffix_len for r in wl.requests], "lora_rank": wl.rank},
         "layer_loop": "hip_graph" if not args.no_graph else "eager",
+        "gather_schedule": ("layer 0 in the assembly, layer l + 1 inside layer l's attention launch" if fold
+                            else "all layers in the assembly"),
         "breakdown_ms_per_step_eager": {k: round(v, 4) for k, v in breakdown.items()},
         "gemms": gemms,
         "weight_bytes": weight_bytes,

@@ -7,7 +7,8 @@ are Qwen3 decoder stacks, section 5.1).
 Per layer l, on the residual stream h [T][H] of the T suffix tokens:
     x   = RMSNorm(h) * gamma_in                      attuner_rms_norm
     qkv = x [W_q | W_k | W_v]^T + LoRA on q          attuner_qproj_lora
-    o   = attention over artifacts + causal suffix   attuner_suffix_attn
+    o   = attention over artifacts + causal suffix   attuner_suffix_attn (or _gather: the
+                                                     launch also copies layer l + 1's pages)
     h   = h + o W_o^T                                attuner_linear (residual, in place)
     x   = RMSNorm(h) * gamma_post                    attuner_rms_norm
     g   = silu(x W_gate^T) * (x W_up^T)              attuner_gate_up_swiglu
@@ -28,7 +29,7 @@ row j at row 2j + 1 (see interleave_gate_up).
 from __future__ import annotations
 
 from dataclasses import dataclass, field
-from typing import Callable, List, Optional, Sequence
+from typing import Callable, List, Optional, Sequence, Tuple
 
 import torch
 
@@ -111,13 +112,17 @@ class DecoderStack:
 
     def layers(self, cu_ctx, art_len, pos0, req_kv: torch.Tensor, cache_rows: int, stream=None,
                first: int = 0, count: Optional[int] = None,
-               mark: Optional[Callable[[Optional[str]], None]] = None) -> None:
+               mark: Optional[Callable[[Optional[str]], None]] = None,
+               gather: Optional[Tuple[torch.Tensor, int]] = None) -> None:
         """Decoder layers first .. first + count - 1 (default: all) over h, in
         place.  cu_ctx / art_len / pos0 as attuner_suffix_attn takes them (from
         the cache assembly).  Makes no host-to-device copy, so a caller may
         capture it into a graph.  mark, if given, is called with the name of
         each step (one of STEPS) before its call and with None after the last
-        (e.g. to record timing events)."""
+        (e.g. to record timing events).  gather, if given, is (block_table,
+        n_entries) of the last attuner_assemble_table call: then the cache
+        need only hold layer `first`'s artifact pages, and each layer's
+        attention launch copies the next layer's (attuner_suffix_attn_gather)."""
         c, w, ld = self.ctx, self.w, self.nq + 2 * self.nkv
         q, k, v = self.qkv[:, :self.nq], self.qkv[:, self.nq:self.nq + self.nkv], self.qkv[:, self.nq + self.nkv:]
         count = len(w.layers) - first if count is None else count
@@ -130,8 +135,12 @@ class DecoderStack:
             c.qproj_lora(self.x, lw.wqkv, lw.a, lw.b, w.rank if lw.a is not None else 0, w.scale, self.nq, self.qkv,
                          stream=stream)
             m("suffix_attn")
-            c.suffix_attn(l, self.cu_q, cu_ctx, art_len, pos0, q, ld, k, v, ld, lw.gamma_q, lw.gamma_k, req_kv,
-                          cache_rows, self.o, stream=stream)
+            if gather is not None and l + 1 < first + count:
+                c.suffix_attn_gather(l, self.cu_q, cu_ctx, art_len, pos0, q, ld, k, v, ld, lw.gamma_q, lw.gamma_k,
+                                     req_kv, cache_rows, self.o, gather[0], gather[1], l + 1, stream=stream)
+            else:
+                c.suffix_attn(l, self.cu_q, cu_ctx, art_len, pos0, q, ld, k, v, ld, lw.gamma_q, lw.gamma_k, req_kv,
+                              cache_rows, self.o, stream=stream)
             m("o_proj")
             c.linear(self.o.view(-1, self.nq), lw.wo, self.h, residual=self.h, stream=stream)
             m("post_norm")

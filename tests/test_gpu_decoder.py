@@ -290,6 +290,19 @@ def test_decoder_stack_two_layers_then_decode():
         stack.layers(g.cu_ctx, g.art_len, g.pos0, g.req_kv, g.rows)
         ids = stack.first_token().cpu().numpy()
         h_pre, x_last = host_f64(stack.h), host_f64(stack.x_last)
+        # the same prefill with layer 0's pages gathered first and layer 1's
+        # copied inside layer 0's attention launch: h, the first tokens and
+        # the cache bit for bit as above
+        _say("decoder stack: pages copied inside the attention launches")
+        kv2, bt2 = torch.zeros_like(g.req_kv), torch.zeros_like(g.block_table)
+        g.ctx.assemble_table(g.requests, g.suffix_cap, bt2, g.rows)
+        g.ctx.gather_layers(bt2, g.n_entries, 0, 1, kv2, g.rows)
+        stack.embed(np.concatenate(tokens).tolist())
+        stack.layers(g.cu_ctx, g.art_len, g.pos0, kv2, g.rows, gather=(bt2, g.n_entries))
+        assert np.array_equal(stack.first_token().cpu().numpy(), ids)
+        assert np.array_equal(host_f64(stack.h), h_pre)
+        assert torch.equal(kv2.view(torch.int16), g.req_kv.view(torch.int16))
+        del kv2, bt2
         dec = []
         for j in range(n_dec):
             ctx_len = [g.art_len[r] + wl.requests[r].suffix_len + j for r in range(n_req)]
