@@ -11,7 +11,8 @@ twice in one request); the long-context Qwen3-8B shape over two layers (the
 launch the step times, with key splits); suffixes of one to three tokens over
 long artifacts (the copy outweighs the attention, most of it runs after the
 tile loop); an artifact in the host pool (the call copies in a launch of its
-own first); a batch with no suffix tokens; and the argument errors."""
+own first); a batch with no suffix tokens; the argument errors; and the
+chained layer loop captured in a HIP graph and replayed."""
 
 import numpy as np
 import pytest
@@ -180,5 +181,65 @@ def test_gather_attn_no_suffix_and_errors():
         assert e.value.status == -1
         torch.cuda.synchronize()
         assert not bf16_to_host(kv).reshape(got.shape)[:2].any()   # the rejected calls wrote nothing
+    finally:
+        g.close()
+
+
+def test_gather_attn_graph_replays():
+    """The chained layer loop captured in one HIP graph (layer 0's gather,
+    then each layer's attention copying the next layer's pages), replayed
+    three times into a cleared cache with eager work between the replays:
+    every replay gives the eager chain's O, LSE and cache bit for bit."""
+    g = GpuWorkload(_three_layer(100), layers=(0, 1, 2))
+    try:
+        L = len(g.layers)
+        ins = [_qkv(g, li) for li in range(L)]
+        kv = torch.zeros_like(g.req_kv)
+        bt = torch.zeros_like(g.block_table)
+        g.ctx.assemble_table(g.requests, g.suffix_cap, bt, g.rows)
+        s = g.wl.shape
+        outs = [(torch.empty(ins[li][3], s.n_q_heads, s.head_dim, dtype=torch.bfloat16, device="cuda"),
+                 torch.empty(ins[li][3], s.n_q_heads, dtype=torch.float32, device="cuda")) for li in range(L)]
+
+        def chain(stream=None):
+            g.ctx.gather_layers(bt, g.n_entries, 0, 1, kv, g.rows, stream=stream)
+            nq, nkv = s.q_dim, s.kv_dim
+            ld = nq + 2 * nkv
+            for li in range(L):
+                qkv, gq, gk, _ = ins[li]
+                args = (li, g.cu_q, g.cu_ctx, g.art_len, g.pos0, qkv[:, :nq], ld, qkv[:, nq:nq + nkv],
+                        qkv[:, nq + nkv:], ld, gq, gk, kv, g.rows, outs[li][0])
+                if li + 1 < L:
+                    g.ctx.suffix_attn_gather(*args, bt, g.n_entries, li + 1, outs[li][1], stream=stream)
+                else:
+                    g.ctx.suffix_attn(*args, outs[li][1], stream=stream)
+
+        _say("graph of the chained layer loop: eager reference")
+        chain()
+        torch.cuda.synchronize()
+        want = [(o.clone(), l.clone()) for o, l in outs]
+        kv_want = kv.clone()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        graph = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap):
+            chain(stream=cap)
+        torch.cuda.synchronize()
+        for rep in range(3):
+            _say(f"graph replay {rep}")
+            kv.zero_()
+            for o, l in outs:
+                o.zero_()
+                l.zero_()
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            for li in range(L):
+                assert torch.equal(_bits(outs[li][0]), _bits(want[li][0])), f"replay {rep}: O of layer {li}"
+                assert torch.equal(_bits(outs[li][1]), _bits(want[li][1])), f"replay {rep}: LSE of layer {li}"
+            assert torch.equal(kv.view(torch.int16), kv_want.view(torch.int16)), f"replay {rep}: cache"
+            _ = (torch.ones(1 << 20, device="cuda") * 2).sum().item()   # eager work between replays
+        del graph
     finally:
         g.close()
