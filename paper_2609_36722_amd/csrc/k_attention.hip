@@ -50,6 +50,13 @@
 // (fp32), and a second kernel merges them.  (Merging inside this kernel would need
 // agent-scope release/acquire between workgroups, which on gfx950 writes back
 // and invalidates the XCD's L2 and costs the other workgroups their K/V reuse.)
+//
+// A second instantiation (GATHER) also copies another layer's artifact pages
+// from the pool into the request cache, so that a layer-by-layer prefill has
+// layer l + 1's cache assembled by the end of layer l's attention: each wave
+// moves 1 KiB chunks through three LDS slots of its own with the same DMA
+// form of the load, issued after a tile's K/V copies, and stores each chunk
+// from LDS three tiles later.
 
 #include "common.h"
 #include "kernels.h"
