@@ -424,11 +424,13 @@ attuner_status attuner_suffix_attn(attuner_ctx* ctx, int32_t layer, int32_t n_re
  *   ATTUNER_ERANGE) and != layer (else ATTUNER_EINVAL): the attention
  *   reads `layer`'s rows while the copy writes gather_layer's.
  * The copy rides in the attention launch when every page of that table is
- * in the HBM pool, 8 n_kv_heads is a power of two and one layer's pool and
- * cache planes are below 4 GiB; otherwise (host or staged pages, other
- * shapes, no suffix tokens) the call runs attuner_gather_layers first and
- * then attuner_suffix_attn, on `stream`.  Other arguments, outputs and
- * errors as attuner_suffix_attn. */
+ * in the HBM pool, 8 n_kv_heads is a power of two, one layer's pool and
+ * cache planes are below 4 GiB, and the attention's key tiles can carry at
+ * least half of the copy (each wave moves 1 KiB per tile it passes);
+ * otherwise (host or staged pages, other shapes, no suffix tokens, short
+ * key ranges) the copy runs as a gather launch of its own on `stream`,
+ * before the attention.  Other arguments, outputs and errors as
+ * attuner_suffix_attn. */
 attuner_status attuner_suffix_attn_gather(attuner_ctx* ctx, int32_t layer, int32_t n_req, const int32_t* cu_q,
                                           const int32_t* cu_ctx, const int32_t* art_len, const int32_t* pos0,
                                           const void* q_raw, int64_t ld_q, const void* k_raw, const void* v_raw,

@@ -622,6 +622,35 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
   p.n_split = n_split;
   p.n_units = units;
   if (gather != nullptr) {
+    // Each workgroup takes an equal share of the copy's 1 KiB chunks, and
+    // each of its 8 waves moves one chunk per key tile it passes; what the
+    // tiles do not cover is copied after the tile loop, at a lower rate than
+    // a gather launch of its own.  When that remainder would exceed half
+    // the copy (short key ranges), the copy runs as its own launch instead.
+    const int n_slab = 2 * c->cfg.n_kv_heads;
+    const int64_t chunks = gather->entries * n_slab * 4;
+    const int64_t wgs = (int64_t)units * c->cfg.n_kv_heads;
+    const int64_t per_wg = (chunks + wgs - 1) / wgs;
+    int64_t left = 0;
+    for (size_t i = 0; i < order.size(); ++i) {
+      const AttnReq& rq = p.req[i];
+      for (int qb = 0; qb < rq.n_qblk; ++qb) {
+        const int64_t kv_len = (int64_t)rq.art_len + std::min(rq.q_len, (qb + 1) * 64);
+        const int64_t n_tiles = (kv_len + 63) / 64, per = (n_tiles + rq.n_split - 1) / rq.n_split;
+        for (int sp = 0; sp < rq.n_split; ++sp) {
+          const int64_t tb = std::min(n_tiles, sp * per), syncs = std::min(n_tiles, tb + per) - tb;
+          left += c->cfg.n_kv_heads * std::max<int64_t>(0, per_wg - 8 * syncs);
+        }
+      }
+    }
+    if (2 * left > chunks) {
+      HIP_TRY(launch_gather(gather->table, gather->entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages,
+                            c->stage_pool, c->stage_pages, gather->layer, 1, c->cfg.n_kv_heads, gather->req_kv,
+                            gather->cache_rows, stream));
+      gather = nullptr;
+    }
+  }
+  if (gather != nullptr) {
     const int n_slab = 2 * c->cfg.n_kv_heads;
     const int64_t chunks = gather->entries * n_slab * 4;
     const int64_t wgs = (int64_t)units * c->cfg.n_kv_heads;

@@ -498,13 +498,29 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
     if (tb + 1 < te) dma_tile(kb, vb, (tb + 1) * BKV, kv_len, k_base + kStage, v_base + kStage, dl, wave);
   }
   if constexpr (GATHER) {
-    // the chunks still in LDS, then the rest of the wave's chunks directly
+    // the chunks still in LDS, then the rest of the wave's chunks directly,
+    // eight loads in flight at a time (short key ranges leave most of the
+    // copy to this loop, and one chunk at a time would pay a memory latency
+    // per kilobyte)
     __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
     for (int n = max(0, g_syncs - kGSlots); n < min(g_syncs, g_count); ++n) g_store(n);
-    for (int n = g_syncs; n < g_count; ++n) {
-      uint32_t so, dof;
-      if (g_addr(g_first + n * (NTHREADS / 64), so, dof))
-        __builtin_nontemporal_store(__builtin_nontemporal_load(g_src + so), g_dst + dof);
+    constexpr int kGBatch = 8;
+    for (int n0 = g_syncs; n0 < g_count; n0 += kGBatch) {
+      u32x4 v[kGBatch];
+      uint32_t dof[kGBatch];
+      bool ok[kGBatch];
+#pragma unroll
+      for (int i = 0; i < kGBatch; ++i) {
+        // every lane loads (a row past n_valid reads row 0 of its page; past
+        // the wave's last chunk, that chunk again): only the stores are masked
+        uint32_t so;
+        const int n = min(n0 + i, g_count - 1);
+        ok[i] = g_addr(g_first + n * (NTHREADS / 64), so, dof[i]) && n0 + i < g_count;
+        v[i] = __builtin_nontemporal_load(g_src + so);
+      }
+#pragma unroll
+      for (int i = 0; i < kGBatch; ++i)
+        if (ok[i]) __builtin_nontemporal_store(v[i], g_dst + dof[i]);
     }
   }
   l_i += __shfl_xor(l_i, 32, 64);  // the two lanes of a token hold its two partial sums

@@ -6,13 +6,16 @@ request cache must agree bit for bit, and each request's cached rows must
 hold its artifacts in order (the oracle's assembly: rows cu_ctx[r] ..
 cu_ctx[r] + art_len[r] - 1).
 
-Cases: a three-layer batch of four requests (ragged last pages, an artifact
-twice in one request); the long-context Qwen3-8B shape over two layers (the
-launch the step times, with key splits); suffixes of one to three tokens over
-long artifacts (the copy outweighs the attention, most of it runs after the
-tile loop); an artifact in the host pool (the call copies in a launch of its
-own first); a batch with no suffix tokens; the argument errors; and the
-chained layer loop captured in a HIP graph and replayed."""
+Cases (the library's launch tracer tells which path ran): a three-layer
+batch of four requests (ragged last pages, an artifact twice in one
+request; the copy rides, partly after the tile loop where a request's key
+range is short); the Qwen3-4B and the long-context Qwen3-8B shapes over two
+layers (the launches the step times, with key splits); the three-layer
+batch with short suffixes and suffixes of one to three tokens over long
+artifacts (too few key tiles to carry the copy: a gather launch of its own);
+an artifact in the host pool (likewise); a batch with no suffix tokens; the
+argument errors; and the chained layer loop captured in a HIP graph and
+replayed."""
 
 import numpy as np
 import pytest
@@ -32,9 +35,10 @@ def _say(msg):
     print(f"[case] {msg}", flush=True)
 
 
-def _three_layer(index=96):
+def _three_layer(index=96, suffixes=(400, 300, 257, 129)):
     return custom_workload("gather-3l", index, ModelShape(hidden=2560), [700, 1500, 333, 64, 16],
-                           [Request((0, 1), 40), Request((2,), 100), Request((3, 1, 0), 7), Request((4, 4), 129)],
+                           [Request((0, 1), suffixes[0]), Request((2,), suffixes[1]), Request((3, 1, 0), suffixes[2]),
+                            Request((4, 4), suffixes[3])],
                            n_layers=3, rank=8, scale=2.0, gamma="uniform")
 
 
@@ -90,7 +94,7 @@ def _check_artifact_rows(g, kv_host):
                 f"request {r} plane {plane}"
 
 
-def _chain(g, name):
+def _chain(g, name, fused):
     """Reference: cache assembled for every layer, then suffix_attn per layer.
     Chained: layer 0's pages, then layer l's attention copies layer l + 1's
     (the last layer's copies layer 0 again, which leaves it unchanged)."""
@@ -108,23 +112,48 @@ def _chain(g, name):
     assert list(cu) == list(g.cu_ctx) and list(al) == list(g.art_len)
     g.ctx.gather_layers(bt, g.n_entries, 0, 1, kv, g.rows)
     got = []
+    g.ctx.trace_begin()
     for li in range(L):
         nxt = li + 1 if li + 1 < L else 0
         _say(f"{name}: suffix_attn_gather layer {li}, copy layer {nxt}")
         got.append(_call(g, li, ins[li], kv, nxt, bt))
     torch.cuda.synchronize()
+    launches = {k: v[0] for k, v in g.ctx.trace_end().items()}
+    _say(f"{name}: launches {launches}")
+    # which path ran: the copy inside every attention launch, or (short key
+    # ranges, host pages) a gather launch of its own before each attention
+    if fused:
+        assert launches.get("attention_gather_kernel") == L and "gather_kernel" not in launches, launches
+    else:
+        assert launches.get("gather_kernel") == L and "attention_gather_kernel" not in launches, launches
     for li in range(L):
         assert torch.equal(_bits(got[li][0]), _bits(ref[li][0])), f"{name}: O of layer {li}"
         assert torch.equal(_bits(got[li][1]), _bits(ref[li][1])), f"{name}: LSE of layer {li}"
     kv_got = bf16_to_host(kv)
     assert np.array_equal(kv_got, kv_ref), f"{name}: request cache"
-    return bt
+    return launches
 
 
 def test_gather_attn_three_layers_bit_exact():
     g = GpuWorkload(_three_layer(), layers=(0, 1, 2))
     try:
-        _chain(g, "3-layer batch")
+        _chain(g, "3-layer batch", fused=True)
+    finally:
+        g.close()
+
+
+def test_gather_attn_short_batch_three_layers():
+    g = GpuWorkload(_three_layer(101, (40, 100, 7, 129)), layers=(0, 1, 2))
+    try:
+        _chain(g, "3-layer batch, short suffixes", fused=False)
+    finally:
+        g.close()
+
+
+def test_gather_attn_c2_two_layers():
+    g = GpuWorkload(sd.make_workload("c2", gamma="uniform"), layers=(0, 1))
+    try:
+        _chain(g, "c2 layers 0-1", fused=True)
     finally:
         g.close()
 
@@ -132,7 +161,7 @@ def test_gather_attn_three_layers_bit_exact():
 def test_gather_attn_long_context_two_layers():
     g = GpuWorkload(sd.make_workload("c5", gamma="uniform"), layers=(0, 1))
     try:
-        _chain(g, "c5 layers 0-1")
+        _chain(g, "c5 layers 0-1", fused=True)
     finally:
         g.close()
 
@@ -140,7 +169,7 @@ def test_gather_attn_long_context_two_layers():
 def test_gather_attn_short_suffixes():
     g = GpuWorkload(_short_suffix(), layers=(0, 1))
     try:
-        _chain(g, "1-3 token suffixes")
+        _chain(g, "1-3 token suffixes", fused=False)
     finally:
         g.close()
 
@@ -148,7 +177,7 @@ def test_gather_attn_short_suffixes():
 def test_gather_attn_host_pages_fall_back():
     g = GpuWorkload(_three_layer(98), layers=(0, 1, 2), host_artifacts=(1,))
     try:
-        _chain(g, "host-pool artifact")
+        _chain(g, "host-pool artifact", fused=False)
     finally:
         g.close()
 
