@@ -563,14 +563,21 @@ size_t split_row_bytes(const attuner_ctx* c) {
 // part_buf / part_bytes: a caller-provided buffer for the key-split
 // partials (the plan is then limited to what fits); null: the context's
 // workspace, grown as needed.
-// A copy of one layer's pages that the attention launch carries (AttnParams g_*).
+// A copy of one layer's pages that the attention launch carries (AttnParams
+// g_*), or with `apart` a gather launch of its own before the attention.
 struct GatherArgs {
   const int32_t* table;
   int64_t entries;
   int32_t layer;
   uint16_t* req_kv;
   int64_t cache_rows;
+  bool apart;
 };
+
+hipError_t launch_gather_apart(attuner_ctx* c, const GatherArgs& g, hipStream_t stream) {
+  return launch_gather(g.table, g.entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages, c->stage_pool,
+                       c->stage_pages, g.layer, 1, c->cfg.n_kv_heads, g.req_kv, g.cache_rows, stream);
+}
 
 attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, int32_t total_q, const void* q,
                              const uint16_t* k_plane, const uint16_t* v_plane, int64_t head_stride, void* o,
@@ -621,6 +628,10 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
     }
   p.n_split = n_split;
   p.n_units = units;
+  if (gather != nullptr && gather->apart) {
+    HIP_TRY(launch_gather_apart(c, *gather, stream));
+    gather = nullptr;
+  }
   if (gather != nullptr) {
     // Each workgroup takes an equal share of the copy's 1 KiB chunks, and
     // each of its 8 waves moves one chunk per key tile it passes; what the
@@ -644,9 +655,7 @@ attuner_status run_attention(attuner_ctx* c, const std::vector<ReqDesc>& reqs, i
       }
     }
     if (2 * left > chunks) {
-      HIP_TRY(launch_gather(gather->table, gather->entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages,
-                            c->stage_pool, c->stage_pages, gather->layer, 1, c->cfg.n_kv_heads, gather->req_kv,
-                            gather->cache_rows, stream));
+      HIP_TRY(launch_gather_apart(c, *gather, stream));
       gather = nullptr;
     }
   }
@@ -1657,7 +1666,12 @@ static attuner_status suffix_attn_impl(attuner_ctx* c, int32_t layer, int32_t n_
   int32_t total_q = 0;
   st = build_reqs(c, n_req, cu_q, cu_ctx, art_len, pos0, cache_rows, &reqs, &total_q);
   if (st != ATTUNER_OK) return st;
-  if (total_q == 0) return ATTUNER_OK;
+  if (total_q == 0) {
+    if (gather == nullptr) return ATTUNER_OK;
+    DeviceGuard dg(c->device);
+    HIP_TRY(launch_gather_apart(c, *gather, static_cast<hipStream_t>(stream)));
+    return ATTUNER_OK;
+  }
   st = check_norm_args(q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q, gamma_k, c);
   if (st != ATTUNER_OK) return st;
   if (!req_kv || !o || !aligned16(req_kv) || !aligned16(o))
@@ -1719,26 +1733,16 @@ attuner_status attuner_suffix_attn_gather(attuner_ctx* c, int32_t layer, int32_t
     return fail(ATTUNER_EINVAL, "gather_layer must differ from layer (the attention reads that layer's rows)");
   if (!req_kv || !aligned16(req_kv)) return fail(ATTUNER_EINVAL, "req_kv must be non-null and 16-byte aligned");
   // the attention launch carries the copy when the table names HBM pages only
-  // and one layer's offsets fit 32 bits; otherwise the gather runs first
+  // and one layer's offsets fit 32 bits; otherwise the copy is a launch of
+  // its own, issued (like the carried one) only once every argument passed
   const int64_t n_slab = 2 * c->cfg.n_kv_heads;
   const bool pow2 = ((n_slab * 4) & (n_slab * 4 - 1)) == 0;
   const bool fits = n_entries * n_slab * 4 < INT32_MAX && c->pool_pages * n_slab * kPageTokens * 16 < (1LL << 32) &&
                     n_slab * cache_rows * 16 < (1LL << 32);
-  int32_t total_q = 0;
-  for (int32_t r = 0; cu_q && r < n_req; ++r) total_q += cu_q[r + 1] - cu_q[r];
-  if (n_entries == 0 || !c->last_hbm_only || !pow2 || !fits || total_q == 0 || !c->pool) {
-    if (n_entries > 0) {
-      DeviceGuard dg(c->device);
-      HIP_TRY(launch_gather(block_table, n_entries, c->pool, c->pool_pages, c->host_pool_dev, c->host_pages,
-                            c->stage_pool, c->stage_pages, gather_layer, 1, c->cfg.n_kv_heads,
-                            static_cast<uint16_t*>(req_kv), cache_rows, static_cast<hipStream_t>(stream)));
-    }
-    return suffix_attn_impl(c, layer, n_req, cu_q, cu_ctx, art_len, pos0, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q,
-                            gamma_k, req_kv, cache_rows, o, lse, stream, false);
-  }
-  const GatherArgs g{block_table, n_entries, gather_layer, static_cast<uint16_t*>(req_kv), cache_rows};
+  const bool apart = !c->last_hbm_only || !pow2 || !fits || !c->pool;
+  const GatherArgs g{block_table, n_entries, gather_layer, static_cast<uint16_t*>(req_kv), cache_rows, apart};
   return suffix_attn_impl(c, layer, n_req, cu_q, cu_ctx, art_len, pos0, q_raw, ld_q, k_raw, v_raw, ld_kv, gamma_q,
-                          gamma_k, req_kv, cache_rows, o, lse, stream, false, &g);
+                          gamma_k, req_kv, cache_rows, o, lse, stream, false, n_entries > 0 ? &g : nullptr);
 }
 
 attuner_status attuner_span_attn(attuner_ctx* c, int32_t layer, int32_t n_spans, const int32_t* cu_q,

@@ -178,6 +178,17 @@ def test_gather_attn_host_pages_fall_back():
     g = GpuWorkload(_three_layer(98), layers=(0, 1, 2), host_artifacts=(1,))
     try:
         _chain(g, "host-pool artifact", fused=False)
+        # a call rejected after the copy was set apart enqueues nothing
+        _say("host-pool artifact: rejected call")
+        kv = torch.zeros_like(g.req_kv)
+        bt = torch.zeros_like(g.block_table)
+        g.ctx.assemble_table(g.requests, g.suffix_cap, bt, g.rows)
+        ins = _qkv(g, 0)
+        with pytest.raises(AttunerError) as e:
+            _call(g, 3, ins, kv, 1, bt)                     # no layer 3 to attend over
+        assert e.value.status == -1
+        torch.cuda.synchronize()
+        assert not bf16_to_host(kv).any()
     finally:
         g.close()
 
