@@ -70,8 +70,8 @@ def parse():
     ov = ap.add_mutually_exclusive_group()
     ov.add_argument("--fold-gather", dest="gather_mode", action="store_const", const="fold", default=None,
                     help="gather layer 0 first, then let layer l's attention launch copy layer l + 1's pages "
-                         "(attuner_suffix_attn_gather; the default: measured on MI355X against the better of "
-                         "the two below, -0.6%% per step at c5, -3.8%% at c3, -7.0%% at c2)")
+                         "(attuner_suffix_attn_gather).  Default with several layers: this or --overlap-gather, "
+                         "whichever is faster on the device (both are timed before the timed region)")
     ov.add_argument("--overlap-gather", dest="gather_mode", action="store_const", const="overlap",
                     help="gather layer by layer on a second stream beside the layer loop")
     ov.add_argument("--gather-first", dest="gather_mode", action="store_const", const="first",
@@ -244,9 +244,11 @@ def kernel_traffic(kernel_file, workload, kernel):
         with open(path) as f:
             rec = json.load(f)
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-        if rec.get("source_sha256") != sha or rec.get("kernel") != kernel:
+        if rec.get("source_sha256") != sha:
             return None
-        return float(rec["hbm_bytes_per_launch"])
+        if kernel in rec.get("by_kernel", {}):
+            return float(rec["by_kernel"][kernel])
+        return float(rec["hbm_bytes_per_launch"]) if rec.get("kernel") == kernel else None
     except Exception:
         return None
 
@@ -423,38 +425,30 @@ def main():
         log(args, f"copy probe: {args.copy_probe_mb} MiB read + written by one elementwise kernel")
         del a_src, a_dst
 
-    # default: the fold; one layer has no next layer to carry, and its gather
-    # goes beside the projection on a second stream from 100 MB (measured at
-    # c4, one layer of 16 requests: 1.361-1.378 against 1.370-1.382 ms)
+    # The gather schedule.  With several layers the candidates are the copy
+    # carried in the attention launches (fold) and the per-layer gathers on a
+    # second stream (overlap): which is faster depends on the box (c5 on
+    # three boxes: fold -0.6 %, +0.9 %, +1.1 %), so unless a schedule is
+    # named both are timed on this device before the timed region and the
+    # faster one runs there.  One layer has no next layer to carry: its
+    # gather goes beside the projection on a second stream from 100 MB
+    # (measured at c4, one layer of 16 requests: 1.361-1.378 against
+    # 1.370-1.382 ms), else first.
     one_layer_bytes = gather_bytes(s, sum(wl.art_len(r) for r in wl.requests), 1)
-    mode = args.gather_mode or ("fold" if NL > 1 else "overlap" if one_layer_bytes >= 100e6 else "first")
-    overlap = mode == "overlap" and not staged
-    fold = mode == "fold" and not staged and NL > 1
+    if args.gather_mode:
+        cands = [args.gather_mode]
+    elif NL > 1 and not staged:
+        cands = ["fold", "overlap"]
+    else:
+        cands = ["overlap" if one_layer_bytes >= 100e6 else "first"]
+    overlap = fold = False
 
-    log(args, f"warmup {args.warmup} steps")
-    for i in range(args.warmup):
-        run_step(None, 0, fold=fold)
-    torch.cuda.synchronize()
+    def set_mode(m):
+        nonlocal overlap, fold
+        overlap = m == "overlap" and not staged
+        fold = m == "fold" and not staged and NL > 1
 
-    # per-kernel times: eager steps with events around every call, and the
-    # library's launch tracer for each kernel on its own
-    n_ev = max(1, min(args.steps, 5))
-    evs = make_events(n_ev)
-    for _ in range(2):   # the first pass is discarded (see TRACE_PASSES)
-        ctx.trace_begin()
-        for i in range(n_ev):
-            run_step(evs, i, fold=fold)
-        torch.cuda.synchronize()
-        ktimes = ctx.trace_end()
-    kern_ms = {c: sum(a.elapsed_time(b) for a, b in evs[c]) / len(evs[c]) for c in cats}
-    per_kernel = {k: {"launches": n, "avg_ms": round(t / n, 5), "max_ms": round(mx, 5)}
-                  for k, (n, t, mx) in ktimes.items()}
-    # the dominant kernel: with the fold, the launches that also copy the next layer's pages
-    attn_kname = "attention_gather_kernel" if fold else "attention_kernel"
-    attn_kernel_ms = ktimes[attn_kname][1] / ktimes[attn_kname][0]
-    log(args, "kernel avg ms: " + ", ".join(f"{k} {v['avg_ms']:.4f} (x{v['launches']})" for k, v in per_kernel.items()))
-
-    # The timed step.  By default (fold) the block table (host plan + upload)
+    # The timed step.  With the fold the block table (host plan + upload)
     # goes first, then layer 0's pages are gathered, and layer l's
     # attuner_suffix_attn_gather copies layer l + 1's pages inside its
     # attention launch.  With --gather-first every layer is gathered first
@@ -515,20 +509,23 @@ def main():
     # graph those copy nodes did not overlap the layer loop's kernels
     # (measured at 36 layers, 8B shapes, 32 x 1024 artifact tokens: 104.3 ms
     # per step replayed against 89.6 ms eager).
-    graph = None
-    if not args.no_graph and not staged:
+    def capture():
+        """The current schedule's layer loop as one HIP graph (None: eager)."""
+        if args.no_graph or staged:
+            return None
         cap = torch.cuda.Stream()
-        graph = torch.cuda.CUDAGraph()
+        g_ = torch.cuda.CUDAGraph()
         cap.wait_stream(stream)
         side.wait_stream(stream)
-        if staged:  # the captured copies are those of the plan current at capture
-            check(lib.attuner_assemble_table_staged(*staged_args), "attuner_assemble_table_staged")
-        elif overlap or fold:  # the captured gathers read the table the last assemble_table call wrote
+        if overlap or fold:  # the captured gathers read the table the last assemble_table call wrote
             check(lib.attuner_assemble_table(*table_args), "attuner_assemble_table")
         torch.cuda.synchronize()
-        with torch.cuda.graph(graph, stream=cap):
+        with torch.cuda.graph(g_, stream=cap):
             layer_loop(cap, qproj_args, attn_args)
         torch.cuda.synchronize()
+        return g_
+
+    graph = None
 
     def timed_step():
         if staged:
@@ -543,6 +540,61 @@ def main():
             layer_loop(stream, qproj_args, attn_args)
         else:
             run_step(None, 0, gather=False)
+
+    log(args, f"warmup {args.warmup} steps")
+    for i in range(args.warmup):
+        run_step(None, 0)
+    torch.cuda.synchronize()
+
+    # the candidates timed on this device, twice in turn (3 + 10 steps each
+    # time, the better of the two kept), the faster one used from here on
+    trials = {}
+    graphs = {}
+    for m in cands:
+        set_mode(m)
+        graphs[m] = capture()
+    for _ in range(2 if len(cands) > 1 else 0):
+        for m in cands:
+            set_mode(m)
+            graph = graphs[m]
+            for _ in range(3):
+                timed_step()
+            torch.cuda.synchronize()
+            a_, b_ = timing_events(2)
+            a_.record(stream)
+            for _ in range(10):
+                timed_step()
+            b_.record(stream)
+            torch.cuda.synchronize()
+            t_ = a_.elapsed_time(b_) / 10
+            trials[m] = round(min(t_, trials.get(m, t_)), 4)
+    mode = min(trials, key=trials.get) if trials else cands[0]
+    set_mode(mode)
+    graph = graphs[mode]
+    if trials:
+        log(args, "gather schedules (ms/step): " + ", ".join(f"{k} {v:.3f}" for k, v in trials.items()) +
+            f" -> {mode}")
+    for i in range(2):
+        run_step(None, 0, fold=fold)
+    torch.cuda.synchronize()
+
+    # per-kernel times: eager steps with events around every call, and the
+    # library's launch tracer for each kernel on its own
+    n_ev = max(1, min(args.steps, 5))
+    evs = make_events(n_ev)
+    for _ in range(2):   # the first pass is discarded (see TRACE_PASSES)
+        ctx.trace_begin()
+        for i in range(n_ev):
+            run_step(evs, i, fold=fold)
+        torch.cuda.synchronize()
+        ktimes = ctx.trace_end()
+    kern_ms = {c: sum(a.elapsed_time(b) for a, b in evs[c]) / len(evs[c]) for c in cats}
+    per_kernel = {k: {"launches": n, "avg_ms": round(t / n, 5), "max_ms": round(mx, 5)}
+                  for k, (n, t, mx) in ktimes.items()}
+    # the dominant kernel: with the fold, the launches that also copy the next layer's pages
+    attn_kname = "attention_gather_kernel" if fold else "attention_kernel"
+    attn_kernel_ms = ktimes[attn_kname][1] / ktimes[attn_kname][0]
+    log(args, "kernel avg ms: " + ", ".join(f"{k} {v['avg_ms']:.4f} (x{v['launches']})" for k, v in per_kernel.items()))
 
     for i in range(2):
         timed_step()
@@ -668,6 +720,7 @@ def main():
                             if staged else "per layer on a second stream beside the layer loop" if overlap
                             else "layer 0 first, layer l + 1 inside layer l's attention launch" if fold
                             else "all layers first"),
+        "gather_schedule_trials_ms": trials or None,
         "artifact_cache": "pinned host memory, moved over the host link every step" if args.host_cache else "HBM",
         "host_transfer": host_transfer,
         "adapter": "merged into W_q (rank-0 projection)" if args.merged else "unmerged, fused into the projection",
