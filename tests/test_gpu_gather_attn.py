@@ -122,9 +122,9 @@ def _chain(g, name, fused):
     _say(f"{name}: launches {launches}")
     # which path ran: the copy inside every attention launch, or (short key
     # ranges, host pages) a gather launch of its own before each attention
-    if fused:
+    if fused is True:
         assert launches.get("attention_gather_kernel") == L and "gather_kernel" not in launches, launches
-    else:
+    elif fused is False:
         assert launches.get("gather_kernel") == L and "attention_gather_kernel" not in launches, launches
     for li in range(L):
         assert torch.equal(_bits(got[li][0]), _bits(ref[li][0])), f"{name}: O of layer {li}"
@@ -281,5 +281,31 @@ def test_gather_attn_graph_replays():
             assert torch.equal(kv.view(torch.int16), kv_want.view(torch.int16)), f"replay {rep}: cache"
             _ = (torch.ones(1 << 20, device="cuda") * 2).sum().item()   # eager work between replays
         del graph
+    finally:
+        g.close()
+
+
+@pytest.mark.parametrize("seed", [601, 602, 603, 604])
+def test_gather_attn_random_batches(seed):
+    """Random batches (1-5 requests, 1-4 artifacts each of 1-2500 tokens,
+    suffixes of 1-700 tokens, 2-3 layers, the 4B or 8B head layout): the
+    chained calls give O, LSE and cache bit for bit as the separate ones,
+    whichever path the library takes."""
+    rng = np.random.default_rng(seed)
+    n_art = int(rng.integers(2, 7))
+    lengths = [int(v) for v in rng.integers(1, 2500, size=n_art)]
+    reqs = []
+    for _ in range(int(rng.integers(1, 6))):
+        arts = tuple(int(a) for a in rng.integers(0, n_art, size=int(rng.integers(1, 5))))
+        reqs.append(Request(arts, int(rng.integers(1, 700))))
+    hidden = 2560 if seed % 2 else 4096
+    wl = custom_workload(f"gather-rand-{seed}", seed, ModelShape(hidden=hidden), lengths, reqs,
+                         n_layers=3, rank=8, scale=1.0, gamma="uniform")
+    layers = (0, 1, 2) if seed % 3 else (0, 1)
+    _say(f"seed {seed}: artifacts {lengths}, requests {[(r.artifact_ids, r.suffix_len) for r in reqs]}")
+    g = GpuWorkload(wl, layers=layers)
+    try:
+        launches = _chain(g, f"random batch {seed}", fused=None)
+        assert launches.get("attention_gather_kernel", 0) + launches.get("gather_kernel", 0) == len(layers)
     finally:
         g.close()
