@@ -616,6 +616,40 @@ attuner_status attuner_trace_begin(attuner_ctx* ctx);
 attuner_status attuner_trace_end(attuner_ctx* ctx, attuner_kernel_time* out, int32_t max_entries,
                                  int32_t* n_entries);
 
+/* --------------------------------------------------------------------------
+ * Bounds-checked build (a debugging aid; no passage of the paper defines it:
+ * it guards the paged assembly of section 2 and appendix A.3).
+ * libattuner_checked.so is this library compiled with device-side tests,
+ * before each use, of every block-table entry the gather and the attention
+ * launch's page copy read (page id within its pool, n_valid within a page,
+ * destination rows within the request-cache plane), of the page ids the
+ * store writes, and of the query rows and key ranges the attention and
+ * decode launches read (within the buffers they were given).  A failed test
+ * sets one of the bits below in a word in device memory and the access is
+ * skipped (that entry, or the whole workgroup), so a corrupted table or range
+ * is reported instead of faulting; results of skipped work are undefined.
+ * Same entry points and arguments as libattuner.so.
+ * ------------------------------------------------------------------------ */
+#define ATTUNER_VIOL_GATHER_PAGE (1u << 0)   /* gather: page id past its pool, or that pool absent */
+#define ATTUNER_VIOL_GATHER_ROWS (1u << 1)   /* gather: n_valid past a page, or rows past the cache plane */
+#define ATTUNER_VIOL_STORE_PAGE (1u << 2)    /* store: page id past the pool */
+#define ATTUNER_VIOL_ATTN_RANGE (1u << 3)    /* attention: query rows or key range past its buffers */
+#define ATTUNER_VIOL_COPY_ENTRY (1u << 4)    /* attention's page copy: entry outside its pool or cache plane */
+#define ATTUNER_VIOL_DECODE_RANGE (1u << 5)  /* decode: key range past the cache plane */
+
+/* *checked = 1 in libattuner_checked.so, 0 in libattuner.so.  No device work.
+ * Errors: EINVAL (null checked). */
+attuner_status attuner_bounds_checked(int32_t* checked);
+
+/* Waits for all work on `device` to finish (a blocking diagnostic call; not
+ * for use while a stream is capturing), then stores in *bits the OR of the
+ * ATTUNER_VIOL_* bits the kernels have set on that device since the last
+ * reset, and clears them when reset != 0.  The ordinary build stores 0 and
+ * touches no device.
+ * Errors: EINVAL (null bits, device out of range), EDEVICE (a HIP error,
+ * including one left by earlier work on the device). */
+attuner_status attuner_bounds_violations(int32_t device, int32_t reset, uint32_t* bits);
+
 #ifdef __cplusplus
 }
 #endif

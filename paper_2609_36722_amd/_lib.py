@@ -8,7 +8,14 @@ from __future__ import annotations
 import ctypes as C
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libattuner.so")
+_PKG = os.path.dirname(os.path.abspath(__file__))
+# ATTUNER_LIB_VARIANT=checked loads the bounds-checked build (same ABI) instead
+VARIANTS = {"": "libattuner.so", "checked": "libattuner_checked.so"}
+VARIANT = os.environ.get("ATTUNER_LIB_VARIANT", "")
+if VARIANT not in VARIANTS:
+    raise RuntimeError(f"ATTUNER_LIB_VARIANT={VARIANT!r}: expected one of {sorted(VARIANTS)}")
+LIB_PATH = os.path.join(_PKG, VARIANTS[VARIANT])
+CHECKED_LIB_PATH = os.path.join(_PKG, VARIANTS["checked"])
 
 STATUS = {0: "ATTUNER_OK", -1: "ATTUNER_EINVAL", -2: "ATTUNER_ENOMEM", -3: "ATTUNER_ENOENT",
           -4: "ATTUNER_EDEVICE", -5: "ATTUNER_ERANGE"}
@@ -89,22 +96,29 @@ SIGNATURES = {
                                        _vp, _vp, _vp]),
     "attuner_trace_begin": (C.c_int, [_vp]),
     "attuner_trace_end": (C.c_int, [_vp, C.POINTER(KernelTimeC), _i32, _i32p]),
+    "attuner_bounds_checked": (C.c_int, [_i32p]),
+    "attuner_bounds_violations": (C.c_int, [_i32, _i32, C.POINTER(C.c_uint32)]),
 }
 
 _LIB = None
 
 
+def load(path: str) -> C.CDLL:
+    """Load one build of the library and declare its exports."""
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run `python -m paper_2609_36722_amd.build` "
+                           "(or __graft_entry__.build()) first")
+    handle = C.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(handle, name)
+        fn.restype = res
+        fn.argtypes = args
+    return handle
+
+
 def lib() -> C.CDLL:
-    """Load libattuner.so once and declare its exports."""
+    """The library every binding call goes to (LIB_PATH), loaded once."""
     global _LIB
     if _LIB is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2609_36722_amd.build` "
-                               "(or __graft_entry__.build()) first")
-        handle = C.CDLL(LIB_PATH)
-        for name, (res, args) in SIGNATURES.items():
-            fn = getattr(handle, name)
-            fn.restype = res
-            fn.argtypes = args
-        _LIB = handle
+        _LIB = load(LIB_PATH)
     return _LIB

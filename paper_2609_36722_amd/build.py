@@ -20,6 +20,8 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG_DIR, "libattuner.so")
+# the same sources with device-side bounds tests (-DATTUNER_CHECKED)
+CHECKED_LIB_PATH = os.path.join(PKG_DIR, "libattuner_checked.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -45,15 +47,22 @@ def sources():
 
 
 def build(verbose: bool = False, jobs: int = 8) -> str:
-    """Compile every HIP source and link the shared library; return its path."""
-    os.makedirs(BUILD_DIR, exist_ok=True)
+    """Compile every HIP source and link libattuner.so and, from the same
+    sources with -DATTUNER_CHECKED, libattuner_checked.so; return the first's path."""
+    _build_one(LIB_PATH, BUILD_DIR, [], verbose, jobs)
+    _build_one(CHECKED_LIB_PATH, os.path.join(BUILD_DIR, "checked"), ["-DATTUNER_CHECKED"], verbose, jobs)
+    return LIB_PATH
+
+
+def _build_one(lib_path: str, obj_dir: str, defines, verbose: bool, jobs: int) -> None:
+    os.makedirs(obj_dir, exist_ok=True)
     srcs = sources()
-    objs = [os.path.join(BUILD_DIR, os.path.basename(s)[:-4] + ".o") for s in srcs]
+    objs = [os.path.join(obj_dir, os.path.basename(s)[:-4] + ".o") for s in srcs]
 
     def compile_one(pair):
         src, obj = pair
         extra = EXTRA_FLAGS.get(os.path.basename(src), [])
-        out = _run([HIPCC, *COMMON_FLAGS, *DEVICE_FLAGS, *extra, "-c", src, "-o", obj])
+        out = _run([HIPCC, *COMMON_FLAGS, *DEVICE_FLAGS, *defines, *extra, "-c", src, "-o", obj])
         return src, out
 
     with cf.ThreadPoolExecutor(max_workers=max(1, min(jobs, len(srcs)))) as ex:
@@ -62,12 +71,11 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
                 print(f"[build] {os.path.relpath(src, ROOT)}", flush=True)
             if verbose and out.strip():
                 print(out, flush=True)
-    tmp = LIB_PATH + ".tmp"
+    tmp = lib_path + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, lib_path)
     if verbose:
-        print(f"[build] linked {os.path.relpath(LIB_PATH, ROOT)}", flush=True)
-    return LIB_PATH
+        print(f"[build] linked {os.path.relpath(lib_path, ROOT)}", flush=True)
 
 
 if __name__ == "__main__":

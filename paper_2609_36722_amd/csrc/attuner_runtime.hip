@@ -1940,4 +1940,35 @@ attuner_status attuner_trace_end(attuner_ctx* c, attuner_kernel_time* out, int32
   return ATTUNER_OK;
 }
 
+attuner_status attuner_bounds_checked(int32_t* checked) {
+  if (!checked) return fail(ATTUNER_EINVAL, "null checked");
+#ifdef ATTUNER_CHECKED
+  *checked = 1;
+#else
+  *checked = 0;
+#endif
+  return ATTUNER_OK;
+}
+
+attuner_status attuner_bounds_violations(int32_t device, int32_t reset, uint32_t* bits) {
+  if (!bits) return fail(ATTUNER_EINVAL, "null bits");
+  *bits = 0;
+#ifdef ATTUNER_CHECKED
+  int n_dev = 0;
+  HIP_TRY(hipGetDeviceCount(&n_dev));
+  if (device < 0 || device >= n_dev) return fail(ATTUNER_EINVAL, "device %d of %d", device, n_dev);
+  DeviceGuard dg(device);
+  HIP_TRY(hipDeviceSynchronize());
+  unsigned int v = 0;
+  HIP_TRY(read_violations_gather(&v, reset != 0));
+  HIP_TRY(read_violations_attention(&v, reset != 0));
+  HIP_TRY(read_violations_decode(&v, reset != 0));
+  *bits = v;
+#else
+  (void)device;
+  (void)reset;
+#endif
+  return ATTUNER_OK;
+}
+
 }  // extern "C"

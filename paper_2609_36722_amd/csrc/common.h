@@ -16,6 +16,49 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
+// ---- bounds-checked build ----------------------------------------------------
+// Compiled with -DATTUNER_CHECKED (libattuner_checked.so), the kernels test
+// every block-table entry, page id and key range against the extents of their
+// launch before they use it.  A failed test sets its bit (kViol*) in the
+// violation word of the kernel's source file and the access is skipped (a
+// workgroup whose whole range is wrong returns before its first barrier), so a
+// bad table shows up as a flag instead of a memory fault.  In the ordinary
+// build the tests compile away.
+#ifdef ATTUNER_CHECKED
+constexpr bool kChecked = true;
+#else
+constexpr bool kChecked = false;
+#endif
+constexpr unsigned kViolGatherPage = 1u << 0;  // gather: page id past its pool (or that pool absent)
+constexpr unsigned kViolGatherRows = 1u << 1;  // gather: n_valid past a page, or rows past the cache plane
+constexpr unsigned kViolStorePage = 1u << 2;   // store: page id past the pool
+constexpr unsigned kViolAttnRange = 1u << 3;   // attention: q rows or key range past its buffers
+constexpr unsigned kViolCopyEntry = 1u << 4;   // attention's page copy: entry out of its pool or cache plane
+constexpr unsigned kViolDecodeRange = 1u << 5; // decode: key range past the cache plane
+
+// One violation word per source file, and the host function that reads (and
+// optionally clears) it on the current device; the ordinary build reads 0.
+#ifdef ATTUNER_CHECKED
+#define ATTUNER_VIOLATION_WORD(word, reader)                                           \
+  __device__ unsigned int word = 0;                                                   \
+  hipError_t reader(unsigned int* bits, bool reset) {                                 \
+    unsigned int v = 0;                                                               \
+    hipError_t e = hipMemcpyFromSymbol(&v, HIP_SYMBOL(word), sizeof v, 0, hipMemcpyDeviceToHost); \
+    if (e != hipSuccess) return e;                                                    \
+    *bits |= v;                                                                       \
+    if (reset && v != 0) {                                                            \
+      const unsigned int zero = 0;                                                    \
+      e = hipMemcpyToSymbol(HIP_SYMBOL(word), &zero, sizeof zero, 0, hipMemcpyHostToDevice); \
+    }                                                                                 \
+    return e;                                                                         \
+  }
+#define ATTUNER_VIOLATE(word, bit) atomicOr(&(word), (bit))
+#else
+#define ATTUNER_VIOLATION_WORD(word, reader) \
+  hipError_t reader(unsigned int*, bool) { return hipSuccess; }
+#define ATTUNER_VIOLATE(word, bit) ((void)0)
+#endif
+
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }

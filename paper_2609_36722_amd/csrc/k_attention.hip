@@ -65,6 +65,8 @@ namespace attuner {
 
 namespace {
 
+ATTUNER_VIOLATION_WORD(g_violations_attn, read_violations_attn_impl)
+
 constexpr int BQ = 64;       // suffix tokens per workgroup (two 32-token halves)
 constexpr int BKV = 64;      // keys per tile
 constexpr int NSTAGE = 4;    // K/V tiles in LDS: i - 1 (its PV), i (its QK), i + 1 and i + 2 in flight
@@ -283,6 +285,14 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
     return base_off + row - base_row;
   };
   const int kv_len = lim(t0 + blk_rows - 1) + 1;  // keys any row of the block sees
+  if constexpr (kChecked) {
+    // the request's q rows and key range lie inside the launch's buffers
+    if (rq.q_start < 0 || rq.q_start + rq.q_len > p.total_q || rq.kv_start < 0 ||
+        (int64_t)rq.kv_start + kv_len > p.kv_head_stride / D) {
+      if (threadIdx.x == 0) ATTUNER_VIOLATE(g_violations_attn, kViolAttnRange);
+      return;
+    }
+  }
   const int n_tiles = (kv_len + BKV - 1) / BKV;
   const int per = (n_tiles + rq.n_split - 1) / rq.n_split;
   const int tb = min(n_tiles, split * per);
@@ -333,6 +343,17 @@ __global__ __launch_bounds__(NTHREADS, 1) void attention_kernel(AttnParams p) {
     const __attribute__((address_space(4))) int32_t* ent =
         (const __attribute__((address_space(4))) int32_t*)p.g_table + 4 * e;  // {page, n_valid, dst_row, req}
     const int row = 4 * qt + (lane >> 4);
+    if constexpr (kChecked) {
+      // an HBM pool page of this layer, rows inside a page and the cache plane
+      const bool ok = ent[0] >= 0 && (ent[0] & ~kPageIdMask) == 0 && ent[0] < p.g_pool_pages && ent[1] >= 0 &&
+                      ent[1] <= kPageTokens && ent[2] >= 0 && (int64_t)ent[2] + ent[1] <= p.g_cache_rows;
+      if (!ok) {
+        if (lane == 0) ATTUNER_VIOLATE(g_violations_attn, kViolCopyEntry);
+        so = (uint32_t)(lane & 15);  // a fetch stays inside page 0; nothing is stored
+        dof = 0;
+        return false;
+      }
+    }
     const bool valid = row < ent[1];
     const uint32_t rr = valid ? (uint32_t)row : 0u;
     so = ((uint32_t)((ent[0] & kPageIdMask) * g_nslab + sl) * kPageTokens + rr) * CH + (uint32_t)(lane & 15);
@@ -634,6 +655,10 @@ __global__ __launch_bounds__(256, 2) void attn_combine_kernel(AttnParams p) {
 }
 
 }  // namespace
+
+hipError_t read_violations_attention(unsigned int* bits, bool reset) {
+  return read_violations_attn_impl(bits, reset);
+}
 
 hipError_t launch_attention(const AttnParams& p, hipStream_t stream) {
   if (p.n_units == 0) return hipSuccess;

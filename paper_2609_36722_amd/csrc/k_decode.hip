@@ -28,6 +28,8 @@ namespace attuner {
 
 namespace {
 
+ATTUNER_VIOLATION_WORD(g_violations_decode, read_violations_decode_impl)
+
 constexpr int D = kHeadDim;
 constexpr int G = 4;                // query heads per KV head
 constexpr int LPK = 8;              // lanes per key
@@ -67,6 +69,13 @@ __global__ __launch_bounds__(NTH) void decode_attention_kernel(const DecodeParam
   const DecodeReq rq = p.req[r];
   const int k0 = (sid - rq.split0) * p.chunk;
   const int k1 = min(rq.n_keys, k0 + p.chunk);
+  if constexpr (kChecked) {
+    // the request's keys lie inside its cache plane
+    if (rq.kv_start < 0 || rq.n_keys < 1 || (int64_t)rq.kv_start + rq.n_keys > p.kv_head_stride / D) {
+      if (threadIdx.x == 0) ATTUNER_VIOLATE(g_violations_decode, kViolDecodeRange);
+      return;
+    }
+  }
   const int grp = threadIdx.x >> 3;
   const int sub = threadIdx.x & 7;
 
@@ -314,6 +323,10 @@ __global__ __launch_bounds__(NTH) void decode_combine_kernel(const DecodeParams 
 }
 
 }  // namespace
+
+hipError_t read_violations_decode(unsigned int* bits, bool reset) {
+  return read_violations_decode_impl(bits, reset);
+}
 
 hipError_t launch_decode_attention(const DecodeParams& p, hipStream_t stream) {
   if (p.total_splits == 0) return hipSuccess;

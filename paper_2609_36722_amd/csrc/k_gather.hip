@@ -38,12 +38,20 @@ namespace {
 
 constexpr int kSlabBatch = 8;
 
+ATTUNER_VIOLATION_WORD(g_violations_gather, read_violations_gather_impl)
+
 __global__ __launch_bounds__(256) void store_pages_kernel(const u32x4* __restrict__ k, const u32x4* __restrict__ v,
                                                           int n_tokens, const int32_t* __restrict__ pages,
                                                           u32x4* __restrict__ pool, int64_t pool_pages, int n_kv) {
   const int pi = blockIdx.x;      // page index within the artifact
   const int layer = blockIdx.y;
   const int page = pages[pi];
+  if constexpr (kChecked) {
+    if (page < 0 || page >= pool_pages) {
+      if (threadIdx.x == 0) ATTUNER_VIOLATE(g_violations_gather, kViolStorePage);
+      return;
+    }
+  }
   const int rr = threadIdx.x >> 4;
   const int chunk = threadIdx.x & 15;
   const int tok = pi * kPageTokens + rr;
@@ -93,6 +101,18 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ ta
 #pragma unroll
   for (int i = 0; i < kGatherRun; ++i) {
     ent[i] = e0 + i < n_entries ? table[e0 + i] : int4{0, 0, 0, 0};
+    if constexpr (kChecked) {
+      const bool rows_ok = ent[i].y >= 0 && ent[i].y <= kPageTokens && ent[i].z >= 0 &&
+                           (int64_t)ent[i].z + ent[i].y <= cache_rows;
+      const bool staged_ = (ent[i].x & kStagePageFlag) != 0, host_ = (ent[i].x & kHostPageFlag) != 0;
+      const u32x4* pool_ = staged_ ? stage_pool : host_ ? host_pool : dev_pool;
+      const int64_t pages_ = pool_ == nullptr ? 0 : staged_ ? stage_pages : host_ ? host_pages : dev_pages;
+      const bool page_ok = ent[i].x >= 0 && (int64_t)(ent[i].x & kPageIdMask) < pages_;
+      if (ent[i].y != 0 && (!rows_ok || !page_ok)) {
+        if (threadIdx.x == 0) ATTUNER_VIOLATE(g_violations_gather, rows_ok ? kViolGatherPage : kViolGatherRows);
+        ent[i].y = 0;  // neither read nor write this entry
+      }
+    }
     if (rr < ent[i].y) {
       const bool host = (ent[i].x & kHostPageFlag) != 0;
       const bool staged = (ent[i].x & kStagePageFlag) != 0;
@@ -109,6 +129,8 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4* __restrict__ ta
 }
 
 }  // namespace
+
+hipError_t read_violations_gather(unsigned int* bits, bool reset) { return read_violations_gather_impl(bits, reset); }
 
 hipError_t launch_store_pages(const uint16_t* k, const uint16_t* v, int n_tokens, const int32_t* pages_dev,
                               int n_pages, uint16_t* pool, int64_t pool_pages, int n_layers, int n_kv,

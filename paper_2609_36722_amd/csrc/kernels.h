@@ -25,6 +25,13 @@ void trace_launch_end(const char* kernel, hipStream_t stream);
     trace_launch_end(name, stream);                                         \
   } while (0)
 
+// Violation words of the bounds-checked build (common.h): OR the file's bits
+// into *bits, clearing them when `reset`; the current device's copy.  The
+// ordinary build adds nothing.
+hipError_t read_violations_gather(unsigned int* bits, bool reset);
+hipError_t read_violations_attention(unsigned int* bits, bool reset);
+hipError_t read_violations_decode(unsigned int* bits, bool reset);
+
 // ---- a0 / a2: pool store and block-table gather ---------------------------
 
 // Copy one artifact (k, v: [n_layers][n_kv][n_tokens][128]) into its pages.

@@ -64,3 +64,22 @@ def test_null_context_is_an_error_not_a_crash():
     assert lib.attuner_gate_up_swiglu(None, 1, None, 64, None, 32, None, None) == -1
     assert lib.attuner_lm_head_argmax(None, 1, None, None, 64, None, None, None) == -1
     lib.attuner_destroy(None)
+
+
+def test_checked_build_exports_the_same_abi():
+    """libattuner_checked.so (device-side bounds tests) exports the same entry
+    points and says which build it is; the ordinary build reports no
+    violations without touching a device."""
+    names = _declared()
+    chk = _lib.load(_lib.CHECKED_LIB_PATH)
+    for n in names:
+        assert hasattr(chk, n), f"{n} not exported by the checked build"
+    flag = C.c_int32(-1)
+    assert chk.attuner_bounds_checked(C.byref(flag)) == 0 and flag.value == 1
+    lib = _lib.load(os.path.join(os.path.dirname(_lib.CHECKED_LIB_PATH), _lib.VARIANTS[""]))
+    assert lib.attuner_bounds_checked(C.byref(flag)) == 0 and flag.value == 0
+    assert lib.attuner_bounds_checked(None) == -1
+    bits = C.c_uint32(7)
+    assert lib.attuner_bounds_violations(0, 1, C.byref(bits)) == 0 and bits.value == 0
+    assert lib.attuner_bounds_violations(0, 1, None) == -1
+    assert chk.attuner_bounds_violations(0, 1, None) == -1
