@@ -263,6 +263,11 @@ def main():
         print(f"bench.py measures one GPU only: the library has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
+    if os.environ.get("ATTUNER_LIB_VARIANT", ""):
+        # the bounds-checked library is a debugging aid: its kernels are not the ones to time
+        print(f"bench.py times the ordinary library only (ATTUNER_LIB_VARIANT="
+              f"{os.environ['ATTUNER_LIB_VARIANT']!r} is set).", file=sys.stderr)
+        sys.exit(2)
     if args.model:
         model_main(args)
         return
